@@ -1,0 +1,45 @@
+"""Plant a plausible mistake in a copy of the oracle (on the CPU) and check
+that at least one pin fails.  This is evidence that the pins constrain every
+step: the group max, the window edge, the local mass, the bias, the scale, the
+routing query, tie-breaking and the backward's chunk and score terms."""
+import os
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+SRC = open(oracle._SRC).read()
+
+MUTANTS = {
+    "group_score_first_head_only": ("if (s > m) m = s;", "if (hh == 0) m = s;",
+                                    [pins.test_hand_worked_example]),
+    "window_edge_off_by_one": ("long lc = floor_div(i - W + 1, S);", "long lc = floor_div(i - W, S);",
+                               [pins.test_hand_worked_example]),
+    "local_mass_misweighted": ("logits[0] = lam0;\n            for (int r = 0; r < st->nsel; ++r) logits[1 + r] = st->shat[r];",
+                               "logits[0] = lam0 - 1.0;\n            for (int r = 0; r < st->nsel; ++r) logits[1 + r] = st->shat[r];",
+                               [lambda: pins.test_p1_chunk1_window1_topall_is_dense_causal(4, 1, 4)]),
+    "bias_dropped": ("+ BIAS(in, b, hl, c);", ";",
+                     [lambda: pins.test_p2_exact_mass_landmarks_top_all_is_dense_causal(4, 5, 50, 2, 1, 2)]),
+    "scale_missing_in_surrogate": ("return (REAL)p->scale * dot_f(QHAT", "return dot_f(QHAT",
+                                   [lambda: pins.test_p1_chunk1_window1_topall_is_dense_causal(1, 1, 1)]),
+    "routing_query_ignored": ("const float* base = in->q_route ? in->q_route : in->q;", "const float* base = in->q;",
+                              [lambda: pins.test_p7_backward_matches_finite_differences(True, True, True)]),
+    "ties_to_larger_index": ("sigma[c] > sigma[best]) best = c;", "sigma[c] >= sigma[best]) best = c;",
+                             [pins.test_ties_go_to_the_smaller_chunk_index]),
+    "bwd_chunk_uses_global_u": ("REAL ds = a * pj * (gv - uc);", "REAL ds = a * pj * (gv - ubar);",
+                                [lambda: pins.test_p7_backward_matches_finite_differences(True, True, True)]),
+    "bwd_score_grad_drops_u": ("REAL dshat = a * (uc - ubar);", "REAL dshat = a * uc;",
+                               [lambda: pins.test_p7_backward_matches_finite_differences(False, False, True)]),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    old, new, checks = MUTANTS[name]
+    assert SRC.count(old) == 1, f"mutation anchor for {name} not unique"
+    lib = oracle.build_variant(SRC.replace(old, new), str(tmp_path / f"mut_{name}.so"))
+    with oracle.swapped_library(lib):
+        for check in checks:
+            with pytest.raises(AssertionError):
+                check()

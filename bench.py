@@ -1,0 +1,284 @@
+"""HiLS attention benchmark on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-decode] [--train] [--no-cpu]
+
+A step is one pass of the operator over one batch of synthetic input.  The
+headline workload is 32K-token causal prefill in bf16 (B=1, Hq=32, Hkv=8,
+d=128, chunk 64, top-16, window 512): every row of the path runs -- landmark
+scoring, group max, top-K selection, local-window attention, per-chunk
+attention and the fusion epilogue.  ``value`` is prefill tokens/s with all
+inputs resident in HBM.  Decode (32 x 131K-token caches) and, with --train,
+fwd+bwd at 4 x 16K are reported beside it in ``extra``.
+
+Timing uses HIP events on the stream the library launches on.  The roofline
+object describes the dominant kernel: its launch is isolated through the
+forced-index mode (HILS_FLAG_GIVEN_IDX launches only the attention kernel).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+METRIC = "HiLS attn tokens/s + decode HBM GB/s & prefill MFMA util vs MI355X peak"
+
+
+def n_candidates(i, S, W):
+    return np.maximum(0, (i - W + 1) // S)
+
+
+def prefill_work(B, Hq, Hkv, N, d, S, K, W):
+    """Algorithmic work of a causal prefill (selected pairs and the window only)."""
+    i = np.arange(N, dtype=np.int64)
+    ncand = n_candidates(i, S, W)
+    nloc = i - ncand * S + 1
+    nsel = np.minimum(K, ncand)
+    attn_flops = B * Hq * 4 * d * float((nloc + S * nsel).sum())   # QK^T and PV, 2 flops per MAC
+    score_flops = B * Hq * 2 * d * float(ncand.sum())                # landmark dot products
+    return attn_flops, score_flops
+
+
+def decode_bytes(B, Hq, Hkv, Hl, ctx, d, S, K, W, elem=2):
+    """Algorithmic HBM bytes of one decode step: landmark scan over C_i, the K
+    retrieved chunks' K/V, the local window's K/V, q in, out + lse out."""
+    i = ctx
+    ncand = int(n_candidates(np.array(i), S, W))
+    nloc = i - ncand * S + 1
+    lmk = B * Hl * ncand * d * elem
+    kv = B * Hkv * (min(K, ncand) * S + nloc) * d * elem * 2
+    qo = B * Hq * d * elem * 2 + B * Hq * 4
+    return lmk + kv + qo, dict(landmarks=lmk, kv=kv, q_out=qo)
+
+
+def source_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(kernel_tag):
+    """HBM traffic per launch from committed rocprofv3 --pmc counters, or None
+    when no counters exist or the kernel source changed since they were taken."""
+    p = os.path.join(ROOT, "profiles", f"{kernel_tag}_pmc.json")
+    if not os.path.exists(p):
+        return None
+    rec = json.load(open(p))
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src) or source_sha(src) != rec["source_sha"]:
+        return None
+    return rec["bytes_per_dispatch"]
+
+
+class Timer:
+    """HIP events on the current (library) stream."""
+
+    def __init__(self, torch):
+        self.torch = torch
+
+    def run(self, fn, steps, warmup):
+        t = self.torch
+        for _ in range(warmup):
+            fn()
+        t.cuda.synchronize()
+        st = t.cuda.current_stream()
+        e0, e1 = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(steps):
+            fn()
+        e1.record(st)
+        t.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps  # ms
+
+
+def bench_prefill(torch, hils, synth, W_, steps, warmup):
+    p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=W_.N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
+                    window=W_.window, dtype=W_.dtype)
+    nc = p.L // p.chunk
+    dt = p.torch_dtype
+    host = {
+        "q": synth.normal_host((p.B, p.Hq, p.N, p.d), synth.seed_for(W_.wid, "q"), p.dtype),
+        "k": synth.normal_host((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "k"), p.dtype),
+        "v": synth.normal_host((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "v"), p.dtype),
+        "lmk": synth.normal_host((p.B, p.Hq, nc, p.d), synth.seed_for(W_.wid, "lmk"), p.dtype),
+    }
+    dev = {k: v.to("cuda", dt).contiguous() for k, v in host.items()}
+    out = torch.empty(p.B, p.Hq, p.N, p.d, dtype=dt, device="cuda")
+    lse = torch.empty(p.B, p.Hq, p.N, dtype=torch.float32, device="cuda")
+    idx = torch.empty(p.B, p.Hkv, p.N, p.topk, dtype=torch.int32, device="cuda")
+
+    def step():
+        hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], out=out, lse=lse, idx=idx)
+
+    timer = Timer(torch)
+    ms = timer.run(step, steps, warmup)
+    pf = hils.Params(**{**p.__dict__, "flags": hils.HILS_FLAG_GIVEN_IDX})
+
+    def attn_only():
+        hils.hils_prefill_fwd(pf, dev["q"], dev["k"], dev["v"], dev["lmk"], out=out, lse=lse, idx=idx)
+
+    ms_attn = timer.run(attn_only, steps, max(1, warmup // 2))
+    return p, host, ms, ms_attn
+
+
+def bench_decode(torch, hils, synth, W_, steps, warmup):
+    p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=1, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
+                    window=W_.window, dtype=W_.dtype)
+    nc = p.L // p.chunk
+    dev = {
+        "q": synth.normal_device((p.B, p.Hq, 1, p.d), synth.seed_for(W_.wid, "q"), p.dtype, "cuda"),
+        "k": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "k"), p.dtype, "cuda"),
+        "v": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "v"), p.dtype, "cuda"),
+        "lmk": synth.normal_device((p.B, p.Hq, nc, p.d), synth.seed_for(W_.wid, "lmk"), p.dtype, "cuda"),
+    }
+    seqlens = torch.full((p.B,), W_.ctx + 1, dtype=torch.int32, device="cuda")
+    out = torch.empty(p.B, p.Hq, 1, p.d, dtype=p.torch_dtype, device="cuda")
+    lse = torch.empty(p.B, p.Hq, 1, dtype=torch.float32, device="cuda")
+    idx = torch.empty(p.B, p.Hkv, 1, p.topk, dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(1, hils.hils_workspace_size(p, hils.HILS_OP_DECODE)), dtype=torch.uint8, device="cuda")
+    # a 512 MB write between steps evicts the caches (L2 + MALL) so the step reads HBM
+    flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device="cuda")
+
+    def step():
+        hils.hils_decode_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], seqlens=seqlens, out=out, lse=lse,
+                             idx=idx, workspace=ws)
+
+    timer = Timer(torch)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    total = 0.0
+    for _ in range(steps):
+        flush.fill_(1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        step()
+        e1.record(st)
+        torch.cuda.synchronize()
+        total += e0.elapsed_time(e1)
+    ms = total / steps
+    nbytes, parts = decode_bytes(p.B, p.Hq, p.Hkv, p.Hq, W_.ctx, p.d, p.chunk, p.topk, p.window)
+    del dev, flush
+    torch.cuda.empty_cache()
+    return {"workload": W_.name, "ms_per_step": round(ms, 4), "tokens_per_s": round(p.B / (ms * 1e-3), 1),
+            "algorithmic_bytes": nbytes, "bytes_breakdown": parts,
+            "hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "frac_hbm_peak": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def bench_train(torch, hils, synth, W_, steps, warmup):
+    p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=W_.N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
+                    window=W_.window, dtype=W_.dtype)
+    nc = p.L // p.chunk
+    dev = {
+        "q": synth.normal_device((p.B, p.Hq, p.N, p.d), synth.seed_for(W_.wid, "q"), p.dtype, "cuda"),
+        "k": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "k"), p.dtype, "cuda"),
+        "v": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "v"), p.dtype, "cuda"),
+        "lmk": synth.normal_device((p.B, p.Hq, nc, p.d), synth.seed_for(W_.wid, "lmk"), p.dtype, "cuda"),
+        "dout": synth.normal_device((p.B, p.Hq, p.N, p.d), synth.seed_for(W_.wid, "dout"), p.dtype, "cuda"),
+    }
+    ws = torch.empty(hils.hils_workspace_size(p, hils.HILS_OP_BWD), dtype=torch.uint8, device="cuda")
+
+    def step():
+        out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"])
+        hils.hils_bwd(p, dev["dout"], dev["q"], dev["k"], dev["v"], dev["lmk"], out, lse, idx, workspace=ws)
+
+    ms = Timer(torch).run(step, steps, warmup)
+    attn, score = prefill_work(p.B, p.Hq, p.Hkv, p.N, p.d, p.chunk, p.topk, p.window)
+    fwd = attn + score
+    bwd = 2.5 * attn + 2 * score  # dq, dk, dv recompute: 10d vs 4d per attended pair; score grads
+    del dev
+    torch.cuda.empty_cache()
+    return {"workload": W_.name, "ms_per_step": round(ms, 3), "tokens_per_s": round(p.B * p.N / (ms * 1e-3), 1),
+            "algorithmic_tflop": round((fwd + bwd) / 1e12, 3),
+            "mfma_frac_useful": round((fwd + bwd) / (ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 5)}
+
+
+def cpu_baseline(W_, host, target_s=20.0):
+    """The oracle (plain fp32 build, as it stands) on a bounded sample of query
+    rows of the same workload, on all host cores; scaled to tokens/s."""
+    import oracle
+
+    threads = len(os.sched_getaffinity(0))
+    os.environ.setdefault("OMP_NUM_THREADS", str(threads))
+    threads = int(os.environ["OMP_NUM_THREADS"])
+    s = oracle.Shape(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, Hl=W_.Hq, N=W_.N, L=W_.L, d=W_.d, chunk=W_.chunk,
+                     topk=W_.topk, window=W_.window, scale=float(np.float32(W_.scale)))
+    arrs = {k: host[k].numpy() for k in ("q", "k", "v", "lmk")}
+    nrows = 64
+    while True:
+        rows = np.stack([np.zeros(nrows, np.int64), np.linspace(0, W_.N - 1, nrows).astype(np.int64)], 1)
+        t0 = time.perf_counter()
+        oracle.fwd(s, arrs["q"], arrs["k"], arrs["v"], arrs["lmk"], rows=rows, prec="f32")
+        dt = time.perf_counter() - t0
+        if dt * threads >= target_s or nrows >= W_.N:
+            break
+        nrows = min(W_.N, int(nrows * max(2.0, min(16.0, target_s / max(dt * threads, 1e-3)))))
+    return {"value": round(nrows / dt, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nrows} query rows evenly spaced over the {W_.N}-token sequence (all {W_.Hq} heads), "
+                      f"fp32 oracle, {dt:.2f} s wall on {threads} threads"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--train", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (the operator has no multi-GPU path); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_02980_amd import hils, synth
+    from paper_2607_02980_amd.configs import WORKLOADS
+
+    torch.cuda.set_device(0)
+    Wp = WORKLOADS["prefill_32k_bf16"]
+    p, host, ms, ms_attn = bench_prefill(torch, hils, synth, Wp, args.steps, args.warmup)
+    attn_flops, score_flops = prefill_work(p.B, p.Hq, p.Hkv, p.N, p.d, p.chunk, p.topk, p.window)
+    achieved = attn_flops / (ms_attn * 1e-3) / 1e12
+    traffic = load_traffic("k_attn_rows_prefill_32k_bf16")
+    res = {
+        "metric": METRIC, "value": round(p.B * p.N / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": Wp.name, "B": p.B, "Hq": p.Hq, "Hkv": p.Hkv, "d": p.d, "seq_len": p.N,
+                   "chunk": p.chunk, "topk": p.topk, "window": p.window, "landmark_heads": p.Hq},
+        "roofline": {"bound": "mfma", "kernel": "k_attn_rows", "achieved": round(achieved, 3),
+                     "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 6),
+                     "traffic": traffic, "kernel_ms": round(ms_attn, 4),
+                     "algorithmic_flop_per_launch": attn_flops},
+        "extra": {"prefill_score_topk_ms": round(ms - ms_attn, 4),
+                  "prefill_useful_mfma_frac_whole_step": round((attn_flops + score_flops) / (ms * 1e-3) / 1e12
+                                                               / BF16_MFMA_PEAK_TFLOPS, 6)},
+    }
+    del p
+    torch.cuda.empty_cache()
+    if not args.no_decode:
+        res["extra"]["decode"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
+                                              max(3, args.steps // 2), 2)
+    if args.train:
+        res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], 3, 1)
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(Wp, host)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,164 @@
+/*
+ * hils.h -- C ABI of the MI355X (gfx950) HiLS attention library, libhils.so.
+ *
+ * HiLS (Hierarchical Landmark Sparse) attention, arXiv 2607.02980:
+ *   - Sec. 2.1: keys are cut into chunks of S tokens, c(j) = floor(j / S).  A
+ *     query at position i attends a local window [l(i), i] whose left edge is
+ *     chunk aligned, l(i) = floor((i - W + 1) / S) * S (clamped at 0), and may
+ *     retrieve any chunk of C_i = {0, ..., l(i)/S - 1}.
+ *   - Eq. (9): every candidate chunk is scored with its landmark (compressed)
+ *     key, s^_ic = scale * <q^_i, k'_c> + b'_c, and the K best chunks I_i are
+ *     kept.  Eq. (11): q^ is an optional routing query (Q-Cal); without it q^ = q.
+ *   - Sec. 4.1 "HiLS-Attention in GQA" and Appendix C: the G = Hq / Hkv query
+ *     heads of a KV group share one selection, ranked by the maximum of their
+ *     per-head scores; ties go to the smaller chunk index.
+ *   - Eq. (10): softmax attention runs separately inside each retrieved chunk
+ *     (intra-chunk softmax) and over the local window; the per-part outputs are
+ *     fused with a softmax over {s^_ic : c in I_i} U {log Z_swa} (Eq. (1)), the
+ *     local window taking its exact mass Z_swa.
+ *   - the backward differentiates Eq. (10) with the selection held fixed, so
+ *     gradients reach the landmark keys and biases of the selected chunks only
+ *     (Sec. 9 notes that unselected chunks receive no gradient).
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is a DEVICE pointer (hipMalloc'd or equivalent)
+ *     unless stated otherwise; `p` (the parameter block) is a HOST pointer.
+ *   - The caller owns every buffer.  The library never allocates device
+ *     memory, never synchronises the device and keeps no state between calls
+ *     other than the thread-local error string.  All work is enqueued on
+ *     `stream` (a hipStream_t; NULL is the default stream) and is complete
+ *     when the stream is.
+ *   - Layouts are row-major and contiguous ("BHSD"):
+ *       q, q_route, out, dout, dq, dq_route : [B, Hq,  N, d]
+ *       k, v, dk, dv                        : [B, Hkv, L, d]   (decode: the caches)
+ *       lmk, dlmk                           : [B, Hl,  L/S, d] (landmark key of each chunk)
+ *       lmk_bias, dlmk_bias                 : [B, Hl,  L/S] float32
+ *       lse                                 : [B, Hq,  N] float32
+ *       idx                                 : [B, Hkv, N, K] int32
+ *     A chunk's K (or V) block is one contiguous S*d span.
+ *   - `dtype` fixes the element type of q, k, v, lmk, q_route, out, dout and
+ *     of every gradient except dlmk_bias (float32 storage or bf16 storage).
+ *     Arithmetic is float32 throughout; outputs are rounded to nearest-even.
+ *   - Landmark heads: Hl == Hq (one landmark key per query head, Appendix C)
+ *     or Hl == Hkv (one per KV group).  The bias has the landmark heads.
+ *   - `idx` rows list the selected chunks in ascending order, padded with -1
+ *     when |C_i| < K.
+ *   - Return value: HILS_OK (0) or an error code; on error nothing has been
+ *     enqueued and hils_last_error() describes the failure.  Argument checks
+ *     run entirely on the host before any HIP call, so they work without a GPU.
+ *     Values that live in device memory (seqlens, a caller-provided idx) are
+ *     not inspected by the host; the kernels clamp them into range (see each
+ *     entry point), so they can never cause an out-of-bounds access.
+ */
+#ifndef HILS_H
+#define HILS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { HILS_F32 = 0, HILS_BF16 = 1 } hils_dtype;
+
+typedef enum {
+    HILS_OK = 0,
+    HILS_ERR_INVALID = 1,     /* a NULL required pointer or an inconsistent shape/value */
+    HILS_ERR_UNSUPPORTED = 2, /* valid, but no kernel for this (d, S, G, K, dtype) yet */
+    HILS_ERR_WORKSPACE = 3,   /* workspace missing or smaller than hils_workspace_size() */
+    HILS_ERR_HIP = 4          /* a HIP launch or runtime call failed */
+} hils_status;
+
+/* Forward flag: consume the caller's `idx` instead of selecting (forced-index
+ * mode: re-use of a selection, and kernel tests).  Entries < 0 or not in C_i
+ * are ignored; entries must be ascending. */
+#define HILS_FLAG_GIVEN_IDX 1u
+
+typedef enum { HILS_OP_PREFILL = 0, HILS_OP_DECODE = 1, HILS_OP_BWD = 2 } hils_op;
+
+typedef struct {
+    int B;          /* sequences */
+    int Hq, Hkv;    /* query heads, KV heads; G = Hq / Hkv query heads share a KV head */
+    int Hl;         /* landmark heads: Hq or Hkv */
+    int N;          /* queries per sequence (prefill, bwd: query n sits at position n; decode: 1) */
+    int L;          /* key positions per sequence (decode: cache capacity); multiple of `chunk` */
+    int d;          /* head dimension */
+    int chunk;      /* S, tokens per chunk */
+    int topk;       /* K, chunks retrieved per query and KV group */
+    int window;     /* W >= 1, local window size before chunk alignment */
+    float scale;    /* multiplies both the token logits and the landmark scores (1/sqrt(d) in the paper) */
+    hils_dtype dtype;
+    unsigned flags; /* HILS_FLAG_* */
+} hils_params;
+
+/* Library version as 10000*major + 100*minor + patch. */
+int hils_version(void);
+
+/* Thread-local description of the last error returned on this thread ("" if none). */
+const char* hils_last_error(void);
+
+/* Bytes of device workspace that entry point `op` needs for parameters `p`
+ * (0 is a valid answer: then workspace may be NULL).  Writes *bytes and
+ * returns HILS_OK, or returns an error code for invalid parameters. */
+int hils_workspace_size(const hils_params* p, int op, size_t* bytes);
+
+/*
+ * Prefill forward: all N queries of each sequence at once (query n at
+ * position n; requires N <= L).  Computes, per (b, KV group, n): the landmark
+ * scores of C_n, the group maximum over the G heads, the top-K selection
+ * (Eq. (9), App. C), the local-window term (Eq. (1)), the per-chunk softmax
+ * terms and their fusion (Eq. (10)).
+ *   q        [B,Hq,N,d]     queries (token logits)
+ *   k, v     [B,Hkv,L,d]    keys and values
+ *   lmk      [B,Hl,L/S,d]   landmark keys k'_c
+ *   lmk_bias [B,Hl,L/S] f32 landmark biases b'_c, or NULL for b' = 0
+ *   q_route  [B,Hq,N,d]     routing queries q^ (Q-Cal, Eq. (11)), or NULL for q^ = q
+ *   out      [B,Hq,N,d]     output (written)
+ *   lse      [B,Hq,N] f32   log of the fusion normaliser, LSE of {s^_ic} U {log Z_swa} (written)
+ *   idx      [B,Hkv,N,K]    selection (written; read instead under HILS_FLAG_GIVEN_IDX)
+ *   workspace, ws_bytes     device scratch of at least hils_workspace_size(p, HILS_OP_PREFILL)
+ *   stream                  hipStream_t
+ */
+int hils_prefill_fwd(const hils_params* p, const void* q, const void* k, const void* v, const void* lmk,
+                     const float* lmk_bias, const void* q_route, void* out, float* lse, int32_t* idx,
+                     void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Decode forward: one new query per sequence (N == 1) against a KV cache.
+ * The caller has already written the new token's k/v at position
+ * seqlens[b] - 1, so the query sits at i = seqlens[b] - 1 and attends keys
+ * j <= i.  Landmark rows exist for every complete chunk.
+ *   seqlens  [B] int32 (device) valid tokens per sequence including the new one,
+ *            or NULL for L; values are clamped into [1, L] by the kernels.
+ * Other arguments as for hils_prefill_fwd with N = 1 (q, q_route, out [B,Hq,1,d];
+ * lse [B,Hq,1]; idx [B,Hkv,1,K]; k, v, lmk, lmk_bias are the caches).
+ */
+int hils_decode_fwd(const hils_params* p, const void* q, const void* k_cache, const void* v_cache,
+                    const void* lmk_cache, const float* lmk_bias, const void* q_route, const int32_t* seqlens,
+                    void* out, float* lse, int32_t* idx, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of the prefill forward with the selection fixed to `idx`.
+ *   dout     [B,Hq,N,d]      upstream gradient dL/d(out)
+ *   q, k, v, lmk, lmk_bias, q_route: the forward's inputs
+ *   out, lse, idx            the forward's outputs (lse and out must come from
+ *                            the same forward that produced idx)
+ *   dq       [B,Hq,N,d]      written; includes the routing gradient when q_route is NULL
+ *   dk, dv   [B,Hkv,L,d]     written (keys no query attends get 0)
+ *   dlmk     [B,Hl,L/S,d]    written (chunks no query selected get 0)
+ *   dlmk_bias[B,Hl,L/S] f32  written, or NULL to skip
+ *   dq_route [B,Hq,N,d]      written when q_route is given (must then be non-NULL)
+ * Deterministic: repeated calls with equal inputs produce identical bits as
+ * long as no chunk is selected by more than 8192 queries of one KV group.
+ */
+int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* k, const void* v,
+             const void* lmk, const float* lmk_bias, const void* q_route, const void* out, const float* lse,
+             const int32_t* idx, void* dq, void* dk, void* dv, void* dlmk, float* dlmk_bias, void* dq_route,
+             void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HILS_H */

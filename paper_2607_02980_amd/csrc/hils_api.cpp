@@ -1,0 +1,172 @@
+// C-ABI of libhils.so: argument validation, workspace sizing and dispatch.
+// Every check runs on the host before any HIP call.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "../../include/hils.h"
+#include "hils_internal.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int ok() {
+    g_err.clear();
+    return HILS_OK;
+}
+
+int check_params(const hils_params* p, int op) {
+    if (!p) return fail(HILS_ERR_INVALID, "params is NULL");
+    if (op != HILS_OP_PREFILL && op != HILS_OP_DECODE && op != HILS_OP_BWD)
+        return fail(HILS_ERR_INVALID, "unknown op %d", op);
+    if (p->B < 1 || p->Hq < 1 || p->Hkv < 1 || p->N < 1 || p->L < 1 || p->d < 1)
+        return fail(HILS_ERR_INVALID, "B, Hq, Hkv, N, L and d must be >= 1 (B=%d Hq=%d Hkv=%d N=%d L=%d d=%d)",
+                    p->B, p->Hq, p->Hkv, p->N, p->L, p->d);
+    if (p->chunk < 1 || p->topk < 1 || p->window < 1)
+        return fail(HILS_ERR_INVALID, "chunk, topk and window must be >= 1 (chunk=%d topk=%d window=%d)", p->chunk,
+                    p->topk, p->window);
+    if (p->Hq % p->Hkv) return fail(HILS_ERR_INVALID, "Hq=%d is not a multiple of Hkv=%d", p->Hq, p->Hkv);
+    if (p->Hl != p->Hq && p->Hl != p->Hkv)
+        return fail(HILS_ERR_INVALID, "Hl=%d must equal Hq=%d or Hkv=%d", p->Hl, p->Hq, p->Hkv);
+    if (p->L % p->chunk) return fail(HILS_ERR_INVALID, "L=%d is not a multiple of chunk=%d", p->L, p->chunk);
+    if (p->dtype != HILS_F32 && p->dtype != HILS_BF16) return fail(HILS_ERR_INVALID, "unknown dtype %d", (int)p->dtype);
+    if (!isfinite(p->scale)) return fail(HILS_ERR_INVALID, "scale is not finite");
+    if (p->flags & ~HILS_FLAG_GIVEN_IDX) return fail(HILS_ERR_INVALID, "unknown flags 0x%x", p->flags);
+    if (op == HILS_OP_DECODE && p->N != 1) return fail(HILS_ERR_INVALID, "decode needs N == 1 (got %d)", p->N);
+    if (op != HILS_OP_DECODE && p->N > p->L)
+        return fail(HILS_ERR_INVALID, "prefill/backward need N <= L (N=%d L=%d)", p->N, p->L);
+    if (p->B > 65535 || p->Hkv > 65535) return fail(HILS_ERR_INVALID, "B and Hkv must be <= 65535");
+    if (op == HILS_OP_BWD && (p->flags & HILS_FLAG_GIVEN_IDX))
+        return fail(HILS_ERR_INVALID, "HILS_FLAG_GIVEN_IDX is a forward flag (the backward always reads idx)");
+    // kernel coverage
+    if (p->chunk != 64) return fail(HILS_ERR_UNSUPPORTED, "chunk=%d: kernels exist for chunk 64 only", p->chunk);
+    if (p->d != 64 && p->d != 128) return fail(HILS_ERR_UNSUPPORTED, "d=%d: kernels exist for d in {64, 128}", p->d);
+    const int G = p->Hq / p->Hkv;
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+        return fail(HILS_ERR_UNSUPPORTED, "group size G=%d: kernels exist for G in {1, 2, 4, 8}", G);
+    if (p->topk > 64) return fail(HILS_ERR_UNSUPPORTED, "topk=%d: kernels exist for topk <= 64", p->topk);
+    return HILS_OK;
+}
+
+size_t ws_bytes_for(const hils_params* p, int op) {
+    switch (op) {
+        case HILS_OP_BWD:
+            return hils::bwd_workspace_layout(p->B, p->Hkv, p->N, p->L, p->topk).total;
+        case HILS_OP_DECODE:
+            return hils::decode_workspace_bytes(p->B, p->Hkv, p->L, p->topk);
+        default:
+            return 0;
+    }
+}
+
+int check_ws(const hils_params* p, int op, const void* ws, size_t bytes) {
+    const size_t need = ws_bytes_for(p, op);
+    if (need == 0) return HILS_OK;
+    if (!ws) return fail(HILS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+    if (bytes < need) return fail(HILS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", bytes, need);
+    return HILS_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(HILS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+#define REQUIRE(ptr) \
+    if (!(ptr)) return fail(HILS_ERR_INVALID, "required pointer '%s' is NULL", #ptr)
+
+hils::FwdArgs fwd_args(const hils_params* p, const void* q, const void* k, const void* v, const void* lmk,
+                       const float* bias, const void* q_route, const int32_t* seqlens, void* out, float* lse,
+                       int32_t* idx, void* ws, size_t ws_bytes, int decode) {
+    hils::FwdArgs a;
+    a.q = q; a.k = k; a.v = v; a.lmk = lmk; a.bias = bias; a.q_route = q_route; a.seqlens = seqlens;
+    a.out = out; a.lse = lse; a.idx = idx;
+    a.B = p->B; a.Hq = p->Hq; a.Hkv = p->Hkv; a.Hl = p->Hl; a.N = p->N; a.L = p->L; a.d = p->d;
+    a.K = p->topk; a.W = p->window; a.scale = p->scale;
+    a.bf16 = p->dtype == HILS_BF16;
+    a.decode = decode;
+    a.given_idx = (p->flags & HILS_FLAG_GIVEN_IDX) ? 1 : 0;
+    a.ws = ws; a.ws_bytes = ws_bytes;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hils_version(void) { return 100; }
+
+const char* hils_last_error(void) { return g_err.c_str(); }
+
+int hils_workspace_size(const hils_params* p, int op, size_t* bytes) {
+    int rc = check_params(p, op);
+    if (rc) return rc;
+    if (!bytes) return fail(HILS_ERR_INVALID, "bytes is NULL");
+    *bytes = ws_bytes_for(p, op);
+    return ok();
+}
+
+int hils_prefill_fwd(const hils_params* p, const void* q, const void* k, const void* v, const void* lmk,
+                     const float* lmk_bias, const void* q_route, void* out, float* lse, int32_t* idx,
+                     void* workspace, size_t ws_bytes, void* stream) {
+    int rc = check_params(p, HILS_OP_PREFILL);
+    if (rc) return rc;
+    REQUIRE(q); REQUIRE(k); REQUIRE(v); REQUIRE(lmk); REQUIRE(out); REQUIRE(lse); REQUIRE(idx);
+    rc = check_ws(p, HILS_OP_PREFILL, workspace, ws_bytes);
+    if (rc) return rc;
+    const hils::FwdArgs a = fwd_args(p, q, k, v, lmk, lmk_bias, q_route, nullptr, out, lse, idx, workspace,
+                                     ws_bytes, 0);
+    return hip_status(hils::launch_prefill_fwd(a, (hipStream_t)stream), "hils_prefill_fwd launch");
+}
+
+int hils_decode_fwd(const hils_params* p, const void* q, const void* k_cache, const void* v_cache,
+                    const void* lmk_cache, const float* lmk_bias, const void* q_route, const int32_t* seqlens,
+                    void* out, float* lse, int32_t* idx, void* workspace, size_t ws_bytes, void* stream) {
+    int rc = check_params(p, HILS_OP_DECODE);
+    if (rc) return rc;
+    REQUIRE(q); REQUIRE(k_cache); REQUIRE(v_cache); REQUIRE(lmk_cache); REQUIRE(out); REQUIRE(lse); REQUIRE(idx);
+    rc = check_ws(p, HILS_OP_DECODE, workspace, ws_bytes);
+    if (rc) return rc;
+    const hils::FwdArgs a = fwd_args(p, q, k_cache, v_cache, lmk_cache, lmk_bias, q_route, seqlens, out, lse, idx,
+                                     workspace, ws_bytes, 1);
+    return hip_status(hils::launch_decode_fwd(a, (hipStream_t)stream), "hils_decode_fwd launch");
+}
+
+int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* k, const void* v, const void* lmk,
+             const float* lmk_bias, const void* q_route, const void* out, const float* lse, const int32_t* idx,
+             void* dq, void* dk, void* dv, void* dlmk, float* dlmk_bias, void* dq_route, void* workspace,
+             size_t ws_bytes, void* stream) {
+    int rc = check_params(p, HILS_OP_BWD);
+    if (rc) return rc;
+    REQUIRE(dout); REQUIRE(q); REQUIRE(k); REQUIRE(v); REQUIRE(lmk); REQUIRE(out); REQUIRE(lse); REQUIRE(idx);
+    REQUIRE(dq); REQUIRE(dk); REQUIRE(dv); REQUIRE(dlmk);
+    if (q_route && !dq_route)
+        return fail(HILS_ERR_INVALID, "q_route is given, so dq_route must be non-NULL");
+    rc = check_ws(p, HILS_OP_BWD, workspace, ws_bytes);
+    if (rc) return rc;
+    hils::BwdArgs a;
+    a.dout = dout; a.q = q; a.k = k; a.v = v; a.lmk = lmk; a.bias = lmk_bias; a.q_route = q_route;
+    a.out = out; a.lse = lse; a.idx = idx;
+    a.dq = dq; a.dk = dk; a.dv = dv; a.dlmk = dlmk; a.dbias = dlmk_bias; a.dq_route = q_route ? dq_route : nullptr;
+    a.B = p->B; a.Hq = p->Hq; a.Hkv = p->Hkv; a.Hl = p->Hl; a.N = p->N; a.L = p->L; a.d = p->d;
+    a.K = p->topk; a.W = p->window; a.scale = p->scale;
+    a.bf16 = p->dtype == HILS_BF16;
+    a.ws = workspace; a.ws_bytes = ws_bytes;
+    return hip_status(hils::launch_bwd(a, (hipStream_t)stream), "hils_bwd launch");
+}
+
+}  // extern "C"

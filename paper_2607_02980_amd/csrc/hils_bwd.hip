@@ -1,0 +1,474 @@
+// HiLS attention backward kernels, gfx950.
+//
+// With g = dO and u = g . out for a (row, head), and L its fusion LSE:
+//   local key j:     w_j = exp(s_j - L);  dv_j += w_j g;  ds_j = w_j (g.v_j - u)
+//   chunk c, key j:  p_j = exp(s_j - log Z_c), a_c = exp(s^_c - L), u_c = g . o_c
+//                    dv_j += a_c p_j g;  ds_j = a_c p_j (g.v_j - u_c)
+//   retrieval score: ds^_c = a_c (u_c - u)
+//   dq += scale ds_j k_j;  dk_j += scale ds_j q;  dq^ += scale ds^_c k'_c;
+//   dk'_c += scale ds^_c q^;  db'_c += ds^_c
+// (Eq. (10) differentiated with the selection fixed; selection gets no gradient.)
+//
+// Kernels:
+//   k_bwd_dq_rows      query-major: dq and dq^ of one (b, group, n) row
+//   k_inv_*            inverse index: for each (b, group, chunk) the rows that selected it
+//   k_bwd_dkdv_chunks  key-major: dk, dv of one chunk from the rows whose local window
+//                      covers it and from the rows that retrieved it, plus dk', db'
+// Everything is accumulated on chip and written once; no floating-point atomics.
+#include "hils_device.hpp"
+#include "hils_dispatch.hpp"
+#include "hils_internal.hpp"
+
+namespace hils {
+
+constexpr int kBlock = 256;
+constexpr int kSortCap = 4096;  // retrieval lists up to this length are sorted (deterministic order)
+
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K) {
+    const size_t bg = (size_t)B * Hkv, nC = (size_t)L / kChunk;
+    BwdWorkspace w;
+    w.counts = 0;
+    w.offsets = align256(w.counts + bg * nC * sizeof(int));
+    w.cursor = align256(w.offsets + bg * (nC + 1) * sizeof(int));
+    w.list = align256(w.cursor + bg * nC * sizeof(int));
+    w.total = align256(w.list + bg * (size_t)N * K * sizeof(int));
+    return w;
+}
+
+// ---------------------------------------------------------------------------
+// dq / dq^ : one workgroup per (n, g, b); parts as in the forward row kernel.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void k_bwd_dq_rows(BwdArgs a) {
+    constexpr int R = (G * D + kBlock - 1) / kBlock;
+    __shared__ float s_q[G][D], s_qr[G][D], s_do[G][D];
+    __shared__ float s_k[kChunk][D + 1];
+    __shared__ float s_v[kChunk][D + 1];
+    __shared__ float s_cs[G][kChunk];
+    __shared__ float s_dsh[G], s_L[G], s_ub[G];
+    __shared__ int s_sel[64];
+    __shared__ int s_nsel;
+
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int n = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const int pos = n;
+    const int ncand = n_candidates(pos, a.W);
+    const int nC = a.L / kChunk;
+    const T* kb = as<T>(a.k) + ((size_t)b * a.Hkv + g) * a.L * D;
+    const T* vb = as<T>(a.v) + ((size_t)b * a.Hkv + g) * a.L * D;
+    const T* qr = as<T>(a.q_route ? a.q_route : a.q);
+
+    for (int e = tid; e < G * D; e += kBlock) {
+        const int hh = e / D, dd = e % D;
+        const size_t off = (((size_t)b * a.Hq + g * G + hh) * a.N + n) * D + dd;
+        s_q[hh][dd] = to_f32(as<T>(a.q)[off]);
+        s_qr[hh][dd] = to_f32(qr[off]);
+        s_do[hh][dd] = to_f32(as<T>(a.dout)[off]);
+    }
+    if (tid == 0) {
+        const int32_t* irow = a.idx + (((size_t)b * a.Hkv + g) * a.N + n) * a.K;
+        int cnt = 0;
+        for (int t = 0; t < a.K; ++t)
+            if (idx_entry_valid(irow, t, ncand)) s_sel[cnt++] = irow[t];
+        s_nsel = cnt;
+    }
+    __syncthreads();
+    for (int hh = wave; hh < G; hh += 4) {
+        const size_t row = ((size_t)b * a.Hq + g * G + hh) * a.N + n;
+        float acc = 0.f;
+        for (int dd = lane; dd < D; dd += kWave) acc += s_do[hh][dd] * to_f32(as<T>(a.out)[row * D + dd]);
+        acc = wave_sum(acc);
+        if (lane == 0) {
+            s_ub[hh] = acc;
+            s_L[hh] = a.lse[row];
+        }
+    }
+    const int nsel = s_nsel;
+    const int c_lo = ncand, c_hi = pos / kChunk;
+    const int nparts = nsel + (c_hi - c_lo + 1);
+    float dq[R], dqh[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) dq[r] = dqh[r] = 0.f;
+
+    for (int part = 0; part < nparts; ++part) {
+        const bool is_chunk = part < nsel;
+        const int c = is_chunk ? s_sel[part] : c_lo + (part - nsel);
+        const int j0 = c * kChunk;
+        const int nk = is_chunk ? kChunk : min(kChunk, pos - j0 + 1);
+        for (int e = tid; e < kChunk * D / 8; e += kBlock) {
+            const int j = e / (D / 8), dd = (e % (D / 8)) * 8;
+            float x[8], y[8];
+            load8(kb + (size_t)(j0 + j) * D + dd, x);
+            load8(vb + (size_t)(j0 + j) * D + dd, y);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                s_k[j][dd + t] = x[t];
+                s_v[j][dd + t] = y[t];
+            }
+        }
+        __syncthreads();
+        for (int hh = wave; hh < G; hh += 4) {
+            const float L = s_L[hh], ub = s_ub[hh];
+            float s = -INFINITY, gv = 0.f;
+            if (lane < nk) {
+                float acc = 0.f, acc2 = 0.f;
+#pragma unroll 16
+                for (int dd = 0; dd < D; ++dd) {
+                    acc += s_q[hh][dd] * s_k[lane][dd];
+                    acc2 += s_do[hh][dd] * s_v[lane][dd];
+                }
+                s = a.scale * acc;
+                gv = acc2;
+            }
+            float ds;
+            if (is_chunk) {
+                const float m = wave_max(s);
+                const float l = wave_sum(fexp(s - m));
+                const float lsec = m + __logf(l);
+                const float p = fexp(s - lsec);
+                const float uc = wave_sum(p * gv);
+                const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+                const T* lr = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
+                float acc = 0.f;
+                for (int dd = lane; dd < D; dd += kWave) acc += s_qr[hh][dd] * to_f32(lr[dd]);
+                acc = wave_sum(acc);
+                const float sh = a.scale * acc + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f);
+                const float al = fexp(sh - L);
+                ds = al * p * (gv - uc);
+                if (lane == 0) s_dsh[hh] = al * (uc - ub);
+            } else {
+                const float w = lane < nk ? fexp(s - L) : 0.f;
+                ds = w * (gv - ub);
+            }
+            s_cs[hh][lane] = ds;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int o = tid + r * kBlock;
+            if (o < G * D) {
+                const int hh = o / D, dd = o % D;
+                float acc = 0.f;
+                for (int j = 0; j < nk; ++j) acc += s_cs[hh][j] * s_k[j][dd];
+                dq[r] += a.scale * acc;
+                if (is_chunk) {
+                    const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+                    const T* lr = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
+                    dqh[r] += a.scale * s_dsh[hh] * to_f32(lr[dd]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int o = tid + r * kBlock;
+        if (o < G * D) {
+            const int hh = o / D, dd = o % D;
+            const size_t off = (((size_t)b * a.Hq + g * G + hh) * a.N + n) * D + dd;
+            if (a.q_route) {
+                as_mut<T>(a.dq)[off] = from_f32<T>(dq[r]);
+                as_mut<T>(a.dq_route)[off] = from_f32<T>(dqh[r]);
+            } else {
+                as_mut<T>(a.dq)[off] = from_f32<T>(dq[r] + dqh[r]);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Inverse index: (b, g, c) -> rows n whose selection holds c.
+// ---------------------------------------------------------------------------
+__global__ void k_fill_i32(int* p, size_t n, int v) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+__device__ __forceinline__ bool entry_of(const BwdArgs& a, size_t e, int* bg, int* n, int* c) {
+    const int slot = (int)(e % a.K);
+    const size_t row = e / a.K;  // (b*Hkv + g)*N + n
+    *n = (int)(row % a.N);
+    *bg = (int)(row / a.N);
+    const int32_t* irow = a.idx + row * a.K;
+    if (!idx_entry_valid(irow, slot, n_candidates(*n, a.W))) return false;
+    *c = irow[slot];
+    return true;
+}
+
+__global__ void k_inv_count(BwdArgs a, int* counts) {
+    const size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= (size_t)a.B * a.Hkv * a.N * a.K) return;
+    int bg, n, c;
+    if (!entry_of(a, e, &bg, &n, &c)) return;
+    atomicAdd(&counts[(size_t)bg * (a.L / kChunk) + c], 1);
+}
+
+// one block per (b, g): exclusive scan of the nC counts into offsets[nC + 1]
+__global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* offsets, int nC) {
+    __shared__ int s_part[kBlock];
+    const int bg = blockIdx.x, tid = threadIdx.x;
+    const int per = (nC + kBlock - 1) / kBlock;
+    const int lo = min(nC, tid * per), hi = min(nC, lo + per);
+    const int* cnt = counts + (size_t)bg * nC;
+    int* off = offsets + (size_t)bg * (nC + 1);
+    int sum = 0;
+    for (int c = lo; c < hi; ++c) sum += cnt[c];
+    s_part[tid] = sum;
+    __syncthreads();
+    if (tid == 0) {
+        int run = 0;
+        for (int t = 0; t < kBlock; ++t) {
+            const int x = s_part[t];
+            s_part[t] = run;
+            run += x;
+        }
+        off[nC] = run;
+    }
+    __syncthreads();
+    int run = s_part[tid];
+    for (int c = lo; c < hi; ++c) {
+        off[c] = run;
+        run += cnt[c];
+    }
+}
+
+__global__ void k_inv_fill(BwdArgs a, const int* offsets, int* cursor, int* list) {
+    const size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= (size_t)a.B * a.Hkv * a.N * a.K) return;
+    int bg, n, c;
+    if (!entry_of(a, e, &bg, &n, &c)) return;
+    const int nC = a.L / kChunk;
+    const int slot = atomicAdd(&cursor[(size_t)bg * nC + c], 1);
+    list[(size_t)bg * a.N * a.K + offsets[(size_t)bg * (nC + 1) + c] + slot] = n;
+}
+
+// ---------------------------------------------------------------------------
+// dk, dv of chunk c (and dk', db' of its landmark heads): one workgroup per (c, g, b).
+// Phase A: rows n in [cS, (c+1)S + W - 2] whose local window covers keys of c.
+// Phase B: rows that retrieved c (sorted ascending when the list fits kSortCap).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void k_bwd_dkdv_chunks(BwdArgs a, const int* offsets, const int* list) {
+    constexpr int RK = kChunk * D / kBlock;
+    constexpr int RL = (G * D + kBlock - 1) / kBlock;
+    __shared__ float s_k[kChunk][D + 1];
+    __shared__ float s_v[kChunk][D + 1];
+    __shared__ float s_q[G][D], s_qr[G][D], s_do[G][D], s_lm[G][D];
+    __shared__ float s_cv[G][kChunk], s_cs[G][kChunk];
+    __shared__ float s_dsh[G], s_L[G], s_db[G];
+    __shared__ int s_list[kSortCap];
+
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const int nC = a.L / kChunk;
+    const int j0 = c * kChunk;
+    const bool per_head_lmk = (a.Hl == a.Hq);
+    const int nLH = per_head_lmk ? G : 1;
+    const T* kb = as<T>(a.k) + ((size_t)b * a.Hkv + g) * a.L * D;
+    const T* vb = as<T>(a.v) + ((size_t)b * a.Hkv + g) * a.L * D;
+    const T* qr_base = as<T>(a.q_route ? a.q_route : a.q);
+
+    for (int e = tid; e < kChunk * D / 8; e += kBlock) {
+        const int j = e / (D / 8), dd = (e % (D / 8)) * 8;
+        float x[8], y[8];
+        load8(kb + (size_t)(j0 + j) * D + dd, x);
+        load8(vb + (size_t)(j0 + j) * D + dd, y);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            s_k[j][dd + t] = x[t];
+            s_v[j][dd + t] = y[t];
+        }
+    }
+    for (int e = tid; e < nLH * D; e += kBlock) {
+        const int lh = e / D, dd = e % D;
+        const int hl = per_head_lmk ? g * G + lh : g;
+        s_lm[lh][dd] = to_f32(as<T>(a.lmk)[(((size_t)b * a.Hl + hl) * nC + c) * D + dd]);
+    }
+    if (tid < G) s_db[tid] = 0.f;
+
+    float dk[RK], dv[RK], dl[RL];
+#pragma unroll
+    for (int r = 0; r < RK; ++r) dk[r] = dv[r] = 0.f;
+#pragma unroll
+    for (int r = 0; r < RL; ++r) dl[r] = 0.f;
+
+    auto process_row = [&](int n, bool retrieval) {
+        __syncthreads();  // previous row's LDS readers are done
+        for (int e = tid; e < G * D; e += kBlock) {
+            const int hh = e / D, dd = e % D;
+            const size_t off = (((size_t)b * a.Hq + g * G + hh) * a.N + n) * D + dd;
+            s_q[hh][dd] = to_f32(as<T>(a.q)[off]);
+            s_do[hh][dd] = to_f32(as<T>(a.dout)[off]);
+            if (retrieval) s_qr[hh][dd] = to_f32(qr_base[off]);
+        }
+        if (tid < G) s_L[tid] = a.lse[((size_t)b * a.Hq + g * G + tid) * a.N + n];
+        __syncthreads();
+        const int nk = retrieval ? kChunk : min(n, j0 + kChunk - 1) - j0 + 1;
+        for (int hh = wave; hh < G; hh += 4) {
+            const size_t row = ((size_t)b * a.Hq + g * G + hh) * a.N + n;
+            float ub = 0.f;
+            for (int dd = lane; dd < D; dd += kWave) ub += s_do[hh][dd] * to_f32(as<T>(a.out)[row * D + dd]);
+            ub = wave_sum(ub);
+            const float L = s_L[hh];
+            float s = -INFINITY, gv = 0.f;
+            if (lane < nk) {
+                float acc = 0.f, acc2 = 0.f;
+#pragma unroll 16
+                for (int dd = 0; dd < D; ++dd) {
+                    acc += s_q[hh][dd] * s_k[lane][dd];
+                    acc2 += s_do[hh][dd] * s_v[lane][dd];
+                }
+                s = a.scale * acc;
+                gv = acc2;
+            }
+            float cv, cs;
+            if (retrieval) {
+                const float m = wave_max(s);
+                const float l = wave_sum(fexp(s - m));
+                const float p = fexp(s - (m + __logf(l)));
+                const float uc = wave_sum(p * gv);
+                const int lh = per_head_lmk ? hh : 0;
+                const int hl = per_head_lmk ? g * G + hh : g;
+                float acc = 0.f;
+                for (int dd = lane; dd < D; dd += kWave) acc += s_qr[hh][dd] * s_lm[lh][dd];
+                acc = wave_sum(acc);
+                const float sh = a.scale * acc + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f);
+                const float al = fexp(sh - L);
+                cv = al * p;
+                cs = al * p * (gv - uc);
+                if (lane == 0) s_dsh[hh] = al * (uc - ub);
+            } else {
+                const float w = lane < nk ? fexp(s - L) : 0.f;
+                cv = w;
+                cs = w * (gv - ub);
+            }
+            s_cv[hh][lane] = cv;
+            s_cs[hh][lane] = cs;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < RK; ++r) {
+            const int e = tid + r * kBlock;
+            const int j = e / D, dd = e % D;
+            float av = 0.f, ak = 0.f;
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) {
+                av += s_cv[hh][j] * s_do[hh][dd];
+                ak += s_cs[hh][j] * s_q[hh][dd];
+            }
+            dv[r] += av;
+            dk[r] += a.scale * ak;
+        }
+        if (retrieval) {
+#pragma unroll
+            for (int r = 0; r < RL; ++r) {
+                const int e = tid + r * kBlock;
+                if (e < nLH * D) {
+                    const int lh = e / D, dd = e % D;
+                    float acc = 0.f;
+                    if (per_head_lmk) {
+                        acc = s_dsh[lh] * s_qr[lh][dd];
+                    } else {
+#pragma unroll
+                        for (int hh = 0; hh < G; ++hh) acc += s_dsh[hh] * s_qr[hh][dd];
+                    }
+                    dl[r] += a.scale * acc;
+                }
+            }
+            if (tid == 0) {
+                for (int hh = 0; hh < G; ++hh) s_db[per_head_lmk ? hh : 0] += s_dsh[hh];
+            }
+        }
+    };
+
+    // phase A: local windows covering this chunk
+    const int n_hi = min(a.N - 1, j0 + kChunk + a.W - 2);
+    for (int n = j0; n <= n_hi; ++n) process_row(n, false);
+
+    // phase B: retrievals of this chunk
+    const size_t bg = (size_t)b * a.Hkv + g;
+    const int beg = offsets[bg * (nC + 1) + c];
+    const int len = offsets[bg * (nC + 1) + c + 1] - beg;
+    const int* seg = list + bg * a.N * a.K + beg;
+    if (len <= kSortCap) {
+        __syncthreads();
+        int P = 1;
+        while (P < len) P <<= 1;
+        for (int t = tid; t < P; t += kBlock) s_list[t] = t < len ? seg[t] : 0x7fffffff;
+        __syncthreads();
+        for (int kk = 2; kk <= P; kk <<= 1) {
+            for (int jj = kk >> 1; jj > 0; jj >>= 1) {
+                for (int t = tid; t < P; t += kBlock) {
+                    const int u = t ^ jj;
+                    if (u > t) {
+                        const int x = s_list[t], y = s_list[u];
+                        const bool up = (t & kk) == 0;
+                        if ((x > y) == up) {
+                            s_list[t] = y;
+                            s_list[u] = x;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        for (int t = 0; t < len; ++t) process_row(s_list[t], true);
+    } else {
+        for (int t = 0; t < len; ++t) process_row(seg[t], true);
+    }
+    __syncthreads();
+
+    T* dkp = as_mut<T>(a.dk) + (bg * a.L + j0) * D;
+    T* dvp = as_mut<T>(a.dv) + (bg * a.L + j0) * D;
+#pragma unroll
+    for (int r = 0; r < RK; ++r) {
+        const int e = tid + r * kBlock;
+        dkp[e] = from_f32<T>(dk[r]);
+        dvp[e] = from_f32<T>(dv[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < RL; ++r) {
+        const int e = tid + r * kBlock;
+        if (e < nLH * D) {
+            const int lh = e / D, dd = e % D;
+            const int hl = per_head_lmk ? g * G + lh : g;
+            as_mut<T>(a.dlmk)[(((size_t)b * a.Hl + hl) * nC + c) * D + dd] = from_f32<T>(dl[r]);
+        }
+    }
+    if (a.dbias && tid < nLH) {
+        const int hl = per_head_lmk ? g * G + tid : g;
+        a.dbias[((size_t)b * a.Hl + hl) * nC + c] = s_db[tid];
+    }
+}
+
+struct BwdRun {
+    template <typename T, int D, int G>
+    static hipError_t run(const BwdArgs& a, hipStream_t s) {
+        const BwdWorkspace w = bwd_workspace_layout(a.B, a.Hkv, a.N, a.L, a.K);
+        char* ws = static_cast<char*>(a.ws);
+        int* counts = reinterpret_cast<int*>(ws + w.counts);
+        int* offsets = reinterpret_cast<int*>(ws + w.offsets);
+        int* cursor = reinterpret_cast<int*>(ws + w.cursor);
+        int* list = reinterpret_cast<int*>(ws + w.list);
+        const int nC = a.L / kChunk;
+        const size_t ncnt = (size_t)a.B * a.Hkv * nC;
+        const size_t nent = (size_t)a.B * a.Hkv * a.N * a.K;
+        const unsigned gc = (unsigned)((ncnt + kBlock - 1) / kBlock);
+        const unsigned ge = (unsigned)((nent + kBlock - 1) / kBlock);
+        hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, counts, ncnt, 0);
+        hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, cursor, ncnt, 0);
+        hipLaunchKernelGGL(k_inv_count, dim3(ge), dim3(kBlock), 0, s, a, counts);
+        hipLaunchKernelGGL(k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, offsets, nC);
+        hipLaunchKernelGGL(k_inv_fill, dim3(ge), dim3(kBlock), 0, s, a, (const int*)offsets, cursor, list);
+        hipLaunchKernelGGL((k_bwd_dq_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((k_bwd_dkdv_chunks<T, D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a,
+                           (const int*)offsets, (const int*)list);
+        return hipGetLastError();
+    }
+};
+
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t s) { return dispatch<BwdRun>(a.bf16, a.d, a.Hq / a.Hkv, a, s); }
+
+}  // namespace hils

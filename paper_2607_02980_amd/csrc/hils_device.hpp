@@ -1,0 +1,181 @@
+// Device-side helpers for the HiLS kernels (gfx950, 64-lane wavefronts).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hils {
+
+constexpr int kWave = 64;
+constexpr int kChunk = 64;  // S: the only chunk size with kernels
+
+// ---- storage types -------------------------------------------------------
+
+struct bf16 {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return __uint_as_float((uint32_t)x.bits << 16); }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ bf16 from_f32<bf16>(float x) {
+    uint32_t u = __float_as_uint(x);
+    bf16 r;
+    if ((u & 0x7fffffffu) > 0x7f800000u) {  // NaN stays NaN
+        r.bits = (uint16_t)((u >> 16) | 0x40u);
+        return r;
+    }
+    u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest, ties to even
+    r.bits = (uint16_t)(u >> 16);
+    return r;
+}
+
+// Load 8 consecutive elements (16 B for bf16, 32 B for f32) as floats.
+__device__ __forceinline__ void load8(const bf16* p, float* o) {
+    const uint4 w = *reinterpret_cast<const uint4*>(p);
+    const uint32_t a[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        o[2 * t] = __uint_as_float(a[t] << 16);
+        o[2 * t + 1] = __uint_as_float(a[t] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void load8(const float* p, float* o) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+
+// ---- wave reductions (all 64 lanes receive the result) --------------------
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+    return x;
+}
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, kWave));
+    return x;
+}
+
+// exp(x) for x <= 0 typically; exact -inf -> 0.
+__device__ __forceinline__ float fexp(float x) { return __expf(x); }
+
+// Order-preserving map float -> uint32 (larger float => larger key; -0 < +0).
+__device__ __forceinline__ uint32_t ordered_key(float f) {
+    uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
+
+// ---- chunk geometry (Sec. 2.1) ------------------------------------------
+
+// |C_i| = l(i)/S for a query at position i, with l(i) clamped at 0.
+__device__ __forceinline__ int n_candidates(int i, int W) {
+    int t = i - W + 1;
+    if (t < 0) return 0;
+    return t / kChunk;
+}
+
+// ---- wave top-K selection ------------------------------------------------
+//
+// One wavefront selects the K best of n candidates (score sc[e], chunk id[e]),
+// ordered by score descending and then id ascending (ties to the smaller
+// chunk, Eq. (9) rank with that reading of ties).  sc/id live in LDS.  The
+// chosen ids are written ascending to out_id[0..m) with their scores to
+// out_sc, m = min(K, n) is returned (to every lane).
+//
+// Method: exact radix select.  T = the m-th largest 32-bit order key is built
+// bit by bit with ballot counts; everything above T is kept, and among the
+// entries equal to T the `need` smallest ids are kept (a second bitwise
+// search, only when T is tied).  No sorting network and no data movement
+// besides the final compaction.
+__device__ __forceinline__ int wave_count_ge(const float* sc, int n, uint32_t t) {
+    const int lane = __lane_id();
+    int c = 0;
+    for (int base = 0; base < n; base += kWave) {
+        const int e = base + lane;
+        const bool pr = e < n && ordered_key(sc[e]) >= t;
+        c += popc64(__ballot(pr));
+    }
+    return c;
+}
+
+__device__ inline int wave_topk(const float* sc, const int* id, int n, int K, int* out_id, float* out_sc,
+                                int* tmp_id, float* tmp_sc) {
+    const int lane = __lane_id();
+    const int m = n < K ? n : K;
+    if (m <= 0) return 0;
+    uint32_t T = 0;
+    bool all = (n <= K);
+    int cnt_gt = 0, need = 0;
+    uint32_t id_thr = 0x7fffffffu;
+    if (!all) {
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t t = T | (1u << bit);
+            if (wave_count_ge(sc, n, t) >= m) T = t;
+        }
+        cnt_gt = (T == 0xffffffffu) ? 0 : wave_count_ge(sc, n, T + 1);
+        need = m - cnt_gt;
+        int ties = wave_count_ge(sc, n, T) - cnt_gt;
+        if (ties > need) {
+            // need-th smallest id among the entries with key == T
+            uint32_t x = 0;
+            for (int bit = 30; bit >= 0; --bit) {
+                const uint32_t y = x | (1u << bit);
+                int c = 0;
+                for (int base = 0; base < n; base += kWave) {
+                    const int e = base + lane;
+                    const bool pr = e < n && ordered_key(sc[e]) == T && (uint32_t)id[e] < y;
+                    c += popc64(__ballot(pr));
+                }
+                if (c < need) x = y;
+            }
+            id_thr = x;  // keep ties with id <= x
+        }
+    }
+    // compact the chosen entries (any order) into tmp
+    int w = 0;
+    for (int base = 0; base < n; base += kWave) {
+        const int e = base + lane;
+        bool pr = false;
+        if (e < n) {
+            if (all) {
+                pr = true;
+            } else {
+                const uint32_t k = ordered_key(sc[e]);
+                pr = k > T || (k == T && (uint32_t)id[e] <= id_thr);
+            }
+        }
+        const uint64_t bal = __ballot(pr);
+        if (pr) {
+            const int pos = w + popc64(bal & ((1ull << lane) - 1ull));
+            tmp_id[pos] = id[e];
+            tmp_sc[pos] = sc[e];
+        }
+        w += popc64(bal);
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    // rank by id (m <= 64: one entry per lane)
+    if (lane < m) {
+        const int my = tmp_id[lane];
+        int r = 0;
+        for (int t = 0; t < m; ++t) r += tmp_id[t] < my;
+        out_id[r] = my;
+        out_sc[r] = tmp_sc[lane];
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    return m;
+}
+
+}  // namespace hils

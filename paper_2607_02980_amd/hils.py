@@ -1,0 +1,212 @@
+"""ctypes binding of libhils.so -- argument marshalling only.
+
+The entry points keep the C names (``hils_prefill_fwd``, ``hils_decode_fwd``,
+``hils_bwd``, ``hils_workspace_size``, ``hils_last_error``, ``hils_version``).
+They take torch tensors already resident on the GPU, check dtype, shape,
+device and contiguity, allocate missing outputs and the workspace with
+``torch.empty`` and pass raw pointers plus the current HIP stream.  Every step
+of the computation runs in the library's HIP kernels; there is no fallback:
+if ``libhils.so`` is missing or fails to load, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhils.so")
+
+HILS_F32, HILS_BF16 = 0, 1
+HILS_OK, HILS_ERR_INVALID, HILS_ERR_UNSUPPORTED, HILS_ERR_WORKSPACE, HILS_ERR_HIP = range(5)
+HILS_FLAG_GIVEN_IDX = 1
+HILS_OP_PREFILL, HILS_OP_DECODE, HILS_OP_BWD = 0, 1, 2
+
+
+class HilsError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"hils error {code}: {msg}")
+        self.code = code
+
+
+class hils_params(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int), ("Hq", ctypes.c_int), ("Hkv", ctypes.c_int), ("Hl", ctypes.c_int),
+                ("N", ctypes.c_int), ("L", ctypes.c_int), ("d", ctypes.c_int), ("chunk", ctypes.c_int),
+                ("topk", ctypes.c_int), ("window", ctypes.c_int), ("scale", ctypes.c_float),
+                ("dtype", ctypes.c_int), ("flags", ctypes.c_uint)]
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2607_02980_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    P = ctypes.POINTER(hils_params)
+    lib.hils_version.restype = ctypes.c_int
+    lib.hils_last_error.restype = ctypes.c_char_p
+    lib.hils_workspace_size.argtypes = [P, ctypes.c_int, ctypes.POINTER(sz)]
+    lib.hils_prefill_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.hils_decode_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.hils_bwd.argtypes = [P] + [vp] * 17 + [sz, vp]
+    for f in (lib.hils_workspace_size, lib.hils_prefill_fwd, lib.hils_decode_fwd, lib.hils_bwd):
+        f.restype = ctypes.c_int
+    return lib
+
+
+LIB = _load()
+
+
+@dataclass
+class Params:
+    """Python mirror of ``hils_params``."""
+    B: int
+    Hq: int
+    Hkv: int
+    N: int
+    L: int
+    d: int
+    chunk: int = 64
+    topk: int = 16
+    window: int = 512
+    scale: float | None = None
+    dtype: str = "bf16"
+    Hl: int = 0
+    flags: int = 0
+
+    def c(self) -> hils_params:
+        return hils_params(self.B, self.Hq, self.Hkv, self.Hl or self.Hq, self.N, self.L, self.d, self.chunk,
+                           self.topk, self.window, float(self.scale if self.scale is not None else self.d ** -0.5),
+                           HILS_BF16 if self.dtype == "bf16" else HILS_F32, self.flags)
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+
+def hils_version() -> int:
+    return LIB.hils_version()
+
+
+def hils_last_error() -> str:
+    return LIB.hils_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != HILS_OK:
+        raise HilsError(rc, hils_last_error())
+
+
+def hils_workspace_size(p: Params, op: int) -> int:
+    n = ctypes.c_size_t(0)
+    cp = p.c()
+    _check(LIB.hils_workspace_size(ctypes.byref(cp), op, ctypes.byref(n)))
+    return n.value
+
+
+def _ptr(t, name, shape=None, dtype=None, required=True):
+    if t is None:
+        if required:
+            raise ValueError(f"{name} is required")
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _workspace(p: Params, op: int, workspace):
+    n = hils_workspace_size(p, op)
+    if workspace is None:
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device="cuda")
+    if workspace.numel() < n:
+        raise ValueError(f"workspace has {workspace.numel()} bytes, {n} needed")
+    return workspace, n
+
+
+def _shapes(p: Params):
+    nc = p.L // p.chunk
+    Hl = p.Hl or p.Hq
+    return {"q": (p.B, p.Hq, p.N, p.d), "kv": (p.B, p.Hkv, p.L, p.d), "lmk": (p.B, Hl, nc, p.d),
+            "bias": (p.B, Hl, nc), "lse": (p.B, p.Hq, p.N), "idx": (p.B, p.Hkv, p.N, p.topk)}
+
+
+def hils_prefill_fwd(p: Params, q, k, v, lmk, lmk_bias=None, q_route=None, out=None, lse=None, idx=None,
+                     workspace=None):
+    """Prefill forward.  Returns (out, lse, idx).  With ``p.flags & HILS_FLAG_GIVEN_IDX``
+    the given ``idx`` is consumed instead of selected."""
+    S, dt = _shapes(p), p.torch_dtype
+    if out is None:
+        out = torch.empty(S["q"], dtype=dt, device=q.device)
+    if lse is None:
+        lse = torch.empty(S["lse"], dtype=torch.float32, device=q.device)
+    if idx is None:
+        if p.flags & HILS_FLAG_GIVEN_IDX:
+            raise ValueError("HILS_FLAG_GIVEN_IDX needs idx")
+        idx = torch.empty(S["idx"], dtype=torch.int32, device=q.device)
+    ws, n = _workspace(p, HILS_OP_PREFILL, workspace)
+    cp = p.c()
+    _check(LIB.hils_prefill_fwd(
+        ctypes.byref(cp), _ptr(q, "q", S["q"], dt), _ptr(k, "k", S["kv"], dt), _ptr(v, "v", S["kv"], dt),
+        _ptr(lmk, "lmk", S["lmk"], dt), _ptr(lmk_bias, "lmk_bias", S["bias"], torch.float32, False),
+        _ptr(q_route, "q_route", S["q"], dt, False), _ptr(out, "out", S["q"], dt),
+        _ptr(lse, "lse", S["lse"], torch.float32), _ptr(idx, "idx", S["idx"], torch.int32),
+        _ptr(ws, "workspace"), n, _stream()))
+    return out, lse, idx
+
+
+def hils_decode_fwd(p: Params, q, k_cache, v_cache, lmk_cache, lmk_bias=None, q_route=None, seqlens=None,
+                    out=None, lse=None, idx=None, workspace=None):
+    """Decode forward (N == 1).  Returns (out, lse, idx)."""
+    S, dt = _shapes(p), p.torch_dtype
+    if out is None:
+        out = torch.empty(S["q"], dtype=dt, device=q.device)
+    if lse is None:
+        lse = torch.empty(S["lse"], dtype=torch.float32, device=q.device)
+    if idx is None:
+        if p.flags & HILS_FLAG_GIVEN_IDX:
+            raise ValueError("HILS_FLAG_GIVEN_IDX needs idx")
+        idx = torch.empty(S["idx"], dtype=torch.int32, device=q.device)
+    ws, n = _workspace(p, HILS_OP_DECODE, workspace)
+    cp = p.c()
+    _check(LIB.hils_decode_fwd(
+        ctypes.byref(cp), _ptr(q, "q", S["q"], dt), _ptr(k_cache, "k_cache", S["kv"], dt),
+        _ptr(v_cache, "v_cache", S["kv"], dt), _ptr(lmk_cache, "lmk_cache", S["lmk"], dt),
+        _ptr(lmk_bias, "lmk_bias", S["bias"], torch.float32, False), _ptr(q_route, "q_route", S["q"], dt, False),
+        _ptr(seqlens, "seqlens", (p.B,), torch.int32, False), _ptr(out, "out", S["q"], dt),
+        _ptr(lse, "lse", S["lse"], torch.float32), _ptr(idx, "idx", S["idx"], torch.int32),
+        _ptr(ws, "workspace"), n, _stream()))
+    return out, lse, idx
+
+
+def hils_bwd(p: Params, dout, q, k, v, lmk, out, lse, idx, lmk_bias=None, q_route=None, want_dbias=True,
+             workspace=None):
+    """Backward with the selection fixed to ``idx``.  Returns dict(dq, dk, dv, dlmk, dlmk_bias, dq_route)."""
+    S, dt = _shapes(p), p.torch_dtype
+    dev = q.device
+    dq = torch.empty(S["q"], dtype=dt, device=dev)
+    dk = torch.empty(S["kv"], dtype=dt, device=dev)
+    dv = torch.empty(S["kv"], dtype=dt, device=dev)
+    dlmk = torch.empty(S["lmk"], dtype=dt, device=dev)
+    dbias = torch.empty(S["bias"], dtype=torch.float32, device=dev) if want_dbias else None
+    dqr = torch.empty(S["q"], dtype=dt, device=dev) if q_route is not None else None
+    ws, n = _workspace(p, HILS_OP_BWD, workspace)
+    cp = p.c()
+    _check(LIB.hils_bwd(
+        ctypes.byref(cp), _ptr(dout, "dout", S["q"], dt), _ptr(q, "q", S["q"], dt), _ptr(k, "k", S["kv"], dt),
+        _ptr(v, "v", S["kv"], dt), _ptr(lmk, "lmk", S["lmk"], dt),
+        _ptr(lmk_bias, "lmk_bias", S["bias"], torch.float32, False), _ptr(q_route, "q_route", S["q"], dt, False),
+        _ptr(out, "out", S["q"], dt), _ptr(lse, "lse", S["lse"], torch.float32),
+        _ptr(idx, "idx", S["idx"], torch.int32), _ptr(dq, "dq"), _ptr(dk, "dk"), _ptr(dv, "dv"),
+        _ptr(dlmk, "dlmk"), _ptr(dbias, "dbias", required=False), _ptr(dqr, "dq_route", required=False),
+        _ptr(ws, "workspace"), n, _stream()))
+    return {"dq": dq, "dk": dk, "dv": dv, "dlmk": dlmk, "dlmk_bias": dbias, "dq_route": dqr}

@@ -1,0 +1,158 @@
+"""The C-ABI boundary on the CPU: the library loads, exports every function
+``include/hils.h`` declares, and rejects every invalid argument with its
+documented code and a message before any HIP call (these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hils.h")
+LIBPATH = os.path.join(ROOT, "paper_2607_02980_amd", "libhils.so")
+
+
+@pytest.fixture(scope="module")
+def hils():
+    if not os.path.exists(LIBPATH):
+        from paper_2607_02980_amd import build
+
+        build.build()
+    from paper_2607_02980_amd import hils as h
+
+    return h
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hils_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(hils):
+    names = declared_functions()
+    assert {"hils_prefill_fwd", "hils_decode_fwd", "hils_bwd", "hils_workspace_size", "hils_last_error"} <= set(names)
+    lib = ctypes.CDLL(LIBPATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in hils.h but not exported"
+    assert hils.hils_version() >= 100
+
+
+def params(hils, **kw):
+    base = dict(B=1, Hq=8, Hkv=2, N=256, L=256, d=128, chunk=64, topk=8, window=128, dtype="bf16")
+    base.update(kw)
+    return hils.Params(**base)
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+def call_prefill(hils, p, **override):
+    ptrs = dict(q=FAKE, k=FAKE, v=FAKE, lmk=FAKE, bias=None, q_route=None, out=FAKE, lse=FAKE, idx=FAKE, ws=None)
+    ptrs.update(override)
+    cp = p.c()
+    return hils.LIB.hils_prefill_fwd(ctypes.byref(cp), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["lmk"], ptrs["bias"],
+                                     ptrs["q_route"], ptrs["out"], ptrs["lse"], ptrs["idx"], ptrs["ws"], 0, None)
+
+
+@pytest.mark.parametrize("kw,code,msg", [
+    (dict(Hq=6, Hkv=4), 1, "multiple of Hkv"),
+    (dict(Hl=4), 1, "Hl=4"),
+    (dict(L=250, N=250), 1, "multiple of chunk"),
+    (dict(N=512), 1, "N <= L"),
+    (dict(topk=0), 1, ">= 1"),
+    (dict(window=0), 1, ">= 1"),
+    (dict(B=0), 1, ">= 1"),
+    (dict(flags=4), 1, "unknown flags"),
+    (dict(chunk=32), 2, "chunk 64"),
+    (dict(d=96), 2, "d in {64, 128}"),
+    (dict(Hq=6, Hkv=2), 2, "G=3"),
+    (dict(Hq=32, Hkv=2), 2, "G=16"),
+    (dict(topk=65), 2, "topk <= 64"),
+])
+def test_prefill_rejects_invalid_params(hils, kw, code, msg):
+    rc = call_prefill(hils, params(hils, **kw))
+    assert rc == code
+    assert msg in hils.hils_last_error()
+
+
+@pytest.mark.parametrize("name", ["q", "k", "v", "lmk", "out", "lse", "idx"])
+def test_prefill_rejects_null_pointers(hils, name):
+    rc = call_prefill(hils, params(hils), **{name: None})
+    assert rc == hils.HILS_ERR_INVALID
+    assert f"'{name}'" in hils.hils_last_error()
+
+
+def test_params_null_and_bad_dtype_and_scale(hils):
+    assert hils.LIB.hils_prefill_fwd(None, *([FAKE] * 4), None, None, FAKE, FAKE, FAKE, None, 0, None) == 1
+    p = params(hils).c()
+    p.dtype = 7
+    n = ctypes.c_size_t()
+    assert hils.LIB.hils_workspace_size(ctypes.byref(p), 0, ctypes.byref(n)) == 1
+    p = params(hils).c()
+    p.scale = float("inf")
+    assert hils.LIB.hils_workspace_size(ctypes.byref(p), 0, ctypes.byref(n)) == 1
+    assert "scale" in hils.hils_last_error()
+
+
+def test_decode_requires_single_query(hils):
+    p = params(hils, N=2).c()
+    rc = hils.LIB.hils_decode_fwd(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, FAKE, FAKE,
+                                  None, 0, None)
+    assert rc == hils.HILS_ERR_INVALID and "N == 1" in hils.hils_last_error()
+
+
+def test_workspace_sizes_and_workspace_errors(hils):
+    p = params(hils, B=2, N=1024, L=1024)
+    assert hils.hils_workspace_size(p, hils.HILS_OP_PREFILL) >= 0
+    need = hils.hils_workspace_size(p, hils.HILS_OP_BWD)
+    nC = 1024 // 64
+    assert need >= 4 * (2 * 2 * 1024 * 8 + 3 * 2 * 2 * nC)
+    cp = p.c()
+    args = [ctypes.byref(cp)] + [FAKE] * 5 + [None, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None]
+    rc = hils.LIB.hils_bwd(*args, None, 0, None)
+    assert rc == hils.HILS_ERR_WORKSPACE and "NULL" in hils.hils_last_error()
+    rc = hils.LIB.hils_bwd(*args, FAKE, need - 1, None)
+    assert rc == hils.HILS_ERR_WORKSPACE and f"{need} needed" in hils.hils_last_error()
+
+
+def test_bwd_route_gradient_needs_its_buffer(hils):
+    p = params(hils)
+    cp = p.c()
+    need = hils.hils_workspace_size(p, hils.HILS_OP_BWD)
+    args = [ctypes.byref(cp), FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+            None, None, FAKE, need, None]
+    assert hils.LIB.hils_bwd(*args) == hils.HILS_ERR_INVALID
+    assert "dq_route" in hils.hils_last_error()
+
+
+def test_bwd_rejects_forced_index_flag(hils):
+    p = params(hils, flags=1)
+    n = ctypes.c_size_t()
+    cp = p.c()
+    assert hils.LIB.hils_workspace_size(ctypes.byref(cp), 2, ctypes.byref(n)) == hils.HILS_ERR_INVALID
+
+
+def test_binding_refuses_host_tensors(hils):
+    import torch
+
+    p = params(hils, dtype="f32", N=64, L=64)
+    q = torch.zeros(1, 8, 64, 128)
+    with pytest.raises(ValueError):
+        hils._ptr(q, "q")
+
+
+def test_error_string_is_thread_local(hils):
+    import threading
+
+    call_prefill(hils, params(hils, chunk=32))
+    seen = {}
+
+    def other():
+        seen["msg"] = hils.hils_last_error()
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen["msg"] == ""
+    assert "chunk" in hils.hils_last_error()

@@ -182,10 +182,11 @@ def dense_weights(shape: Shape, q, k, lmk, idx, bias=None, q_route=None, qpos=No
 
 
 def bwd(shape: Shape, dout, q, k, v, lmk, idx, bias=None, q_route=None, qpos=None, rows=None,
-        prec: str = "f64", want_dbias: bool = True):
+        prec: str = "f64", want_dbias: bool = True, only_group: int = -1):
     """Backward with the selection fixed to ``idx``.  Returns dict(dq, dk, dv,
     dlmk, dbias, dq_route); ``dq_route`` is None (folded into dq) unless a
-    routing query is given.  With ``rows`` only those rows contribute."""
+    routing query is given.  With ``rows`` only those rows contribute; with
+    ``only_group`` >= 0 only that KV group's gradients are computed."""
     lib = _lib(prec)
     R = _real(prec)
     s = shape
@@ -207,7 +208,7 @@ def bwd(shape: Shape, dout, q, k, v, lmk, idx, bias=None, q_route=None, qpos=Non
     sh = s.c()
     rc = fn(ctypes.byref(sh), _ptr(dout), _ptr(q), _ptr(k), _ptr(v), _ptr(lmk), _ptr(bias), _ptr(q_route),
             _ptr(qpos), _ptr(rows_a), ctypes.c_int(nrows), _ptr(idx), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlmk),
-            _ptr(dbias), _ptr(dqr))
+            _ptr(dbias), _ptr(dqr), ctypes.c_int(only_group))
     if rc:
         raise ValueError(f"oracle bwd failed with code {rc}")
     return {"dq": dq, "dk": dk, "dv": dv, "dlmk": dlmk, "dbias": dbias, "dq_route": dqr}

@@ -537,11 +537,13 @@ static void backward_row(const inputs* in, int b, int g, int n, const int32_t* i
 /* Backward.  Accumulates (+=) into dq, dk, dv, dlmk, dbias (may be NULL) and
  * dq_route (NULL: the routing-query gradient is added to dq) the
  * contributions of the listed rows (NULL: all rows), with idx as selected by
- * the forward.  Returns 0 or a negative code as for the forward. */
+ * the forward.  only_group >= 0 restricts the work to that KV group (a
+ * sampled check of one group's gradients).  Returns 0 or a negative code as
+ * for the forward. */
 int API(bwd)(const hils_oracle_shape* p, const float* dout, const float* q, const float* k, const float* v,
              const float* lmk, const float* bias, const float* q_route, const int32_t* qpos, const int32_t* rows,
              int nrows, const int32_t* idx, REAL* dq, REAL* dk, REAL* dv, REAL* dlmk, REAL* dbias,
-             REAL* dq_route) {
+             REAL* dq_route, int only_group) {
     if (check_shape(p)) return -1;
     inputs in = {p, q, k, v, lmk, bias, q_route, qpos};
     int rc = check_positions(&in);
@@ -552,6 +554,7 @@ int API(bwd)(const hils_oracle_shape* p, const float* dout, const float* q, cons
 #pragma omp parallel for schedule(dynamic, 1)
     for (long bg = 0; bg < (long)p->B * p->Hkv; ++bg) {
         int b = (int)(bg / p->Hkv), g = (int)(bg % p->Hkv);
+        if (only_group >= 0 && g != only_group) continue;
         for (long r = 0; r < total; ++r) {
             int rb = rows ? rows[2 * r] : (int)(r / p->N);
             int rn = rows ? rows[2 * r + 1] : (int)(r % p->N);

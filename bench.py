@@ -145,8 +145,10 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
     lse = torch.empty(p.B, p.Hq, 1, dtype=torch.float32, device="cuda")
     idx = torch.empty(p.B, p.Hkv, 1, p.topk, dtype=torch.int32, device="cuda")
     ws = torch.empty(max(1, hils.hils_workspace_size(p, hils.HILS_OP_DECODE)), dtype=torch.uint8, device="cuda")
-    # a 512 MB write between steps evicts the caches (L2 + MALL) so the step reads HBM
-    flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device="cuda")
+    # reading 1 GiB between steps evicts L2 and MALL with clean lines, so the
+    # timed step streams from HBM without paying for dirty write-backs
+    flush = torch.ones(2 ** 28, dtype=torch.float32, device="cuda")
+    sink = torch.empty((), dtype=torch.float32, device="cuda")
 
     def step():
         hils.hils_decode_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], seqlens=seqlens, out=out, lse=lse,
@@ -159,7 +161,7 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
     st = torch.cuda.current_stream()
     total = 0.0
     for _ in range(steps):
-        flush.fill_(1)
+        torch.sum(flush, dim=0, out=sink)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(st)
         step()
@@ -168,7 +170,7 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
         total += e0.elapsed_time(e1)
     ms = total / steps
     nbytes, parts = decode_bytes(p.B, p.Hq, p.Hkv, p.Hq, W_.ctx, p.d, p.chunk, p.topk, p.window)
-    del dev, flush
+    del dev, flush, sink
     torch.cuda.empty_cache()
     return {"workload": W_.name, "ms_per_step": round(ms, 4), "tokens_per_s": round(p.B / (ms * 1e-3), 1),
             "algorithmic_bytes": nbytes, "bytes_breakdown": parts,

@@ -133,6 +133,7 @@ int hils_prefill_fwd(const hils_params* p, const void* q, const void* k, const v
  *            or NULL for L; values are clamped into [1, L] by the kernels.
  * Other arguments as for hils_prefill_fwd with N = 1 (q, q_route, out [B,Hq,1,d];
  * lse [B,Hq,1]; idx [B,Hkv,1,K]; k, v, lmk, lmk_bias are the caches).
+ * Windows above 4032 tokens return HILS_ERR_UNSUPPORTED.
  */
 int hils_decode_fwd(const hils_params* p, const void* q, const void* k_cache, const void* v_cache,
                     const void* lmk_cache, const float* lmk_bias, const void* q_route, const int32_t* seqlens,

@@ -59,6 +59,8 @@ int check_params(const hils_params* p, int op) {
     if (G != 1 && G != 2 && G != 4 && G != 8)
         return fail(HILS_ERR_UNSUPPORTED, "group size G=%d: kernels exist for G in {1, 2, 4, 8}", G);
     if (p->topk > 64) return fail(HILS_ERR_UNSUPPORTED, "topk=%d: kernels exist for topk <= 64", p->topk);
+    if (op == HILS_OP_DECODE && p->window > 4032)
+        return fail(HILS_ERR_UNSUPPORTED, "window=%d: the decode kernels cover windows <= 4032", p->window);
     return HILS_OK;
 }
 
@@ -67,7 +69,7 @@ size_t ws_bytes_for(const hils_params* p, int op) {
         case HILS_OP_BWD:
             return hils::bwd_workspace_layout(p->B, p->Hkv, p->N, p->L, p->topk).total;
         case HILS_OP_DECODE:
-            return hils::decode_workspace_bytes(p->B, p->Hkv, p->L, p->topk);
+            return hils::decode_workspace_bytes(p->B, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window);
         default:
             return 0;
     }

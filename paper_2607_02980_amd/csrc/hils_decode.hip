@@ -1,0 +1,496 @@
+// HiLS attention decode forward, gfx950.  One new query per sequence; the
+// work is a stream over HBM (landmark scan, then K/V gathers), so the kernels
+// are organised for coalesced, many-in-flight loads rather than for math.
+//
+//   A  k_dec_scan_local  grid (nslices + nlocal, Hkv, B)
+//        x <  nslices : scores SLICE candidate chunks of one KV group
+//                       (s^_hc for the G heads, max over heads, Eq. (9) / App. C)
+//                       and keeps the slice's top-K (exact wave radix select)
+//        x >= nslices : one 64-key piece of the local window [l(i), i] (Eq. (1)):
+//                       per-head max, sum and unnormalised P.V of the piece
+//   B  k_dec_merge       grid (Hkv, B): top-K over the slices' survivors -> idx
+//   C  k_dec_chunks      grid (K, Hkv, B): the intra-chunk softmax of one selected
+//                       chunk (Eq. (10)) and its surrogate score s^_hc
+//   D  k_dec_combine     grid (Hkv, B): local pieces merged by online softmax,
+//                       then the fusion softmax over {s^_hc} U {log Z_swa} -> out, lse
+// Parts (local pieces and chunks) leave a record {m, l, s^, o[d]} per head.
+#include "hils_device.hpp"
+#include "hils_dispatch.hpp"
+#include "hils_internal.hpp"
+
+namespace hils {
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kSlice = 256;       // candidate chunks per scan workgroup
+constexpr int kMaxLocalPieces = 64;  // local window pieces per row (W <= 4032)
+
+struct DecLayout {
+    int nC, nslices, nlocal, nparts;  // nparts = K + nlocal records per (b, g)
+    size_t cand, parts, total;        // byte offsets
+};
+
+__host__ __device__ inline int local_pieces_max(int W) { return (W + 62) / 64 + 1; }
+
+__host__ __device__ inline DecLayout dec_layout(int B, int Hkv, int G, int d, int L, int K, int W) {
+    DecLayout o;
+    o.nC = L / kChunk;
+    o.nslices = (o.nC + kSlice - 1) / kSlice;
+    o.nlocal = local_pieces_max(W);
+    o.nparts = K + o.nlocal;
+    const size_t bg = (size_t)B * Hkv;
+    o.cand = 0;
+    o.parts = ((bg * o.nslices * K * 8) + 255) & ~(size_t)255;
+    o.total = o.parts + ((bg * o.nparts * G * (4 + d) * 4 + 255) & ~(size_t)255);
+    return o;
+}
+
+__device__ __forceinline__ int decode_position(const FwdArgs& a, int b) {
+    int len = a.seqlens ? a.seqlens[b] : a.L;
+    len = len < 1 ? 1 : (len > a.L ? a.L : len);
+    return len - 1;
+}
+
+// Record of one part for one head: m, l, s^, (pad), o[D] (unnormalised).
+template <int D>
+__device__ __forceinline__ float* part_record(const FwdArgs& a, const DecLayout& ly, int b, int g, int part, int hh,
+                                              int G) {
+    float* base = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.parts);
+    return base + ((((size_t)b * a.Hkv + g) * ly.nparts + part) * G + hh) * (4 + D);
+}
+
+// Shared memory of a part: K and V of 64 keys (raw storage rows padded by 16 B), q, P.
+template <typename T, int D, int G>
+struct PartSmem {
+    static constexpr int kRowBytes = D * (int)sizeof(T) + 16;
+    unsigned char kv[2][kChunk * kRowBytes];
+    float q[G][D];
+    float p[G][kChunk];
+};
+
+template <int G>
+struct ScanSmem {
+    float score[G][kSlice];
+    float sig[kSlice];
+    int id[kSlice];
+    int oid[64], tid[64];
+    float osc[64], tsc[64];
+};
+
+// 8 consecutive elements of an LDS row as floats (one 16-byte read for bf16).
+__device__ __forceinline__ void lds_load8(const unsigned char* p, float* o, bf16) {
+    const uint4 w = *reinterpret_cast<const uint4*>(p);
+    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        o[2 * t] = __uint_as_float(u[t] << 16);
+        o[2 * t + 1] = __uint_as_float(u[t] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void lds_load8(const unsigned char* p, float* o, float) {
+    const float4 x = *reinterpret_cast<const float4*>(p);
+    const float4 y = *reinterpret_cast<const float4*>(p + 16);
+    o[0] = x.x; o[1] = x.y; o[2] = x.z; o[3] = x.w; o[4] = y.x; o[5] = y.y; o[6] = y.z; o[7] = y.w;
+}
+// 2 consecutive elements of an LDS row as floats.
+__device__ __forceinline__ float2 lds_load2(const unsigned char* p, bf16) {
+    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+}
+__device__ __forceinline__ float2 lds_load2(const unsigned char* p, float) {
+    return *reinterpret_cast<const float2*>(p);
+}
+
+// One 64-key part (a local-window piece or a retrieved chunk) of row (b, g):
+// per head m = max_j s_j, l = sum_j exp(s_j - m), o = sum_j exp(s_j - m) v_j.
+template <typename T, int D, int G>
+__device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G>& sm, int b, int g, int part, int c,
+                         int nk, bool is_chunk) {
+    constexpr int RB = PartSmem<T, D, G>::kRowBytes;
+    constexpr int PIECES = D * (int)sizeof(T) / 16;  // 16-byte pieces per row
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const size_t kv_off = (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
+    const unsigned char* kg = reinterpret_cast<const unsigned char*>(as<T>(a.k) + kv_off);
+    const unsigned char* vg = reinterpret_cast<const unsigned char*>(as<T>(a.v) + kv_off);
+    // All 64 rows lie inside the cache (c < L/64), so every load is in bounds;
+    // rows past the query position are loaded but never read back.
+    constexpr int PPT = kChunk * PIECES / kBlock;  // pieces per thread per matrix
+    uint4 xk[PPT], xv[PPT];
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+        const int e = tid + u * kBlock, j = e / PIECES, pc = e % PIECES;
+        xk[u] = *reinterpret_cast<const uint4*>(kg + (size_t)j * D * sizeof(T) + pc * 16);
+        xv[u] = *reinterpret_cast<const uint4*>(vg + (size_t)j * D * sizeof(T) + pc * 16);
+    }
+    // retrieved chunk: its landmark rows and the routing queries, fetched with K/V
+    // (lane pairs: elements 2*lane, 2*lane+1 of head `wave + 4*u`)
+    constexpr int HPW = (G + 3) / 4;  // heads per wave
+    float lm2[HPW][2], qr2[HPW][2];
+#pragma unroll
+    for (int u = 0; u < HPW; ++u) {
+        lm2[u][0] = lm2[u][1] = qr2[u][0] = qr2[u][1] = 0.f;
+        const int hh = wave + 4 * u;
+        if (is_chunk && hh < G && 2 * lane < D) {
+            const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+            const T* qr = as<T>(a.q_route ? a.q_route : a.q) + ((size_t)b * a.Hq + g * G + hh) * D + 2 * lane;
+            const T* lr = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * ly.nC + c) * D + 2 * lane;
+            qr2[u][0] = to_f32(qr[0]);
+            qr2[u][1] = to_f32(qr[1]);
+            lm2[u][0] = to_f32(lr[0]);
+            lm2[u][1] = to_f32(lr[1]);
+        }
+    }
+    const T* q = as<T>(a.q) + ((size_t)b * a.Hq + g * G) * D;  // the group's G rows are contiguous
+    constexpr int QV = G * D / 8;
+    float qx[8];
+    const int qe = tid * 8;
+    if (tid < QV) load8(q + qe, qx);
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+        const int e = tid + u * kBlock, j = e / PIECES, pc = e % PIECES;
+        *reinterpret_cast<uint4*>(&sm.kv[0][j * RB + pc * 16]) = xk[u];
+        *reinterpret_cast<uint4*>(&sm.kv[1][j * RB + pc * 16]) = xv[u];
+    }
+    if (tid < QV) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) sm.q[(qe + t) / D][(qe + t) % D] = qx[t];
+    }
+    __syncthreads();
+    for (int hh = wave; hh < G; hh += kBlock / kWave) {
+        float s = -INFINITY;
+        if (lane < nk) {
+            const unsigned char* kr = &sm.kv[0][lane * RB];
+            float acc = 0.f;
+#pragma unroll 4
+            for (int dd = 0; dd < D; dd += 8) {
+                float x[8];
+                lds_load8(kr + dd * sizeof(T), x, T{});
+                const float4 qa = *reinterpret_cast<const float4*>(&sm.q[hh][dd]);
+                const float4 qb = *reinterpret_cast<const float4*>(&sm.q[hh][dd + 4]);
+                acc += qa.x * x[0] + qa.y * x[1] + qa.z * x[2] + qa.w * x[3];
+                acc += qb.x * x[4] + qb.y * x[5] + qb.z * x[6] + qb.w * x[7];
+            }
+            s = a.scale * acc;
+        }
+        const float m = wave_max(s);
+        const float pj = lane < nk ? fexp(s - m) : 0.f;
+        const float l = wave_sum(pj);
+        sm.p[hh][lane] = pj;
+        float sh = -INFINITY;
+        if (is_chunk) {
+            const int u = (hh - wave) / 4;
+            const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+            const float acc = wave_sum(qr2[u][0] * lm2[u][0] + qr2[u][1] * lm2[u][1]);
+            sh = a.scale * acc + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * ly.nC + c] : 0.f);
+        }
+        if (lane == 0) {
+            float* r = part_record<D>(a, ly, b, g, part, hh, G);
+            r[0] = m;
+            r[1] = l;
+            r[2] = sh;
+        }
+    }
+    __syncthreads();
+    for (int o = tid; o < G * D / 2; o += kBlock) {
+        const int hh = (2 * o) / D, dd = (2 * o) % D;
+        float acc0 = 0.f, acc1 = 0.f;
+        for (int j = 0; j < nk; ++j) {
+            const float pj = sm.p[hh][j];
+            const float2 v = lds_load2(&sm.kv[1][j * RB + dd * sizeof(T)], T{});
+            acc0 += pj * v.x;
+            acc1 += pj * v.y;
+        }
+        float* r = part_record<D>(a, ly, b, g, part, hh, G);
+        r[4 + dd] = acc0;
+        r[5 + dd] = acc1;
+    }
+}
+
+template <int D>
+__device__ void empty_part(const FwdArgs& a, const DecLayout& ly, int b, int g, int part, int G) {
+    for (int hh = threadIdx.x; hh < G; hh += kBlock) {
+        float* r = part_record<D>(a, ly, b, g, part, hh, G);
+        r[0] = -INFINITY;
+        r[1] = 0.f;
+        r[2] = -INFINITY;
+    }
+}
+
+// ---- A: landmark scan slices + local-window pieces -------------------------
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void k_dec_scan_local(FwdArgs a) {
+    const int b = blockIdx.z, g = blockIdx.y;
+    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+    const int pos = decode_position(a, b);
+    const int ncand = n_candidates(pos, a.W);
+
+    // the scan and the part share one LDS allocation
+    __shared__ __align__(16) unsigned char smem[sizeof(PartSmem<T, D, G>) > sizeof(ScanSmem<G>)
+                                                     ? sizeof(PartSmem<T, D, G>)
+                                                     : sizeof(ScanSmem<G>)];
+    if ((int)blockIdx.x < ly.nslices && a.given_idx) return;  // forced selection: no scan
+    if ((int)blockIdx.x >= ly.nslices) {
+        PartSmem<T, D, G>& sm = *reinterpret_cast<PartSmem<T, D, G>*>(smem);
+        const int piece = blockIdx.x - ly.nslices;
+        const int c = ncand + piece;
+        if (c > pos / kChunk) {
+            empty_part<D>(a, ly, b, g, a.K + piece, G);
+            return;
+        }
+        const int nk = min(kChunk, pos - c * kChunk + 1);
+        run_part<T, D, G>(a, ly, sm, b, g, a.K + piece, c, nk, false);
+        return;
+    }
+
+    ScanSmem<G>& ss = *reinterpret_cast<ScanSmem<G>*>(smem);
+    auto& s_score = ss.score;
+    auto& s_sig = ss.sig;
+    auto& s_id = ss.id;
+    auto& s_oid = ss.oid;
+    auto& s_tid = ss.tid;
+    auto& s_osc = ss.osc;
+    auto& s_tsc = ss.tsc;
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int c0 = blockIdx.x * kSlice;
+    const int len = min(kSlice, ncand - c0);
+    float* cand_sc = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.cand);
+    const size_t cbase = (((size_t)b * a.Hkv + g) * ly.nslices + blockIdx.x) * a.K;
+    int* cand_id = reinterpret_cast<int*>(cand_sc + (size_t)a.B * a.Hkv * ly.nslices * a.K);
+    if (len <= 0) {
+        for (int t = tid; t < a.K; t += kBlock) {
+            cand_sc[cbase + t] = -INFINITY;
+            cand_id[cbase + t] = -1;
+        }
+        return;
+    }
+    // lanes_per_row lanes read one landmark row (16 B each); rows_per_step rows per wave load
+    constexpr int LPR = D * (int)sizeof(T) / 16;
+    constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane per load
+    constexpr int RPS = kWave / LPR;
+    const int sub = lane / LPR, seg = lane % LPR;
+    const T* qr = as<T>(a.q_route ? a.q_route : a.q);
+    for (int hh = wave; hh < G; hh += kBlock / kWave) {
+        const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+        float qv[EPL];
+#pragma unroll
+        for (int t = 0; t < EPL; ++t) qv[t] = to_f32(qr[((size_t)b * a.Hq + g * G + hh) * D + seg * EPL + t]);
+        const T* base = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * ly.nC + c0) * D + seg * EPL;
+        // NB independent 16-byte loads per lane are issued before any math; rows
+        // past the slice end re-read the last row (in bounds, result discarded).
+        constexpr int NB = 16;
+        for (int r0 = 0; r0 < len; r0 += RPS * NB) {
+            uint4 x[NB];
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                const int r = min(r0 + u * RPS + sub, len - 1);
+                x[u] = *reinterpret_cast<const uint4*>(base + (size_t)r * D);
+            }
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                float part;
+                if constexpr (sizeof(T) == 2) {
+                    const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+                    part = 0.f;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        part += qv[2 * t] * __uint_as_float(w[t] << 16) +
+                                qv[2 * t + 1] * __uint_as_float(w[t] & 0xffff0000u);
+                } else {
+                    part = qv[0] * __uint_as_float(x[u].x) + qv[1] * __uint_as_float(x[u].y) +
+                           qv[2] * __uint_as_float(x[u].z) + qv[3] * __uint_as_float(x[u].w);
+                }
+                part = group_sum<LPR>(part);
+                const int r = r0 + u * RPS + sub;
+                if (seg == 0 && r < len) s_score[hh][r] = a.scale * part;
+            }
+        }
+    }
+    __syncthreads();
+    for (int r = tid; r < len; r += kBlock) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+            const float bv = a.bias ? a.bias[((size_t)b * a.Hl + hl) * ly.nC + c0 + r] : 0.f;
+            m = fmaxf(m, s_score[hh][r] + bv);
+        }
+        s_sig[r] = m;
+        s_id[r] = c0 + r;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        constexpr int E = kSlice / kWave;
+        float sc[E];
+        int id[E];
+        bool ok[E];
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const int e = r * kWave + lane;
+            ok[r] = e < len;
+            sc[r] = ok[r] ? s_sig[e] : 0.f;
+            id[r] = ok[r] ? s_id[e] : -1;
+        }
+        const int m = wave_topk_reg<E>(sc, id, ok, a.K, s_oid, s_osc, s_tid, s_tsc);
+        for (int t = lane; t < a.K; t += kWave) {
+            cand_sc[cbase + t] = t < m ? s_osc[t] : -INFINITY;
+            cand_id[cbase + t] = t < m ? s_oid[t] : -1;
+        }
+    }
+}
+
+// ---- B: merge the slices' survivors into the final top-K --------------------
+// One 256-thread block per (b, g).  Per round each wave selects the top-K of
+// its 64*kMergeE survivors from registers (all loads in flight together);
+// wave 0 then merges the four lists with the running best.
+constexpr int kMergeE = 8;
+template <int G, int D>
+__global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a) {
+    constexpr int NW = kBlock / kWave;
+    constexpr int E2 = (NW + 1) * 64 / kWave;  // 4 wave lists + running best, <= 64 each
+    __shared__ int s_wid[NW][64], s_tid[NW][64], s_bid[64];
+    __shared__ float s_wsc[NW][64], s_tsc[NW][64], s_bsc[64];
+    __shared__ int s_wn[NW];
+    const int b = blockIdx.y, g = blockIdx.x, tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+    const float* cand_sc = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.cand);
+    const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.Hkv * ly.nslices * a.K);
+    const size_t base = ((size_t)b * a.Hkv + g) * ly.nslices * a.K;
+    const int total = ly.nslices * a.K;
+    int nbest = 0;
+    for (int r0 = 0; r0 < total; r0 += kBlock * kMergeE) {
+        float sc[kMergeE];
+        int id[kMergeE];
+        bool ok[kMergeE];
+#pragma unroll
+        for (int r = 0; r < kMergeE; ++r) {
+            const int e = r0 + (wave * kMergeE + r) * kWave + lane;
+            id[r] = e < total ? cand_id[base + e] : -1;
+            sc[r] = e < total ? cand_sc[base + e] : 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < kMergeE; ++r) ok[r] = id[r] >= 0;
+        const int nw = wave_topk_reg<kMergeE>(sc, id, ok, a.K, s_wid[wave], s_wsc[wave], s_tid[wave], s_tsc[wave]);
+        if (lane == 0) s_wn[wave] = nw;
+        __syncthreads();
+        if (wave == 0) {
+            float sc2[E2];
+            int id2[E2];
+            bool ok2[E2];
+#pragma unroll
+            for (int r = 0; r < E2; ++r) {
+                const int list = r;  // lane indexes the entry inside list r
+                const int cnt = list < NW ? s_wn[list] : nbest;
+                ok2[r] = lane < cnt;
+                id2[r] = ok2[r] ? (list < NW ? s_wid[list][lane] : s_bid[lane]) : -1;
+                sc2[r] = ok2[r] ? (list < NW ? s_wsc[list][lane] : s_bsc[lane]) : 0.f;
+            }
+            __builtin_amdgcn_wave_barrier();
+            nbest = wave_topk_reg<E2>(sc2, id2, ok2, a.K, s_bid, s_bsc, s_tid[0], s_tsc[0]);
+        }
+        __syncthreads();
+    }
+    if (wave == 0) {
+        int32_t* orow = a.idx + ((size_t)b * a.Hkv + g) * a.K;
+        for (int t = lane; t < a.K; t += kWave) orow[t] = t < nbest ? s_bid[t] : -1;
+    }
+}
+
+// ---- C: one selected chunk per workgroup ------------------------------------
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void k_dec_chunks(FwdArgs a) {
+    __shared__ PartSmem<T, D, G> sm;
+    __shared__ int s_c;
+    const int slot = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+    const int pos = decode_position(a, b);
+    if (threadIdx.x == 0) {
+        const int32_t* irow = a.idx + ((size_t)b * a.Hkv + g) * a.K;
+        s_c = idx_entry_valid(irow, slot, n_candidates(pos, a.W)) ? irow[slot] : -1;
+    }
+    __syncthreads();
+    const int c = s_c;
+    if (c < 0) {
+        empty_part<D>(a, ly, b, g, slot, G);
+        return;
+    }
+    run_part<T, D, G>(a, ly, sm, b, g, slot, c, kChunk, true);
+}
+
+// ---- D: fusion -----------------------------------------------------------------
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
+    // Per head: local pieces merge into (lambda0 = log Z_swa, o0); then the fusion
+    // weights are exp(z_t - L) over z = {lambda0} U {s^_c}, L = LSE(z), and each
+    // retrieved chunk contributes exp(s^_c - L) * o_c with o_c its own softmax output.
+    constexpr int kMaxParts = 64 + kMaxLocalPieces;
+    __shared__ float s_w[G][kMaxParts];  // weight of each part's unnormalised o
+    __shared__ float s_lse[G];
+    const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+    for (int hh = wave; hh < G; hh += kBlock / kWave) {
+        // local pieces: lanes < nlocal
+        float m = -INFINITY, l = 0.f;
+        if (lane < ly.nlocal) {
+            const float* r = part_record<D>(a, ly, b, g, a.K + lane, hh, G);
+            m = r[0];
+            l = r[1];
+        }
+        const float m0 = wave_max(m);
+        const float l0 = wave_sum(l > 0.f ? l * fexp(m - m0) : 0.f);
+        const float lam0 = m0 + __logf(l0);
+        // chunks: lanes < K
+        float z = -INFINITY, lc = 0.f;
+        if (lane < a.K) {
+            const float* r = part_record<D>(a, ly, b, g, lane, hh, G);
+            lc = r[1];
+            z = lc > 0.f ? r[2] : -INFINITY;
+        }
+        const float M = fmaxf(wave_max(z), lam0);
+        const float Z = wave_sum(lc > 0.f ? fexp(z - M) : 0.f) + fexp(lam0 - M);
+        const float L = M + __logf(Z);
+        const float a0 = fexp(lam0 - L) / l0;  // applied to each piece as exp(m - m0)
+        if (lane < ly.nlocal) s_w[hh][a.K + lane] = l > 0.f ? a0 * fexp(m - m0) : 0.f;
+        if (lane < a.K) s_w[hh][lane] = lc > 0.f ? fexp(z - L) / lc : 0.f;
+        if (lane == 0) s_lse[hh] = L;
+    }
+    __syncthreads();
+    for (int o = tid; o < G * D; o += kBlock) {
+        const int hh = o / D, dd = o % D;
+        float acc = 0.f;
+#pragma unroll 8
+        for (int pt = 0; pt < ly.nparts; ++pt) {
+            const float w = s_w[hh][pt];
+            const float v = part_record<D>(a, ly, b, g, pt, hh, G)[4 + dd];
+            acc += w != 0.f ? w * v : 0.f;
+        }
+        const size_t row = (size_t)b * a.Hq + g * G + hh;
+        as_mut<T>(a.out)[row * D + dd] = from_f32<T>(acc);
+        if (dd == 0) a.lse[row] = s_lse[hh];
+    }
+}
+
+struct DecRun {
+    template <typename T, int D, int G>
+    static hipError_t run(const FwdArgs& a, hipStream_t s) {
+        const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+        hipLaunchKernelGGL((k_dec_scan_local<T, D, G>), dim3(ly.nslices + ly.nlocal, a.Hkv, a.B), dim3(kBlock), 0,
+                           s, a);
+        if (!a.given_idx) hipLaunchKernelGGL((k_dec_merge<G, D>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((k_dec_chunks<T, D, G>), dim3(a.K, a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((k_dec_combine<T, D, G>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        return hipGetLastError();
+    }
+};
+
+}  // namespace
+
+size_t decode_workspace_bytes(int B, int Hkv, int G, int d, int L, int K, int W) {
+    return dec_layout(B, Hkv, G, d, L, K, W).total;
+}
+
+hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s) {
+    return dispatch<DecRun>(a.bf16, a.d, a.Hq / a.Hkv, a, s);
+}
+
+}  // namespace hils

@@ -65,6 +65,24 @@ __device__ __forceinline__ float wave_max(float x) {
     return x;
 }
 
+// ---- DPP reductions inside groups of 8 / 16 / 32 lanes (no LDS round trip) --
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+// Sum over each aligned group of N lanes (N = 1, 2, 4, 8, 16, 32, 64); every
+// lane of the group receives the group's sum.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+    if constexpr (N >= 2) x += dpp<0xB1>(x);    // quad_perm [1,0,3,2]: lane ^ 1
+    if constexpr (N >= 4) x += dpp<0x4E>(x);    // quad_perm [2,3,0,1]: lane ^ 2
+    if constexpr (N >= 8) x += dpp<0x141>(x);   // row_half_mirror: the other quad of the 8
+    if constexpr (N >= 16) x += dpp<0x140>(x);  // row_mirror: the other half of the 16-lane row
+    if constexpr (N >= 32) x += __shfl_xor(x, 16, kWave);
+    if constexpr (N >= 64) x += __shfl_xor(x, 32, kWave);
+    return x;
+}
+
 // exp(x) for x <= 0 typically; exact -inf -> 0.
 __device__ __forceinline__ float fexp(float x) { return __expf(x); }
 
@@ -175,6 +193,82 @@ __device__ inline int wave_topk(const float* sc, const int* id, int n, int K, in
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    return m;
+}
+
+// Register-resident variant: lane l holds candidates e = l + 64*r (r < E) with
+// score sc[r], chunk id[r] and a valid flag; every pass of the radix select
+// is compares and ballots on registers only.  Same order and outputs as
+// wave_topk.
+template <int E>
+__device__ inline int wave_topk_reg(const float (&sc)[E], const int (&id)[E], const bool (&valid)[E], int K,
+                                    int* out_id, float* out_sc, int* tmp_id, float* tmp_sc) {
+    const int lane = __lane_id();
+    // validity is folded into the key: invalid -> 0, valid -> >= 1 (only the
+    // all-ones NaN pattern maps to 0 and is lifted to 1), so every threshold
+    // t >= 1 below excludes invalid entries with a single compare
+    uint32_t key[E];
+    int n = 0;
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+        const uint32_t k = ordered_key(sc[r]);
+        key[r] = valid[r] ? (k ? k : 1u) : 0u;
+        n += popc64(__ballot(valid[r]));
+    }
+    const int m = n < K ? n : K;
+    if (m <= 0) return 0;
+    auto count_ge = [&](uint32_t t) {
+        int c = 0;
+#pragma unroll
+        for (int r = 0; r < E; ++r) c += popc64(__ballot(key[r] >= t));
+        return c;
+    };
+    uint32_t T = 0, id_thr = 0x7fffffffu;
+    const bool all = (n <= K);
+    if (!all) {
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t t = T | (1u << bit);
+            if (count_ge(t) >= m) T = t;
+        }
+        // T >= 1 here: m valid entries have keys >= 1
+        const int cnt_gt = (T == 0xffffffffu) ? 0 : count_ge(T + 1);
+        const int need = m - cnt_gt;
+        const int ties = count_ge(T) - cnt_gt;
+        if (ties > need) {
+            uint32_t x = 0;
+            for (int bit = 30; bit >= 0; --bit) {
+                const uint32_t y = x | (1u << bit);
+                int c = 0;
+#pragma unroll
+                for (int r = 0; r < E; ++r) c += popc64(__ballot(key[r] == T && (uint32_t)id[r] < y));
+                if (c < need) x = y;
+            }
+            id_thr = x;
+        }
+    }
+    int w = 0;
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+        const bool pr = key[r] != 0u && (all || key[r] > T || (key[r] == T && (uint32_t)id[r] <= id_thr));
+        const uint64_t bal = __ballot(pr);
+        if (pr) {
+            const int pos = w + popc64(bal & ((1ull << lane) - 1ull));
+            tmp_id[pos] = id[r];
+            tmp_sc[pos] = sc[r];
+        }
+        w += popc64(bal);
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    if (lane < m) {
+        const int my = tmp_id[lane];
+        int rk = 0;
+        for (int t = 0; t < m; ++t) rk += tmp_id[t] < my;
+        out_id[rk] = my;
+        out_sc[rk] = tmp_sc[lane];
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     return m;
 }
 

@@ -248,13 +248,7 @@ struct FwdRun {
     }
 };
 
-size_t decode_workspace_bytes(int, int, int, int) { return 0; }
-
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s) {
-    return dispatch<FwdRun>(a.bf16, a.d, a.Hq / a.Hkv, a, s);
-}
-
-hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s) {
     return dispatch<FwdRun>(a.bf16, a.d, a.Hq / a.Hkv, a, s);
 }
 

@@ -58,7 +58,7 @@ struct BwdWorkspace {
 };
 BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K);
 
-size_t decode_workspace_bytes(int B, int Hkv, int L, int K);
+size_t decode_workspace_bytes(int B, int Hkv, int G, int d, int L, int K, int W);
 
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s);

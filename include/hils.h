@@ -119,6 +119,7 @@ int hils_workspace_size(const hils_params* p, int op, size_t* bytes);
  *   idx      [B,Hkv,N,K]    selection (written; read instead under HILS_FLAG_GIVEN_IDX)
  *   workspace, ws_bytes     device scratch of at least hils_workspace_size(p, HILS_OP_PREFILL)
  *   stream                  hipStream_t
+ * Deterministic: repeated calls with equal inputs give identical bits.
  */
 int hils_prefill_fwd(const hils_params* p, const void* q, const void* k, const void* v, const void* lmk,
                      const float* lmk_bias, const void* q_route, void* out, float* lse, int32_t* idx,

@@ -71,7 +71,8 @@ size_t ws_bytes_for(const hils_params* p, int op) {
         case HILS_OP_DECODE:
             return hils::decode_workspace_bytes(p->B, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window);
         default:
-            return 0;
+            return hils::prefill_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk,
+                                                 p->dtype == HILS_BF16);
     }
 }
 

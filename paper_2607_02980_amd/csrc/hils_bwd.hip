@@ -24,16 +24,17 @@ namespace hils {
 constexpr int kBlock = 256;
 constexpr int kSortCap = 4096;  // retrieval lists up to this length are sorted (deterministic order)
 
-static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base);
 
 BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K) {
-    const size_t bg = (size_t)B * Hkv, nC = (size_t)L / kChunk;
+    const InvLayout iv = inv_layout(B, Hkv, N, L, K, 0);
     BwdWorkspace w;
-    w.counts = 0;
-    w.offsets = align256(w.counts + bg * nC * sizeof(int));
-    w.cursor = align256(w.offsets + bg * (nC + 1) * sizeof(int));
-    w.list = align256(w.cursor + bg * nC * sizeof(int));
-    w.total = align256(w.list + bg * (size_t)N * K * sizeof(int));
+    w.counts = iv.counts;
+    w.offsets = iv.offsets;
+    w.cursor = iv.cursor;
+    w.list = iv.list;
+    w.total = iv.end;
     return w;
 }
 
@@ -186,23 +187,76 @@ __global__ void k_fill_i32(int* p, size_t n, int v) {
     if (i < n) p[i] = v;
 }
 
-__device__ __forceinline__ bool entry_of(const BwdArgs& a, size_t e, int* bg, int* n, int* c) {
-    const int slot = (int)(e % a.K);
-    const size_t row = e / a.K;  // (b*Hkv + g)*N + n
-    *n = (int)(row % a.N);
-    *bg = (int)(row / a.N);
-    const int32_t* irow = a.idx + row * a.K;
-    if (!idx_entry_valid(irow, slot, n_candidates(*n, a.W))) return false;
+// Entries are processed per (b, g) in blocks of kInvRows rows; a block first
+// counts its entries per chunk in LDS and then touches each global counter
+// once, so global atomics scale with (blocks x chunks touched), not entries.
+// List entries are (n << 6) | slot (slot < K <= 64).
+constexpr int kInvRows = 256;
+constexpr int kInvHist = 8192;  // chunks counted in LDS; larger L falls back to global atomics
+
+__device__ __forceinline__ bool entry_valid(const InvArgs& a, const int32_t* irow, int slot, int n, int* c) {
+    if (!idx_entry_valid(irow, slot, n_candidates(n, a.W))) return false;
     *c = irow[slot];
     return true;
 }
 
-__global__ void k_inv_count(BwdArgs a, int* counts) {
-    const size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= (size_t)a.B * a.Hkv * a.N * a.K) return;
-    int bg, n, c;
-    if (!entry_of(a, e, &bg, &n, &c)) return;
-    atomicAdd(&counts[(size_t)bg * (a.L / kChunk) + c], 1);
+// grid (ceil(N / kInvRows), B*Hkv)
+__global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int* counts) {
+    __shared__ int s_hist[kInvHist];
+    const int bg = blockIdx.y, n0 = blockIdx.x * kInvRows, tid = threadIdx.x;
+    const int nC = a.L / kChunk;
+    const bool lds = nC <= kInvHist;
+    int* gcnt = counts + (size_t)bg * nC;
+    if (lds)
+        for (int c = tid; c < nC; c += kBlock) s_hist[c] = 0;
+    __syncthreads();
+    const int rows = min(kInvRows, a.N - n0);
+    for (int e = tid; e < rows * a.K; e += kBlock) {
+        const int n = n0 + e / a.K, slot = e % a.K;
+        const int32_t* irow = a.idx + ((size_t)bg * a.N + n) * a.K;
+        int c;
+        if (!entry_valid(a, irow, slot, n, &c)) continue;
+        if (lds)
+            atomicAdd(&s_hist[c], 1);
+        else
+            atomicAdd(&gcnt[c], 1);
+    }
+    __syncthreads();
+    if (lds)
+        for (int c = tid; c < nC; c += kBlock)
+            if (s_hist[c]) atomicAdd(&gcnt[c], s_hist[c]);
+}
+
+__global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, const int* offsets, int* cursor, int* list) {
+    __shared__ int s_hist[kInvHist];
+    const int bg = blockIdx.y, n0 = blockIdx.x * kInvRows, tid = threadIdx.x;
+    const int nC = a.L / kChunk;
+    const bool lds = nC <= kInvHist;
+    int* gcur = cursor + (size_t)bg * nC;
+    const int* off = offsets + (size_t)bg * (nC + 1);
+    int* lst = list + (size_t)bg * a.N * a.K;
+    const int rows = min(kInvRows, a.N - n0);
+    if (lds) {
+        for (int c = tid; c < nC; c += kBlock) s_hist[c] = 0;
+        __syncthreads();
+        for (int e = tid; e < rows * a.K; e += kBlock) {
+            const int n = n0 + e / a.K, slot = e % a.K;
+            int c;
+            if (entry_valid(a, a.idx + ((size_t)bg * a.N + n) * a.K, slot, n, &c)) atomicAdd(&s_hist[c], 1);
+        }
+        __syncthreads();
+        // reserve this block's range of every chunk it touches; s_hist becomes the running position
+        for (int c = tid; c < nC; c += kBlock)
+            if (s_hist[c]) s_hist[c] = off[c] + atomicAdd(&gcur[c], s_hist[c]);
+        __syncthreads();
+    }
+    for (int e = tid; e < rows * a.K; e += kBlock) {
+        const int n = n0 + e / a.K, slot = e % a.K;
+        int c;
+        if (!entry_valid(a, a.idx + ((size_t)bg * a.N + n) * a.K, slot, n, &c)) continue;
+        const int pos = lds ? atomicAdd(&s_hist[c], 1) : off[c] + atomicAdd(&gcur[c], 1);
+        lst[pos] = (n << 6) | slot;
+    }
 }
 
 // one block per (b, g): exclusive scan of the nC counts into offsets[nC + 1]
@@ -234,14 +288,73 @@ __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* off
     }
 }
 
-__global__ void k_inv_fill(BwdArgs a, const int* offsets, int* cursor, int* list) {
-    const size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= (size_t)a.B * a.Hkv * a.N * a.K) return;
-    int bg, n, c;
-    if (!entry_of(a, e, &bg, &n, &c)) return;
+InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base) {
+    const size_t bg = (size_t)B * Hkv, nC = (size_t)L / kChunk;
+    InvLayout w;
+    w.counts = align256(base);
+    w.offsets = align256(w.counts + bg * nC * sizeof(int));
+    w.cursor = align256(w.offsets + bg * (nC + 1) * sizeof(int));
+    w.list = align256(w.cursor + bg * nC * sizeof(int));
+    w.max_work = bg * ((size_t)N * K / kInvSeg + nC);
+    w.work = align256(w.list + bg * (size_t)N * K * sizeof(int));
+    w.nwork = align256(w.work + w.max_work * sizeof(int4));
+    w.end = align256(w.nwork + sizeof(int));
+    return w;
+}
+
+// Work list: every (bg, c) list is cut into segments of kInvSeg entries.
+// One block: a running count over (bg, c) in order assigns each segment a slot.
+__global__ __launch_bounds__(kBlock) void k_inv_work(const int* offsets, int nbg, int nC, int4* work, int* nwork) {
+    __shared__ int s_part[kBlock];
+    const int tid = threadIdx.x;
+    const long total = (long)nbg * nC;
+    const long per = (total + kBlock - 1) / kBlock;
+    const long lo = min(total, (long)tid * per), hi = min(total, lo + per);
+    auto nseg = [&](long i) {
+        const int bg = (int)(i / nC), c = (int)(i % nC);
+        const int* off = offsets + (size_t)bg * (nC + 1);
+        const int len = off[c + 1] - off[c];
+        return (len + kInvSeg - 1) / kInvSeg;
+    };
+    int sum = 0;
+    for (long i = lo; i < hi; ++i) sum += nseg(i);
+    s_part[tid] = sum;
+    __syncthreads();
+    if (tid == 0) {
+        int run = 0;
+        for (int t = 0; t < kBlock; ++t) {
+            const int x = s_part[t];
+            s_part[t] = run;
+            run += x;
+        }
+        *nwork = run;
+    }
+    __syncthreads();
+    int run = s_part[tid];
+    for (long i = lo; i < hi; ++i) {
+        const int ns = nseg(i);
+        for (int sgi = 0; sgi < ns; ++sgi) work[run + sgi] = make_int4((int)(i / nC), (int)(i % nC), sgi, 0);
+        run += ns;
+    }
+}
+
+void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStream_t s) {
+    char* base = static_cast<char*>(ws);
+    int* counts = reinterpret_cast<int*>(base + w.counts);
+    int* offsets = reinterpret_cast<int*>(base + w.offsets);
+    int* cursor = reinterpret_cast<int*>(base + w.cursor);
+    int* list = reinterpret_cast<int*>(base + w.list);
     const int nC = a.L / kChunk;
-    const int slot = atomicAdd(&cursor[(size_t)bg * nC + c], 1);
-    list[(size_t)bg * a.N * a.K + offsets[(size_t)bg * (nC + 1) + c] + slot] = n;
+    const size_t ncnt = (size_t)a.B * a.Hkv * nC;
+    const unsigned gc = (unsigned)((ncnt + kBlock - 1) / kBlock);
+    const dim3 grows((a.N + kInvRows - 1) / kInvRows, a.B * a.Hkv);
+    hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, counts, ncnt, 0);
+    hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, cursor, ncnt, 0);
+    hipLaunchKernelGGL(k_inv_count, grows, dim3(kBlock), 0, s, a, counts);
+    hipLaunchKernelGGL(k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, offsets, nC);
+    hipLaunchKernelGGL(k_inv_fill, grows, dim3(kBlock), 0, s, a, (const int*)offsets, cursor, list);
+    hipLaunchKernelGGL(k_inv_work, dim3(1), dim3(kBlock), 0, s, (const int*)offsets, a.B * a.Hkv, nC,
+                       reinterpret_cast<int4*>(base + w.work), reinterpret_cast<int*>(base + w.nwork));
 }
 
 // ---------------------------------------------------------------------------
@@ -414,9 +527,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dkdv_chunks(BwdArgs a, const int
                 __syncthreads();
             }
         }
-        for (int t = 0; t < len; ++t) process_row(s_list[t], true);
+        for (int t = 0; t < len; ++t) process_row(s_list[t] >> 6, true);
     } else {
-        for (int t = 0; t < len; ++t) process_row(seg[t], true);
+        for (int t = 0; t < len; ++t) process_row(seg[t] >> 6, true);
     }
     __syncthreads();
 
@@ -446,25 +559,16 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dkdv_chunks(BwdArgs a, const int
 struct BwdRun {
     template <typename T, int D, int G>
     static hipError_t run(const BwdArgs& a, hipStream_t s) {
-        const BwdWorkspace w = bwd_workspace_layout(a.B, a.Hkv, a.N, a.L, a.K);
+        const InvLayout w = inv_layout(a.B, a.Hkv, a.N, a.L, a.K, 0);
         char* ws = static_cast<char*>(a.ws);
-        int* counts = reinterpret_cast<int*>(ws + w.counts);
-        int* offsets = reinterpret_cast<int*>(ws + w.offsets);
-        int* cursor = reinterpret_cast<int*>(ws + w.cursor);
-        int* list = reinterpret_cast<int*>(ws + w.list);
+        const int* offsets = reinterpret_cast<const int*>(ws + w.offsets);
+        const int* list = reinterpret_cast<const int*>(ws + w.list);
         const int nC = a.L / kChunk;
-        const size_t ncnt = (size_t)a.B * a.Hkv * nC;
-        const size_t nent = (size_t)a.B * a.Hkv * a.N * a.K;
-        const unsigned gc = (unsigned)((ncnt + kBlock - 1) / kBlock);
-        const unsigned ge = (unsigned)((nent + kBlock - 1) / kBlock);
-        hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, counts, ncnt, 0);
-        hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, cursor, ncnt, 0);
-        hipLaunchKernelGGL(k_inv_count, dim3(ge), dim3(kBlock), 0, s, a, counts);
-        hipLaunchKernelGGL(k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, offsets, nC);
-        hipLaunchKernelGGL(k_inv_fill, dim3(ge), dim3(kBlock), 0, s, a, (const int*)offsets, cursor, list);
+        const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
+        launch_inverse_index(ia, w, a.ws, s);
         hipLaunchKernelGGL((k_bwd_dq_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
         hipLaunchKernelGGL((k_bwd_dkdv_chunks<T, D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a,
-                           (const int*)offsets, (const int*)list);
+                           offsets, list);
         return hipGetLastError();
     }
 };

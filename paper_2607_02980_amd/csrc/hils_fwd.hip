@@ -1,4 +1,5 @@
-// HiLS attention forward kernels (prefill and decode), gfx950.
+// HiLS attention prefill forward, fp32 storage, gfx950 (the bf16 path runs on
+// MFMA in hils_prefill.hip).
 //
 // Row kernels: one wavefront scores and selects for one (b, KV group, query)
 // row; one 256-thread workgroup computes the local-window term, the per-chunk
@@ -248,7 +249,7 @@ struct FwdRun {
     }
 };
 
-hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s) {
+hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s) {
     return dispatch<FwdRun>(a.bf16, a.d, a.Hq / a.Hkv, a, s);
 }
 

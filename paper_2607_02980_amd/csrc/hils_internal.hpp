@@ -52,6 +52,29 @@ struct BwdArgs {
     size_t ws_bytes;
 };
 
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Inverse index of a selection: for every (b, g, chunk) the rows n that chose it.
+struct InvArgs {
+    const int32_t* idx;
+    int B, Hkv, N, K, W, L;
+};
+struct InvLayout {
+    size_t counts, offsets, cursor, list;  // byte offsets from the workspace base
+    size_t work;    // work items (bg, chunk, segment) of at most kInvSeg list entries each
+    size_t nwork;   // one int: number of work items
+    size_t end;
+    size_t max_work;  // upper bound of work items (grid size of the consumers)
+};
+constexpr int kInvSeg = 256;  // list entries per work item
+InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base);
+void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStream_t s);
+
+// Work item encoding: bg * (nC * segs_max) ... decoded by the consumers.
+struct WorkItem {
+    int bg, c, seg;
+};
+
 // Workspace layout of the backward (byte offsets from ws).
 struct BwdWorkspace {
     size_t counts, offsets, cursor, list, total;
@@ -60,7 +83,10 @@ BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K);
 
 size_t decode_workspace_bytes(int B, int Hkv, int G, int d, int L, int K, int W);
 
+size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16);
+
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s);
+hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s);  // fp32 storage
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);
 

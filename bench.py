@@ -1,18 +1,20 @@
 """HiLS attention benchmark on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-decode] [--train] [--no-cpu]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-decode] [--no-train] [--no-cpu]
 
 A step is one pass of the operator over one batch of synthetic input.  The
 headline workload is 32K-token causal prefill in bf16 (B=1, Hq=32, Hkv=8,
 d=128, chunk 64, top-16, window 512): every row of the path runs -- landmark
 scoring, group max, top-K selection, local-window attention, per-chunk
 attention and the fusion epilogue.  ``value`` is prefill tokens/s with all
-inputs resident in HBM.  Decode (32 x 131K-token caches) and, with --train,
-fwd+bwd at 4 x 16K are reported beside it in ``extra``.
+inputs resident in HBM.  Decode (32 x 131K-token caches) and fwd+bwd at
+4 x 16K are reported beside it in ``extra``.
 
-Timing uses HIP events on the stream the library launches on.  The roofline
-object describes the dominant kernel: its launch is isolated through the
-forced-index mode (HILS_FLAG_GIVEN_IDX launches only the attention kernel).
+Timing uses HIP events on the stream the library launches on: the step is
+bracketed by two events, and the library's optional per-kernel timing mode
+brackets every kernel launch inside the timed steps.  The roofline object
+describes the dominant kernel (largest total time): its average launch
+duration against its algorithmic FLOPs or bytes, whichever bound is tighter.
 """
 from __future__ import annotations
 
@@ -47,6 +49,34 @@ def prefill_work(B, Hq, Hkv, N, d, S, K, W):
     attn_flops = B * Hq * 4 * d * float((nloc + S * nsel).sum())   # QK^T and PV, 2 flops per MAC
     score_flops = B * Hq * 2 * d * float(ncand.sum())                # landmark dot products
     return attn_flops, score_flops
+
+
+def prefill_kernel_model(B, Hq, Hkv, N, L, d, S, K, W, elem=2):
+    """Per-kernel algorithmic FLOPs and HBM bytes of one bf16 prefill launch.
+
+    k_pf_score : landmark scores over C_i (2d per head-candidate); reads q, the
+                 landmarks once, writes idx and the row reference score.
+    k_pf_chunks: per selected (row, head, chunk) QK^T + PV over 64 keys (4d*64)
+                 and the surrogate score (2d); reads q and the chunk's K/V once
+                 per chunk, writes one bf16 partial (d) + weight per (row, head, slot).
+    k_pf_local : window QK^T + PV (4d per key); reads q, K/V, the partials and
+                 weights, writes out and lse.
+    """
+    i = np.arange(N, dtype=np.int64)
+    ncand = n_candidates(i, S, W)
+    nloc = i - ncand * S + 1
+    nsel = float(np.minimum(K, ncand).sum())
+    qbytes = B * Hq * N * d * elem
+    kvbytes = 2 * B * Hkv * L * d * elem
+    partials = B * Hq * nsel * (d * elem + 4)
+    return {
+        "k_pf_score": {"flop": B * Hq * 2 * d * float(ncand.sum()),
+                       "bytes": qbytes + B * Hq * (L // S) * d * elem + B * Hkv * N * (K + 1) * 4},
+        "k_pf_chunks": {"flop": B * Hq * (4 * d * S + 2 * d) * nsel,
+                        "bytes": qbytes + kvbytes + partials},
+        "k_pf_local": {"flop": B * Hq * 4 * d * float(nloc.sum()),
+                       "bytes": qbytes + kvbytes + partials + qbytes + B * Hq * N * 4 + B * Hkv * N * K * 4},
+    }
 
 
 def decode_bytes(B, Hq, Hkv, Hl, ctx, d, S, K, W, elem=2):
@@ -101,6 +131,8 @@ class Timer:
 
 
 def bench_prefill(torch, hils, synth, W_, steps, warmup):
+    """Times `steps` prefill calls (HIP events on the library's stream) with
+    per-kernel timing enabled; returns (params, host inputs, ms/step, kernels)."""
     p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=W_.N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
                     window=W_.window, dtype=W_.dtype)
     nc = p.L // p.chunk
@@ -115,19 +147,23 @@ def bench_prefill(torch, hils, synth, W_, steps, warmup):
     out = torch.empty(p.B, p.Hq, p.N, p.d, dtype=dt, device="cuda")
     lse = torch.empty(p.B, p.Hq, p.N, dtype=torch.float32, device="cuda")
     idx = torch.empty(p.B, p.Hkv, p.N, p.topk, dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(1, hils.hils_workspace_size(p, hils.HILS_OP_PREFILL)), dtype=torch.uint8, device="cuda")
 
     def step():
-        hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], out=out, lse=lse, idx=idx)
+        hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], out=out, lse=lse, idx=idx, workspace=ws)
 
-    timer = Timer(torch)
-    ms = timer.run(step, steps, warmup)
-    pf = hils.Params(**{**p.__dict__, "flags": hils.HILS_FLAG_GIVEN_IDX})
-
-    def attn_only():
-        hils.hils_prefill_fwd(pf, dev["q"], dev["k"], dev["v"], dev["lmk"], out=out, lse=lse, idx=idx)
-
-    ms_attn = timer.run(attn_only, steps, max(1, warmup // 2))
-    return p, host, ms, ms_attn
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    hils.hils_timing_enable(True)
+    ms = Timer(torch).run(step, steps, 0)
+    kernels = hils.hils_timing_read()
+    hils.hils_timing_enable(False)
+    for k in kernels.values():
+        k["avg_ms"] = k["total_ms"] / max(1, k["launches"])
+    del dev, ws
+    torch.cuda.empty_cache()
+    return p, host, ms, kernels
 
 
 def bench_decode(torch, hils, synth, W_, steps, warmup):
@@ -154,12 +190,12 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
         hils.hils_decode_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], seqlens=seqlens, out=out, lse=lse,
                              idx=idx, workspace=ws)
 
-    timer = Timer(torch)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     st = torch.cuda.current_stream()
     total = 0.0
+    hils.hils_timing_enable(True)
     for _ in range(steps):
         torch.sum(flush, dim=0, out=sink)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -168,6 +204,8 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
         e1.record(st)
         torch.cuda.synchronize()
         total += e0.elapsed_time(e1)
+    kernels = hils.hils_timing_read()
+    hils.hils_timing_enable(False)
     ms = total / steps
     nbytes, parts = decode_bytes(p.B, p.Hq, p.Hkv, p.Hq, W_.ctx, p.d, p.chunk, p.topk, p.window)
     del dev, flush, sink
@@ -175,7 +213,8 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
     return {"workload": W_.name, "ms_per_step": round(ms, 4), "tokens_per_s": round(p.B / (ms * 1e-3), 1),
             "algorithmic_bytes": nbytes, "bytes_breakdown": parts,
             "hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-            "frac_hbm_peak": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            "frac_hbm_peak": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "kernels_avg_ms": {k: round(v["total_ms"] / max(1, v["launches"]), 4) for k, v in kernels.items()}}
 
 
 def bench_train(torch, hils, synth, W_, steps, warmup):
@@ -195,7 +234,13 @@ def bench_train(torch, hils, synth, W_, steps, warmup):
         out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"])
         hils.hils_bwd(p, dev["dout"], dev["q"], dev["k"], dev["v"], dev["lmk"], out, lse, idx, workspace=ws)
 
-    ms = Timer(torch).run(step, steps, warmup)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    hils.hils_timing_enable(True)
+    ms = Timer(torch).run(step, steps, 0)
+    kernels = hils.hils_timing_read()
+    hils.hils_timing_enable(False)
     attn, score = prefill_work(p.B, p.Hq, p.Hkv, p.N, p.d, p.chunk, p.topk, p.window)
     fwd = attn + score
     bwd = 2.5 * attn + 2 * score  # dq, dk, dv recompute: 10d vs 4d per attended pair; score grads
@@ -203,7 +248,8 @@ def bench_train(torch, hils, synth, W_, steps, warmup):
     torch.cuda.empty_cache()
     return {"workload": W_.name, "ms_per_step": round(ms, 3), "tokens_per_s": round(p.B * p.N / (ms * 1e-3), 1),
             "algorithmic_tflop": round((fwd + bwd) / 1e12, 3),
-            "mfma_frac_useful": round((fwd + bwd) / (ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 5)}
+            "mfma_frac_useful": round((fwd + bwd) / (ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 5),
+            "kernels_avg_ms": {k: round(v["total_ms"] / max(1, v["launches"]), 3) for k, v in kernels.items()}}
 
 
 def cpu_baseline(W_, host, target_s=20.0):
@@ -237,8 +283,11 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--train", action="store_true")
+    ap.add_argument("--no-train", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first copy 1 GiB device-to-device (a plain copy kernel of known size, used to "
+                         "calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (the operator has no multi-GPU path); "
@@ -251,31 +300,52 @@ def main():
     from paper_2607_02980_amd.configs import WORKLOADS
 
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        x = torch.ones(2 ** 28, dtype=torch.float32, device="cuda")
+        y = x.clone()
+        torch.cuda.synchronize()
+        del x, y
     Wp = WORKLOADS["prefill_32k_bf16"]
-    p, host, ms, ms_attn = bench_prefill(torch, hils, synth, Wp, args.steps, args.warmup)
+    p, host, ms, kernels = bench_prefill(torch, hils, synth, Wp, args.steps, args.warmup)
+    model = prefill_kernel_model(p.B, p.Hq, p.Hkv, p.N, p.L, p.d, p.chunk, p.topk, p.window)
+    table = {}
+    for name, k in kernels.items():
+        row = {"avg_ms": round(k["avg_ms"], 4), "launches": k["launches"]}
+        if name in model:
+            t = k["avg_ms"] * 1e-3
+            f, b = model[name]["flop"], model[name]["bytes"]
+            row.update({"flop": f, "bytes": b, "tflops": round(f / t / 1e12, 2), "gbs": round(b / t / 1e9, 1),
+                        "bound": "mfma" if f / (BF16_MFMA_PEAK_TFLOPS * 1e12) >= b / (HBM_PEAK_GBS * 1e9) else "hbm"})
+        table[name] = row
+    dom = max((n for n in table if n in model), key=lambda n: kernels[n]["total_ms"])
+    d = table[dom]
+    if d["bound"] == "mfma":
+        achieved, peak, unit = d["tflops"], BF16_MFMA_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        achieved, peak, unit = d["gbs"], HBM_PEAK_GBS, "GB/s"
     attn_flops, score_flops = prefill_work(p.B, p.Hq, p.Hkv, p.N, p.d, p.chunk, p.topk, p.window)
-    achieved = attn_flops / (ms_attn * 1e-3) / 1e12
-    traffic = load_traffic("k_attn_rows_prefill_32k_bf16")
     res = {
         "metric": METRIC, "value": round(p.B * p.N / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": Wp.name, "B": p.B, "Hq": p.Hq, "Hkv": p.Hkv, "d": p.d, "seq_len": p.N,
                    "chunk": p.chunk, "topk": p.topk, "window": p.window, "landmark_heads": p.Hq},
-        "roofline": {"bound": "mfma", "kernel": "k_attn_rows", "achieved": round(achieved, 3),
-                     "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 6),
-                     "traffic": traffic, "kernel_ms": round(ms_attn, 4),
-                     "algorithmic_flop_per_launch": attn_flops},
-        "extra": {"prefill_score_topk_ms": round(ms - ms_attn, 4),
-                  "prefill_useful_mfma_frac_whole_step": round((attn_flops + score_flops) / (ms * 1e-3) / 1e12
-                                                               / BF16_MFMA_PEAK_TFLOPS, 6)},
+        "roofline": {"bound": d["bound"], "kernel": dom, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": round(achieved / peak, 5), "traffic": load_traffic(f"{dom}_{Wp.name}"),
+                     "algorithmic_per_launch": {"flop": d["flop"], "bytes": d["bytes"]},
+                     "kernel_avg_ms": d["avg_ms"]},
+        "extra": {"prefill_kernels": table,
+                  "prefill_useful_mfma_frac": round((attn_flops + score_flops) / (ms * 1e-3) / 1e12
+                                                    / BF16_MFMA_PEAK_TFLOPS, 5)},
     }
     del p
     torch.cuda.empty_cache()
     if not args.no_decode:
         res["extra"]["decode"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
                                               max(3, args.steps // 2), 2)
-    if args.train:
+        res["extra"]["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"],
+                                                 max(3, args.steps // 2), 2)
+    if not args.no_train:
         res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], 3, 1)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(Wp, host)

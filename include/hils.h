@@ -25,7 +25,8 @@
  *     unless stated otherwise; `p` (the parameter block) is a HOST pointer.
  *   - The caller owns every buffer.  The library never allocates device
  *     memory, never synchronises the device and keeps no state between calls
- *     other than the thread-local error string.  All work is enqueued on
+ *     other than the thread-local error string (and, only while the optional
+ *     timing mode is enabled, its event records).  All work is enqueued on
  *     `stream` (a hipStream_t; NULL is the default stream) and is complete
  *     when the stream is.
  *   - Layouts are row-major and contiguous ("BHSD"):
@@ -158,6 +159,23 @@ int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* 
              const void* lmk, const float* lmk_bias, const void* q_route, const void* out, const float* lse,
              const int32_t* idx, void* dq, void* dk, void* dv, void* dlmk, float* dlmk_bias, void* dq_route,
              void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Optional per-kernel timing, for profiling (not needed to use the operator).
+ * hils_timing_enable(1) makes every kernel that the library launches from the
+ * calling thread be bracketed by two HIP events on the launch's stream (this
+ * is the one piece of state the library keeps, per thread, while enabled);
+ * hils_timing_enable(0) discards the records.
+ * hils_timing_read() waits for the recorded events, then reports per kernel
+ * name (in first-launch order): names as a '\n'-separated list in `names`
+ * (HOST buffer of names_len bytes, NUL-terminated, may be NULL), the summed
+ * milliseconds in total_ms[k] and the launch count in launches[k] (HOST arrays
+ * of max_kernels entries, may be NULL); *n_kernels receives the number of
+ * distinct kernels.  The records are then cleared.
+ */
+int hils_timing_enable(int on);
+int hils_timing_read(char* names, size_t names_len, float* total_ms, int* launches, int max_kernels,
+                     int* n_kernels);
 
 #ifdef __cplusplus
 }

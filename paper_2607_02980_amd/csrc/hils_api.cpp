@@ -3,8 +3,10 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <string.h>
 
 #include <string>
+#include <vector>
 
 #include "../../include/hils.h"
 #include "hils_internal.hpp"
@@ -12,6 +14,21 @@
 namespace {
 
 thread_local std::string g_err;
+
+struct TimedLaunch {
+    const char* name;
+    hipEvent_t e0, e1;
+};
+thread_local bool g_timing = false;
+thread_local std::vector<TimedLaunch> g_launches;
+
+void release_launches() {
+    for (auto& t : g_launches) {
+        (void)hipEventDestroy(t.e0);
+        (void)hipEventDestroy(t.e1);
+    }
+    g_launches.clear();
+}
 
 int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 int fail(int code, const char* fmt, ...) {
@@ -109,7 +126,66 @@ hils::FwdArgs fwd_args(const hils_params* p, const void* q, const void* k, const
 
 }  // namespace
 
+namespace hils {
+bool timing_on() { return g_timing; }
+void timing_begin(const char* name, hipStream_t s) {
+    TimedLaunch t{name, nullptr, nullptr};
+    if (hipEventCreate(&t.e0) != hipSuccess || hipEventCreate(&t.e1) != hipSuccess) return;
+    (void)hipEventRecord(t.e0, s);
+    g_launches.push_back(t);
+}
+void timing_end(hipStream_t s) {
+    if (!g_launches.empty()) (void)hipEventRecord(g_launches.back().e1, s);
+}
+}  // namespace hils
+
 extern "C" {
+
+int hils_timing_enable(int on) {
+    g_timing = on != 0;
+    if (!g_timing) release_launches();
+    return ok();
+}
+
+int hils_timing_read(char* names, size_t names_len, float* total_ms, int* launches, int max_kernels,
+                     int* n_kernels) {
+    if (!n_kernels) return fail(HILS_ERR_INVALID, "n_kernels is NULL");
+    std::vector<std::string> order;
+    std::vector<float> tot;
+    std::vector<int> cnt;
+    for (auto& t : g_launches) {
+        float ms = 0.f;
+        if (hipEventSynchronize(t.e1) != hipSuccess || hipEventElapsedTime(&ms, t.e0, t.e1) != hipSuccess) {
+            release_launches();
+            return fail(HILS_ERR_HIP, "reading kernel timing events failed");
+        }
+        size_t k = 0;
+        while (k < order.size() && order[k] != t.name) ++k;
+        if (k == order.size()) {
+            order.push_back(t.name);
+            tot.push_back(0.f);
+            cnt.push_back(0);
+        }
+        tot[k] += ms;
+        cnt[k] += 1;
+    }
+    release_launches();
+    *n_kernels = (int)order.size();
+    std::string joined;
+    for (size_t k = 0; k < order.size() && (int)k < max_kernels; ++k) {
+        if (total_ms) total_ms[k] = tot[k];
+        if (launches) launches[k] = cnt[k];
+        joined += order[k];
+        joined += '\n';
+    }
+    if (names && names_len) {
+        const size_t n = joined.size() < names_len - 1 ? joined.size() : names_len - 1;
+        memcpy(names, joined.data(), n);
+        names[n] = 0;
+    }
+    return ok();
+}
+
 
 int hils_version(void) { return 100; }
 

@@ -348,12 +348,12 @@ void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStr
     const size_t ncnt = (size_t)a.B * a.Hkv * nC;
     const unsigned gc = (unsigned)((ncnt + kBlock - 1) / kBlock);
     const dim3 grows((a.N + kInvRows - 1) / kInvRows, a.B * a.Hkv);
-    hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, counts, ncnt, 0);
-    hipLaunchKernelGGL(k_fill_i32, dim3(gc), dim3(kBlock), 0, s, cursor, ncnt, 0);
-    hipLaunchKernelGGL(k_inv_count, grows, dim3(kBlock), 0, s, a, counts);
-    hipLaunchKernelGGL(k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, offsets, nC);
-    hipLaunchKernelGGL(k_inv_fill, grows, dim3(kBlock), 0, s, a, (const int*)offsets, cursor, list);
-    hipLaunchKernelGGL(k_inv_work, dim3(1), dim3(kBlock), 0, s, (const int*)offsets, a.B * a.Hkv, nC,
+    HILS_LAUNCH("k_fill_i32", k_fill_i32, dim3(gc), dim3(kBlock), 0, s, counts, ncnt, 0);
+    HILS_LAUNCH("k_fill_i32", k_fill_i32, dim3(gc), dim3(kBlock), 0, s, cursor, ncnt, 0);
+    HILS_LAUNCH("k_inv_count", k_inv_count, grows, dim3(kBlock), 0, s, a, counts);
+    HILS_LAUNCH("k_inv_scan", k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, offsets, nC);
+    HILS_LAUNCH("k_inv_fill", k_inv_fill, grows, dim3(kBlock), 0, s, a, (const int*)offsets, cursor, list);
+    HILS_LAUNCH("k_inv_work", k_inv_work, dim3(1), dim3(kBlock), 0, s, (const int*)offsets, a.B * a.Hkv, nC,
                        reinterpret_cast<int4*>(base + w.work), reinterpret_cast<int*>(base + w.nwork));
 }
 
@@ -566,8 +566,8 @@ struct BwdRun {
         const int nC = a.L / kChunk;
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
         launch_inverse_index(ia, w, a.ws, s);
-        hipLaunchKernelGGL((k_bwd_dq_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
-        hipLaunchKernelGGL((k_bwd_dkdv_chunks<T, D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a,
+        HILS_LAUNCH("k_bwd_dq_rows", (k_bwd_dq_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        HILS_LAUNCH("k_bwd_dkdv_chunks", (k_bwd_dkdv_chunks<T, D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a,
                            offsets, list);
         return hipGetLastError();
     }

@@ -474,11 +474,11 @@ struct DecRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
         const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
-        hipLaunchKernelGGL((k_dec_scan_local<T, D, G>), dim3(ly.nslices + ly.nlocal, a.Hkv, a.B), dim3(kBlock), 0,
+        HILS_LAUNCH("k_dec_scan_local", (k_dec_scan_local<T, D, G>), dim3(ly.nslices + ly.nlocal, a.Hkv, a.B), dim3(kBlock), 0,
                            s, a);
-        if (!a.given_idx) hipLaunchKernelGGL((k_dec_merge<G, D>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
-        hipLaunchKernelGGL((k_dec_chunks<T, D, G>), dim3(a.K, a.Hkv, a.B), dim3(kBlock), 0, s, a);
-        hipLaunchKernelGGL((k_dec_combine<T, D, G>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        if (!a.given_idx) HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        HILS_LAUNCH("k_dec_chunks", (k_dec_chunks<T, D, G>), dim3(a.K, a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }
 };

@@ -242,9 +242,9 @@ struct FwdRun {
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
         if (!a.given_idx) {
             const long rows = (long)a.B * a.Hkv * a.N;
-            hipLaunchKernelGGL((k_score_topk_rows<T, D, G>), dim3((unsigned)((rows + 3) / 4)), dim3(kBlock), 0, s, a);
+            HILS_LAUNCH("k_score_topk_rows", (k_score_topk_rows<T, D, G>), dim3((unsigned)((rows + 3) / 4)), dim3(kBlock), 0, s, a);
         }
-        hipLaunchKernelGGL((k_attn_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        HILS_LAUNCH("k_attn_rows", (k_attn_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }
 };

@@ -54,6 +54,20 @@ struct BwdArgs {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Optional per-kernel timing (hils_timing_enable): every launch is bracketed by
+// HIP events on its stream when timing is on for the calling thread.
+bool timing_on();
+void timing_begin(const char* name, hipStream_t s);
+void timing_end(hipStream_t s);
+
+#define HILS_LAUNCH(NAME, KERNEL, GRID, BLOCK, LDS, STREAM, ...)              \
+    do {                                                                       \
+        const bool hils_timed_ = ::hils::timing_on();                          \
+        if (hils_timed_) ::hils::timing_begin(NAME, STREAM);                   \
+        hipLaunchKernelGGL(KERNEL, GRID, BLOCK, LDS, STREAM, __VA_ARGS__);     \
+        if (hils_timed_) ::hils::timing_end(STREAM);                           \
+    } while (0)
+
 // Inverse index of a selection: for every (b, g, chunk) the rows n that chose it.
 struct InvArgs {
     const int32_t* idx;

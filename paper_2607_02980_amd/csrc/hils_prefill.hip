@@ -531,18 +531,18 @@ struct PfRun {
         float* wgt = reinterpret_cast<float*>(ws + ly.wgt);
         float* ref = reinterpret_cast<float*>(ws + ly.ref);
         if (a.given_idx) {
-            hipLaunchKernelGGL((k_pf_ref_given<D, G>), dim3(a.N, a.Hkv, a.B), dim3(kWave), 0, s, a, ref);
+            HILS_LAUNCH("k_pf_ref_given", (k_pf_ref_given<D, G>), dim3(a.N, a.Hkv, a.B), dim3(kWave), 0, s, a, ref);
         } else {
-            hipLaunchKernelGGL((k_pf_score<D, G>), dim3((a.N + kSQ - 1) / kSQ, a.Hkv, a.B), dim3(kBlock), 0, s, a,
+            HILS_LAUNCH("k_pf_score", (k_pf_score<D, G>), dim3((a.N + kSQ - 1) / kSQ, a.Hkv, a.B), dim3(kBlock), 0, s, a,
                                ref);
         }
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
         launch_inverse_index(ia, ly.inv, a.ws, s);
-        hipLaunchKernelGGL((k_pf_chunks<D, G>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
+        HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
                            reinterpret_cast<const int*>(ws + ly.inv.offsets), reinterpret_cast<const int*>(ws + ly.inv.list),
                            reinterpret_cast<const int4*>(ws + ly.inv.work), reinterpret_cast<const int*>(ws + ly.inv.nwork),
                            (const float*)ref, part, wgt);
-        hipLaunchKernelGGL((k_pf_local<D, G>), dim3((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B),
+        HILS_LAUNCH("k_pf_local", (k_pf_local<D, G>), dim3((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B),
                            dim3(kBlock), 0, s, a, (const float*)ref, (const bf16*)part, (const float*)wgt);
         return hipGetLastError();
     }

@@ -49,7 +49,11 @@ def _load():
     lib.hils_prefill_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_decode_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_bwd.argtypes = [P] + [vp] * 17 + [sz, vp]
-    for f in (lib.hils_workspace_size, lib.hils_prefill_fwd, lib.hils_decode_fwd, lib.hils_bwd):
+    lib.hils_timing_enable.argtypes = [ctypes.c_int]
+    lib.hils_timing_read.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(ctypes.c_float),
+                                     ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
+    for f in (lib.hils_workspace_size, lib.hils_prefill_fwd, lib.hils_decode_fwd, lib.hils_bwd,
+              lib.hils_timing_enable, lib.hils_timing_read):
         f.restype = ctypes.c_int
     return lib
 
@@ -210,3 +214,20 @@ def hils_bwd(p: Params, dout, q, k, v, lmk, out, lse, idx, lmk_bias=None, q_rout
         _ptr(dlmk, "dlmk"), _ptr(dbias, "dbias", required=False), _ptr(dqr, "dq_route", required=False),
         _ptr(ws, "workspace"), n, _stream()))
     return {"dq": dq, "dk": dk, "dv": dv, "dlmk": dlmk, "dlmk_bias": dbias, "dq_route": dqr}
+
+
+def hils_timing_enable(on: bool = True) -> None:
+    """Bracket every library kernel launch of this thread with HIP events."""
+    _check(LIB.hils_timing_enable(int(bool(on))))
+
+
+def hils_timing_read(max_kernels: int = 64) -> dict:
+    """Per kernel name: {"launches": n, "total_ms": t} for the launches recorded
+    since timing was enabled (or last read); clears the records."""
+    names = ctypes.create_string_buffer(4096)
+    ms = (ctypes.c_float * max_kernels)()
+    cnt = (ctypes.c_int * max_kernels)()
+    nk = ctypes.c_int(0)
+    _check(LIB.hils_timing_read(names, 4096, ms, cnt, max_kernels, ctypes.byref(nk)))
+    keys = [k for k in names.value.decode().split("\n") if k]
+    return {k: {"launches": cnt[i], "total_ms": ms[i]} for i, k in enumerate(keys[: nk.value])}

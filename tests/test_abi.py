@@ -156,3 +156,9 @@ def test_error_string_is_thread_local(hils):
     t.join()
     assert seen["msg"] == ""
     assert "chunk" in hils.hils_last_error()
+
+
+def test_timing_mode_without_launches(hils):
+    hils.hils_timing_enable(True)
+    assert hils.hils_timing_read() == {}
+    hils.hils_timing_enable(False)

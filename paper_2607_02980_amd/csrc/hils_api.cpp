@@ -84,6 +84,8 @@ int check_params(const hils_params* p, int op) {
 size_t ws_bytes_for(const hils_params* p, int op) {
     switch (op) {
         case HILS_OP_BWD:
+            if (p->dtype == HILS_BF16)
+                return hils::bwd_mfma_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk);
             return hils::bwd_workspace_layout(p->B, p->Hkv, p->N, p->L, p->topk).total;
         case HILS_OP_DECODE:
             return hils::decode_workspace_bytes(p->B, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window);

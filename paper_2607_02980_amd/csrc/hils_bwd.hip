@@ -1,4 +1,5 @@
-// HiLS attention backward kernels, gfx950.
+// HiLS attention backward for fp32 storage (VALU), and the inverse index that the
+// bf16 backward (MFMA) and the bf16 prefill share, gfx950.
 //
 // With g = dO and u = g . out for a (row, head), and L its fusion LSE:
 //   local key j:     w_j = exp(s_j - L);  dv_j += w_j g;  ds_j = w_j (g.v_j - u)
@@ -15,6 +16,8 @@
 //   k_bwd_dkdv_chunks  key-major: dk, dv of one chunk from the rows whose local window
 //                      covers it and from the rows that retrieved it, plus dk', db'
 // Everything is accumulated on chip and written once; no floating-point atomics.
+#include <type_traits>
+
 #include "hils_device.hpp"
 #include "hils_dispatch.hpp"
 #include "hils_internal.hpp"
@@ -338,7 +341,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_work(const int* offsets, int nbg
     }
 }
 
-void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStream_t s) {
+void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStream_t s, bool work_list) {
     char* base = static_cast<char*>(ws);
     int* counts = reinterpret_cast<int*>(base + w.counts);
     int* offsets = reinterpret_cast<int*>(base + w.offsets);
@@ -353,7 +356,8 @@ void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStr
     HILS_LAUNCH("k_inv_count", k_inv_count, grows, dim3(kBlock), 0, s, a, counts);
     HILS_LAUNCH("k_inv_scan", k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, offsets, nC);
     HILS_LAUNCH("k_inv_fill", k_inv_fill, grows, dim3(kBlock), 0, s, a, (const int*)offsets, cursor, list);
-    HILS_LAUNCH("k_inv_work", k_inv_work, dim3(1), dim3(kBlock), 0, s, (const int*)offsets, a.B * a.Hkv, nC,
+    if (work_list)
+        HILS_LAUNCH("k_inv_work", k_inv_work, dim3(1), dim3(kBlock), 0, s, (const int*)offsets, a.B * a.Hkv, nC,
                        reinterpret_cast<int4*>(base + w.work), reinterpret_cast<int*>(base + w.nwork));
 }
 
@@ -559,6 +563,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dkdv_chunks(BwdArgs a, const int
 struct BwdRun {
     template <typename T, int D, int G>
     static hipError_t run(const BwdArgs& a, hipStream_t s) {
+        if constexpr (!std::is_same<T, float>::value) return hipErrorInvalidValue;  // bf16: launch_bwd_mfma
         const InvLayout w = inv_layout(a.B, a.Hkv, a.N, a.L, a.K, 0);
         char* ws = static_cast<char*>(a.ws);
         const int* offsets = reinterpret_cast<const int*>(ws + w.offsets);
@@ -573,6 +578,9 @@ struct BwdRun {
     }
 };
 
-hipError_t launch_bwd(const BwdArgs& a, hipStream_t s) { return dispatch<BwdRun>(a.bf16, a.d, a.Hq / a.Hkv, a, s); }
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t s) {
+    if (a.bf16) return launch_bwd_mfma(a, s);
+    return dispatch<BwdRun>(0, a.d, a.Hq / a.Hkv, a, s);
+}
 
 }  // namespace hils

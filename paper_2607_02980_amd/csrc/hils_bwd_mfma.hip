@@ -1,0 +1,692 @@
+// HiLS attention backward on MFMA (bf16 storage, fp32 accumulation), gfx950.
+//
+// The gradient of Eq. (10) with the selection held fixed.  With g = dO_i,
+// u = g . out_i and L = the forward's fusion log-sum-exp of a (row, head):
+//   local key j:    w_j = exp(s_j - L);  dv_j += w_j g;  ds_j = w_j (g.v_j - u)
+//   chunk c, key j: p_j = exp(s_j - lse_c), a_c = exp(s^_c - L), u_c = sum_j p_j g.v_j,
+//                   dv_j += a_c p_j g;  ds_j = a_c p_j (g.v_j - u_c);  ds^_c = a_c (u_c - u)
+//   dq += scale ds_j k_j;  dk_j += scale ds_j q;  dq^ += scale ds^_c k'_c;
+//   dk'_c += scale ds^_c q^;  db'_c += ds^_c
+//
+// Kernels (one launch each, in this order):
+//   k_bwd_u        u per (row, head)
+//   inverse index  the rows that retrieved each (b, g, chunk); k_inv_sort puts every
+//                  list in ascending row order so that the sums below have one order
+//   k_bwd_keys     one block per (b, g, chunk c), 64 (row, head) pairs per step: first
+//                  the rows whose local window covers keys of c, then the rows that
+//                  retrieved c.  Phase 1, one 16-pair tile per wave: S^T = K Q^T and
+//                  GV^T = V dO^T on MFMA, the softmax terms, ds; for retrieving rows also
+//                  the chunk's share of dq (K^T ds^T, stored as a bf16 partial of the
+//                  row's slot) and ds^_c.  Phase 2, one 16-key block per wave: dK and dV
+//                  as MFMA reductions over the step's 64 pairs, read back from LDS.
+//                  dk, dv, dk', db' of chunk c are written once (no atomics).
+//   k_bwd_dq       query-major: dq over the local window (the forward's local tile with
+//                  ds in place of p), plus the row's slot partials and scale ds^ k'.
+#include "hils_device.hpp"
+#include "hils_dispatch.hpp"
+#include "hils_internal.hpp"
+#include "hils_mfma.hpp"
+
+namespace hils {
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kPairs = 64;          // (row, head) pairs per step of k_bwd_keys
+constexpr int kSortWin = 8192;      // rows per bitmap pass of k_inv_sort
+constexpr int kSortWords = kSortWin / 32;
+static_assert(kSortWords % 256 == 0, "k_inv_sort scans whole runs of words per thread");
+
+struct BwLayout {
+    size_t u, dqp, dsh, sorted, inv_base;
+    InvLayout inv;
+    size_t total;
+};
+
+// u [B, Hq, N] f32 | dq partials [B, Hq, N, K, d] bf16 | ds^ [B, Hq, N, K] f32 |
+// sorted lists [B, Hkv, N*K] i32 | inverse index
+BwLayout bw_layout(int B, int Hq, int Hkv, int N, int L, int d, int K) {
+    BwLayout w;
+    w.u = 0;
+    w.dqp = align256(w.u + (size_t)B * Hq * N * sizeof(float));
+    w.dsh = align256(w.dqp + (size_t)B * Hq * N * K * d * sizeof(uint16_t));
+    w.sorted = align256(w.dsh + (size_t)B * Hq * N * K * sizeof(float));
+    w.inv_base = align256(w.sorted + (size_t)B * Hkv * N * K * sizeof(int));
+    w.inv = inv_layout(B, Hkv, N, L, K, w.inv_base);
+    w.total = w.inv.end;
+    return w;
+}
+
+template <int D>
+struct BT {
+    static constexpr int KS = D / 32;    // 32-wide k-steps over the head dim
+    static constexpr int DB = D / 16;    // 16-wide blocks of the head dim
+    static constexpr int KROW = D + 8;   // padded K / V row (bf16)
+    static constexpr int TROW = 64 + 8;  // padded transposed row: 64 keys or 64 pairs
+};
+
+__device__ __forceinline__ uint16_t bfbits(float x) { return from_f32<bf16>(x).bits; }
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+    return (uint32_t)bfbits(lo) | ((uint32_t)bfbits(hi) << 16);
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Stage K rows, V rows and K^T of 64 keys.
+template <int D>
+__device__ __forceinline__ void stage_k_v_kt(const bf16* kb, const bf16* vb, bf16* s_k, bf16* s_v, bf16* s_kt) {
+    constexpr int KROW = BT<D>::KROW, TROW = BT<D>::TROW;
+    constexpr int PPT = kChunk * D / 8 / kBlock;
+    const int tid = threadIdx.x;
+    uint4 xk[PPT], xv[PPT];
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+        const int e = tid + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+        xk[u] = *reinterpret_cast<const uint4*>(kb + (size_t)j * D + d8);
+        xv[u] = *reinterpret_cast<const uint4*>(vb + (size_t)j * D + d8);
+    }
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+        const int e = tid + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+        *reinterpret_cast<uint4*>(s_k + j * KROW + d8) = xk[u];
+        *reinterpret_cast<uint4*>(s_v + j * KROW + d8) = xv[u];
+        const uint32_t w[4] = {xk[u].x, xk[u].y, xk[u].z, xk[u].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            s_kt[(d8 + 2 * t) * TROW + j].bits = (uint16_t)(w[t] & 0xffffu);
+            s_kt[(d8 + 2 * t + 1) * TROW + j].bits = (uint16_t)(w[t] >> 16);
+        }
+    }
+}
+
+// Operand (A or B) read from a padded row-major tile: rows r0 + l%16, the 8
+// consecutive columns k0 + (l/16)*8 ...
+template <int ROW>
+__device__ __forceinline__ bf16x8 row_operand(const bf16* base, int r0, int k0, int lane) {
+    return ld_bf16x8(base + (r0 + lane % 16) * ROW + k0 + (lane / 16) * 8);
+}
+
+// A operand over 32 keys in the order in which S^T accumulators hold them: rows
+// m0 + l%16 of a [m][64 keys] tile, keys 32t + (l/16)*4 + {0..3} then 32t + 16 + (l/16)*4 + {0..3}.
+template <int ROW>
+__device__ __forceinline__ bf16x8 perm_operand(const bf16* base, int m0, int t, int lane) {
+    const bf16* r = base + (m0 + lane % 16) * ROW + 32 * t + (lane / 16) * 4;
+    const uint2 lo = *reinterpret_cast<const uint2*>(r);
+    const uint2 hi = *reinterpret_cast<const uint2*>(r + 16);
+    return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+}
+
+// The matching B operand from two S^T accumulator blocks (keys 32t.. and 32t+16..).
+__device__ __forceinline__ bf16x8 pack_perm(const float* e0, const float* e1) {
+    const float x[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
+    return pack_bf16x8(x);
+}
+
+// ---------------------------------------------------------------------------
+// u = dO . out, one wave per (row, head)
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_bwd_u(BwdArgs a, float* u) {
+    const size_t rows = (size_t)a.B * a.Hq * a.N;
+    const size_t r = (size_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    if (r >= rows) return;
+    float acc = 0.f;
+    for (int d = lane * 2; d < D; d += 2 * kWave) {
+        const uint32_t go = *reinterpret_cast<const uint32_t*>(as<bf16>(a.dout) + r * D + d);
+        const uint32_t oo = *reinterpret_cast<const uint32_t*>(as<bf16>(a.out) + r * D + d);
+        acc += bf_lo(go) * bf_lo(oo) + bf_hi(go) * bf_hi(oo);
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) u[r] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// Ascending-row copy of every (b, g, chunk) list.  Rows in a list are distinct
+// (a row names a chunk at most once), so a bitmap over rows gives each entry its
+// rank; rows are taken in windows of kSortWin.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void k_inv_sort(const int* offsets, const int* list, int* sorted, int N, int K,
+                                                     int nC, int W) {
+    __shared__ uint32_t s_bits[kSortWords];
+    __shared__ int s_pre[kSortWords];
+    __shared__ int s_wave[kBlock / kWave];
+    const int c = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+    const int beg = offsets[(size_t)bg * (nC + 1) + c];
+    const int len = offsets[(size_t)bg * (nC + 1) + c + 1] - beg;
+    if (len == 0) return;
+    const int* src = list + (size_t)bg * N * K + beg;
+    int* dst = sorted + (size_t)bg * N * K + beg;
+    // the first row whose candidate set contains c
+    const int row_lo = min(N, max(0, (c + 1) * kChunk + W - 1));
+    int base = 0;
+    for (int w0 = row_lo; w0 < N; w0 += kSortWin) {
+        for (int i = tid; i < kSortWords; i += kBlock) s_bits[i] = 0u;
+        __syncthreads();
+        for (int e = tid; e < len; e += kBlock) {
+            const int n = (src[e] >> 6) - w0;
+            if (n >= 0 && n < kSortWin) atomicOr(&s_bits[n >> 5], 1u << (n & 31));
+        }
+        __syncthreads();
+        // exclusive prefix of the word popcounts: each thread scans a run of words
+        constexpr int PER = kSortWords / kBlock;
+        int run = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) run += __popc(s_bits[tid * PER + i]);
+        int incl = run;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int y = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += y;
+        }
+        if (lane == kWave - 1) s_wave[w] = incl;
+        __syncthreads();
+        int excl = incl - run;
+        for (int i = 0; i < w; ++i) excl += s_wave[i];
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            s_pre[tid * PER + i] = excl;
+            excl += __popc(s_bits[tid * PER + i]);
+        }
+        int total = 0;
+        for (int i = 0; i < kBlock / kWave; ++i) total += s_wave[i];
+        __syncthreads();
+        for (int e = tid; e < len; e += kBlock) {
+            const int ent = src[e];
+            const int n = (ent >> 6) - w0;
+            if (n >= 0 && n < kSortWin) {
+                const int wd = n >> 5;
+                dst[base + s_pre[wd] + __popc(s_bits[wd] & ((1u << (n & 31)) - 1u))] = ent;
+            }
+        }
+        base += total;
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Key-major pass: dK, dV, dK', db' of one chunk and the retrieved chunks' dq partials
+// ---------------------------------------------------------------------------
+template <int D>
+struct KeySmem {
+    static constexpr int KROW = BT<D>::KROW, TROW = BT<D>::TROW;
+    bf16 k[kChunk * KROW];
+    bf16 v[kChunk * KROW];
+    bf16 kt[D * TROW];
+    bf16 qt[D * TROW];        // Q^T of the step's pairs: [d][pair]
+    bf16 dot[D * TROW];       // dO^T, same layout
+    bf16 pt[kChunk * TROW];   // dV weights, transposed: [key][pair]
+    bf16 dst[kChunk * TROW];  // ds, transposed: [key][pair]
+    float dsh[kPairs];        // ds^_c per pair (retrieval steps)
+    int rows[kPairs];
+    int slots[kPairs];
+};
+
+template <int D, int G>
+__global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offsets, const int* sorted, const float* u,
+                                                     bf16* dqp, float* dshat) {
+    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, TROW = BT<D>::TROW, KROW = BT<D>::KROW;
+    constexpr int R = kPairs / G;              // rows per step
+    constexpr int HT = G > 4 ? G / 4 : 1;      // heads in one wave's 16-pair tile
+    __shared__ __align__(16) KeySmem<D> sm;
+    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int nC = a.L / kChunk;
+    const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const size_t bg = (size_t)b * a.Hkv + g;
+    const int j0 = c * kChunk;
+    const bool per_head_lmk = (a.Hl == a.Hq);
+    const bf16* qb = as<bf16>(a.q);
+    const bf16* gob = as<bf16>(a.dout);
+    const bf16* rb = as<bf16>(a.q_route ? a.q_route : a.q);
+    stage_k_v_kt<D>(as<bf16>(a.k) + (bg * a.L + j0) * D, as<bf16>(a.v) + (bg * a.L + j0) * D, sm.k, sm.v, sm.kt);
+
+    // this lane's pair in phase 1 and the first head of the wave's tile
+    const int pair = w * 16 + lane % 16;
+    const int hh = pair / R, r = pair % R;
+    const int h = g * G + hh;
+    const int hfirst = (w * 16) / R;
+    const int hl = per_head_lmk ? h : g;
+
+    f32x4 dk[DB], dv[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dk[db] = dv[db] = zero4();
+    float dl[HT][2], dbias[HT];
+#pragma unroll
+    for (int t = 0; t < HT; ++t) dl[t][0] = dl[t][1] = dbias[t] = 0.f;
+
+    const int n_lo = j0, n_hi = min(a.N - 1, j0 + kChunk + a.W - 2);
+    const int nlocal = max(0, n_hi - n_lo + 1);
+    const int beg = offsets[bg * (nC + 1) + c];
+    const int nret = offsets[bg * (nC + 1) + c + 1] - beg;
+    const int* seg = sorted + bg * a.N * a.K + beg;
+    const int nsteps_local = (nlocal + R - 1) / R;
+    const int nsteps = nsteps_local + (nret + R - 1) / R;
+
+    for (int st = 0; st < nsteps; ++st) {
+        const bool retrieval = st >= nsteps_local;
+        __syncthreads();  // the previous step's tiles are consumed
+        if (tid < R) {
+            int n = -1, slot = 0;
+            if (!retrieval) {
+                const int e = st * R + tid;
+                if (e < nlocal) n = n_lo + e;
+            } else {
+                const int e = (st - nsteps_local) * R + tid;
+                if (e < nret) {
+                    n = seg[e] >> 6;
+                    slot = seg[e] & 63;
+                }
+            }
+            sm.rows[tid] = n;
+            sm.slots[tid] = slot;
+        }
+        __syncthreads();
+
+        // ---- phase 1: this wave's 16 pairs against the 64 keys ----
+        const int qn = sm.rows[r];
+        const bool qv = qn >= 0;
+        const size_t qrow = ((size_t)b * a.Hq + h) * a.N + (qv ? qn : 0);
+        bf16x8 bq[KS], bo[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int d0 = ks * 32 + (lane / 16) * 8;
+            const uint4 uq = qv ? *reinterpret_cast<const uint4*>(qb + qrow * D + d0) : make_uint4(0, 0, 0, 0);
+            const uint4 uo = qv ? *reinterpret_cast<const uint4*>(gob + qrow * D + d0) : make_uint4(0, 0, 0, 0);
+            bq[ks] = as_bf16x8(uq);
+            bo[ks] = as_bf16x8(uo);
+            const uint32_t wq[4] = {uq.x, uq.y, uq.z, uq.w}, wo[4] = {uo.x, uo.y, uo.z, uo.w};
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                sm.qt[(d0 + 2 * t) * TROW + pair].bits = (uint16_t)(wq[t] & 0xffffu);
+                sm.qt[(d0 + 2 * t + 1) * TROW + pair].bits = (uint16_t)(wq[t] >> 16);
+                sm.dot[(d0 + 2 * t) * TROW + pair].bits = (uint16_t)(wo[t] & 0xffffu);
+                sm.dot[(d0 + 2 * t + 1) * TROW + pair].bits = (uint16_t)(wo[t] >> 16);
+            }
+        }
+        f32x4 s4[4], gv4[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            s4[kb] = zero4();
+            gv4[kb] = zero4();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                s4[kb] = mfma16x16x32(row_operand<KROW>(sm.k, kb * 16, ks * 32, lane), bq[ks], s4[kb]);
+                gv4[kb] = mfma16x16x32(row_operand<KROW>(sm.v, kb * 16, ks * 32, lane), bo[ks], gv4[kb]);
+            }
+        }
+        const float Lr = qv ? a.lse[qrow] : 0.f;
+        const float ub = qv ? u[qrow] : 0.f;
+        float pw[4][4], ds[4][4];
+        if (!retrieval) {
+            const int ell = n_candidates(qn, a.W) * kChunk;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int j = j0 + kb * 16 + (lane / 16) * 4 + i;
+                    const bool valid = qv && j <= qn && j >= ell;
+                    const float wgt = valid ? fexp(a.scale * s4[kb][i] - Lr) : 0.f;
+                    pw[kb][i] = wgt;
+                    ds[kb][i] = wgt * (gv4[kb][i] - ub);
+                }
+        } else {
+            // surrogate score s^_c of the pair: lanes hold 8*KS dims each
+            const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
+            float part = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const int d0 = ks * 32 + (lane / 16) * 8;
+                const uint4 lv = *reinterpret_cast<const uint4*>(lrow + d0);
+                const uint4 qq = a.q_route ? (qv ? *reinterpret_cast<const uint4*>(rb + qrow * D + d0)
+                                                 : make_uint4(0, 0, 0, 0))
+                                           : __builtin_bit_cast(uint4, bq[ks]);
+                const uint32_t lw[4] = {lv.x, lv.y, lv.z, lv.w}, qw[4] = {qq.x, qq.y, qq.z, qq.w};
+#pragma unroll
+                for (int t = 0; t < 4; ++t) part += bf_lo(lw[t]) * bf_lo(qw[t]) + bf_hi(lw[t]) * bf_hi(qw[t]);
+            }
+            part += __shfl_xor(part, 16, kWave);
+            part += __shfl_xor(part, 32, kWave);
+            const float shat = a.scale * part + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f);
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, a.scale * s4[kb][i]);
+            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+            float sum = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pw[kb][i] = fexp(a.scale * s4[kb][i] - mx);
+                    sum += pw[kb][i];
+                }
+            sum += __shfl_xor(sum, 16, kWave);
+            sum += __shfl_xor(sum, 32, kWave);
+            const float inv = 1.f / sum;
+            float uc = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pw[kb][i] *= inv;
+                    uc += pw[kb][i] * gv4[kb][i];
+                }
+            uc += __shfl_xor(uc, 16, kWave);
+            uc += __shfl_xor(uc, 32, kWave);
+            const float al = qv ? fexp(shat - Lr) : 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    ds[kb][i] = al * pw[kb][i] * (gv4[kb][i] - uc);
+                    pw[kb][i] *= al;
+                }
+            const float dsh = al * (uc - ub);
+            if (lane < 16) sm.dsh[pair] = dsh;
+            if (qv && lane < 16) dshat[qrow * a.K + sm.slots[r]] = dsh;
+        }
+        // dV weights and ds, transposed, for phase 2
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int key = kb * 16 + (lane / 16) * 4 + i;
+                sm.pt[key * TROW + pair].bits = bfbits(pw[kb][i]);
+                sm.dst[key * TROW + pair].bits = bfbits(ds[kb][i]);
+            }
+        if (retrieval) {
+            // the chunk's share of dq: dq^T = scale K^T ds^T, into the row's slot partial
+            const bf16x8 b0 = pack_perm(ds[0], ds[1]);
+            const bf16x8 b1 = pack_perm(ds[2], ds[3]);
+            bf16* prow = dqp + (qrow * a.K + sm.slots[r]) * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                f32x4 o = zero4();
+                o = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 0, lane), b0, o);
+                o = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 1, lane), b1, o);
+                if (qv)
+                    *reinterpret_cast<uint2*>(prow + db * 16 + (lane / 16) * 4) =
+                        make_uint2(pack2(a.scale * o[0], a.scale * o[1]), pack2(a.scale * o[2], a.scale * o[3]));
+            }
+            // dk' and db': lanes own dims 2*lane, 2*lane+1; the tile's 16 pairs in order
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (2 * lane < D) {
+                for (int p = 0; p < 16; ++p) {
+                    const int pp = w * 16 + p;
+                    const int nr = sm.rows[pp % R];
+                    if (nr < 0) continue;
+                    const int ht = pp / R - hfirst;
+                    const float x = sm.dsh[pp];
+                    const uint32_t qq = *reinterpret_cast<const uint32_t*>(
+                        rb + (((size_t)b * a.Hq + g * G + pp / R) * a.N + nr) * D + 2 * lane);
+#pragma unroll
+                    for (int t = 0; t < HT; ++t)
+                        if (t == ht) {
+                            dl[t][0] += x * bf_lo(qq);
+                            dl[t][1] += x * bf_hi(qq);
+                            dbias[t] += x;
+                        }
+                }
+            }
+        }
+        __syncthreads();
+        // ---- phase 2: keys [16w, 16w+16) x all dims, reduced over the 64 pairs ----
+        bf16x8 ak[2], av[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            ak[t] = row_operand<TROW>(sm.dst, w * 16, t * 32, lane);
+            av[t] = row_operand<TROW>(sm.pt, w * 16, t * 32, lane);
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                dk[db] = mfma16x16x32(ak[t], row_operand<TROW>(sm.qt, db * 16, t * 32, lane), dk[db]);
+                dv[db] = mfma16x16x32(av[t], row_operand<TROW>(sm.dot, db * 16, t * 32, lane), dv[db]);
+            }
+    }
+
+    // ---- dK, dV of the chunk (lane: key 16w + (l/16)*4 + i, dim 16db + l%16) ----
+    bf16* dkp = as_mut<bf16>(a.dk) + (bg * a.L + j0) * D;
+    bf16* dvp = as_mut<bf16>(a.dv) + (bg * a.L + j0) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int key = w * 16 + (lane / 16) * 4 + i, d = db * 16 + lane % 16;
+            dkp[key * D + d] = from_f32<bf16>(a.scale * dk[db][i]);
+            dvp[key * D + d] = from_f32<bf16>(dv[db][i]);
+        }
+    // ---- dK', db': per-wave sums, then per landmark head ----
+    __syncthreads();
+    float* s_red = reinterpret_cast<float*>(sm.qt);  // [4 waves][HT][D]
+    float* s_rb = reinterpret_cast<float*>(sm.pt);   // [4 waves][HT]
+#pragma unroll
+    for (int t = 0; t < HT; ++t) {
+        if (2 * lane < D) {
+            s_red[(w * HT + t) * D + 2 * lane] = a.scale * dl[t][0];
+            s_red[(w * HT + t) * D + 2 * lane + 1] = a.scale * dl[t][1];
+        }
+        if (lane == 0) s_rb[w * HT + t] = dbias[t];
+    }
+    __syncthreads();
+    // head hh sits in the waves ww with hfirst(ww) <= hh < hfirst(ww) + HT
+    auto head_sum = [&](int head, int d) {
+        float v = 0.f;
+        for (int ww = 0; ww < 4; ++ww) {
+            const int t = head - (ww * 16) / R;
+            if (t >= 0 && t < HT) v += d >= 0 ? s_red[(ww * HT + t) * D + d] : s_rb[ww * HT + t];
+        }
+        return v;
+    };
+    const int nLH = per_head_lmk ? G : 1;
+    for (int e = tid; e < nLH * D; e += kBlock) {
+        const int lh = e / D, d = e % D;
+        float v = 0.f;
+        if (per_head_lmk) {
+            v = head_sum(lh, d);
+        } else {
+            for (int head = 0; head < G; ++head) v += head_sum(head, d);
+        }
+        const int hl_out = per_head_lmk ? g * G + lh : g;
+        as_mut<bf16>(a.dlmk)[(((size_t)b * a.Hl + hl_out) * nC + c) * D + d] = from_f32<bf16>(v);
+    }
+    if (a.dbias && tid < nLH) {
+        float v = 0.f;
+        if (per_head_lmk) {
+            v = head_sum(tid, -1);
+        } else {
+            for (int head = 0; head < G; ++head) v += head_sum(head, -1);
+        }
+        const int hl_out = per_head_lmk ? g * G + tid : g;
+        a.dbias[((size_t)b * a.Hl + hl_out) * nC + c] = v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Query-major dq: local window, then the row's retrieved-chunk partials
+// ---------------------------------------------------------------------------
+template <int G>
+struct DqCfg {
+    static constexpr int QB = 8 / G;          // 16-row blocks per workgroup
+    static constexpr int QT = 16 * QB;        // rows per workgroup
+    static constexpr int ITEMS = G * QB;      // (head, 16-row block) items: 8
+    static constexpr int IPW = ITEMS / 4;     // items per wave: 2
+};
+
+template <int D>
+struct DqSmem {
+    static constexpr int KROW = BT<D>::KROW, TROW = BT<D>::TROW;
+    bf16 k[kChunk * KROW];
+    bf16 v[kChunk * KROW];
+    bf16 kt[D * TROW];
+};
+
+template <int D, int G>
+__global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, const bf16* dqp, const float* dshat) {
+    using C = DqCfg<G>;
+    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, TROW = BT<D>::TROW, IPW = C::IPW;
+    __shared__ __align__(16) DqSmem<D> sm;
+    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int ntiles = (a.N + C::QT - 1) / C::QT;
+    const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
+    const int q0 = tile * C::QT;
+    const int qlast = min(q0 + C::QT - 1, a.N - 1);
+    const int kbeg = n_candidates(q0, a.W) * kChunk;
+    const size_t bg = (size_t)b * a.Hkv + g;
+    const int nC = a.L / kChunk;
+
+    bf16x8 bq[IPW][KS], bo[IPW][KS];
+    f32x4 dq[IPW][DB];
+    float Lr[IPW], ub[IPW];
+#pragma unroll
+    for (int it = 0; it < IPW; ++it) {
+        const int item = w + 4 * it;
+        const int hh = item / C::QB, qb = item % C::QB;
+        const int nq = min(q0 + qb * 16 + lane % 16, a.N - 1);
+        const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            bq[it][ks] = ld_bf16x8(as<bf16>(a.q) + qrow * D + ks * 32 + (lane / 16) * 8);
+            bo[it][ks] = ld_bf16x8(as<bf16>(a.dout) + qrow * D + ks * 32 + (lane / 16) * 8);
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db) dq[it][db] = zero4();
+        Lr[it] = a.lse[qrow];
+        ub[it] = u[qrow];
+    }
+    for (int j0 = kbeg; j0 <= qlast; j0 += kChunk) {
+        __syncthreads();
+        stage_k_v_kt<D>(as<bf16>(a.k) + (bg * a.L + j0) * D, as<bf16>(a.v) + (bg * a.L + j0) * D, sm.k, sm.v,
+                        sm.kt);
+        __syncthreads();
+#pragma unroll
+        for (int it = 0; it < IPW; ++it) {
+            const int item = w + 4 * it;
+            const int qb = item % C::QB;
+            const int nq = q0 + qb * 16 + lane % 16;
+            const int ell = n_candidates(nq, a.W) * kChunk;
+            f32x4 s4[4], gv4[4];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                s4[kb] = zero4();
+                gv4[kb] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    s4[kb] = mfma16x16x32(row_operand<KROW>(sm.k, kb * 16, ks * 32, lane), bq[it][ks], s4[kb]);
+                    gv4[kb] = mfma16x16x32(row_operand<KROW>(sm.v, kb * 16, ks * 32, lane), bo[it][ks], gv4[kb]);
+                }
+            }
+            float ds[4][4];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int j = j0 + kb * 16 + (lane / 16) * 4 + i;
+                    const bool valid = nq < a.N && j <= nq && j >= ell;
+                    const float wgt = valid ? fexp(a.scale * s4[kb][i] - Lr[it]) : 0.f;
+                    ds[kb][i] = wgt * (gv4[kb][i] - ub[it]);
+                }
+            const bf16x8 b0 = pack_perm(ds[0], ds[1]);
+            const bf16x8 b1 = pack_perm(ds[2], ds[3]);
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                dq[it][db] = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 0, lane), b0, dq[it][db]);
+                dq[it][db] = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 1, lane), b1, dq[it][db]);
+            }
+        }
+    }
+    // epilogue (lane: row l%16 of the block, dims 16db + (l/16)*4 + {0..3})
+#pragma unroll
+    for (int it = 0; it < IPW; ++it) {
+        const int item = w + 4 * it;
+        const int hh = item / C::QB, qb = item % C::QB;
+        const int nq = q0 + qb * 16 + lane % 16;
+        if (nq >= a.N) continue;
+        const int h = g * G + hh;
+        const int hl = (a.Hl == a.Hq) ? h : g;
+        const size_t row = ((size_t)b * a.Hq + h) * a.N + nq;
+        const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
+        const int ncand = n_candidates(nq, a.W);
+        f32x4 acc[DB], accr[DB];
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            acc[db] = dq[it][db] * a.scale;
+            accr[db] = zero4();
+        }
+        for (int k = 0; k < a.K; ++k) {
+            if (!idx_entry_valid(irow, k, ncand)) continue;
+            const int cc = irow[k];
+            const float x = a.scale * dshat[row * a.K + k];
+            const bf16* prow = dqp + (row * a.K + k) * D;
+            const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + cc) * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int d0 = db * 16 + (lane / 16) * 4;
+                const uint2 pv = *reinterpret_cast<const uint2*>(prow + d0);
+                const uint2 lv = *reinterpret_cast<const uint2*>(lrow + d0);
+                acc[db][0] += bf_lo(pv.x);
+                acc[db][1] += bf_hi(pv.x);
+                acc[db][2] += bf_lo(pv.y);
+                acc[db][3] += bf_hi(pv.y);
+                accr[db][0] += x * bf_lo(lv.x);
+                accr[db][1] += x * bf_hi(lv.x);
+                accr[db][2] += x * bf_lo(lv.y);
+                accr[db][3] += x * bf_hi(lv.y);
+            }
+        }
+        bf16* dqo = as_mut<bf16>(a.dq) + row * D;
+        bf16* dqr = a.dq_route ? as_mut<bf16>(a.dq_route) + row * D : nullptr;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const int d0 = db * 16 + (lane / 16) * 4;
+            f32x4 x = acc[db];
+            if (!dqr) x += accr[db];
+            *reinterpret_cast<uint2*>(dqo + d0) = make_uint2(pack2(x[0], x[1]), pack2(x[2], x[3]));
+            if (dqr)
+                *reinterpret_cast<uint2*>(dqr + d0) =
+                    make_uint2(pack2(accr[db][0], accr[db][1]), pack2(accr[db][2], accr[db][3]));
+        }
+    }
+}
+
+struct BwRun {
+    template <typename T, int D, int G>
+    static hipError_t run(const BwdArgs& a, hipStream_t s) {
+        const BwLayout ly = bw_layout(a.B, a.Hq, a.Hkv, a.N, a.L, D, a.K);
+        char* ws = static_cast<char*>(a.ws);
+        float* u = reinterpret_cast<float*>(ws + ly.u);
+        bf16* dqp = reinterpret_cast<bf16*>(ws + ly.dqp);
+        float* dsh = reinterpret_cast<float*>(ws + ly.dsh);
+        int* sorted = reinterpret_cast<int*>(ws + ly.sorted);
+        const int* offsets = reinterpret_cast<const int*>(ws + ly.inv.offsets);
+        const int nC = a.L / kChunk;
+        const size_t rows = (size_t)a.B * a.Hq * a.N;
+        HILS_LAUNCH("k_bwd_u", (k_bwd_u<D>), dim3((unsigned)((rows + 3) / 4)), dim3(kBlock), 0, s, a, u);
+        const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
+        launch_inverse_index(ia, ly.inv, a.ws, s, false);
+        HILS_LAUNCH("k_inv_sort", k_inv_sort, dim3(nC, a.B * a.Hkv), dim3(kBlock), 0, s, offsets,
+                    reinterpret_cast<const int*>(ws + ly.inv.list), sorted, a.N, a.K, nC, a.W);
+        HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a, offsets,
+                    (const int*)sorted, (const float*)u, dqp, dsh);
+        HILS_LAUNCH("k_bwd_dq", (k_bwd_dq<D, G>), dim3((a.N + DqCfg<G>::QT - 1) / DqCfg<G>::QT, a.Hkv, a.B),
+                    dim3(kBlock), 0, s, a, (const float*)u, (const bf16*)dqp, (const float*)dsh);
+        return hipGetLastError();
+    }
+};
+
+}  // namespace
+
+size_t bwd_mfma_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K) {
+    return bw_layout(B, Hq, Hkv, N, L, d, K).total;
+}
+
+hipError_t launch_bwd_mfma(const BwdArgs& a, hipStream_t s) { return dispatch<BwRun>(1, a.d, a.Hq / a.Hkv, a, s); }
+
+}  // namespace hils

@@ -82,7 +82,9 @@ struct InvLayout {
 };
 constexpr int kInvSeg = 256;  // list entries per work item
 InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base);
-void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStream_t s);
+// work_list = false skips the (bg, chunk, segment) work items (consumers that walk
+// whole lists do not read them).
+void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStream_t s, bool work_list = true);
 
 // Work item encoding: bg * (nC * segs_max) ... decoded by the consumers.
 struct WorkItem {
@@ -102,6 +104,8 @@ size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int 
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s);  // fp32 storage
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s);
-hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);       // fp32 storage
+hipError_t launch_bwd_mfma(const BwdArgs& a, hipStream_t s);  // bf16 storage
+size_t bwd_mfma_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K);
 
 }  // namespace hils

@@ -16,6 +16,13 @@ CASES = {
     "bf16_Hl_eq_Hkv_window1": (dict(B=1, Hq=8, Hkv=2, Hl=2, N=768, L=768, d=64, topk=6, window=1), 303, True, False),
     "f32_G8_bias_boosted": (dict(B=1, Hq=8, Hkv=1, N=600, L=640, d=128, topk=5, window=64, dtype="f32"), 304, True,
                             True),
+    "bf16_G8_route_bias_ragged": (dict(B=1, Hq=8, Hkv=1, N=600, L=640, d=128, topk=5, window=64), 305, True, True),
+    "bf16_G1_d64": (dict(B=2, Hq=2, Hkv=2, N=500, L=512, d=64, topk=3, window=70), 306, False, False),
+    "bf16_G2_Hl_eq_Hkv_topk_exceeds": (dict(B=1, Hq=4, Hkv=2, Hl=2, N=1100, L=1152, d=128, topk=16, window=100),
+                                       307, True, False),
+    "bf16_G8_Hl_eq_Hkv_d64": (dict(B=1, Hq=8, Hkv=1, Hl=1, N=400, L=448, d=64, topk=4, window=64), 308, False,
+                              False),
+    "bf16_all_local": (dict(B=1, Hq=4, Hkv=1, N=200, L=256, d=64, topk=4, window=512), 309, False, False),
 }
 
 

@@ -16,10 +16,14 @@
 //                  the rows whose local window covers keys of c, then the rows that
 //                  retrieved c.  Phase 1, one 16-pair tile per wave: S^T = K Q^T and
 //                  GV^T = V dO^T on MFMA, the softmax terms, ds; for retrieving rows also
-//                  the chunk's share of dq (K^T ds^T, stored as a bf16 partial of the
-//                  row's slot) and ds^_c.  Phase 2, one 16-key block per wave: dK and dV
-//                  as MFMA reductions over the step's 64 pairs, read back from LDS.
-//                  dk, dv, dk', db' of chunk c are written once (no atomics).
+//                  s^_c (one more MFMA against the landmark rows), the chunk's share of
+//                  dq (K^T ds^T, stored as a bf16 partial of the row's slot) and ds^_c.
+//                  Phase 2, one 16-key block per wave: dK and dV as MFMA reductions over
+//                  the step's 64 pairs, and dk' as one more (heads x pairs) product.
+//                  The operands of phase 2 are read back from row-major LDS tiles with
+//                  transposing reads (ds_read_b64_tr_b16); the next step's rows are
+//                  fetched while the current step computes.  dk, dv, dk', db' of chunk c
+//                  are written once (no atomics).
 //   k_bwd_dq       query-major: dq over the local window (the forward's local tile with
 //                  ds in place of p), plus the row's slot partials and scale ds^ k'.
 #include "hils_device.hpp"
@@ -35,7 +39,7 @@ constexpr int kBlock = 256;
 constexpr int kPairs = 64;          // (row, head) pairs per step of k_bwd_keys
 constexpr int kSortWin = 8192;      // rows per bitmap pass of k_inv_sort
 constexpr int kSortWords = kSortWin / 32;
-static_assert(kSortWords % 256 == 0, "k_inv_sort scans whole runs of words per thread");
+static_assert(kSortWords % kBlock == 0, "k_inv_sort scans whole runs of words per thread");
 
 struct BwLayout {
     size_t u, dqp, dsh, sorted, inv_base;
@@ -61,64 +65,48 @@ template <int D>
 struct BT {
     static constexpr int KS = D / 32;    // 32-wide k-steps over the head dim
     static constexpr int DB = D / 16;    // 16-wide blocks of the head dim
-    static constexpr int KROW = D + 8;   // padded K / V row (bf16)
-    static constexpr int TROW = 64 + 8;  // padded transposed row: 64 keys or 64 pairs
+    static constexpr int KROW = D + 8;   // padded row of a [64][D] tile (bf16)
+    static constexpr int PROW = 64 + 8;  // padded row of a [64 pairs][64 keys] tile
+    static constexpr int HROW = 16 + 8;  // padded row of the [64 pairs][16 heads] tile
 };
-
-__device__ __forceinline__ uint16_t bfbits(float x) { return from_f32<bf16>(x).bits; }
-
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-    return (uint32_t)bfbits(lo) | ((uint32_t)bfbits(hi) << 16);
-}
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Stage K rows, V rows and K^T of 64 keys.
+// 64 rows of D bf16 (K or V of one chunk) held in registers, and their store
+// into a padded row-major LDS tile.
 template <int D>
-__device__ __forceinline__ void stage_k_v_kt(const bf16* kb, const bf16* vb, bf16* s_k, bf16* s_v, bf16* s_kt) {
-    constexpr int KROW = BT<D>::KROW, TROW = BT<D>::TROW;
-    constexpr int PPT = kChunk * D / 8 / kBlock;
-    const int tid = threadIdx.x;
-    uint4 xk[PPT], xv[PPT];
+struct Rows {
+    static constexpr int PPT = kChunk * D / 8 / kBlock;
+    uint4 x[PPT];
+};
+template <int D>
+__device__ __forceinline__ Rows<D> load_rows(const bf16* src) {
+    Rows<D> r;
 #pragma unroll
-    for (int u = 0; u < PPT; ++u) {
-        const int e = tid + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
-        xk[u] = *reinterpret_cast<const uint4*>(kb + (size_t)j * D + d8);
-        xv[u] = *reinterpret_cast<const uint4*>(vb + (size_t)j * D + d8);
+    for (int u = 0; u < Rows<D>::PPT; ++u) {
+        const int e = threadIdx.x + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+        r.x[u] = *reinterpret_cast<const uint4*>(src + (size_t)j * D + d8);
     }
+    return r;
+}
+template <int D>
+__device__ __forceinline__ void store_rows(bf16* tile, const Rows<D>& r) {
 #pragma unroll
-    for (int u = 0; u < PPT; ++u) {
-        const int e = tid + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
-        *reinterpret_cast<uint4*>(s_k + j * KROW + d8) = xk[u];
-        *reinterpret_cast<uint4*>(s_v + j * KROW + d8) = xv[u];
-        const uint32_t w[4] = {xk[u].x, xk[u].y, xk[u].z, xk[u].w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            s_kt[(d8 + 2 * t) * TROW + j].bits = (uint16_t)(w[t] & 0xffffu);
-            s_kt[(d8 + 2 * t + 1) * TROW + j].bits = (uint16_t)(w[t] >> 16);
-        }
+    for (int u = 0; u < Rows<D>::PPT; ++u) {
+        const int e = threadIdx.x + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+        *reinterpret_cast<uint4*>(tile + j * BT<D>::KROW + d8) = r.x[u];
     }
 }
 
-// Operand (A or B) read from a padded row-major tile: rows r0 + l%16, the 8
-// consecutive columns k0 + (l/16)*8 ...
+// Operand read from a padded row-major tile: rows r0 + l%16, the 8 consecutive
+// columns k0 + (l/16)*8 ...
 template <int ROW>
 __device__ __forceinline__ bf16x8 row_operand(const bf16* base, int r0, int k0, int lane) {
     return ld_bf16x8(base + (r0 + lane % 16) * ROW + k0 + (lane / 16) * 8);
 }
 
-// A operand over 32 keys in the order in which S^T accumulators hold them: rows
-// m0 + l%16 of a [m][64 keys] tile, keys 32t + (l/16)*4 + {0..3} then 32t + 16 + (l/16)*4 + {0..3}.
-template <int ROW>
-__device__ __forceinline__ bf16x8 perm_operand(const bf16* base, int m0, int t, int lane) {
-    const bf16* r = base + (m0 + lane % 16) * ROW + 32 * t + (lane / 16) * 4;
-    const uint2 lo = *reinterpret_cast<const uint2*>(r);
-    const uint2 hi = *reinterpret_cast<const uint2*>(r + 16);
-    return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-}
-
-// The matching B operand from two S^T accumulator blocks (keys 32t.. and 32t+16..).
+// B operand from two S^T accumulator blocks (keys 32t + (l/16)*4 + i, then +16).
 __device__ __forceinline__ bf16x8 pack_perm(const float* e0, const float* e1) {
     const float x[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
     return pack_bf16x8(x);
@@ -211,100 +199,129 @@ __global__ __launch_bounds__(kBlock) void k_inv_sort(const int* offsets, const i
 // ---------------------------------------------------------------------------
 template <int D>
 struct KeySmem {
-    static constexpr int KROW = BT<D>::KROW, TROW = BT<D>::TROW;
-    bf16 k[kChunk * KROW];
-    bf16 v[kChunk * KROW];
-    bf16 kt[D * TROW];
-    bf16 qt[D * TROW];        // Q^T of the step's pairs: [d][pair]
-    bf16 dot[D * TROW];       // dO^T, same layout
-    bf16 pt[kChunk * TROW];   // dV weights, transposed: [key][pair]
-    bf16 dst[kChunk * TROW];  // ds, transposed: [key][pair]
-    float dsh[kPairs];        // ds^_c per pair (retrieval steps)
-    int rows[kPairs];
-    int slots[kPairs];
+    static constexpr int KROW = BT<D>::KROW, PROW = BT<D>::PROW, HROW = BT<D>::HROW;
+    bf16 k[kChunk * KROW];   // K of the chunk, row-major
+    bf16 v[kChunk * KROW];   // V
+    bf16 q[kPairs * KROW];   // q of the step's pairs, row-major [pair][d]
+    bf16 g[kPairs * KROW];   // dO
+    bf16 qr[kPairs * KROW];  // q^ (routing queries given)
+    bf16 p[kPairs * PROW];   // dV weights [pair][key]
+    bf16 ds[kPairs * PROW];  // ds [pair][key]
+    bf16 h[kPairs * HROW];   // ds^_c in the columns of the pair's landmark head
+    float db[4][16];
+};
+
+// The per-pair operands of one step: row entry (n << 6 | slot, or -1), q, dO, q^, L, u.
+template <int KS>
+struct PairOps {
+    uint4 q[KS], o[KS], qr[KS];
+    float L, u;
+    int ent;
 };
 
 template <int D, int G>
 __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offsets, const int* sorted, const float* u,
                                                      bf16* dqp, float* dshat) {
-    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, TROW = BT<D>::TROW, KROW = BT<D>::KROW;
+    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, PROW = BT<D>::PROW, HROW = BT<D>::HROW;
     constexpr int R = kPairs / G;              // rows per step
     constexpr int HT = G > 4 ? G / 4 : 1;      // heads in one wave's 16-pair tile
+    constexpr int DBW = DB / 4;                // dk' blocks of the head dim per wave
     __shared__ __align__(16) KeySmem<D> sm;
-    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const size_t bg = (size_t)b * a.Hkv + g;
     const int j0 = c * kChunk;
     const bool per_head_lmk = (a.Hl == a.Hq);
+    const bool route = a.q_route != nullptr;
     const bf16* qb = as<bf16>(a.q);
     const bf16* gob = as<bf16>(a.dout);
-    const bf16* rb = as<bf16>(a.q_route ? a.q_route : a.q);
-    stage_k_v_kt<D>(as<bf16>(a.k) + (bg * a.L + j0) * D, as<bf16>(a.v) + (bg * a.L + j0) * D, sm.k, sm.v, sm.kt);
+    const bf16* rb = as<bf16>(a.q_route);
+    store_rows<D>(sm.k, load_rows<D>(as<bf16>(a.k) + (bg * a.L + j0) * D));
+    store_rows<D>(sm.v, load_rows<D>(as<bf16>(a.v) + (bg * a.L + j0) * D));
 
-    // this lane's pair in phase 1 and the first head of the wave's tile
+    // this lane's pair in phase 1
     const int pair = w * 16 + lane % 16;
     const int hh = pair / R, r = pair % R;
     const int h = g * G + hh;
     const int hfirst = (w * 16) / R;
     const int hl = per_head_lmk ? h : g;
+    // landmark rows as the A operand of s^: row m = head hfirst + m of the tile (per-head
+    // landmarks) or the group's one landmark (m = 0)
+    bf16x8 aL[KS];
+    {
+        const int m = lane % 16;
+        const bool has = per_head_lmk ? m < HT : m == 0;
+        const int hlm = per_head_lmk ? g * G + hfirst + m : g;
+        const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + (has ? hlm : 0)) * nC + c) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            aL[ks] = has ? ld_bf16x8(lrow + ks * 32 + lg * 8) : as_bf16x8(make_uint4(0, 0, 0, 0));
+    }
+    const int hloc = per_head_lmk ? hh - hfirst : 0;
+    const float bias_h = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
 
-    f32x4 dk[DB], dv[DB];
+    f32x4 dk[DB], dv[DB], dkl[DBW];
 #pragma unroll
     for (int db = 0; db < DB; ++db) dk[db] = dv[db] = zero4();
-    float dl[HT][2], dbias[HT];
 #pragma unroll
-    for (int t = 0; t < HT; ++t) dl[t][0] = dl[t][1] = dbias[t] = 0.f;
+    for (int t = 0; t < DBW; ++t) dkl[t] = zero4();
+    float dbl = 0.f;
 
     const int n_lo = j0, n_hi = min(a.N - 1, j0 + kChunk + a.W - 2);
     const int nlocal = max(0, n_hi - n_lo + 1);
     const int beg = offsets[bg * (nC + 1) + c];
     const int nret = offsets[bg * (nC + 1) + c + 1] - beg;
     const int* seg = sorted + bg * a.N * a.K + beg;
-    const int nsteps_local = (nlocal + R - 1) / R;
-    const int nsteps = nsteps_local + (nret + R - 1) / R;
+    const int nsl = (nlocal + R - 1) / R;
+    const int nst = nsl + (nret + R - 1) / R;
 
-    for (int st = 0; st < nsteps; ++st) {
-        const bool retrieval = st >= nsteps_local;
-        __syncthreads();  // the previous step's tiles are consumed
-        if (tid < R) {
-            int n = -1, slot = 0;
-            if (!retrieval) {
-                const int e = st * R + tid;
-                if (e < nlocal) n = n_lo + e;
-            } else {
-                const int e = (st - nsteps_local) * R + tid;
-                if (e < nret) {
-                    n = seg[e] >> 6;
-                    slot = seg[e] & 63;
-                }
-            }
-            sm.rows[tid] = n;
-            sm.slots[tid] = slot;
+    auto entry_of = [&](int s) -> int {
+        if (s >= nst) return -1;
+        if (s < nsl) {
+            const int e = s * R + r;
+            return e < nlocal ? (n_lo + e) << 6 : -1;
         }
-        __syncthreads();
-
-        // ---- phase 1: this wave's 16 pairs against the 64 keys ----
-        const int qn = sm.rows[r];
-        const bool qv = qn >= 0;
-        const size_t qrow = ((size_t)b * a.Hq + h) * a.N + (qv ? qn : 0);
-        bf16x8 bq[KS], bo[KS];
+        const int e = (s - nsl) * R + r;
+        return e < nret ? seg[e] : -1;
+    };
+    auto load_ops = [&](int ent, PairOps<KS>& x) {
+        x.ent = ent;
+        const bool ok = ent >= 0;
+        const size_t row = ((size_t)b * a.Hq + h) * a.N + (ok ? (ent >> 6) : 0);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const int d0 = ks * 32 + (lane / 16) * 8;
-            const uint4 uq = qv ? *reinterpret_cast<const uint4*>(qb + qrow * D + d0) : make_uint4(0, 0, 0, 0);
-            const uint4 uo = qv ? *reinterpret_cast<const uint4*>(gob + qrow * D + d0) : make_uint4(0, 0, 0, 0);
-            bq[ks] = as_bf16x8(uq);
-            bo[ks] = as_bf16x8(uo);
-            const uint32_t wq[4] = {uq.x, uq.y, uq.z, uq.w}, wo[4] = {uo.x, uo.y, uo.z, uo.w};
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                sm.qt[(d0 + 2 * t) * TROW + pair].bits = (uint16_t)(wq[t] & 0xffffu);
-                sm.qt[(d0 + 2 * t + 1) * TROW + pair].bits = (uint16_t)(wq[t] >> 16);
-                sm.dot[(d0 + 2 * t) * TROW + pair].bits = (uint16_t)(wo[t] & 0xffffu);
-                sm.dot[(d0 + 2 * t + 1) * TROW + pair].bits = (uint16_t)(wo[t] >> 16);
-            }
+            const int d0 = ks * 32 + lg * 8;
+            x.q[ks] = ok ? *reinterpret_cast<const uint4*>(qb + row * D + d0) : make_uint4(0, 0, 0, 0);
+            x.o[ks] = ok ? *reinterpret_cast<const uint4*>(gob + row * D + d0) : make_uint4(0, 0, 0, 0);
+            x.qr[ks] = (ok && route) ? *reinterpret_cast<const uint4*>(rb + row * D + d0) : make_uint4(0, 0, 0, 0);
         }
+        x.L = ok ? a.lse[row] : 0.f;
+        x.u = ok ? u[row] : 0.f;
+    };
+
+    PairOps<KS> cur;
+    load_ops(entry_of(0), cur);
+    int ent_next = entry_of(1);
+    for (int st = 0; st < nst; ++st) {
+        const bool retrieval = st >= nsl;
+        const int ent_after = entry_of(st + 2);
+        PairOps<KS> nxt;
+        load_ops(ent_next, nxt);
+
+        const bool qv = cur.ent >= 0;
+        const int qn = cur.ent >> 6, slot = cur.ent & 63;
+        const size_t qrow = ((size_t)b * a.Hq + h) * a.N + (qv ? qn : 0);
+        __syncthreads();  // the previous step's tiles are consumed
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int d0 = ks * 32 + lg * 8;
+            *reinterpret_cast<uint4*>(sm.q + pair * KROW + d0) = cur.q[ks];
+            *reinterpret_cast<uint4*>(sm.g + pair * KROW + d0) = cur.o[ks];
+            if (retrieval && route) *reinterpret_cast<uint4*>(sm.qr + pair * KROW + d0) = cur.qr[ks];
+        }
+
+        // ---- phase 1: this wave's 16 pairs against the 64 keys ----
         f32x4 s4[4], gv4[4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
@@ -312,43 +329,34 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
             gv4[kb] = zero4();
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                s4[kb] = mfma16x16x32(row_operand<KROW>(sm.k, kb * 16, ks * 32, lane), bq[ks], s4[kb]);
-                gv4[kb] = mfma16x16x32(row_operand<KROW>(sm.v, kb * 16, ks * 32, lane), bo[ks], gv4[kb]);
+                s4[kb] = mfma16x16x32(row_operand<KROW>(sm.k, kb * 16, ks * 32, lane), as_bf16x8(cur.q[ks]), s4[kb]);
+                gv4[kb] = mfma16x16x32(row_operand<KROW>(sm.v, kb * 16, ks * 32, lane), as_bf16x8(cur.o[ks]), gv4[kb]);
             }
         }
-        const float Lr = qv ? a.lse[qrow] : 0.f;
-        const float ub = qv ? u[qrow] : 0.f;
         float pw[4][4], ds[4][4];
+        float dsh = 0.f;
         if (!retrieval) {
             const int ell = n_candidates(qn, a.W) * kChunk;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int j = j0 + kb * 16 + (lane / 16) * 4 + i;
+                    const int j = j0 + kb * 16 + lg * 4 + i;
                     const bool valid = qv && j <= qn && j >= ell;
-                    const float wgt = valid ? fexp(a.scale * s4[kb][i] - Lr) : 0.f;
+                    const float wgt = valid ? fexp(a.scale * s4[kb][i] - cur.L) : 0.f;
                     pw[kb][i] = wgt;
-                    ds[kb][i] = wgt * (gv4[kb][i] - ub);
+                    ds[kb][i] = wgt * (gv4[kb][i] - cur.u);
                 }
         } else {
-            // surrogate score s^_c of the pair: lanes hold 8*KS dims each
-            const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
-            float part = 0.f;
+            // s^_c of the pair: landmark rows (A) against the pair's q^ (B)
+            f32x4 sh4 = zero4();
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const int d0 = ks * 32 + (lane / 16) * 8;
-                const uint4 lv = *reinterpret_cast<const uint4*>(lrow + d0);
-                const uint4 qq = a.q_route ? (qv ? *reinterpret_cast<const uint4*>(rb + qrow * D + d0)
-                                                 : make_uint4(0, 0, 0, 0))
-                                           : __builtin_bit_cast(uint4, bq[ks]);
-                const uint32_t lw[4] = {lv.x, lv.y, lv.z, lv.w}, qw[4] = {qq.x, qq.y, qq.z, qq.w};
+            for (int ks = 0; ks < KS; ++ks) sh4 = mfma16x16x32(aL[ks], as_bf16x8(route ? cur.qr[ks] : cur.q[ks]), sh4);
+            float mine = sh4[0];
 #pragma unroll
-                for (int t = 0; t < 4; ++t) part += bf_lo(lw[t]) * bf_lo(qw[t]) + bf_hi(lw[t]) * bf_hi(qw[t]);
-            }
-            part += __shfl_xor(part, 16, kWave);
-            part += __shfl_xor(part, 32, kWave);
-            const float shat = a.scale * part + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f);
+            for (int i = 1; i < 4; ++i)
+                if (hloc == i) mine = sh4[i];
+            const float shat = a.scale * __shfl(mine, lane % 16, kWave) + bias_h;
             float mx = -INFINITY;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
@@ -377,7 +385,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                 }
             uc += __shfl_xor(uc, 16, kWave);
             uc += __shfl_xor(uc, 32, kWave);
-            const float al = qv ? fexp(shat - Lr) : 0.f;
+            const float al = qv ? fexp(shat - cur.L) : 0.f;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -385,71 +393,75 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                     ds[kb][i] = al * pw[kb][i] * (gv4[kb][i] - uc);
                     pw[kb][i] *= al;
                 }
-            const float dsh = al * (uc - ub);
-            if (lane < 16) sm.dsh[pair] = dsh;
-            if (qv && lane < 16) dshat[qrow * a.K + sm.slots[r]] = dsh;
-        }
-        // dV weights and ds, transposed, for phase 2
+            dsh = al * (uc - cur.u);
+            if (qv && lane < 16) dshat[qrow * a.K + slot] = dsh;
+            // H row of the pair: ds^ split into a bf16 head and its bf16 residual, in
+            // columns m and 8 + m of its landmark head m (the product then keeps ds^ to
+            // about fp32 accuracy)
+            if (lane < 16) {
+                const int col = per_head_lmk ? hh : 0;
+                const float hi = to_f32(from_f32<bf16>(dsh)), lo = dsh - hi;
+                float hv[16];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+                for (int t = 0; t < 16; ++t) hv[t] = t == col ? hi : (t == col + 8 ? lo : 0.f);
+                uint32_t wds[8];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key = kb * 16 + (lane / 16) * 4 + i;
-                sm.pt[key * TROW + pair].bits = bfbits(pw[kb][i]);
-                sm.dst[key * TROW + pair].bits = bfbits(ds[kb][i]);
+                for (int t = 0; t < 8; ++t) wds[t] = pack_bf16x2(hv[2 * t], hv[2 * t + 1]);
+                *reinterpret_cast<uint4*>(sm.h + pair * HROW) = make_uint4(wds[0], wds[1], wds[2], wds[3]);
+                *reinterpret_cast<uint4*>(sm.h + pair * HROW + 8) = make_uint4(wds[4], wds[5], wds[6], wds[7]);
             }
+            // db': sum ds^ over the pairs of each head of the tile
+            const float hs = (R >= 16) ? group_sum<16>(dsh) : group_sum<8>(dsh);
+            if (lane < 16 && (lane % (R >= 16 ? 16 : 8)) == 0) dbl += hs;
+        }
+        // dV weights and ds, row-major [pair][key]
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            const int key = kb * 16 + lg * 4;
+            *reinterpret_cast<uint2*>(sm.p + pair * PROW + key) =
+                make_uint2(pack_bf16x2(pw[kb][0], pw[kb][1]), pack_bf16x2(pw[kb][2], pw[kb][3]));
+            *reinterpret_cast<uint2*>(sm.ds + pair * PROW + key) =
+                make_uint2(pack_bf16x2(ds[kb][0], ds[kb][1]), pack_bf16x2(ds[kb][2], ds[kb][3]));
+        }
         if (retrieval) {
             // the chunk's share of dq: dq^T = scale K^T ds^T, into the row's slot partial
             const bf16x8 b0 = pack_perm(ds[0], ds[1]);
             const bf16x8 b1 = pack_perm(ds[2], ds[3]);
-            bf16* prow = dqp + (qrow * a.K + sm.slots[r]) * D;
+            bf16* prow = dqp + (qrow * a.K + slot) * D;
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
                 f32x4 o = zero4();
-                o = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 0, lane), b0, o);
-                o = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 1, lane), b1, o);
+                o = mfma16x16x32(tr_operand_perm(sm.k, KROW, 0, db * 16, lane), b0, o);
+                o = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, o);
                 if (qv)
-                    *reinterpret_cast<uint2*>(prow + db * 16 + (lane / 16) * 4) =
-                        make_uint2(pack2(a.scale * o[0], a.scale * o[1]), pack2(a.scale * o[2], a.scale * o[3]));
-            }
-            // dk' and db': lanes own dims 2*lane, 2*lane+1; the tile's 16 pairs in order
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            if (2 * lane < D) {
-                for (int p = 0; p < 16; ++p) {
-                    const int pp = w * 16 + p;
-                    const int nr = sm.rows[pp % R];
-                    if (nr < 0) continue;
-                    const int ht = pp / R - hfirst;
-                    const float x = sm.dsh[pp];
-                    const uint32_t qq = *reinterpret_cast<const uint32_t*>(
-                        rb + (((size_t)b * a.Hq + g * G + pp / R) * a.N + nr) * D + 2 * lane);
-#pragma unroll
-                    for (int t = 0; t < HT; ++t)
-                        if (t == ht) {
-                            dl[t][0] += x * bf_lo(qq);
-                            dl[t][1] += x * bf_hi(qq);
-                            dbias[t] += x;
-                        }
-                }
+                    *reinterpret_cast<uint2*>(prow + db * 16 + lg * 4) =
+                        make_uint2(pack_bf16x2(a.scale * o[0], a.scale * o[1]),
+                                   pack_bf16x2(a.scale * o[2], a.scale * o[3]));
             }
         }
         __syncthreads();
-        // ---- phase 2: keys [16w, 16w+16) x all dims, reduced over the 64 pairs ----
-        bf16x8 ak[2], av[2];
+        // ---- phase 2: keys [16w, 16w+16) x all dims over the 64 pairs; dk' blocks w, w+4 ----
+        bf16x8 ads[2], ap[2], ah[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            ak[t] = row_operand<TROW>(sm.dst, w * 16, t * 32, lane);
-            av[t] = row_operand<TROW>(sm.pt, w * 16, t * 32, lane);
+            ads[t] = tr_operand(sm.ds, PROW, t * 32, w * 16, lane);
+            ap[t] = tr_operand(sm.p, PROW, t * 32, w * 16, lane);
+            if (retrieval) ah[t] = tr_operand(sm.h, HROW, t * 32, 0, lane);
         }
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                dk[db] = mfma16x16x32(ak[t], row_operand<TROW>(sm.qt, db * 16, t * 32, lane), dk[db]);
-                dv[db] = mfma16x16x32(av[t], row_operand<TROW>(sm.dot, db * 16, t * 32, lane), dv[db]);
+                const bf16x8 bq = tr_operand(sm.q, KROW, t * 32, db * 16, lane);
+                dk[db] = mfma16x16x32(ads[t], bq, dk[db]);
+                dv[db] = mfma16x16x32(ap[t], tr_operand(sm.g, KROW, t * 32, db * 16, lane), dv[db]);
+                if (retrieval && db % 4 == w) {
+                    const bf16x8 bqr = route ? tr_operand(sm.qr, KROW, t * 32, db * 16, lane) : bq;
+                    dkl[db / 4] = mfma16x16x32(ah[t], bqr, dkl[db / 4]);
+                }
             }
+        cur = nxt;
+        ent_next = ent_after;
     }
 
     // ---- dK, dV of the chunk (lane: key 16w + (l/16)*4 + i, dim 16db + l%16) ----
@@ -459,53 +471,36 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
     for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int key = w * 16 + (lane / 16) * 4 + i, d = db * 16 + lane % 16;
+            const int key = w * 16 + lg * 4 + i, d = db * 16 + lane % 16;
             dkp[key * D + d] = from_f32<bf16>(a.scale * dk[db][i]);
             dvp[key * D + d] = from_f32<bf16>(dv[db][i]);
         }
-    // ---- dK', db': per-wave sums, then per landmark head ----
-    __syncthreads();
-    float* s_red = reinterpret_cast<float*>(sm.qt);  // [4 waves][HT][D]
-    float* s_rb = reinterpret_cast<float*>(sm.pt);   // [4 waves][HT]
-#pragma unroll
-    for (int t = 0; t < HT; ++t) {
-        if (2 * lane < D) {
-            s_red[(w * HT + t) * D + 2 * lane] = a.scale * dl[t][0];
-            s_red[(w * HT + t) * D + 2 * lane + 1] = a.scale * dl[t][1];
-        }
-        if (lane == 0) s_rb[w * HT + t] = dbias[t];
-    }
-    __syncthreads();
-    // head hh sits in the waves ww with hfirst(ww) <= hh < hfirst(ww) + HT
-    auto head_sum = [&](int head, int d) {
-        float v = 0.f;
-        for (int ww = 0; ww < 4; ++ww) {
-            const int t = head - (ww * 16) / R;
-            if (t >= 0 && t < HT) v += d >= 0 ? s_red[(ww * HT + t) * D + d] : s_rb[ww * HT + t];
-        }
-        return v;
-    };
+    // ---- dK' (lane: rows (l/16)*4 + i = head m and its residual row m + 8 in lane l ^ 32,
+    // dim 16(w + 4t) + l%16) ----
     const int nLH = per_head_lmk ? G : 1;
-    for (int e = tid; e < nLH * D; e += kBlock) {
-        const int lh = e / D, d = e % D;
-        float v = 0.f;
-        if (per_head_lmk) {
-            v = head_sum(lh, d);
-        } else {
-            for (int head = 0; head < G; ++head) v += head_sum(head, d);
+#pragma unroll
+    for (int t = 0; t < DBW; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float v = dkl[t][i] + __shfl_xor(dkl[t][i], 32, kWave);
+            const int m = lg * 4 + i, d = (w + 4 * t) * 16 + lane % 16;
+            if (lg < 2 && m < nLH) {
+                const int hl_out = per_head_lmk ? g * G + m : g;
+                as_mut<bf16>(a.dlmk)[(((size_t)b * a.Hl + hl_out) * nC + c) * D + d] = from_f32<bf16>(a.scale * v);
+            }
         }
-        const int hl_out = per_head_lmk ? g * G + lh : g;
-        as_mut<bf16>(a.dlmk)[(((size_t)b * a.Hl + hl_out) * nC + c) * D + d] = from_f32<bf16>(v);
-    }
-    if (a.dbias && tid < nLH) {
-        float v = 0.f;
-        if (per_head_lmk) {
-            v = head_sum(tid, -1);
-        } else {
-            for (int head = 0; head < G; ++head) v += head_sum(head, -1);
+    // ---- db': per-lane head sums of the four waves ----
+    if (a.dbias) {
+        if (lane < 16) sm.db[w][lane] = dbl;
+        __syncthreads();
+        if (tid < nLH) {
+            float v = 0.f;
+            for (int ww = 0; ww < 4; ++ww)
+                for (int l = 0; l < 16; ++l)
+                    if (!per_head_lmk || (ww * 16 + l) / R == tid) v += sm.db[ww][l];
+            const int hl_out = per_head_lmk ? g * G + tid : g;
+            a.dbias[((size_t)b * a.Hl + hl_out) * nC + c] = v;
         }
-        const int hl_out = per_head_lmk ? g * G + tid : g;
-        a.dbias[((size_t)b * a.Hl + hl_out) * nC + c] = v;
     }
 }
 
@@ -522,18 +517,17 @@ struct DqCfg {
 
 template <int D>
 struct DqSmem {
-    static constexpr int KROW = BT<D>::KROW, TROW = BT<D>::TROW;
+    static constexpr int KROW = BT<D>::KROW;
     bf16 k[kChunk * KROW];
     bf16 v[kChunk * KROW];
-    bf16 kt[D * TROW];
 };
 
 template <int D, int G>
 __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, const bf16* dqp, const float* dshat) {
     using C = DqCfg<G>;
-    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, TROW = BT<D>::TROW, IPW = C::IPW;
+    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, IPW = C::IPW;
     __shared__ __align__(16) DqSmem<D> sm;
-    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave, lg = lane / 16;
     const int ntiles = (a.N + C::QT - 1) / C::QT;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
     const int q0 = tile * C::QT;
@@ -541,6 +535,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
     const int kbeg = n_candidates(q0, a.W) * kChunk;
     const size_t bg = (size_t)b * a.Hkv + g;
     const int nC = a.L / kChunk;
+    const bf16* kbase = as<bf16>(a.k) + bg * a.L * D;
+    const bf16* vbase = as<bf16>(a.v) + bg * a.L * D;
+
+    Rows<D> xk = load_rows<D>(kbase + (size_t)kbeg * D);
+    Rows<D> xv = load_rows<D>(vbase + (size_t)kbeg * D);
 
     bf16x8 bq[IPW][KS], bo[IPW][KS];
     f32x4 dq[IPW][DB];
@@ -553,8 +552,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
         const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            bq[it][ks] = ld_bf16x8(as<bf16>(a.q) + qrow * D + ks * 32 + (lane / 16) * 8);
-            bo[it][ks] = ld_bf16x8(as<bf16>(a.dout) + qrow * D + ks * 32 + (lane / 16) * 8);
+            bq[it][ks] = ld_bf16x8(as<bf16>(a.q) + qrow * D + ks * 32 + lg * 8);
+            bo[it][ks] = ld_bf16x8(as<bf16>(a.dout) + qrow * D + ks * 32 + lg * 8);
         }
 #pragma unroll
         for (int db = 0; db < DB; ++db) dq[it][db] = zero4();
@@ -563,9 +562,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
     }
     for (int j0 = kbeg; j0 <= qlast; j0 += kChunk) {
         __syncthreads();
-        stage_k_v_kt<D>(as<bf16>(a.k) + (bg * a.L + j0) * D, as<bf16>(a.v) + (bg * a.L + j0) * D, sm.k, sm.v,
-                        sm.kt);
+        store_rows<D>(sm.k, xk);
+        store_rows<D>(sm.v, xv);
         __syncthreads();
+        if (j0 + kChunk <= qlast) {  // the next key tile, fetched during this one
+            xk = load_rows<D>(kbase + (size_t)(j0 + kChunk) * D);
+            xv = load_rows<D>(vbase + (size_t)(j0 + kChunk) * D);
+        }
 #pragma unroll
         for (int it = 0; it < IPW; ++it) {
             const int item = w + 4 * it;
@@ -588,7 +591,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int j = j0 + kb * 16 + (lane / 16) * 4 + i;
+                    const int j = j0 + kb * 16 + lg * 4 + i;
                     const bool valid = nq < a.N && j <= nq && j >= ell;
                     const float wgt = valid ? fexp(a.scale * s4[kb][i] - Lr[it]) : 0.f;
                     ds[kb][i] = wgt * (gv4[kb][i] - ub[it]);
@@ -597,8 +600,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
             const bf16x8 b1 = pack_perm(ds[2], ds[3]);
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                dq[it][db] = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 0, lane), b0, dq[it][db]);
-                dq[it][db] = mfma16x16x32(perm_operand<TROW>(sm.kt, db * 16, 1, lane), b1, dq[it][db]);
+                dq[it][db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 0, db * 16, lane), b0, dq[it][db]);
+                dq[it][db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, dq[it][db]);
             }
         }
     }
@@ -628,7 +631,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
             const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + cc) * D;
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                const int d0 = db * 16 + (lane / 16) * 4;
+                const int d0 = db * 16 + lg * 4;
                 const uint2 pv = *reinterpret_cast<const uint2*>(prow + d0);
                 const uint2 lv = *reinterpret_cast<const uint2*>(lrow + d0);
                 acc[db][0] += bf_lo(pv.x);
@@ -645,13 +648,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
         bf16* dqr = a.dq_route ? as_mut<bf16>(a.dq_route) + row * D : nullptr;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-            const int d0 = db * 16 + (lane / 16) * 4;
+            const int d0 = db * 16 + lg * 4;
             f32x4 x = acc[db];
             if (!dqr) x += accr[db];
-            *reinterpret_cast<uint2*>(dqo + d0) = make_uint2(pack2(x[0], x[1]), pack2(x[2], x[3]));
+            *reinterpret_cast<uint2*>(dqo + d0) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
             if (dqr)
-                *reinterpret_cast<uint2*>(dqr + d0) =
-                    make_uint2(pack2(accr[db][0], accr[db][1]), pack2(accr[db][2], accr[db][3]));
+                *reinterpret_cast<uint2*>(dqr + d0) = make_uint2(pack_bf16x2(accr[db][0], accr[db][1]),
+                                                                 pack_bf16x2(accr[db][2], accr[db][3]));
         }
     }
 }

@@ -22,17 +22,23 @@ template <typename T>
 __device__ __forceinline__ T from_f32(float x);
 template <>
 __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+// Round to nearest, ties to even, with the hardware conversion (v_cvt_pk_bf16_f32
+// on gfx950; it agrees bit for bit with the integer rounding x + 0x7fff + lsb on
+// finite inputs, denormals included, and keeps NaN a NaN).
 template <>
 __device__ __forceinline__ bf16 from_f32<bf16>(float x) {
-    uint32_t u = __float_as_uint(x);
     bf16 r;
-    if ((u & 0x7fffffffu) > 0x7f800000u) {  // NaN stays NaN
-        r.bits = (uint16_t)((u >> 16) | 0x40u);
-        return r;
-    }
-    u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest, ties to even
-    r.bits = (uint16_t)(u >> 16);
+    r.bits = __builtin_bit_cast(uint16_t, static_cast<__bf16>(x));
     return r;
+}
+
+// Two floats to a packed bf16 pair (lo in the low half).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+    bf16x2_t v;
+    v[0] = static_cast<__bf16>(lo);
+    v[1] = static_cast<__bf16>(hi);
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // Load 8 consecutive elements (16 B for bf16, 32 B for f32) as floats.

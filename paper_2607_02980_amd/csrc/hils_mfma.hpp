@@ -26,13 +26,46 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast
 
 // Round 8 floats to bf16 (nearest-even) into one MFMA operand.
 __device__ __forceinline__ bf16x8 pack_bf16x8(const float* x) {
-    uint32_t w[4];
+    bf16x8 r;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const uint32_t lo = from_f32<bf16>(x[2 * t]).bits, hi = from_f32<bf16>(x[2 * t + 1]).bits;
-        w[t] = lo | (hi << 16);
-    }
-    return as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+    for (int j = 0; j < 8; ++j) r[j] = static_cast<__bf16>(x[j]);
+    return r;
+}
+
+// ds_read_b64_tr_b16 (gfx950 LDS transpose read).  In every 16-lane group,
+// lane t receives element t%4 of the 8-byte words addressed by lanes 4j + t/4
+// of its group, j = 0..3 (layout checked on the hardware).
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4i16 lds_read_tr16(const void* p) {
+    typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
+}
+
+// MFMA operand from a row-major LDS tile X[k][n] (row stride ld elements, rows
+// 8-byte aligned): lane l receives X[k0 + (l/16)*8 + j][n0 + l%16], j = 0..7,
+// i.e. a B operand over (k, n), or an A operand over (m = n, k).
+template <typename E>
+__device__ __forceinline__ bf16x8 tr_operand(const E* X, int ld, int k0, int n0, int lane) {
+    const int g = lane / 16, s = lane % 16;
+    const E* p = X + (size_t)(k0 + g * 8 + s / 4) * ld + n0 + 4 * (s % 4);
+    const v4i16 a = lds_read_tr16(p);
+    const v4i16 b = lds_read_tr16(p + 4 * ld);
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 c = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, c);
+}
+
+// The same over the 32 rows k0 + {4g..4g+3} U {16+4g..16+4g+3} (g = l/16): the
+// key order in which a pair of 16x16 accumulator blocks holds 32 keys.
+template <typename E>
+__device__ __forceinline__ bf16x8 tr_operand_perm(const E* X, int ld, int k0, int n0, int lane) {
+    const int g = lane / 16, s = lane % 16;
+    const E* p = X + (size_t)(k0 + g * 4 + s / 4) * ld + n0 + 4 * (s % 4);
+    const v4i16 a = lds_read_tr16(p);
+    const v4i16 b = lds_read_tr16(p + 16 * ld);
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 c = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, c);
 }
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }

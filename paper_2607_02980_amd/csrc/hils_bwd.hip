@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq_rows(BwdArgs a) {
     __shared__ int s_sel[64];
     __shared__ int s_nsel;
 
-    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int n = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int pos = n;
     const int ncand = n_candidates(pos, a.W);
@@ -377,7 +377,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dkdv_chunks(BwdArgs a, const int
     __shared__ float s_dsh[G], s_L[G], s_db[G];
     __shared__ int s_list[kSortCap];
 
-    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int nC = a.L / kChunk;
     const int j0 = c * kChunk;

@@ -17,12 +17,13 @@
 //                  retrieved c.  Phase 1, one 16-pair tile per wave: S^T = K Q^T and
 //                  GV^T = V dO^T on MFMA, the softmax terms, ds; for retrieving rows also
 //                  s^_c (one more MFMA against the landmark rows), the chunk's share of
-//                  dq (K^T ds^T, stored as a bf16 partial of the row's slot) and ds^_c.
-//                  Phase 2, one 16-key block per wave: dK and dV as MFMA reductions over
-//                  the step's 64 pairs, and dk' as one more (heads x pairs) product.
-//                  The operands of phase 2 are read back from row-major LDS tiles with
-//                  transposing reads (ds_read_b64_tr_b16); the next step's rows are
-//                  fetched while the current step computes.  dk, dv, dk', db' of chunk c
+//                  dq (K^T ds^T / scale, a bf16 partial of the row's slot) and ds^_c.
+//                  K and V stay in registers as the phase-1 operands.  Phase 2, 32 keys
+//                  x half the head dim per wave: dK and dV as MFMA reductions over the
+//                  step's 64 pairs, and dk' as one more (heads x pairs) product, with
+//                  operands read back from row-major LDS tiles by transposing reads
+//                  (ds_read_b64_tr_b16).  The next step's rows are fetched while the
+//                  current step computes.  dk, dv, dk', db' of chunk c
 //                  are written once (no atomics).
 //   k_bwd_dq       query-major: dq over the local window (the forward's local tile with
 //                  ds in place of p), plus the row's slot partials and scale ds^ k'.
@@ -141,7 +142,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_sort(const int* offsets, const i
     __shared__ uint32_t s_bits[kSortWords];
     __shared__ int s_pre[kSortWords];
     __shared__ int s_wave[kBlock / kWave];
-    const int c = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+    const int c = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x, lane = tid % kWave, w = wave_id();
     const int beg = offsets[(size_t)bg * (nC + 1) + c];
     const int len = offsets[(size_t)bg * (nC + 1) + c + 1] - beg;
     if (len == 0) return;
@@ -197,48 +198,70 @@ __global__ __launch_bounds__(kBlock) void k_inv_sort(const int* offsets, const i
 // ---------------------------------------------------------------------------
 // Key-major pass: dK, dV, dK', db' of one chunk and the retrieved chunks' dq partials
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, bool ROUTE>
 struct KeySmem {
     static constexpr int KROW = BT<D>::KROW, PROW = BT<D>::PROW, HROW = BT<D>::HROW;
-    bf16 k[kChunk * KROW];   // K of the chunk, row-major
-    bf16 v[kChunk * KROW];   // V
-    bf16 q[kPairs * KROW];   // q of the step's pairs, row-major [pair][d]
-    bf16 g[kPairs * KROW];   // dO
-    bf16 qr[kPairs * KROW];  // q^ (routing queries given)
-    bf16 p[kPairs * PROW];   // dV weights [pair][key]
-    bf16 ds[kPairs * PROW];  // ds [pair][key]
-    bf16 h[kPairs * HROW];   // ds^_c in the columns of the pair's landmark head
+    bf16 k[kChunk * KROW];                  // K of the chunk, row-major (K^T operands of dq)
+    bf16 q[kPairs * KROW];                  // q of the step's pairs, row-major [pair][d]
+    bf16 g[kPairs * KROW];                  // dO
+    bf16 qr[ROUTE ? kPairs * KROW : 8];     // q^ (routing queries given)
+    bf16 p[kPairs * PROW];                  // dV weights [pair][key]
+    bf16 ds[kPairs * PROW];                 // ds [pair][key]
+    bf16 h[kPairs * HROW];                  // ds^_c in the columns of the pair's landmark head
     float db[4][16];
 };
 
-// The per-pair operands of one step: row entry (n << 6 | slot, or -1), q, dO, q^, L, u.
-template <int KS>
+// The per-pair operands of one step: row entry (n << 6 | slot, or -1), q, dO, q^,
+// L * log2(e) (+inf for an empty pair, which zeroes all its weights) and u.
+template <int KS, bool ROUTE>
 struct PairOps {
-    uint4 q[KS], o[KS], qr[KS];
-    float L, u;
+    uint4 q[KS], o[KS], qr[ROUTE ? KS : 1];
+    float L2, u;
     int ent;
 };
 
-template <int D, int G>
+template <int D, int G, bool ROUTE>
 __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offsets, const int* sorted, const float* u,
                                                      bf16* dqp, float* dshat) {
     constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, PROW = BT<D>::PROW, HROW = BT<D>::HROW;
     constexpr int R = kPairs / G;              // rows per step
     constexpr int HT = G > 4 ? G / 4 : 1;      // heads in one wave's 16-pair tile
-    constexpr int DBW = DB / 4;                // dk' blocks of the head dim per wave
-    __shared__ __align__(16) KeySmem<D> sm;
-    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave, lg = lane / 16;
+    constexpr int DH = DB / 2;                 // phase 2: head-dim blocks per wave
+    constexpr int DBW = DB / 4;                // dk' head-dim blocks per wave
+    __shared__ __align__(16) KeySmem<D, ROUTE> sm;
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const size_t bg = (size_t)b * a.Hkv + g;
     const int j0 = c * kChunk;
     const bool per_head_lmk = (a.Hl == a.Hq);
-    const bool route = a.q_route != nullptr;
     const bf16* qb = as<bf16>(a.q);
     const bf16* gob = as<bf16>(a.dout);
     const bf16* rb = as<bf16>(a.q_route);
-    store_rows<D>(sm.k, load_rows<D>(as<bf16>(a.k) + (bg * a.L + j0) * D));
-    store_rows<D>(sm.v, load_rows<D>(as<bf16>(a.v) + (bg * a.L + j0) * D));
+    const float c1 = a.scale * kLog2e;
+
+    // K and V of the chunk as phase-1 A operands, in registers for the whole block
+    // (lane: key kb*16 + l%16, dims ks*32 + (l/16)*8 ...); wave w also stores key block w
+    // of K into LDS for the K^T operands of the dq partials
+    bf16x8 kA[4][KS], vA[4][KS];
+    {
+        const bf16* kb0 = as<bf16>(a.k) + (bg * a.L + j0) * D;
+        const bf16* vb0 = as<bf16>(a.v) + (bg * a.L + j0) * D;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const size_t off = (size_t)(kb * 16 + lane % 16) * D + ks * 32 + lg * 8;
+                kA[kb][ks] = ld_bf16x8(kb0 + off);
+                vA[kb][ks] = ld_bf16x8(vb0 + off);
+            }
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            if (kb == w)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    *reinterpret_cast<bf16x8*>(sm.k + (kb * 16 + lane % 16) * KROW + ks * 32 + lg * 8) = kA[kb][ks];
+    }
 
     // this lane's pair in phase 1
     const int pair = w * 16 + lane % 16;
@@ -261,9 +284,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
     const int hloc = per_head_lmk ? hh - hfirst : 0;
     const float bias_h = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
 
-    f32x4 dk[DB], dv[DB], dkl[DBW];
+    // phase 2 ownership: keys [32 kh, 32 kh + 32) x head-dim blocks [dh DH, dh DH + DH)
+    const int kh = w % 2, dh = w / 2;
+    f32x4 dk[2][DH], dv[2][DH], dkl[DBW];
 #pragma unroll
-    for (int db = 0; db < DB; ++db) dk[db] = dv[db] = zero4();
+    for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+        for (int dl = 0; dl < DH; ++dl) dk[kb2][dl] = dv[kb2][dl] = zero4();
 #pragma unroll
     for (int t = 0; t < DBW; ++t) dkl[t] = zero4();
     float dbl = 0.f;
@@ -285,7 +312,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
         const int e = (s - nsl) * R + r;
         return e < nret ? seg[e] : -1;
     };
-    auto load_ops = [&](int ent, PairOps<KS>& x) {
+    auto load_ops = [&](int ent, PairOps<KS, ROUTE>& x) {
         x.ent = ent;
         const bool ok = ent >= 0;
         const size_t row = ((size_t)b * a.Hq + h) * a.N + (ok ? (ent >> 6) : 0);
@@ -294,20 +321,20 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
             const int d0 = ks * 32 + lg * 8;
             x.q[ks] = ok ? *reinterpret_cast<const uint4*>(qb + row * D + d0) : make_uint4(0, 0, 0, 0);
             x.o[ks] = ok ? *reinterpret_cast<const uint4*>(gob + row * D + d0) : make_uint4(0, 0, 0, 0);
-            x.qr[ks] = (ok && route) ? *reinterpret_cast<const uint4*>(rb + row * D + d0) : make_uint4(0, 0, 0, 0);
+            if constexpr (ROUTE)
+                x.qr[ks] = ok ? *reinterpret_cast<const uint4*>(rb + row * D + d0) : make_uint4(0, 0, 0, 0);
         }
-        x.L = ok ? a.lse[row] : 0.f;
+        x.L2 = ok ? a.lse[row] * kLog2e : INFINITY;
         x.u = ok ? u[row] : 0.f;
     };
 
-    PairOps<KS> cur;
-    load_ops(entry_of(0), cur);
-    int ent_next = entry_of(1);
-    for (int st = 0; st < nst; ++st) {
+    // one step: compute with `cur` while `nxt` (the following step) and the entry after
+    // it are fetched
+    auto step = [&](int st, const PairOps<KS, ROUTE>& cur, PairOps<KS, ROUTE>& nxt, int& ent_next) {
         const bool retrieval = st >= nsl;
         const int ent_after = entry_of(st + 2);
-        PairOps<KS> nxt;
         load_ops(ent_next, nxt);
+        ent_next = ent_after;
 
         const bool qv = cur.ent >= 0;
         const int qn = cur.ent >> 6, slot = cur.ent & 63;
@@ -318,7 +345,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
             const int d0 = ks * 32 + lg * 8;
             *reinterpret_cast<uint4*>(sm.q + pair * KROW + d0) = cur.q[ks];
             *reinterpret_cast<uint4*>(sm.g + pair * KROW + d0) = cur.o[ks];
-            if (retrieval && route) *reinterpret_cast<uint4*>(sm.qr + pair * KROW + d0) = cur.qr[ks];
+            if constexpr (ROUTE)
+                if (retrieval) *reinterpret_cast<uint4*>(sm.qr + pair * KROW + d0) = cur.qr[ks];
         }
 
         // ---- phase 1: this wave's 16 pairs against the 64 keys ----
@@ -329,21 +357,21 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
             gv4[kb] = zero4();
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                s4[kb] = mfma16x16x32(row_operand<KROW>(sm.k, kb * 16, ks * 32, lane), as_bf16x8(cur.q[ks]), s4[kb]);
-                gv4[kb] = mfma16x16x32(row_operand<KROW>(sm.v, kb * 16, ks * 32, lane), as_bf16x8(cur.o[ks]), gv4[kb]);
+                s4[kb] = mfma16x16x32(kA[kb][ks], as_bf16x8(cur.q[ks]), s4[kb]);
+                gv4[kb] = mfma16x16x32(vA[kb][ks], as_bf16x8(cur.o[ks]), gv4[kb]);
             }
         }
         float pw[4][4], ds[4][4];
-        float dsh = 0.f;
         if (!retrieval) {
-            const int ell = n_candidates(qn, a.W) * kChunk;
+            // rows of the step below j0 + 63 see only part of the chunk (j <= n)
+            const bool diag = st * R < kChunk - 1;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int j = j0 + kb * 16 + lg * 4 + i;
-                    const bool valid = qv && j <= qn && j >= ell;
-                    const float wgt = valid ? fexp(a.scale * s4[kb][i] - cur.L) : 0.f;
+                    float x = fmaf(s4[kb][i], c1, -cur.L2);
+                    if (diag && j0 + kb * 16 + lg * 4 + i > qn) x = -INFINITY;
+                    const float wgt = fexp2(x);
                     pw[kb][i] = wgt;
                     ds[kb][i] = wgt * (gv4[kb][i] - cur.u);
                 }
@@ -351,7 +379,12 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
             // s^_c of the pair: landmark rows (A) against the pair's q^ (B)
             f32x4 sh4 = zero4();
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) sh4 = mfma16x16x32(aL[ks], as_bf16x8(route ? cur.qr[ks] : cur.q[ks]), sh4);
+            for (int ks = 0; ks < KS; ++ks) {
+                if constexpr (ROUTE)
+                    sh4 = mfma16x16x32(aL[ks], as_bf16x8(cur.qr[ks]), sh4);
+                else
+                    sh4 = mfma16x16x32(aL[ks], as_bf16x8(cur.q[ks]), sh4);
+            }
             float mine = sh4[0];
 #pragma unroll
             for (int i = 1; i < 4; ++i)
@@ -359,41 +392,36 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
             const float shat = a.scale * __shfl(mine, lane % 16, kWave) + bias_h;
             float mx = -INFINITY;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, a.scale * s4[kb][i]);
+            for (int kb = 0; kb < 4; ++kb) mx = fmaxf(mx, fmaxf(fmaxf(s4[kb][0], s4[kb][1]), fmaxf(s4[kb][2], s4[kb][3])));
             mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
             mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-            float sum = 0.f;
+            const float m2 = mx * c1;
+            float sum = 0.f, ue = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    pw[kb][i] = fexp(a.scale * s4[kb][i] - mx);
-                    sum += pw[kb][i];
+                    const float e = fexp2(fmaf(s4[kb][i], c1, -m2));
+                    pw[kb][i] = e;
+                    sum += e;
+                    ue = fmaf(e, gv4[kb][i], ue);
                 }
             sum += __shfl_xor(sum, 16, kWave);
             sum += __shfl_xor(sum, 32, kWave);
+            ue += __shfl_xor(ue, 16, kWave);
+            ue += __shfl_xor(ue, 32, kWave);
             const float inv = 1.f / sum;
-            float uc = 0.f;
+            const float uc = ue * inv;
+            const float al = qv ? fexp2(fmaf(shat, kLog2e, -cur.L2)) : 0.f;
+            const float f = al * inv;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    pw[kb][i] *= inv;
-                    uc += pw[kb][i] * gv4[kb][i];
+                    pw[kb][i] *= f;
+                    ds[kb][i] = pw[kb][i] * (gv4[kb][i] - uc);
                 }
-            uc += __shfl_xor(uc, 16, kWave);
-            uc += __shfl_xor(uc, 32, kWave);
-            const float al = qv ? fexp(shat - cur.L) : 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    ds[kb][i] = al * pw[kb][i] * (gv4[kb][i] - uc);
-                    pw[kb][i] *= al;
-                }
-            dsh = al * (uc - cur.u);
+            const float dsh = al * (uc - cur.u);
             if (qv && lane < 16) dshat[qrow * a.K + slot] = dsh;
             // H row of the pair: ds^ split into a bf16 head and its bf16 residual, in
             // columns m and 8 + m of its landmark head m (the product then keeps ds^ to
@@ -424,7 +452,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                 make_uint2(pack_bf16x2(ds[kb][0], ds[kb][1]), pack_bf16x2(ds[kb][2], ds[kb][3]));
         }
         if (retrieval) {
-            // the chunk's share of dq: dq^T = scale K^T ds^T, into the row's slot partial
+            // the chunk's share of dq / scale: K^T ds^T, into the row's slot partial
             const bf16x8 b0 = pack_perm(ds[0], ds[1]);
             const bf16x8 b1 = pack_perm(ds[2], ds[3]);
             bf16* prow = dqp + (qrow * a.K + slot) * D;
@@ -435,55 +463,74 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                 o = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, o);
                 if (qv)
                     *reinterpret_cast<uint2*>(prow + db * 16 + lg * 4) =
-                        make_uint2(pack_bf16x2(a.scale * o[0], a.scale * o[1]),
-                                   pack_bf16x2(a.scale * o[2], a.scale * o[3]));
+                        make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
             }
         }
         __syncthreads();
-        // ---- phase 2: keys [16w, 16w+16) x all dims over the 64 pairs; dk' blocks w, w+4 ----
-        bf16x8 ads[2], ap[2], ah[2];
+        // ---- phase 2: keys [32kh, 32kh + 32) x head-dim blocks of dh, over the 64 pairs ----
+        bf16x8 ads[2][2], ap[2][2], ah[2];
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            ads[t] = tr_operand(sm.ds, PROW, t * 32, w * 16, lane);
-            ap[t] = tr_operand(sm.p, PROW, t * 32, w * 16, lane);
-            if (retrieval) ah[t] = tr_operand(sm.h, HROW, t * 32, 0, lane);
-        }
+        for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+            for (int t = 0; t < 2; ++t) {
+                ads[kb2][t] = tr_operand(sm.ds, PROW, t * 32, (2 * kh + kb2) * 16, lane);
+                ap[kb2][t] = tr_operand(sm.p, PROW, t * 32, (2 * kh + kb2) * 16, lane);
+            }
+        if (retrieval)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) ah[t] = tr_operand(sm.h, HROW, t * 32, 0, lane);
+#pragma unroll
+        for (int dl = 0; dl < DH; ++dl) {
+            const int db = dh * DH + dl;
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 const bf16x8 bq = tr_operand(sm.q, KROW, t * 32, db * 16, lane);
-                dk[db] = mfma16x16x32(ads[t], bq, dk[db]);
-                dv[db] = mfma16x16x32(ap[t], tr_operand(sm.g, KROW, t * 32, db * 16, lane), dv[db]);
-                if (retrieval && db % 4 == w) {
-                    const bf16x8 bqr = route ? tr_operand(sm.qr, KROW, t * 32, db * 16, lane) : bq;
-                    dkl[db / 4] = mfma16x16x32(ah[t], bqr, dkl[db / 4]);
+                const bf16x8 bgo = tr_operand(sm.g, KROW, t * 32, db * 16, lane);
+#pragma unroll
+                for (int kb2 = 0; kb2 < 2; ++kb2) {
+                    dk[kb2][dl] = mfma16x16x32(ads[kb2][t], bq, dk[kb2][dl]);
+                    dv[kb2][dl] = mfma16x16x32(ap[kb2][t], bgo, dv[kb2][dl]);
+                }
+                if (retrieval && dl / DBW == kh) {
+                    if constexpr (ROUTE)
+                        dkl[dl % DBW] = mfma16x16x32(ah[t], tr_operand(sm.qr, KROW, t * 32, db * 16, lane), dkl[dl % DBW]);
+                    else
+                        dkl[dl % DBW] = mfma16x16x32(ah[t], bq, dkl[dl % DBW]);
                 }
             }
-        cur = nxt;
-        ent_next = ent_after;
+        }
+    };
+
+    PairOps<KS, ROUTE> opa, opb;
+    load_ops(entry_of(0), opa);
+    int ent_next = entry_of(1);
+    for (int st = 0; st < nst; st += 2) {
+        step(st, opa, opb, ent_next);
+        if (st + 1 < nst) step(st + 1, opb, opa, ent_next);
     }
 
-    // ---- dK, dV of the chunk (lane: key 16w + (l/16)*4 + i, dim 16db + l%16) ----
+    // ---- dK, dV of the chunk (lane: key 16(2kh + kb2) + (l/16)*4 + i, dim 16 db + l%16) ----
     bf16* dkp = as_mut<bf16>(a.dk) + (bg * a.L + j0) * D;
     bf16* dvp = as_mut<bf16>(a.dv) + (bg * a.L + j0) * D;
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+    for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int key = w * 16 + lg * 4 + i, d = db * 16 + lane % 16;
-            dkp[key * D + d] = from_f32<bf16>(a.scale * dk[db][i]);
-            dvp[key * D + d] = from_f32<bf16>(dv[db][i]);
-        }
+        for (int dl = 0; dl < DH; ++dl)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int key = (2 * kh + kb2) * 16 + lg * 4 + i, d = (dh * DH + dl) * 16 + lane % 16;
+                dkp[key * D + d] = from_f32<bf16>(a.scale * dk[kb2][dl][i]);
+                dvp[key * D + d] = from_f32<bf16>(dv[kb2][dl][i]);
+            }
     // ---- dK' (lane: rows (l/16)*4 + i = head m and its residual row m + 8 in lane l ^ 32,
-    // dim 16(w + 4t) + l%16) ----
+    // dim 16(dh DH + kh DBW + t) + l%16) ----
     const int nLH = per_head_lmk ? G : 1;
 #pragma unroll
     for (int t = 0; t < DBW; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const float v = dkl[t][i] + __shfl_xor(dkl[t][i], 32, kWave);
-            const int m = lg * 4 + i, d = (w + 4 * t) * 16 + lane % 16;
+            const int m = lg * 4 + i, d = (dh * DH + kh * DBW + t) * 16 + lane % 16;
             if (lg < 2 && m < nLH) {
                 const int hl_out = per_head_lmk ? g * G + m : g;
                 as_mut<bf16>(a.dlmk)[(((size_t)b * a.Hl + hl_out) * nC + c) * D + d] = from_f32<bf16>(a.scale * v);
@@ -527,7 +574,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
     using C = DqCfg<G>;
     constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, IPW = C::IPW;
     __shared__ __align__(16) DqSmem<D> sm;
-    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave, lg = lane / 16;
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int ntiles = (a.N + C::QT - 1) / C::QT;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
     const int q0 = tile * C::QT;
@@ -620,7 +667,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
         f32x4 acc[DB], accr[DB];
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-            acc[db] = dq[it][db] * a.scale;
+            acc[db] = dq[it][db];
             accr[db] = zero4();
         }
         for (int k = 0; k < a.K; ++k) {
@@ -649,7 +696,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
             const int d0 = db * 16 + lg * 4;
-            f32x4 x = acc[db];
+            f32x4 x = acc[db] * a.scale;
             if (!dqr) x += accr[db];
             *reinterpret_cast<uint2*>(dqo + d0) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
             if (dqr)
@@ -676,8 +723,12 @@ struct BwRun {
         launch_inverse_index(ia, ly.inv, a.ws, s, false);
         HILS_LAUNCH("k_inv_sort", k_inv_sort, dim3(nC, a.B * a.Hkv), dim3(kBlock), 0, s, offsets,
                     reinterpret_cast<const int*>(ws + ly.inv.list), sorted, a.N, a.K, nC, a.W);
-        HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a, offsets,
-                    (const int*)sorted, (const float*)u, dqp, dsh);
+        if (a.q_route)
+            HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, true>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a, offsets,
+                        (const int*)sorted, (const float*)u, dqp, dsh);
+        else
+            HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, false>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a, offsets,
+                        (const int*)sorted, (const float*)u, dqp, dsh);
         HILS_LAUNCH("k_bwd_dq", (k_bwd_dq<D, G>), dim3((a.N + DqCfg<G>::QT - 1) / DqCfg<G>::QT, a.Hkv, a.B),
                     dim3(kBlock), 0, s, a, (const float*)u, (const bf16*)dqp, (const float*)dsh);
         return hipGetLastError();

@@ -109,7 +109,7 @@ __device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G
                          int nk, bool is_chunk) {
     constexpr int RB = PartSmem<T, D, G>::kRowBytes;
     constexpr int PIECES = D * (int)sizeof(T) / 16;  // 16-byte pieces per row
-    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const size_t kv_off = (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
     const unsigned char* kg = reinterpret_cast<const unsigned char*>(as<T>(a.k) + kv_off);
     const unsigned char* vg = reinterpret_cast<const unsigned char*>(as<T>(a.v) + kv_off);
@@ -251,7 +251,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan_local(FwdArgs a) {
     auto& s_tid = ss.tid;
     auto& s_osc = ss.osc;
     auto& s_tsc = ss.tsc;
-    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int c0 = blockIdx.x * kSlice;
     const int len = min(kSlice, ncand - c0);
     float* cand_sc = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.cand);
@@ -351,7 +351,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a) {
     __shared__ int s_wid[NW][64], s_tid[NW][64], s_bid[64];
     __shared__ float s_wsc[NW][64], s_tsc[NW][64], s_bsc[64];
     __shared__ int s_wn[NW];
-    const int b = blockIdx.y, g = blockIdx.x, tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int b = blockIdx.y, g = blockIdx.x, tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
     const float* cand_sc = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.cand);
     const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.Hkv * ly.nslices * a.K);
@@ -426,7 +426,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
     constexpr int kMaxParts = 64 + kMaxLocalPieces;
     __shared__ float s_w[G][kMaxParts];  // weight of each part's unnormalised o
     __shared__ float s_lse[G];
-    const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
     for (int hh = wave; hh < G; hh += kBlock / kWave) {
         // local pieces: lanes < nlocal

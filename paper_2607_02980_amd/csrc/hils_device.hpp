@@ -9,6 +9,12 @@ namespace hils {
 constexpr int kWave = 64;
 constexpr int kChunk = 64;  // S: the only chunk size with kernels
 
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar) value.
+// Conditions built from it compile to scalar branches; this matters for MFMA,
+// which does not honour the EXEC mask, so an MFMA under a lane-masked branch
+// that the compiler cannot prove uniform still runs when every lane is off.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave); }
+
 // ---- storage types -------------------------------------------------------
 
 struct bf16 {
@@ -91,6 +97,9 @@ __device__ __forceinline__ float group_sum(float x) {
 
 // exp(x) for x <= 0 typically; exact -inf -> 0.
 __device__ __forceinline__ float fexp(float x) { return __expf(x); }
+// 2^x with the hardware instruction (v_exp_f32); exp(x) = fexp2(x * kLog2e).
+constexpr float kLog2e = 1.4426950408889634f;
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Order-preserving map float -> uint32 (larger float => larger key; -0 < +0).
 __device__ __forceinline__ uint32_t ordered_key(float f) {

@@ -36,7 +36,7 @@ __global__ __launch_bounds__(kBlock) void k_score_topk_rows(FwdArgs a) {
     __shared__ int s_tid[4][64];
     __shared__ float s_tsc[4][64];
 
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int wave = wave_id(), lane = threadIdx.x % kWave;
     const long row = (long)blockIdx.x * 4 + wave;
     if (row >= (long)a.B * a.Hkv * a.N) return;  // whole wave leaves; no block barriers below
     const int n = (int)(row % a.N);
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kBlock) void k_attn_rows(FwdArgs a) {
     __shared__ int s_sel[64];
     __shared__ int s_nsel;
 
-    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int n = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int pos = query_position(a, b, n);
     const int ncand = n_candidates(pos, a.W);

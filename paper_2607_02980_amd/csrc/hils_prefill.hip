@@ -122,7 +122,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
     __shared__ float s_sig[kSQ][kSL + 1];
     __shared__ int s_tid[4][64], s_oid[4][64];
     __shared__ float s_tsc[4][64], s_osc[4][64];
-    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
     const int ntiles = (a.N + kSQ - 1) / kSQ;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
     const int q0 = tile * kSQ;
@@ -261,7 +261,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
     __shared__ __align__(16) bf16 s_k[kChunk * Tiles<D>::KROW];
     __shared__ __align__(16) bf16 s_vt[D * Tiles<D>::VROW];
-    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
     const int nC = a.L / kChunk;
     if ((int)blockIdx.x >= *nwork) return;
     const int4 wi = work[blockIdx.x];
@@ -370,7 +370,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB, IPW = C::IPW;
     __shared__ __align__(16) bf16 s_k[kChunk * Tiles<D>::KROW];
     __shared__ __align__(16) bf16 s_vt[D * Tiles<D>::VROW];
-    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
     const int ntiles = (a.N + C::QT - 1) / C::QT;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
     const int q0 = tile * C::QT;

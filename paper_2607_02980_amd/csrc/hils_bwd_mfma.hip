@@ -71,6 +71,14 @@ struct BT {
     static constexpr int HROW = 16 + 8;  // padded row of the [64 pairs][16 heads] tile
 };
 
+// The value, moved through a vector register: the compiler then treats it as
+// per-lane and selects with it instead of branching.
+__device__ __forceinline__ int in_vgpr(int x) {
+    int y;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
+    return y;
+}
+
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -303,15 +311,21 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
     const int nsl = (nlocal + R - 1) / R;
     const int nst = nsl + (nret + R - 1) / R;
 
+    // Loads below are branch-free (indices clamped to a valid row, the result masked
+    // afterwards) so that the compiler can count outstanding loads exactly and the
+    // prefetch of the next step is not drained by a full wait at every step.
     auto entry_of = [&](int s) -> int {
-        if (s >= nst) return -1;
-        if (s < nsl) {
-            const int e = s * R + r;
-            return e < nlocal ? (n_lo + e) << 6 : -1;
-        }
-        const int e = (s - nsl) * R + r;
-        return e < nret ? seg[e] : -1;
+        // `loc` goes through a vector register so that the choice below is a select,
+        // not a scalar branch around the load
+        const int loc = in_vgpr(s < nsl ? 1 : 0);
+        const int e = loc ? s * R + r : (s - nsl) * R + r;
+        const int lim = loc ? nlocal : nret;
+        const int got = seg[min(max(e, 0), max(nret - 1, 0))];
+        const int ent = loc ? (n_lo + e) << 6 : got;
+        return (s < nst && e < lim) ? ent : -1;
     };
+    // An empty pair (ent < 0) reads row 0 and gets L = +inf, so that every weight
+    // and gradient term it produces is exactly zero.
     auto load_ops = [&](int ent, PairOps<KS, ROUTE>& x) {
         x.ent = ent;
         const bool ok = ent >= 0;
@@ -319,13 +333,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             const int d0 = ks * 32 + lg * 8;
-            x.q[ks] = ok ? *reinterpret_cast<const uint4*>(qb + row * D + d0) : make_uint4(0, 0, 0, 0);
-            x.o[ks] = ok ? *reinterpret_cast<const uint4*>(gob + row * D + d0) : make_uint4(0, 0, 0, 0);
-            if constexpr (ROUTE)
-                x.qr[ks] = ok ? *reinterpret_cast<const uint4*>(rb + row * D + d0) : make_uint4(0, 0, 0, 0);
+            x.q[ks] = *reinterpret_cast<const uint4*>(qb + row * D + d0);
+            x.o[ks] = *reinterpret_cast<const uint4*>(gob + row * D + d0);
+            if constexpr (ROUTE) x.qr[ks] = *reinterpret_cast<const uint4*>(rb + row * D + d0);
         }
-        x.L2 = ok ? a.lse[row] * kLog2e : INFINITY;
-        x.u = ok ? u[row] : 0.f;
+        const float L = a.lse[row];
+        x.L2 = ok ? L * kLog2e : INFINITY;
+        x.u = u[row];
     };
 
     // one step: compute with `cur` while `nxt` (the following step) and the entry after

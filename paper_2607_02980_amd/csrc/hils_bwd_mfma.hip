@@ -469,16 +469,13 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
             // the chunk's share of dq / scale: K^T ds^T, into the row's slot partial
             const bf16x8 b0 = pack_perm(ds[0], ds[1]);
             const bf16x8 b1 = pack_perm(ds[2], ds[3]);
-            bf16* prow = dqp + (qrow * a.K + slot) * D;
+            f32x4 od[DB];
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                f32x4 o = zero4();
-                o = mfma16x16x32(tr_operand_perm(sm.k, KROW, 0, db * 16, lane), b0, o);
-                o = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, o);
-                if (qv)
-                    *reinterpret_cast<uint2*>(prow + db * 16 + lg * 4) =
-                        make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+                od[db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 0, db * 16, lane), b0, zero4());
+                od[db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, od[db]);
             }
+            if (qv) store_lane_order<D>(dqp + (qrow * a.K + slot) * D, od, lg);
         }
         __syncthreads();
         // ---- phase 2: keys [32kh, 32kh + 32) x head-dim blocks of dh, over the 64 pairs ----
@@ -684,25 +681,39 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
             acc[db] = dq[it][db];
             accr[db] = zero4();
         }
-        for (int k = 0; k < a.K; ++k) {
-            if (!idx_entry_valid(irow, k, ncand)) continue;
-            const int cc = irow[k];
-            const float x = a.scale * dshat[row * a.K + k];
-            const bf16* prow = dqp + (row * a.K + k) * D;
-            const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + cc) * D;
+        // the row's slots, SB at a time with every load in flight before use
+        constexpr int SB = D >= 128 ? 4 : 8;
+        int prev = -1;
+        for (int k0 = 0; k0 < a.K; k0 += SB) {
+            float xk[SB];
+            bool okk[SB];
+            uint4 pv[SB][D / 32];
+            uint2 lv[SB][DB];
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d0 = db * 16 + lg * 4;
-                const uint2 pv = *reinterpret_cast<const uint2*>(prow + d0);
-                const uint2 lv = *reinterpret_cast<const uint2*>(lrow + d0);
-                acc[db][0] += bf_lo(pv.x);
-                acc[db][1] += bf_hi(pv.x);
-                acc[db][2] += bf_lo(pv.y);
-                acc[db][3] += bf_hi(pv.y);
-                accr[db][0] += x * bf_lo(lv.x);
-                accr[db][1] += x * bf_hi(lv.x);
-                accr[db][2] += x * bf_lo(lv.y);
-                accr[db][3] += x * bf_hi(lv.y);
+            for (int u = 0; u < SB; ++u) {
+                const int k = min(k0 + u, a.K - 1);
+                const int cc = irow[k];
+                const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
+                prev = cc;  // idx_entry_valid compares with the previous entry as written
+                const float xv = dshat[row * a.K + k];
+                xk[u] = ok ? a.scale * xv : 0.f;
+                okk[u] = ok;
+                const int kk = ok ? k : 0, ck = ok ? cc : 0;
+                load_lane_order<D>(dqp + (row * a.K + kk) * D, lg, pv[u]);
+                const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + ck) * D;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) lv[u][db] = *reinterpret_cast<const uint2*>(lrow + db * 16 + lg * 4);
+            }
+#pragma unroll
+            for (int u = 0; u < SB; ++u) {
+                fma_lane_order<D>(pv[u], 1.f, okk[u], acc);
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    accr[db][0] += xk[u] * bf_lo(lv[u][db].x);
+                    accr[db][1] += xk[u] * bf_hi(lv[u][db].x);
+                    accr[db][2] += xk[u] * bf_lo(lv[u][db].y);
+                    accr[db][3] += xk[u] * bf_hi(lv[u][db].y);
+                }
             }
         }
         bf16* dqo = as_mut<bf16>(a.dq) + row * D;

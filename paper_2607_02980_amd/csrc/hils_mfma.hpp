@@ -68,6 +68,50 @@ __device__ __forceinline__ bf16x8 tr_operand_perm(const E* X, int ld, int k0, in
     return __builtin_bit_cast(bf16x8, c);
 }
 
+// "Lane order" of a D-vector held as O^T accumulators (DB = D/16 blocks, lane
+// group lg = l/16 holding d = 16 db + 4 lg + i): element d is stored at position
+// lg * D/4 + 4 db + i, so that the four lanes of a row move 64 contiguous bytes
+// each (D = 128) with 16-byte accesses.  Used for the per-slot partial vectors
+// that one kernel writes and another reads in the same lane layout.
+template <int D>
+__device__ __forceinline__ void store_lane_order(bf16* row, const f32x4* o, int lg) {
+    uint32_t w[D / 8];
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+        w[2 * db] = pack_bf16x2(o[db][0], o[db][1]);
+        w[2 * db + 1] = pack_bf16x2(o[db][2], o[db][3]);
+    }
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) {
+        const u32x4 v = {w[4 * t], w[4 * t + 1], w[4 * t + 2], w[4 * t + 3]};
+        reinterpret_cast<u32x4*>(row + lg * (D / 4))[t] = v;
+    }
+}
+
+// Loads a lane-order vector; fma_lane_order adds wgt times it to acc (O^T layout).
+template <int D>
+__device__ __forceinline__ void load_lane_order(const bf16* row, int lg, uint4* x) {
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) x[t] = reinterpret_cast<const uint4*>(row + lg * (D / 4))[t];
+}
+// (ok = false adds nothing, whatever bits x holds.)
+template <int D>
+__device__ __forceinline__ void fma_lane_order(const uint4* x, float wgt, bool ok, f32x4* acc) {
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) {
+        const uint32_t v[4] = {ok ? x[t].x : 0u, ok ? x[t].y : 0u, ok ? x[t].z : 0u, ok ? x[t].w : 0u};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int db = 2 * t + h;
+            acc[db][0] += wgt * __uint_as_float(v[2 * h] << 16);
+            acc[db][1] += wgt * __uint_as_float(v[2 * h] & 0xffff0000u);
+            acc[db][2] += wgt * __uint_as_float(v[2 * h + 1] << 16);
+            acc[db][3] += wgt * __uint_as_float(v[2 * h + 1] & 0xffff0000u);
+        }
+    }
+}
+
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
 // Block index remap so that consecutive logical blocks run on the same XCD

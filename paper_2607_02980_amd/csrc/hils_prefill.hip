@@ -22,9 +22,11 @@
 // queries on N).  The accumulator then holds, in lane l, 4 consecutive keys of
 // query l%16, which is exactly the B-operand layout of O^T = V^T P^T when the
 // keys of a 32-key step are taken in the order the accumulators hold them
-// ({4g..4g+3} U {16+4g..16+4g+3} for lane group g = l/16); V^T is staged in
-// LDS so the matching A-operand reads are two 8-byte loads.  Every O^T value a
-// lane holds belongs to its own query, so softmax rescaling is lane-local.
+// ({4g..4g+3} U {16+4g..16+4g+3} for lane group g = l/16); V stays row-major in
+// LDS and the matching A operands come from transposing reads
+// (ds_read_b64_tr_b16).  Every O^T value a lane holds belongs to its own query,
+// so softmax rescaling is lane-local.  Per-slot partial vectors are stored in
+// the accumulators' lane order (store_lane_order).
 #include "hils_device.hpp"
 #include "hils_dispatch.hpp"
 #include "hils_internal.hpp"
@@ -44,7 +46,8 @@ struct PfLayout {
     size_t total;
 };
 
-// part [B, Hq, N, K, d] bf16, wgt [B, Hq, N, K] f32, ref [B, Hkv, N] f32, inverse index
+// part [B, Hq, N, K, d] bf16 (each d-vector in lane order), wgt [B, Hq, N, K] f32,
+// ref [B, Hkv, N] f32, inverse index
 PfLayout pf_layout(int B, int Hq, int Hkv, int N, int L, int d, int K) {
     PfLayout w;
     w.part = 0;
@@ -60,33 +63,32 @@ template <int D>
 struct Tiles {
     static constexpr int KS = D / 32;      // k-steps over the head dimension
     static constexpr int DB = D / 16;      // 16-wide blocks of the head dimension
-    static constexpr int KROW = D + 8;     // bf16 per padded K row in LDS
-    static constexpr int VROW = 64 + 8;    // bf16 per padded V^T row in LDS
+    static constexpr int KROW = D + 8;     // bf16 per padded K / V row in LDS
+    static constexpr int PPT = kChunk * D / 8 / kBlock;  // 16-byte pieces of a K or V block per thread
 };
 
-// Stage one 64-key block: K rows (padded) and V transposed into LDS.
+// One 64-key block of K or V in registers (PPT 16-byte pieces per thread), and its
+// store into a padded row-major LDS tile.
 template <int D>
-__device__ __forceinline__ void stage_kv(const bf16* kb, const bf16* vb, bf16* s_k, bf16* s_vt) {
-    constexpr int KROW = Tiles<D>::KROW, VROW = Tiles<D>::VROW;
-    constexpr int PPT = kChunk * D / 8 / kBlock;  // 16-byte pieces per thread
-    const int tid = threadIdx.x;
-    uint4 xk[PPT], xv[PPT];
+struct KVRegs {
+    uint4 x[Tiles<D>::PPT];
+};
+template <int D>
+__device__ __forceinline__ KVRegs<D> load_block(const bf16* src) {
+    KVRegs<D> r;
 #pragma unroll
-    for (int u = 0; u < PPT; ++u) {
-        const int e = tid + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
-        xk[u] = *reinterpret_cast<const uint4*>(kb + (size_t)j * D + d8);
-        xv[u] = *reinterpret_cast<const uint4*>(vb + (size_t)j * D + d8);
+    for (int u = 0; u < Tiles<D>::PPT; ++u) {
+        const int e = threadIdx.x + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+        r.x[u] = *reinterpret_cast<const uint4*>(src + (size_t)j * D + d8);
     }
+    return r;
+}
+template <int D>
+__device__ __forceinline__ void store_block(bf16* tile, const KVRegs<D>& r) {
 #pragma unroll
-    for (int u = 0; u < PPT; ++u) {
-        const int e = tid + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
-        *reinterpret_cast<uint4*>(s_k + j * KROW + d8) = xk[u];
-        const uint32_t w[4] = {xv[u].x, xv[u].y, xv[u].z, xv[u].w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            s_vt[(d8 + 2 * t) * VROW + j].bits = (uint16_t)(w[t] & 0xffffu);
-            s_vt[(d8 + 2 * t + 1) * VROW + j].bits = (uint16_t)(w[t] >> 16);
-        }
+    for (int u = 0; u < Tiles<D>::PPT; ++u) {
+        const int e = threadIdx.x + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+        *reinterpret_cast<uint4*>(tile + j * Tiles<D>::KROW + d8) = r.x[u];
     }
 }
 
@@ -96,13 +98,11 @@ __device__ __forceinline__ bf16x8 k_operand(const bf16* s_k, int kb, int ks, int
     return ld_bf16x8(s_k + (kb * 16 + lane % 16) * Tiles<D>::KROW + ks * 32 + (lane / 16) * 8);
 }
 
-// A operand of O^T = V^T P^T for dims block db and 32-key step t (permuted key order).
+// A operand of O^T = V^T P^T for dims block db and 32-key step t (permuted key
+// order), read from row-major V with transposing loads.
 template <int D>
-__device__ __forceinline__ bf16x8 vt_operand(const bf16* s_vt, int db, int t, int lane) {
-    const bf16* row = s_vt + (db * 16 + lane % 16) * Tiles<D>::VROW + 32 * t + (lane / 16) * 4;
-    const uint2 lo = *reinterpret_cast<const uint2*>(row);
-    const uint2 hi = *reinterpret_cast<const uint2*>(row + 16);
-    return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+__device__ __forceinline__ bf16x8 vt_operand(const bf16* s_v, int db, int t, int lane) {
+    return tr_operand_perm(s_v, Tiles<D>::KROW, 32 * t, db * 16, lane);
 }
 
 // B operand of O^T = V^T P^T from exponentiated S^T accumulators of key blocks 2t, 2t+1.
@@ -254,14 +254,18 @@ __global__ __launch_bounds__(kWave) void k_pf_ref_given(FwdArgs a, float* ref_ou
 // P3: retrieved chunks, chunk-major
 // ---------------------------------------------------------------------------
 // One block per work item: kInvSeg consecutive entries of one (b, g, chunk) list.
-template <int D, int G>
+// Units of work are (16 entries, head) pairs; wave w takes units w, w + 4, ...
+// K and V^T of the chunk are held in registers as MFMA operands for the whole
+// block, and the next unit's rows are fetched while the current one computes.
+template <int D, int G, bool ROUTE>
 __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offsets, const int* list,
                                                       const int4* work, const int* nwork, const float* ref,
                                                       bf16* part, float* wgt) {
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
+    constexpr int HW = G > 4 ? 2 : 1;  // heads a wave visits
     __shared__ __align__(16) bf16 s_k[kChunk * Tiles<D>::KROW];
-    __shared__ __align__(16) bf16 s_vt[D * Tiles<D>::VROW];
-    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
+    __shared__ __align__(16) bf16 s_v[kChunk * Tiles<D>::KROW];
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
     if ((int)blockIdx.x >= *nwork) return;
     const int4 wi = work[blockIdx.x];
@@ -272,84 +276,117 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
     const int len = min(kInvSeg, offsets[bg * (nC + 1) + c + 1] - beg);
     if (len <= 0) return;
     const int* seg = list + bg * a.N * a.K + beg;
-    stage_kv<D>(as<bf16>(a.k) + (bg * a.L + (size_t)c * kChunk) * D, as<bf16>(a.v) + (bg * a.L + (size_t)c * kChunk) * D,
-                s_k, s_vt);
+    store_block<D>(s_k, load_block<D>(as<bf16>(a.k) + (bg * a.L + (size_t)c * kChunk) * D));
+    store_block<D>(s_v, load_block<D>(as<bf16>(a.v) + (bg * a.L + (size_t)c * kChunk) * D));
     __syncthreads();
+    bf16x8 kA[4][KS], vA[DB][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kA[kb][ks] = k_operand<D>(s_k, kb, ks, lane);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) vA[db][t] = vt_operand<D>(s_v, db, t, lane);
+    // landmark rows of the wave's heads as the A operand of s^ (row 0 of the tile)
+    bf16x8 aL[HW][KS];
+    float bias_h[HW];
+#pragma unroll
+    for (int x = 0; x < HW; ++x) {
+        const int hh = (w + 4 * x) % G, h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
+        const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            aL[x][ks] = (lane % 16 == 0) ? ld_bf16x8(lrow + ks * 32 + lg * 8) : as_bf16x8(make_uint4(0, 0, 0, 0));
+        bias_h[x] = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
+    }
+    const float c1 = a.scale * kLog2e;
     const bf16* qbase = as<bf16>(a.q);
     const bf16* rbase = as<bf16>(a.q_route);
-    for (int e0 = 0; e0 < len; e0 += 16) {
-        const int e = e0 + lane % 16;
-        const bool qv = e < len;
-        const int ent = qv ? seg[e] : 0;
-        const int n = ent >> 6, slot = ent & 63;
-        const float rf = qv ? ref[bg * a.N + n] : 0.f;
-        for (int hh = w; hh < G; hh += 4) {
-            const int h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
-            const size_t qrow = ((size_t)b * a.Hq + h) * a.N + n;
-            bf16x8 bq[KS];
+    const int nunits = ((len + 15) / 16) * G;
+
+    struct Ops {
+        uint4 q[KS], qr[ROUTE ? KS : 1];
+        float rf;
+        int ent;
+    };
+    // branch-free loads: an entry past the end reads the last entry's row
+    auto load_ops = [&](int u, Ops& x) {
+        const int grp = u / G, hh = u % G;
+        const int e = min(grp * 16 + lane % 16, len - 1);
+        const int ent = seg[e];
+        x.ent = (u < nunits && grp * 16 + lane % 16 < len) ? ent : -1;
+        const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + (ent >> 6);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                bq[ks] = qv ? ld_bf16x8(qbase + qrow * D + ks * 32 + (lane / 16) * 8) : as_bf16x8(make_uint4(0, 0, 0, 0));
-            // surrogate score s^ = q^ . k'_c: the landmark row is row 0 of the A tile
-            f32x4 sh4 = zero4();
-            const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 al = (lane % 16 == 0) ? ld_bf16x8(lrow + ks * 32 + (lane / 16) * 8)
-                                                   : as_bf16x8(make_uint4(0, 0, 0, 0));
-                const bf16x8 br = (rbase && qv) ? ld_bf16x8(rbase + qrow * D + ks * 32 + (lane / 16) * 8) : bq[ks];
-                sh4 = mfma16x16x32(al, br, sh4);
-            }
-            float shat = __shfl(sh4[0], lane % 16, kWave);
-            shat = a.scale * shat + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f);
-            // S^T = K_c Q^T
-            f32x4 st[4];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                st[kb] = zero4();
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(k_operand<D>(s_k, kb, ks, lane), bq[ks], st[kb]);
-            }
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    st[kb][i] *= a.scale;
-                    mx = fmaxf(mx, st[kb][i]);
-                }
-            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-            float sum = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) sum += fexp(st[kb][i] - mx);
-            sum += __shfl_xor(sum, 16, kWave);
-            sum += __shfl_xor(sum, 32, kWave);
-            // intra-chunk softmax: p_j = exp(s_j - lse_c)
-            const float off = qv ? -(mx + __logf(sum)) : -INFINITY;
-            float ex[4][4];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) ex[kb][i] = fexp(st[kb][i] + off);
-            const bf16x8 pb0 = p_operand(ex[0], ex[1]);
-            const bf16x8 pb1 = p_operand(ex[2], ex[3]);
-            bf16* prow = part + (qrow * a.K + slot) * D;
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                f32x4 o = zero4();
-                o = mfma16x16x32(vt_operand<D>(s_vt, db, 0, lane), pb0, o);
-                o = mfma16x16x32(vt_operand<D>(s_vt, db, 1, lane), pb1, o);
-                if (qv) {
-                    const uint32_t lo = from_f32<bf16>(o[0]).bits | ((uint32_t)from_f32<bf16>(o[1]).bits << 16);
-                    const uint32_t hi = from_f32<bf16>(o[2]).bits | ((uint32_t)from_f32<bf16>(o[3]).bits << 16);
-                    *reinterpret_cast<uint2*>(prow + db * 16 + (lane / 16) * 4) = make_uint2(lo, hi);
-                }
-            }
-            if (qv && lane < 16) wgt[qrow * a.K + slot] = fexp(shat - rf);
+        for (int ks = 0; ks < KS; ++ks) {
+            x.q[ks] = *reinterpret_cast<const uint4*>(qbase + qrow * D + ks * 32 + lg * 8);
+            if constexpr (ROUTE) x.qr[ks] = *reinterpret_cast<const uint4*>(rbase + qrow * D + ks * 32 + lg * 8);
         }
+        x.rf = ref[bg * a.N + (ent >> 6)];
+    };
+    auto unit = [&](int u, const Ops& cur, Ops& nxt) {
+        load_ops(u + 4, nxt);
+        const int hh = u % G, x = HW > 1 ? (u / 4) % 2 : 0;
+        const bool qv = cur.ent >= 0;
+        const int n = cur.ent >> 6, slot = cur.ent & 63;
+        const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + (qv ? n : 0);
+        // surrogate score s^ = q^ . k'_c: the landmark row is row 0 of the A tile
+        f32x4 sh4 = zero4();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if constexpr (ROUTE)
+                sh4 = mfma16x16x32(aL[x][ks], as_bf16x8(cur.qr[ks]), sh4);
+            else
+                sh4 = mfma16x16x32(aL[x][ks], as_bf16x8(cur.q[ks]), sh4);
+        }
+        const float shat = a.scale * __shfl(sh4[0], lane % 16, kWave) + bias_h[x];
+        // S^T = K_c Q^T and the intra-chunk softmax p_j = exp(s_j - lse_c)
+        f32x4 st[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            st[kb] = zero4();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(kA[kb][ks], as_bf16x8(cur.q[ks]), st[kb]);
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) mx = fmaxf(mx, fmaxf(fmaxf(st[kb][0], st[kb][1]), fmaxf(st[kb][2], st[kb][3])));
+        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        const float m2 = mx * c1;
+        float ex[4][4], sum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                ex[kb][i] = fexp2(fmaf(st[kb][i], c1, -m2));
+                sum += ex[kb][i];
+            }
+        sum += __shfl_xor(sum, 16, kWave);
+        sum += __shfl_xor(sum, 32, kWave);
+        const float inv = 1.f / sum;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ex[kb][i] *= inv;
+        const bf16x8 pb0 = p_operand(ex[0], ex[1]);
+        const bf16x8 pb1 = p_operand(ex[2], ex[3]);
+        f32x4 o[DB];
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            o[db] = mfma16x16x32(vA[db][0], pb0, zero4());
+            o[db] = mfma16x16x32(vA[db][1], pb1, o[db]);
+        }
+        if (qv) {
+            store_lane_order<D>(part + (qrow * a.K + slot) * D, o, lg);
+            if (lane < 16) wgt[qrow * a.K + slot] = fexp2((shat - cur.rf) * kLog2e);
+        }
+    };
+    Ops opa, opb;
+    load_ops(w, opa);
+    for (int u = w; u < nunits; u += 8) {
+        unit(u, opa, opb);
+        if (u + 4 < nunits) unit(u + 4, opb, opa);
     }
 }
 
@@ -369,20 +406,25 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
     using C = LocalCfg<G>;
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB, IPW = C::IPW;
     __shared__ __align__(16) bf16 s_k[kChunk * Tiles<D>::KROW];
-    __shared__ __align__(16) bf16 s_vt[D * Tiles<D>::VROW];
-    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
+    __shared__ __align__(16) bf16 s_v[kChunk * Tiles<D>::KROW];
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int ntiles = (a.N + C::QT - 1) / C::QT;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
     const int q0 = tile * C::QT;
     const int qlast = min(q0 + C::QT - 1, a.N - 1);
     const int kbeg = n_candidates(q0, a.W) * kChunk;
+    const int kfull = n_candidates(qlast, a.W) * kChunk;  // keys >= kfull are in every row's window...
     const size_t bg = (size_t)b * a.Hkv + g;
     const bf16* kbase = as<bf16>(a.k) + bg * a.L * D;
     const bf16* vbase = as<bf16>(a.v) + bg * a.L * D;
+    const float c1 = a.scale * kLog2e;
+
+    KVRegs<D> nk = load_block<D>(kbase + (size_t)kbeg * D);
+    KVRegs<D> nv = load_block<D>(vbase + (size_t)kbeg * D);
 
     bf16x8 bq[IPW][KS];
     f32x4 o[IPW][DB];
-    float m[IPW], l[IPW];
+    float m[IPW], l[IPW];  // running max (log2 units) and sum
 #pragma unroll
     for (int it = 0; it < IPW; ++it) {
         const int item = w + 4 * it;
@@ -395,21 +437,27 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
             const int nq = min(q0 + qb * 16 + lane % 16, a.N - 1);
             const bf16* qrow = as<bf16>(a.q) + (((size_t)b * a.Hq + g * G + hh) * a.N + nq) * D;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) bq[it][ks] = ld_bf16x8(qrow + ks * 32 + (lane / 16) * 8);
+            for (int ks = 0; ks < KS; ++ks) bq[it][ks] = ld_bf16x8(qrow + ks * 32 + lg * 8);
         }
     }
 
     for (int j0 = kbeg; j0 <= qlast; j0 += kChunk) {
         __syncthreads();
-        stage_kv<D>(kbase + (size_t)j0 * D, vbase + (size_t)j0 * D, s_k, s_vt);
+        store_block<D>(s_k, nk);
+        store_block<D>(s_v, nv);
         __syncthreads();
+        if (j0 + kChunk <= qlast) {  // the next key block, fetched during this one
+            nk = load_block<D>(kbase + (size_t)(j0 + kChunk) * D);
+            nv = load_block<D>(vbase + (size_t)(j0 + kChunk) * D);
+        }
+        // ...and below every row of the tile: such blocks need no mask
+        const bool full = j0 >= kfull && j0 + kChunk - 1 <= q0;
 #pragma unroll
         for (int it = 0; it < IPW; ++it) {
             const int item = w + 4 * it;
             if (item >= C::ITEMS) continue;
             const int qb = item % C::QB;
             const int nq = q0 + qb * 16 + lane % 16;
-            const int ell = n_candidates(nq, a.W) * kChunk;
             f32x4 st[4];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) {
@@ -418,26 +466,37 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
                 for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(k_operand<D>(s_k, kb, ks, lane), bq[it][ks], st[kb]);
             }
             float mx = -INFINITY;
+            if (full) {
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+                for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int j = j0 + kb * 16 + (lane / 16) * 4 + i;
-                    const bool valid = nq < a.N && j <= nq && j >= ell;
-                    st[kb][i] = valid ? a.scale * st[kb][i] : -INFINITY;
-                    mx = fmaxf(mx, st[kb][i]);
-                }
+                    for (int i = 0; i < 4; ++i) {
+                        st[kb][i] *= c1;
+                        mx = fmaxf(mx, st[kb][i]);
+                    }
+            } else {
+                const int ell = n_candidates(nq, a.W) * kChunk;
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int j = j0 + kb * 16 + lg * 4 + i;
+                        const bool valid = nq < a.N && j <= nq && j >= ell;
+                        st[kb][i] = valid ? st[kb][i] * c1 : -INFINITY;
+                        mx = fmaxf(mx, st[kb][i]);
+                    }
+            }
             mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
             mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
             const float mnew = fmaxf(m[it], mx);
             const float muse = mnew == -INFINITY ? 0.f : mnew;
-            const float alpha = fexp(m[it] - muse);
+            const float alpha = fexp2(m[it] - muse);
             float ex[4][4], psum = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    ex[kb][i] = fexp(st[kb][i] - muse);
+                    ex[kb][i] = fexp2(st[kb][i] - muse);
                     psum += ex[kb][i];
                 }
             psum += __shfl_xor(psum, 16, kWave);
@@ -448,25 +507,25 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
             const bf16x8 pb1 = p_operand(ex[2], ex[3]);
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) o[it][db][i] *= alpha;
-                o[it][db] = mfma16x16x32(vt_operand<D>(s_vt, db, 0, lane), pb0, o[it][db]);
-                o[it][db] = mfma16x16x32(vt_operand<D>(s_vt, db, 1, lane), pb1, o[it][db]);
+                o[it][db] *= alpha;
+                o[it][db] = mfma16x16x32(vt_operand<D>(s_v, db, 0, lane), pb0, o[it][db]);
+                o[it][db] = mfma16x16x32(vt_operand<D>(s_v, db, 1, lane), pb1, o[it][db]);
             }
         }
     }
 
-    // fusion epilogue
+    // fusion epilogue (lane: row l%16 of the item, dims 16 db + 4 lg + i)
+    constexpr int SB = D >= 128 ? 4 : 8;  // slots whose loads are in flight together
     bf16* out = as_mut<bf16>(a.out);
 #pragma unroll
     for (int it = 0; it < IPW; ++it) {
         const int item = w + 4 * it;
         if (item >= C::ITEMS) continue;
         const int hh = item / C::QB, qb = item % C::QB;
-        const int nq = q0 + qb * 16 + lane % 16;
-        if (nq >= a.N) continue;
+        const int nq = min(q0 + qb * 16 + lane % 16, a.N - 1);
+        const bool rowv = q0 + qb * 16 + lane % 16 < a.N;
         const size_t row = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
-        const float lam0 = m[it] + __logf(l[it]);
+        const float lam0 = (m[it] + __log2f(l[it])) * (1.f / kLog2e);  // local log-sum-exp
         const float rf = ref[bg * a.N + nq];
         // the row's retrieved chunks: slots in idx order, valid entries only
         const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
@@ -475,31 +534,26 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
         f32x4 av[DB];
 #pragma unroll
         for (int db = 0; db < DB; ++db) av[db] = zero4();
-        // slots in groups of SB, every load of a group issued before any use
-        constexpr int SB = 4;
+        int prev = -1;
         for (int k0 = 0; k0 < a.K; k0 += SB) {
             float wk[SB];
-            uint2 pv[SB][DB];
+            bool okk[SB];
+            uint4 pv[SB][D / 32];
 #pragma unroll
             for (int u = 0; u < SB; ++u) {
-                const int k = k0 + u;
-                const bool ok = k < a.K && idx_entry_valid(irow, k, ncand);
-                wk[u] = ok ? wgt[row * a.K + k] : 0.f;
-                const bf16* prow = part + (row * a.K + (ok ? k : 0)) * D;
-#pragma unroll
-                for (int db = 0; db < DB; ++db)
-                    pv[u][db] = ok ? *reinterpret_cast<const uint2*>(prow + db * 16 + (lane / 16) * 4) : make_uint2(0, 0);
+                const int k = min(k0 + u, a.K - 1);
+                const int cc = irow[k];
+                const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
+                prev = cc;  // idx_entry_valid compares with the previous entry as written
+                const float wv = wgt[row * a.K + k];
+                wk[u] = ok ? wv : 0.f;
+                okk[u] = ok;
+                load_lane_order<D>(part + (row * a.K + (ok ? k : 0)) * D, lg, pv[u]);
             }
 #pragma unroll
             for (int u = 0; u < SB; ++u) {
                 zs += wk[u];
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    av[db][0] += wk[u] * __uint_as_float(pv[u][db].x << 16);
-                    av[db][1] += wk[u] * __uint_as_float(pv[u][db].x & 0xffff0000u);
-                    av[db][2] += wk[u] * __uint_as_float(pv[u][db].y << 16);
-                    av[db][3] += wk[u] * __uint_as_float(pv[u][db].y & 0xffff0000u);
-                }
+                fma_lane_order<D>(pv[u], wk[u], okk[u], av);
             }
         }
         const float M = fmaxf(lam0, rf);
@@ -507,18 +561,16 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
         const float wc = zs > 0.f ? fexp(rf - M) : 0.f;
         const float Z = fexp(lam0 - M) + wc * zs;
         const float inv = 1.f / Z;
+        if (rowv) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-            const int d0 = db * 16 + (lane / 16) * 4;
-            const float r0 = (wl * o[it][db][0] + wc * av[db][0]) * inv;
-            const float r1 = (wl * o[it][db][1] + wc * av[db][1]) * inv;
-            const float r2 = (wl * o[it][db][2] + wc * av[db][2]) * inv;
-            const float r3 = (wl * o[it][db][3] + wc * av[db][3]) * inv;
-            const uint32_t lo = from_f32<bf16>(r0).bits | ((uint32_t)from_f32<bf16>(r1).bits << 16);
-            const uint32_t hi = from_f32<bf16>(r2).bits | ((uint32_t)from_f32<bf16>(r3).bits << 16);
-            *reinterpret_cast<uint2*>(out + row * D + d0) = make_uint2(lo, hi);
+            for (int db = 0; db < DB; ++db) {
+                const int d0 = db * 16 + lg * 4;
+                const f32x4 r = (wl * o[it][db] + wc * av[db]) * inv;
+                *reinterpret_cast<uint2*>(out + row * D + d0) =
+                    make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+            }
+            if (lane < 16) a.lse[row] = M + __logf(Z);
         }
-        if (lane < 16) a.lse[row] = M + __logf(Z);
     }
 }
 
@@ -538,10 +590,16 @@ struct PfRun {
         }
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
         launch_inverse_index(ia, ly.inv, a.ws, s);
-        HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
-                           reinterpret_cast<const int*>(ws + ly.inv.offsets), reinterpret_cast<const int*>(ws + ly.inv.list),
-                           reinterpret_cast<const int4*>(ws + ly.inv.work), reinterpret_cast<const int*>(ws + ly.inv.nwork),
-                           (const float*)ref, part, wgt);
+        const int* offsets = reinterpret_cast<const int*>(ws + ly.inv.offsets);
+        const int* list = reinterpret_cast<const int*>(ws + ly.inv.list);
+        const int4* work = reinterpret_cast<const int4*>(ws + ly.inv.work);
+        const int* nwork = reinterpret_cast<const int*>(ws + ly.inv.nwork);
+        if (a.q_route)
+            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, true>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
+                        offsets, list, work, nwork, (const float*)ref, part, wgt);
+        else
+            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
+                        offsets, list, work, nwork, (const float*)ref, part, wgt);
         HILS_LAUNCH("k_pf_local", (k_pf_local<D, G>), dim3((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B),
                            dim3(kBlock), 0, s, a, (const float*)ref, (const bf16*)part, (const float*)wgt);
         return hipGetLastError();

@@ -395,7 +395,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
 // ---------------------------------------------------------------------------
 template <int G>
 struct LocalCfg {
-    static constexpr int QB = G >= 8 ? 1 : 8 / G;  // 16-query blocks per tile
+    static constexpr int QB = G >= 4 ? 1 : 4 / G;  // 16-query blocks per tile
     static constexpr int QT = 16 * QB;
     static constexpr int ITEMS = G * QB;           // (head, query block) items
     static constexpr int IPW = (ITEMS + 3) / 4;    // items per wave

@@ -403,12 +403,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
 #pragma unroll
             for (int i = 1; i < 4; ++i)
                 if (hloc == i) mine = sh4[i];
-            const float shat = a.scale * __shfl(mine, lane % 16, kWave) + bias_h;
+            const float shat = a.scale * group0_bcast(mine) + bias_h;
             float mx = -INFINITY;
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) mx = fmaxf(mx, fmaxf(fmaxf(s4[kb][0], s4[kb][1]), fmaxf(s4[kb][2], s4[kb][3])));
-            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+            mx = group4_max(mx);
             const float m2 = mx * c1;
             float sum = 0.f, ue = 0.f;
 #pragma unroll
@@ -420,10 +419,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                     sum += e;
                     ue = fmaf(e, gv4[kb][i], ue);
                 }
-            sum += __shfl_xor(sum, 16, kWave);
-            sum += __shfl_xor(sum, 32, kWave);
-            ue += __shfl_xor(ue, 16, kWave);
-            ue += __shfl_xor(ue, 32, kWave);
+            sum = group4_sum(sum);
+            ue = group4_sum(ue);
             const float inv = 1.f / sum;
             const float uc = ue * inv;
             const float al = qv ? fexp2(fmaf(shat, kLog2e, -cur.L2)) : 0.f;

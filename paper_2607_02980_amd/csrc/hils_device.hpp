@@ -96,6 +96,35 @@ __device__ __forceinline__ float group_sum(float x) {
 }
 
 // exp(x) for x <= 0 typically; exact -inf -> 0.
+// Sum / max over the four lanes l % 16 + {0, 16, 32, 48} (the lane groups of an
+// MFMA accumulator column), with the gfx950 lane swaps v_permlane16_swap and
+// v_permlane32_swap (VALU, no LDS round trip).  permlane16_swap(x, x) leaves each
+// lane with {x, x of lane l ^ 16} in its two results, permlane32_swap likewise for
+// l ^ 32 (checked on the hardware); every lane ends with the same bits.
+__device__ __forceinline__ float group4_sum(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const uint32_t v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ float group4_max(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const uint32_t v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// Every lane gets the value of lane l % 16 (lane group 0), with the same swaps.
+__device__ __forceinline__ float group0_bcast(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t y = __builtin_amdgcn_permlane16_swap(u, u, false, false)[0];   // rows {0, 0, 2, 2}
+    return __uint_as_float(__builtin_amdgcn_permlane32_swap(y, y, false, false)[0]);  // rows {0, 0, 0, 0}
+}
+
 __device__ __forceinline__ float fexp(float x) { return __expf(x); }
 // 2^x with the hardware instruction (v_exp_f32); exp(x) = fexp2(x * kLog2e).
 constexpr float kLog2e = 1.4426950408889634f;

@@ -339,7 +339,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
             else
                 sh4 = mfma16x16x32(aL[x][ks], as_bf16x8(cur.q[ks]), sh4);
         }
-        const float shat = a.scale * __shfl(sh4[0], lane % 16, kWave) + bias_h[x];
+        const float shat = a.scale * group0_bcast(sh4[0]) + bias_h[x];
         // S^T = K_c Q^T and the intra-chunk softmax p_j = exp(s_j - lse_c)
         f32x4 st[4];
 #pragma unroll
@@ -351,8 +351,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
         float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) mx = fmaxf(mx, fmaxf(fmaxf(st[kb][0], st[kb][1]), fmaxf(st[kb][2], st[kb][3])));
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        mx = group4_max(mx);
         const float m2 = mx * c1;
         float ex[4][4], sum = 0.f;
 #pragma unroll
@@ -362,8 +361,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
                 ex[kb][i] = fexp2(fmaf(st[kb][i], c1, -m2));
                 sum += ex[kb][i];
             }
-        sum += __shfl_xor(sum, 16, kWave);
-        sum += __shfl_xor(sum, 32, kWave);
+        sum = group4_sum(sum);
         const float inv = 1.f / sum;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
@@ -486,8 +484,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
                         mx = fmaxf(mx, st[kb][i]);
                     }
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+            mx = group4_max(mx);
             const float mnew = fmaxf(m[it], mx);
             const float muse = mnew == -INFINITY ? 0.f : mnew;
             const float alpha = fexp2(m[it] - muse);
@@ -499,8 +496,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
                     ex[kb][i] = fexp2(st[kb][i] - muse);
                     psum += ex[kb][i];
                 }
-            psum += __shfl_xor(psum, 16, kWave);
-            psum += __shfl_xor(psum, 32, kWave);
+            psum = group4_sum(psum);
             l[it] = l[it] * alpha + psum;
             m[it] = mnew;
             const bf16x8 pb0 = p_operand(ex[0], ex[1]);

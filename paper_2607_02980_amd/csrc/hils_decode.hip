@@ -2,21 +2,26 @@
 // work is a stream over HBM (landmark scan, then K/V gathers), so the kernels
 // are organised for coalesced, many-in-flight loads rather than for math.
 //
-//   A  k_dec_scan_local  grid (nslices + nlocal, Hkv, B)
-//        x <  nslices : scores SLICE candidate chunks of one KV group
-//                       (s^_hc for the G heads, max over heads, Eq. (9) / App. C)
-//                       and keeps the slice's top-K (exact wave radix select)
-//        x >= nslices : one 64-key piece of the local window [l(i), i] (Eq. (1)):
-//                       per-head max, sum and unnormalised P.V of the piece
-//   B  k_dec_merge       grid (Hkv, B): top-K over the slices' survivors -> idx
-//   C  k_dec_chunks      grid (K, Hkv, B): the intra-chunk softmax of one selected
-//                       chunk (Eq. (10)) and its surrogate score s^_hc
-//   D  k_dec_combine     grid (Hkv, B): local pieces merged by online softmax,
-//                       then the fusion softmax over {s^_hc} U {log Z_swa} -> out, lse
+//   A  k_dec_scan     grid (nslices, Hkv, B): scores SLICE candidate chunks of one
+//                     KV group (s^_hc for the G heads, max over heads, Eq. (9) /
+//                     App. C) and keeps the slice's top-K (exact wave radix select).
+//                     Small LDS, so many slices stream per CU while others select.
+//   B  k_dec_merge    grid (Hkv, B): top-K over the slices' survivors -> idx
+//   C  k_dec_parts    grid (K + nlocal, Hkv, B)
+//        x <  K     : the intra-chunk softmax of selected chunk x (Eq. (10)) and
+//                     its surrogate score s^_hc
+//        x >= K     : one 64-key piece of the local window [l(i), i] (Eq. (1))
+//                     (bf16: on MFMA, run_part_mfma)
+//   A part (chunk or piece) leaves per head its max, sum and unnormalised P.V.
+//   D  k_dec_combine  grid (Hkv, B): local pieces merged by online softmax,
+//                     then the fusion softmax over {s^_hc} U {log Z_swa} -> out, lse
 // Parts (local pieces and chunks) leave a record {m, l, s^, o[d]} per head.
+#include <type_traits>
+
 #include "hils_device.hpp"
 #include "hils_dispatch.hpp"
 #include "hils_internal.hpp"
+#include "hils_mfma.hpp"
 
 namespace hils {
 
@@ -195,15 +200,141 @@ __device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G
     for (int o = tid; o < G * D / 2; o += kBlock) {
         const int hh = (2 * o) / D, dd = (2 * o) % D;
         float acc0 = 0.f, acc1 = 0.f;
-        for (int j = 0; j < nk; ++j) {
-            const float pj = sm.p[hh][j];
-            const float2 v = lds_load2(&sm.kv[1][j * RB + dd * sizeof(T)], T{});
-            acc0 += pj * v.x;
-            acc1 += pj * v.y;
+        if (nk == kChunk) {  // full part: every LDS read of the loop in flight together
+#pragma unroll 16
+            for (int j = 0; j < kChunk; ++j) {
+                const float pj = sm.p[hh][j];
+                const float2 v = lds_load2(&sm.kv[1][j * RB + dd * sizeof(T)], T{});
+                acc0 += pj * v.x;
+                acc1 += pj * v.y;
+            }
+        } else {
+            for (int j = 0; j < nk; ++j) {
+                const float pj = sm.p[hh][j];
+                const float2 v = lds_load2(&sm.kv[1][j * RB + dd * sizeof(T)], T{});
+                acc0 += pj * v.x;
+                acc1 += pj * v.y;
+            }
         }
         float* r = part_record<D>(a, ly, b, g, part, hh, G);
         r[4 + dd] = acc0;
         r[5 + dd] = acc1;
+    }
+}
+
+// The same part on MFMA for bf16 storage.  Wave w owns keys [16w, 16w + 16):
+// S^T = K Q^T (16 keys x the G heads as MFMA columns) from K rows and q read
+// straight from HBM; after the block-wide max and sum per head, O^T = V^T P^T
+// (v_mfma 16x16x16) with P^T taken from the accumulators as they are and V^T
+// from the wave's 16 V rows in LDS by one transposing read per 16 dims.  The
+// four waves' O^T partials are summed through LDS.
+template <int D, int G>
+struct PartSmemM {
+    bf16 v[kChunk * (D + 8)];
+    float m[4][16], l[4][16];
+    float o[4][G][D];
+};
+
+template <int D, int G>
+__device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D, G>& sm, int b, int g, int part, int c,
+                              int nk, bool is_chunk) {
+    constexpr int KS = D / 32, DB = D / 16, VROW = D + 8;
+    typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16, n16 = lane % 16;
+    const size_t kv_off = (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
+    const bf16* kg = as<bf16>(a.k) + kv_off;
+    const bf16* vg = as<bf16>(a.v) + kv_off;
+    // A operands: K rows 16w + l%16 (rows past the query position are loaded, in
+    // bounds, and masked out of the softmax); B operands: q of head l%16 (< G)
+    const int key = 16 * w + n16;
+    bf16x8 kA[KS], qB[KS];
+    const bf16* qrow = as<bf16>(a.q) + ((size_t)b * a.Hq + g * G + min(n16, G - 1)) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        kA[ks] = ld_bf16x8(kg + (size_t)key * D + ks * 32 + lg * 8);
+        const bf16x8 qq = ld_bf16x8(qrow + ks * 32 + lg * 8);
+        qB[ks] = n16 < G ? qq : as_bf16x8(make_uint4(0, 0, 0, 0));
+    }
+    // the wave's 16 V rows into LDS; rows at or past nk are zeroed
+    {
+        constexpr int PR = D / 8;  // 16-byte pieces per row
+#pragma unroll
+        for (int u = 0; u < 16 * PR / kWave; ++u) {
+            const int e = lane + u * kWave, r = e / PR, pc = e % PR;
+            const int j = 16 * w + r;
+            const uint4 x = *reinterpret_cast<const uint4*>(vg + (size_t)j * D + pc * 8);
+            *reinterpret_cast<uint4*>(sm.v + j * VROW + pc * 8) = j < nk ? x : make_uint4(0, 0, 0, 0);
+        }
+    }
+    // retrieved chunk: s^ of head wave (+4) from q^ and the landmark row (lane pairs)
+    constexpr int HPW = (G + 3) / 4;
+    float sh[HPW];
+#pragma unroll
+    for (int u = 0; u < HPW; ++u) {
+        sh[u] = -INFINITY;
+        const int hh = w + 4 * u;
+        if (is_chunk && hh < G) {
+            float acc = 0.f;
+            if (2 * lane < D) {
+                const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+                const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q) + ((size_t)b * a.Hq + g * G + hh) * D + 2 * lane;
+                const bf16* lr = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * ly.nC + c) * D + 2 * lane;
+                acc = to_f32(qr[0]) * to_f32(lr[0]) + to_f32(qr[1]) * to_f32(lr[1]);
+            }
+            acc = wave_sum(acc);
+            sh[u] = a.scale * acc + (a.bias ? a.bias[((size_t)b * a.Hl + ((a.Hl == a.Hq) ? g * G + hh : g)) * ly.nC + c] : 0.f);
+        }
+    }
+    // S^T (lane: head l%16, keys 16w + 4(l/16) + i)
+    f32x4 st = zero4();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) st = mfma16x16x32(kA[ks], qB[ks], st);
+    const float c1 = a.scale * kLog2e;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        st[i] = 16 * w + 4 * lg + i < nk ? st[i] * c1 : -INFINITY;
+        mx = fmaxf(mx, st[i]);
+    }
+    mx = group4_max(mx);
+    if (lane < 16) sm.m[w][lane] = mx;
+    __syncthreads();
+    const float M = fmaxf(fmaxf(sm.m[0][n16], sm.m[1][n16]), fmaxf(sm.m[2][n16], sm.m[3][n16]));  // log2 units
+    float p[4], ls = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        p[i] = fexp2(st[i] - M);
+        ls += p[i];
+    }
+    ls = group4_sum(ls);
+    if (lane < 16) sm.l[w][lane] = ls;
+    bf16x4 pb;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pb[i] = static_cast<__bf16>(p[i]);
+    // O^T partial over this wave's keys (lane: head l%16, dims 16db + 4(l/16) + i)
+    const int g4 = lane / 16, s16 = lane % 16;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        const bf16* src = sm.v + (16 * w + 4 * g4 + s16 / 4) * VROW + db * 16 + 4 * (s16 % 4);
+        const v4i16 va = lds_read_tr16(src);
+        const f32x4 o = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, va), pb, zero4(), 0, 0, 0);
+        if (n16 < G) *reinterpret_cast<f32x4*>(&sm.o[w][n16][db * 16 + 4 * lg]) = o;
+    }
+    __syncthreads();
+    for (int e = tid; e < G * D; e += kBlock) {
+        const int hh = e / D, dd = e % D;
+        float* r = part_record<D>(a, ly, b, g, part, hh, G);
+        r[4 + dd] = sm.o[0][hh][dd] + sm.o[1][hh][dd] + sm.o[2][hh][dd] + sm.o[3][hh][dd];
+        if (dd == 0) {
+            r[0] = (fmaxf(fmaxf(sm.m[0][hh], sm.m[1][hh]), fmaxf(sm.m[2][hh], sm.m[3][hh]))) * (1.f / kLog2e);
+            r[1] = sm.l[0][hh] + sm.l[1][hh] + sm.l[2][hh] + sm.l[3][hh];
+        }
+    }
+    // s^ of the wave's heads (lane 0 of the owning wave)
+#pragma unroll
+    for (int u = 0; u < HPW; ++u) {
+        const int hh = w + 4 * u;
+        if (hh < G && lane == 0) part_record<D>(a, ly, b, g, part, hh, G)[2] = sh[u];
     }
 }
 
@@ -217,33 +348,14 @@ __device__ void empty_part(const FwdArgs& a, const DecLayout& ly, int b, int g, 
     }
 }
 
-// ---- A: landmark scan slices + local-window pieces -------------------------
+// ---- A: landmark scan slices --------------------------------------------------
 template <typename T, int D, int G>
-__global__ __launch_bounds__(kBlock) void k_dec_scan_local(FwdArgs a) {
+__global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
     const int b = blockIdx.z, g = blockIdx.y;
     const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
     const int pos = decode_position(a, b);
     const int ncand = n_candidates(pos, a.W);
-
-    // the scan and the part share one LDS allocation
-    __shared__ __align__(16) unsigned char smem[sizeof(PartSmem<T, D, G>) > sizeof(ScanSmem<G>)
-                                                     ? sizeof(PartSmem<T, D, G>)
-                                                     : sizeof(ScanSmem<G>)];
-    if ((int)blockIdx.x < ly.nslices && a.given_idx) return;  // forced selection: no scan
-    if ((int)blockIdx.x >= ly.nslices) {
-        PartSmem<T, D, G>& sm = *reinterpret_cast<PartSmem<T, D, G>*>(smem);
-        const int piece = blockIdx.x - ly.nslices;
-        const int c = ncand + piece;
-        if (c > pos / kChunk) {
-            empty_part<D>(a, ly, b, g, a.K + piece, G);
-            return;
-        }
-        const int nk = min(kChunk, pos - c * kChunk + 1);
-        run_part<T, D, G>(a, ly, sm, b, g, a.K + piece, c, nk, false);
-        return;
-    }
-
-    ScanSmem<G>& ss = *reinterpret_cast<ScanSmem<G>*>(smem);
+    __shared__ ScanSmem<G> ss;
     auto& s_score = ss.score;
     auto& s_sig = ss.sig;
     auto& s_id = ss.id;
@@ -396,14 +508,32 @@ __global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a) {
     }
 }
 
-// ---- C: one selected chunk per workgroup ------------------------------------
+// ---- C: one selected chunk or one local-window piece per workgroup -----------
 template <typename T, int D, int G>
-__global__ __launch_bounds__(kBlock) void k_dec_chunks(FwdArgs a) {
-    __shared__ PartSmem<T, D, G> sm;
+__global__ __launch_bounds__(kBlock) void k_dec_parts(FwdArgs a) {
+    constexpr bool kMfma = sizeof(T) == 2;
+    typedef typename std::conditional<kMfma, PartSmemM<D, G>, PartSmem<T, D, G>>::type Smem;
+    __shared__ Smem sm;
     __shared__ int s_c;
     const int slot = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
     const int pos = decode_position(a, b);
+    auto run = [&](int part, int c, int nk, bool is_chunk) {
+        if constexpr (kMfma)
+            run_part_mfma<D, G>(a, ly, sm, b, g, part, c, nk, is_chunk);
+        else
+            run_part<T, D, G>(a, ly, sm, b, g, part, c, nk, is_chunk);
+    };
+    if (slot >= a.K) {
+        const int piece = slot - a.K;
+        const int c = n_candidates(pos, a.W) + piece;
+        if (c > pos / kChunk) {
+            empty_part<D>(a, ly, b, g, slot, G);
+            return;
+        }
+        run(slot, c, min(kChunk, pos - c * kChunk + 1), false);
+        return;
+    }
     if (threadIdx.x == 0) {
         const int32_t* irow = a.idx + ((size_t)b * a.Hkv + g) * a.K;
         s_c = idx_entry_valid(irow, slot, n_candidates(pos, a.W)) ? irow[slot] : -1;
@@ -414,7 +544,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_chunks(FwdArgs a) {
         empty_part<D>(a, ly, b, g, slot, G);
         return;
     }
-    run_part<T, D, G>(a, ly, sm, b, g, slot, c, kChunk, true);
+    run(slot, c, kChunk, true);
 }
 
 // ---- D: fusion -----------------------------------------------------------------
@@ -474,10 +604,11 @@ struct DecRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
         const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
-        HILS_LAUNCH("k_dec_scan_local", (k_dec_scan_local<T, D, G>), dim3(ly.nslices + ly.nlocal, a.Hkv, a.B), dim3(kBlock), 0,
-                           s, a);
-        if (!a.given_idx) HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
-        HILS_LAUNCH("k_dec_chunks", (k_dec_chunks<T, D, G>), dim3(a.K, a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        if (!a.given_idx) {
+            HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G>), dim3(ly.nslices, a.Hkv, a.B), dim3(kBlock), 0, s, a);
+            HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        }
+        HILS_LAUNCH("k_dec_parts", (k_dec_parts<T, D, G>), dim3(a.K + ly.nlocal, a.Hkv, a.B), dim3(kBlock), 0, s, a);
         HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }

@@ -144,44 +144,59 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
     for (int s0 = 0; s0 < nct; s0 += kSL) {
         const int len = min(kSL, nct - s0);
         const int ncb = (len + 15) / 16;
-        f32x4 sig[NCB];
+        // Wave w scores chunk blocks cb = w + 4j (j < NCB/4) against all kSQ rows of the
+        // tile (4 row tiles), so each landmark operand it loads feeds 4 MFMAs; all of a
+        // head's landmark loads are issued before its MFMAs.
+        constexpr int NJ = NCB / 4, NT = kSQ / 16;
+        f32x4 sig[NT][NJ];
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) sig[cb] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) sig[t][j] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
         for (int hh = 0; hh < G; ++hh) {
             const int h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
-            const int qa = min(qw0 + lane % 16, a.N - 1);
-            bf16x8 aq[KS];
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                aq[ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + h) * a.N + qa) * D + ks * 32 + (lane / 16) * 8);
             const bf16* lbase = lmk + ((size_t)b * a.Hl + hl) * nC * D;
-            const float* bbase = a.bias ? a.bias + ((size_t)b * a.Hl + hl) * nC : nullptr;
+            bf16x8 bl[NJ][KS];
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                if (cb < ncb) {
-                    const int c = min(s0 + cb * 16 + lane % 16, nC - 1);
-                    bf16x8 bl[KS];
+            for (int j = 0; j < NJ; ++j) {
+                const int c = min(s0 + (w + 4 * j) * 16 + lane % 16, nC - 1);
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) bl[ks] = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + (lane / 16) * 8);
+                for (int ks = 0; ks < KS; ++ks) bl[j][ks] = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + (lane / 16) * 8);
+            }
+            float bv[NJ];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const int c = min(s0 + (w + 4 * j) * 16 + lane % 16, nC - 1);
+                bv[j] = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
+            }
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int qa = min(q0 + 16 * t + lane % 16, a.N - 1);
+                bf16x8 aq[KS];
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    aq[ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + h) * a.N + qa) * D + ks * 32 + (lane / 16) * 8);
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
                     f32x4 acc4 = zero4();
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[ks], bl[ks], acc4);
-                    const float bv = bbase ? bbase[c] : 0.f;
+                    for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[ks], bl[j][ks], acc4);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) sig[cb][i] = fmaxf(sig[cb][i], a.scale * acc4[i] + bv);
+                    for (int i = 0; i < 4; ++i) sig[t][j][i] = fmaxf(sig[t][j][i], a.scale * acc4[i] + bv[j]);
                 }
             }
         }
-        // this wave's 16 rows -> LDS (row = 16w + (l/16)*4 + i, column = 16cb + l%16)
+        __syncthreads();  // the previous slice's rows are selected
+        // all rows x this wave's chunk blocks -> LDS (row = 16t + (l/16)*4 + i, column = 16cb + l%16)
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-            if (cb < ncb) {
+        for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) s_sig[16 * w + (lane / 16) * 4 + i][cb * 16 + lane % 16] = sig[cb][i];
-            }
-        }
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            for (int j = 0; j < NJ; ++j)
+                if (w + 4 * j < ncb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        s_sig[16 * t + (lane / 16) * 4 + i][(w + 4 * j) * 16 + lane % 16] = sig[t][j][i];
+        __syncthreads();
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int n = qw0 + r;

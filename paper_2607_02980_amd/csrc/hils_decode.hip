@@ -443,7 +443,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
             sc[r] = ok[r] ? s_sig[e] : 0.f;
             id[r] = ok[r] ? s_id[e] : -1;
         }
-        const int m = wave_topk_reg<E>(sc, id, ok, a.K, s_oid, s_osc, s_tid, s_tsc);
+        const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, s_oid, s_osc, s_tid, s_tsc);  // ids c0 + e*64 + lane
         for (int t = lane; t < a.K; t += kWave) {
             cand_sc[cbase + t] = t < m ? s_osc[t] : -INFINITY;
             cand_id[cbase + t] = t < m ? s_oid[t] : -1;

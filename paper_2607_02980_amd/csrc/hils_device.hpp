@@ -244,7 +244,13 @@ __device__ inline int wave_topk(const float* sc, const int* id, int n, int K, in
 // score sc[r], chunk id[r] and a valid flag; every pass of the radix select
 // is compares and ballots on registers only.  Same order and outputs as
 // wave_topk.
-template <int E>
+// FIRST: the order of the ids.  kTopkUnordered: any order (the survivors are
+// ranked through LDS).  Otherwise the ids ascend over (register, lane) when
+// register FIRST (if >= 0) is taken first and then registers 0, 1, ... in turn;
+// the compaction position is then the ascending rank and out_* are written
+// directly.
+constexpr int kTopkUnordered = -2, kTopkNatural = -1;
+template <int E, int FIRST = kTopkUnordered>
 __device__ inline int wave_topk_reg(const float (&sc)[E], const int (&id)[E], const bool (&valid)[E], int K,
                                     int* out_id, float* out_sc, int* tmp_id, float* tmp_sc) {
     const int lane = __lane_id();
@@ -290,20 +296,26 @@ __device__ inline int wave_topk_reg(const float (&sc)[E], const int (&id)[E], co
             id_thr = x;
         }
     }
+    constexpr bool kOrdered = FIRST != kTopkUnordered;
+    int* dst_id = kOrdered ? out_id : tmp_id;
+    float* dst_sc = kOrdered ? out_sc : tmp_sc;
     int w = 0;
 #pragma unroll
-    for (int r = 0; r < E; ++r) {
+    for (int q = 0; q < E; ++q) {
+        // visiting order: FIRST, then the others ascending
+        const int r = FIRST >= 0 ? (q == 0 ? FIRST : (q - 1 < FIRST ? q - 1 : q)) : q;
         const bool pr = key[r] != 0u && (all || key[r] > T || (key[r] == T && (uint32_t)id[r] <= id_thr));
         const uint64_t bal = __ballot(pr);
         if (pr) {
             const int pos = w + popc64(bal & ((1ull << lane) - 1ull));
-            tmp_id[pos] = id[r];
-            tmp_sc[pos] = sc[r];
+            dst_id[pos] = id[r];
+            dst_sc[pos] = sc[r];
         }
         w += popc64(bal);
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    if (kOrdered) return m;
     if (lane < m) {
         const int my = tmp_id[lane];
         int rk = 0;

@@ -216,7 +216,9 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
             ok[E] = lane < nb[r];
             sc[E] = bsc[r];
             id[E] = bid[r];
-            nb[r] = wave_topk_reg<E + 1>(sc, id, ok, a.K, s_oid[w], s_osc[w], s_tid[w], s_tsc[w]);
+            // ids ascend over (register E: the running best, all below s0; then
+            // registers 0.. : s0 + e*64 + lane)
+            nb[r] = wave_topk_reg<E + 1, E>(sc, id, ok, a.K, s_oid[w], s_osc[w], s_tid[w], s_tsc[w]);
             bsc[r] = lane < nb[r] ? s_osc[w][lane] : 0.f;
             bid[r] = lane < nb[r] ? s_oid[w][lane] : -1;
         }

@@ -214,6 +214,45 @@ def bwd(shape: Shape, dout, q, k, v, lmk, idx, bias=None, q_route=None, qpos=Non
     return {"dq": dq, "dk": dk, "dv": dv, "dlmk": dlmk, "dbias": dbias, "dq_route": dqr}
 
 
+def landmark_fwd(shape: Shape, lq, k, prec: str = "f64"):
+    """Landmark compression (Prop. 3.1): lq [B, Hl, L/S, d] landmark queries q'_c,
+    k [B, Hkv, L, d].  Returns dict(lmk = k'_c [B, Hl, L/S, d], bias = b'_c [B, Hl, L/S])."""
+    lib = _lib(prec)
+    R = _real(prec)
+    s = shape
+    lq, k = _f32(lq), _f32(k)
+    _check(s, lmk=lq, k=k)
+    nc = s.L // s.chunk
+    lmk = np.zeros((s.B, s.Hl, nc, s.d), R)
+    bias = np.zeros((s.B, s.Hl, nc), R)
+    fn = getattr(lib, f"hils_oracle_landmark_fwd_{prec}")
+    fn.restype = ctypes.c_int
+    sh = s.c()
+    if fn(ctypes.byref(sh), _ptr(lq), _ptr(k), _ptr(lmk), _ptr(bias)):
+        raise ValueError("oracle landmark_fwd failed")
+    return {"lmk": lmk, "bias": bias}
+
+
+def landmark_bwd(shape: Shape, lq, k, dlmk, dbias=None, prec: str = "f64"):
+    """Backward of the landmark compression for upstream dlmk (of k'_c) and
+    dbias (of b'_c, None = 0).  Returns dict(dlq [B, Hl, L/S, d], dk [B, Hkv, L, d])."""
+    lib = _lib(prec)
+    R = _real(prec)
+    s = shape
+    lq, k, dlmk, dbias = _f32(lq), _f32(k), _f32(dlmk), _f32(dbias)
+    _check(s, lmk=lq, k=k, bias=dbias)
+    _check(s, lmk=dlmk)
+    nc = s.L // s.chunk
+    dlq = np.zeros((s.B, s.Hl, nc, s.d), R)
+    dk = np.zeros((s.B, s.Hkv, s.L, s.d), R)
+    fn = getattr(lib, f"hils_oracle_landmark_bwd_{prec}")
+    fn.restype = ctypes.c_int
+    sh = s.c()
+    if fn(ctypes.byref(sh), _ptr(lq), _ptr(k), _ptr(dlmk), _ptr(dbias), _ptr(dlq), _ptr(dk)):
+        raise ValueError("oracle landmark_bwd failed")
+    return {"dlq": dlq, "dk": dk}
+
+
 def n_candidates(i: int, chunk: int, window: int) -> int:
     """|C_i| = l(i)/S with l(i) clamped at 0 (Sec. 2.1)."""
     return max(0, (i - window + 1) // chunk)

@@ -19,6 +19,9 @@
  *                 as its own mass.
  *   Eq. (11)      Q-Cal: a routing query q^ (here the optional `q_route`)
  *                 is used only inside the surrogate score.
+ *   Prop. 3.1    landmark compression: k'_c = attention of the landmark query
+ *                 q'_c over its chunk's keys, b'_c = the entropy of that
+ *                 attention (and its backward).
  *   Sec. 4.1 ("HiLS-Attention in GQA") and Appendix C: one selection per
  *                 KV group, ranked by the maximum of the per-head surrogate
  *                 scores; fusion weights stay per head.
@@ -561,6 +564,105 @@ int API(bwd)(const hils_oracle_shape* p, const float* dout, const float* q, cons
             if (rb != b) continue;
             backward_row(&in, b, g, rn, idx, dout, dq, dk, dv, dlmk, dbias, dq_route);
         }
+    }
+    return 0;
+}
+
+/* ---- landmark compression (Prop. 3.1; the section's NEXT step) --------------
+ *
+ * For landmark head hl (KV group g(hl): hl / (Hl / Hkv)) and chunk c with keys
+ * k_j, j in [cS, cS + S), and its landmark query q'_c:
+ *   s_j = scale * q'_c . k_j,   p = softmax(s),
+ *   k'_c = sum_j p_j k_j        (an attention of q'_c over the chunk's own keys),
+ *   b'_c = - sum_j p_j log p_j  (the entropy of p),
+ * with log p_j taken as s_j - LSE(s), which equals it exactly and stays finite
+ * when p_j underflows.
+ *
+ * Layouts: lq, lmk, dlq, dlmk : [B, Hl, L/S, d];  bias, dbias : [B, Hl, L/S];
+ * k, dk : [B, Hkv, L, d]. */
+
+static int lmk_group(const hils_oracle_shape* p, int hl) { return hl / (p->Hl / p->Hkv); }
+
+/* Forward: writes lmk and bias for every (b, hl, c).  Returns 0 or -1 (shape). */
+int API(landmark_fwd)(const hils_oracle_shape* p, const float* lq, const float* k, REAL* lmk, REAL* bias) {
+    if (check_shape(p)) return -1;
+    const long nc = nchunks_of(p), S = p->chunk;
+    const int d = p->d;
+#pragma omp parallel for schedule(dynamic, 4)
+    for (long t = 0; t < (long)p->B * p->Hl * nc; ++t) {
+        const int b = (int)(t / ((long)p->Hl * nc)), hl = (int)(t / nc % p->Hl);
+        const long c = t % nc;
+        const int g = lmk_group(p, hl);
+        const float* qc = lq + (((size_t)b * p->Hl + hl) * nc + c) * d;
+        REAL* s = (REAL*)malloc(sizeof(REAL) * S);
+        for (long j = 0; j < S; ++j)
+            s[j] = p->scale * dot_f(qc, k + (((size_t)b * p->Hkv + g) * p->L + c * S + j) * d, d);
+        const REAL lse = logsumexp(s, S);
+        REAL* kc = lmk + (((size_t)b * p->Hl + hl) * nc + c) * d;
+        for (int u = 0; u < d; ++u) kc[u] = 0;
+        REAL ent = 0;
+        for (long j = 0; j < S; ++j) {
+            const REAL logp = s[j] - lse, pj = EXP(logp);
+            const float* kj = k + (((size_t)b * p->Hkv + g) * p->L + c * S + j) * d;
+            for (int u = 0; u < d; ++u) kc[u] += pj * (REAL)kj[u];
+            ent -= pj * logp;
+        }
+        bias[((size_t)b * p->Hl + hl) * nc + c] = ent;
+        free(s);
+    }
+    return 0;
+}
+
+/* Backward of the compression for upstream gradients dlmk (of k'_c) and dbias
+ * (of b'_c, NULL = 0).  By the chain rule through the two outputs:
+ *   dL/dp_j = dk'_c . k_j - db'_c (log p_j + 1),
+ *   dL/ds_j = p_j (dL/dp_j - sum_m p_m dL/dp_m)            (softmax Jacobian),
+ *   dq'_c   = scale * sum_j dL/ds_j k_j,
+ *   dk_j   += p_j dk'_c + scale * dL/ds_j q'_c              (k_j appears in k'_c and in s_j).
+ * Writes dlq; accumulates (+=) into dk over the landmark heads of each group.
+ * Returns 0 or -1. */
+int API(landmark_bwd)(const hils_oracle_shape* p, const float* lq, const float* k, const float* dlmk,
+                      const float* dbias, REAL* dlq, REAL* dk) {
+    if (check_shape(p)) return -1;
+    const long nc = nchunks_of(p), S = p->chunk;
+    const int d = p->d, per_group = p->Hl / p->Hkv;
+    /* parallel over (b, g, c): the landmark heads of a group write the same dk rows */
+#pragma omp parallel for schedule(dynamic, 4)
+    for (long t = 0; t < (long)p->B * p->Hkv * nc; ++t) {
+        const int b = (int)(t / ((long)p->Hkv * nc)), g = (int)(t / nc % p->Hkv);
+        const long c = t % nc;
+        REAL* s = (REAL*)malloc(sizeof(REAL) * S);
+        REAL* pr = (REAL*)malloc(sizeof(REAL) * S);
+        REAL* gp = (REAL*)malloc(sizeof(REAL) * S);
+        for (int hl = g * per_group; hl < (g + 1) * per_group; ++hl) {
+            const size_t row = ((size_t)b * p->Hl + hl) * nc + c;
+            const float* qc = lq + row * d;
+            const float* dkc = dlmk + row * d;
+            const REAL db = dbias ? (REAL)dbias[row] : 0;
+            for (long j = 0; j < S; ++j)
+                s[j] = p->scale * dot_f(qc, k + (((size_t)b * p->Hkv + g) * p->L + c * S + j) * d, d);
+            const REAL lse = logsumexp(s, S);
+            REAL mean = 0;
+            for (long j = 0; j < S; ++j) {
+                const float* kj = k + (((size_t)b * p->Hkv + g) * p->L + c * S + j) * d;
+                const REAL logp = s[j] - lse;
+                pr[j] = EXP(logp);
+                gp[j] = dot_f(dkc, kj, d) - db * (logp + 1);
+                mean += pr[j] * gp[j];
+            }
+            REAL* dq = dlq + row * d;
+            for (int u = 0; u < d; ++u) dq[u] = 0;
+            for (long j = 0; j < S; ++j) {
+                const float* kj = k + (((size_t)b * p->Hkv + g) * p->L + c * S + j) * d;
+                REAL* dkj = dk + (((size_t)b * p->Hkv + g) * p->L + c * S + j) * d;
+                const REAL ds = pr[j] * (gp[j] - mean);
+                for (int u = 0; u < d; ++u) {
+                    dq[u] += p->scale * ds * (REAL)kj[u];
+                    dkj[u] += pr[j] * (REAL)dkc[u] + p->scale * ds * (REAL)qc[u];
+                }
+            }
+        }
+        free(s); free(pr); free(gp);
     }
     return 0;
 }

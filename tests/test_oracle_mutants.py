@@ -1,12 +1,14 @@
 """Plant a plausible mistake in a copy of the oracle (on the CPU) and check
 that at least one pin fails.  This is evidence that the pins constrain every
 step: the group max, the window edge, the local mass, the bias, the scale, the
-routing query, tie-breaking and the backward's chunk and score terms."""
+routing query, tie-breaking, the backward's chunk and score terms, and the
+landmark compression's entropy, head-to-group map and both backward terms."""
 import os
 
 import pytest
 
 import oracle
+from tests import test_oracle_landmark as lmk
 from tests import test_oracle_pins as pins
 
 SRC = open(oracle._SRC).read()
@@ -31,6 +33,15 @@ MUTANTS = {
                                 [lambda: pins.test_p7_backward_matches_finite_differences(True, True, True)]),
     "bwd_score_grad_drops_u": ("REAL dshat = a * (uc - ubar);", "REAL dshat = a * uc;",
                                [lambda: pins.test_p7_backward_matches_finite_differences(False, False, True)]),
+    # landmark compression (Prop. 3.1)
+    "lmk_entropy_sign": ("ent -= pj * logp;", "ent += pj * logp;", [lmk.test_entropy_range_and_uniform_regime]),
+    "lmk_group_map": ("return hl / (p->Hl / p->Hkv);", "return hl % p->Hkv;",
+                      [lambda: lmk.test_taylor_point_identity_and_gradient(True)]),
+    "lmk_bwd_drops_entropy_term": ("gp[j] = dot_f(dkc, kj, d) - db * (logp + 1);", "gp[j] = dot_f(dkc, kj, d);",
+                                   [lmk.test_taylor_identity_gives_a_null_direction]),
+    "lmk_bwd_drops_key_summary_term": ("dkj[u] += pr[j] * (REAL)dkc[u] + p->scale * ds * (REAL)qc[u];",
+                                       "dkj[u] += p->scale * ds * (REAL)qc[u];",
+                                       [lambda: lmk.test_backward_matches_finite_differences(True, False)]),
 }
 
 

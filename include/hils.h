@@ -76,7 +76,7 @@ typedef enum {
  * are ignored; entries must be ascending. */
 #define HILS_FLAG_GIVEN_IDX 1u
 
-typedef enum { HILS_OP_PREFILL = 0, HILS_OP_DECODE = 1, HILS_OP_BWD = 2 } hils_op;
+typedef enum { HILS_OP_PREFILL = 0, HILS_OP_DECODE = 1, HILS_OP_BWD = 2, HILS_OP_LANDMARK = 3 } hils_op;
 
 typedef struct {
     int B;          /* sequences */
@@ -159,6 +159,39 @@ int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* 
              const void* lmk, const float* lmk_bias, const void* q_route, const void* out, const float* lse,
              const int32_t* idx, void* dq, void* dk, void* dv, void* dlmk, float* dlmk_bias, void* dq_route,
              void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Landmark compression, Prop. 3.1: the landmark key k'_c and bias b'_c of every
+ * chunk from its landmark query q'_c (in the paper, the query of a landmark
+ * token appended to the chunk) and the chunk's own keys:
+ *   s_j = scale * <q'_c, k_j> for the S keys j of chunk c (of the landmark
+ *   head's KV group), p = softmax(s), k'_c = sum_j p_j k_j (the attention of
+ *   q'_c over its chunk), b'_c = -sum_j p_j log p_j (the entropy of p), so that
+ *   scale * <q, k'_c> + b'_c is the first-order Taylor expansion of the chunk's
+ *   log-sum-exp at q = q'_c.  The outputs are the lmk and lmk_bias inputs of the
+ *   attention entry points.
+ *   lq       [B, Hl, L/S, d]   landmark queries (dtype)
+ *   k        [B, Hkv, L, d]    keys (dtype); landmark head hl uses KV group
+ *                              hl / (Hl / Hkv)
+ *   lmk      [B, Hl, L/S, d]   written (dtype)
+ *   lmk_bias [B, Hl, L/S] f32  written
+ * Uses B, Hq, Hkv, Hl, L, d, chunk, scale and dtype of `p`; N, topk and window
+ * are not used (they must still be >= 1).  No workspace.
+ */
+int hils_landmark_fwd(const hils_params* p, const void* lq, const void* k, void* lmk, float* lmk_bias, void* stream);
+
+/*
+ * Backward of hils_landmark_fwd for upstream gradients dlmk (of k'_c) and
+ * dlmk_bias (of b'_c, float32, NULL = 0), e.g. the dlmk / dlmk_bias of hils_bwd:
+ *   dlq [B, Hl, L/S, d]  written: the gradient of the landmark queries
+ *   dk  [B, Hkv, L, d]   written: the compression's gradient of the keys, summed
+ *                        over the landmark heads of each KV group (every key
+ *                        lies in a chunk, so every row is written); add it to
+ *                        the attention's dk for the keys' total gradient.
+ * Same parameter use as hils_landmark_fwd.  No workspace.  Deterministic.
+ */
+int hils_landmark_bwd(const hils_params* p, const void* lq, const void* k, const void* dlmk,
+                      const float* dlmk_bias, void* dlq, void* dk, void* stream);
 
 /*
  * Optional per-kernel timing, for profiling (not needed to use the operator).

@@ -48,7 +48,7 @@ int ok() {
 
 int check_params(const hils_params* p, int op) {
     if (!p) return fail(HILS_ERR_INVALID, "params is NULL");
-    if (op != HILS_OP_PREFILL && op != HILS_OP_DECODE && op != HILS_OP_BWD)
+    if (op != HILS_OP_PREFILL && op != HILS_OP_DECODE && op != HILS_OP_BWD && op != HILS_OP_LANDMARK)
         return fail(HILS_ERR_INVALID, "unknown op %d", op);
     if (p->B < 1 || p->Hq < 1 || p->Hkv < 1 || p->N < 1 || p->L < 1 || p->d < 1)
         return fail(HILS_ERR_INVALID, "B, Hq, Hkv, N, L and d must be >= 1 (B=%d Hq=%d Hkv=%d N=%d L=%d d=%d)",
@@ -64,7 +64,7 @@ int check_params(const hils_params* p, int op) {
     if (!isfinite(p->scale)) return fail(HILS_ERR_INVALID, "scale is not finite");
     if (p->flags & ~HILS_FLAG_GIVEN_IDX) return fail(HILS_ERR_INVALID, "unknown flags 0x%x", p->flags);
     if (op == HILS_OP_DECODE && p->N != 1) return fail(HILS_ERR_INVALID, "decode needs N == 1 (got %d)", p->N);
-    if (op != HILS_OP_DECODE && p->N > p->L)
+    if (op != HILS_OP_DECODE && op != HILS_OP_LANDMARK && p->N > p->L)
         return fail(HILS_ERR_INVALID, "prefill/backward need N <= L (N=%d L=%d)", p->N, p->L);
     if (p->B > 65535 || p->Hkv > 65535) return fail(HILS_ERR_INVALID, "B and Hkv must be <= 65535");
     if (op == HILS_OP_BWD && (p->flags & HILS_FLAG_GIVEN_IDX))
@@ -83,6 +83,8 @@ int check_params(const hils_params* p, int op) {
 
 size_t ws_bytes_for(const hils_params* p, int op) {
     switch (op) {
+        case HILS_OP_LANDMARK:
+            return 0;
         case HILS_OP_BWD:
             if (p->dtype == HILS_BF16)
                 return hils::bwd_mfma_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk);
@@ -248,6 +250,34 @@ int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* 
     a.bf16 = p->dtype == HILS_BF16;
     a.ws = workspace; a.ws_bytes = ws_bytes;
     return hip_status(hils::launch_bwd(a, (hipStream_t)stream), "hils_bwd launch");
+}
+
+static hils::LmkArgs lmk_args(const hils_params* p) {
+    hils::LmkArgs a = {};
+    a.B = p->B; a.Hkv = p->Hkv; a.Hl = p->Hl; a.L = p->L; a.d = p->d;
+    a.scale = p->scale;
+    a.bf16 = p->dtype == HILS_BF16;
+    return a;
+}
+
+int hils_landmark_fwd(const hils_params* p, const void* lq, const void* k, void* lmk, float* lmk_bias,
+                      void* stream) {
+    int rc = check_params(p, HILS_OP_LANDMARK);
+    if (rc) return rc;
+    REQUIRE(lq); REQUIRE(k); REQUIRE(lmk); REQUIRE(lmk_bias);
+    hils::LmkArgs a = lmk_args(p);
+    a.lq = lq; a.k = k; a.lmk = lmk; a.bias = lmk_bias;
+    return hip_status(hils::launch_landmark_fwd(a, (hipStream_t)stream), "hils_landmark_fwd launch");
+}
+
+int hils_landmark_bwd(const hils_params* p, const void* lq, const void* k, const void* dlmk,
+                      const float* dlmk_bias, void* dlq, void* dk, void* stream) {
+    int rc = check_params(p, HILS_OP_LANDMARK);
+    if (rc) return rc;
+    REQUIRE(lq); REQUIRE(k); REQUIRE(dlmk); REQUIRE(dlq); REQUIRE(dk);
+    hils::LmkArgs a = lmk_args(p);
+    a.lq = lq; a.k = k; a.dlmk = dlmk; a.dbias = dlmk_bias; a.dlq = dlq; a.dk = dk;
+    return hip_status(hils::launch_landmark_bwd(a, (hipStream_t)stream), "hils_landmark_bwd launch");
 }
 
 }  // extern "C"

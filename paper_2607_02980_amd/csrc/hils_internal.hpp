@@ -52,6 +52,21 @@ struct BwdArgs {
     size_t ws_bytes;
 };
 
+// Landmark compression (Prop. 3.1), forward and backward.
+struct LmkArgs {
+    const void* lq;      // landmark queries q'_c   [B, Hl, L/S, d]
+    const void* k;       // keys                    [B, Hkv, L, d]
+    void* lmk;           // fwd out: k'_c           [B, Hl, L/S, d]
+    float* bias;         // fwd out: b'_c           [B, Hl, L/S]
+    const void* dlmk;    // bwd in:  dL/dk'_c
+    const float* dbias;  // bwd in:  dL/db'_c (nullable: 0)
+    void* dlq;           // bwd out: dL/dq'_c       [B, Hl, L/S, d]
+    void* dk;            // bwd out: dL/dk          [B, Hkv, L, d]
+    int B, Hkv, Hl, L, d;
+    float scale;
+    int bf16;
+};
+
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Optional per-kernel timing (hils_timing_enable): every launch is bracketed by
@@ -104,6 +119,8 @@ size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int 
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s);  // fp32 storage
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s);
+hipError_t launch_landmark_fwd(const LmkArgs& a, hipStream_t s);
+hipError_t launch_landmark_bwd(const LmkArgs& a, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);       // fp32 storage
 hipError_t launch_bwd_mfma(const BwdArgs& a, hipStream_t s);  // bf16 storage
 size_t bwd_mfma_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K);

@@ -1,7 +1,8 @@
 """ctypes binding of libhils.so -- argument marshalling only.
 
 The entry points keep the C names (``hils_prefill_fwd``, ``hils_decode_fwd``,
-``hils_bwd``, ``hils_workspace_size``, ``hils_last_error``, ``hils_version``).
+``hils_bwd``, ``hils_landmark_fwd``, ``hils_landmark_bwd``,
+``hils_workspace_size``, ``hils_last_error``, ``hils_version``).
 They take torch tensors already resident on the GPU, check dtype, shape,
 device and contiguity, allocate missing outputs and the workspace with
 ``torch.empty`` and pass raw pointers plus the current HIP stream.  Every step
@@ -21,7 +22,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhils.so
 HILS_F32, HILS_BF16 = 0, 1
 HILS_OK, HILS_ERR_INVALID, HILS_ERR_UNSUPPORTED, HILS_ERR_WORKSPACE, HILS_ERR_HIP = range(5)
 HILS_FLAG_GIVEN_IDX = 1
-HILS_OP_PREFILL, HILS_OP_DECODE, HILS_OP_BWD = 0, 1, 2
+HILS_OP_PREFILL, HILS_OP_DECODE, HILS_OP_BWD, HILS_OP_LANDMARK = 0, 1, 2, 3
 
 
 class HilsError(RuntimeError):
@@ -49,11 +50,13 @@ def _load():
     lib.hils_prefill_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_decode_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_bwd.argtypes = [P] + [vp] * 17 + [sz, vp]
+    lib.hils_landmark_fwd.argtypes = [P, vp, vp, vp, vp, vp]
+    lib.hils_landmark_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
     lib.hils_timing_enable.argtypes = [ctypes.c_int]
     lib.hils_timing_read.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(ctypes.c_float),
                                      ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
     for f in (lib.hils_workspace_size, lib.hils_prefill_fwd, lib.hils_decode_fwd, lib.hils_bwd,
-              lib.hils_timing_enable, lib.hils_timing_read):
+              lib.hils_landmark_fwd, lib.hils_landmark_bwd, lib.hils_timing_enable, lib.hils_timing_read):
         f.restype = ctypes.c_int
     return lib
 
@@ -214,6 +217,34 @@ def hils_bwd(p: Params, dout, q, k, v, lmk, out, lse, idx, lmk_bias=None, q_rout
         _ptr(dlmk, "dlmk"), _ptr(dbias, "dbias", required=False), _ptr(dqr, "dq_route", required=False),
         _ptr(ws, "workspace"), n, _stream()))
     return {"dq": dq, "dk": dk, "dv": dv, "dlmk": dlmk, "dlmk_bias": dbias, "dq_route": dqr}
+
+
+def hils_landmark_fwd(p: Params, lq, k, lmk=None, lmk_bias=None):
+    """Landmark compression (Prop. 3.1): lq [B, Hl, L/S, d] landmark queries and
+    k [B, Hkv, L, d] -> (lmk [B, Hl, L/S, d], lmk_bias [B, Hl, L/S] float32)."""
+    S, dt = _shapes(p), p.torch_dtype
+    dev = k.device
+    lmk = torch.empty(S["lmk"], dtype=dt, device=dev) if lmk is None else lmk
+    lmk_bias = torch.empty(S["bias"], dtype=torch.float32, device=dev) if lmk_bias is None else lmk_bias
+    cp = p.c()
+    _check(LIB.hils_landmark_fwd(ctypes.byref(cp), _ptr(lq, "lq", S["lmk"], dt), _ptr(k, "k", S["kv"], dt),
+                                 _ptr(lmk, "lmk", S["lmk"], dt), _ptr(lmk_bias, "lmk_bias", S["bias"], torch.float32),
+                                 _stream()))
+    return lmk, lmk_bias
+
+
+def hils_landmark_bwd(p: Params, lq, k, dlmk, dlmk_bias=None, dlq=None, dk=None):
+    """Backward of hils_landmark_fwd -> (dlq [B, Hl, L/S, d], dk [B, Hkv, L, d])."""
+    S, dt = _shapes(p), p.torch_dtype
+    dev = k.device
+    dlq = torch.empty(S["lmk"], dtype=dt, device=dev) if dlq is None else dlq
+    dk = torch.empty(S["kv"], dtype=dt, device=dev) if dk is None else dk
+    cp = p.c()
+    _check(LIB.hils_landmark_bwd(ctypes.byref(cp), _ptr(lq, "lq", S["lmk"], dt), _ptr(k, "k", S["kv"], dt),
+                                 _ptr(dlmk, "dlmk", S["lmk"], dt),
+                                 _ptr(dlmk_bias, "dlmk_bias", S["bias"], torch.float32, False),
+                                 _ptr(dlq, "dlq", S["lmk"], dt), _ptr(dk, "dk", S["kv"], dt), _stream()))
+    return dlq, dk
 
 
 def hils_timing_enable(on: bool = True) -> None:

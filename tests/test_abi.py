@@ -162,3 +162,23 @@ def test_timing_mode_without_launches(hils):
     hils.hils_timing_enable(True)
     assert hils.hils_timing_read() == {}
     hils.hils_timing_enable(False)
+
+
+def test_landmark_entry_points_validate_on_the_host(hils):
+    # N > L is fine for the compression (N is not used); no workspace is needed
+    p = params(hils, N=4096, L=256)
+    assert hils.hils_workspace_size(p, hils.HILS_OP_LANDMARK) == 0
+    cp = p.c()
+    assert hils.LIB.hils_landmark_fwd(ctypes.byref(cp), FAKE, FAKE, None, FAKE, None) == hils.HILS_ERR_INVALID
+    assert "lmk" in hils.hils_last_error()
+    assert hils.LIB.hils_landmark_fwd(ctypes.byref(cp), FAKE, FAKE, FAKE, None, None) == hils.HILS_ERR_INVALID
+    assert "lmk_bias" in hils.hils_last_error()
+    assert hils.LIB.hils_landmark_bwd(ctypes.byref(cp), FAKE, FAKE, FAKE, None, FAKE, None, None) == \
+        hils.HILS_ERR_INVALID
+    assert "dk" in hils.hils_last_error()
+    bad = params(hils, L=200).c()
+    assert hils.LIB.hils_landmark_fwd(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, None) == hils.HILS_ERR_INVALID
+    assert "multiple of chunk" in hils.hils_last_error()
+    odd = params(hils, d=96).c()
+    assert hils.LIB.hils_landmark_bwd(ctypes.byref(odd), FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == \
+        hils.HILS_ERR_UNSUPPORTED

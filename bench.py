@@ -259,6 +259,32 @@ def bench_train(torch, hils, synth, W_, steps, warmup):
             "kernels_avg_ms": {k: round(v["total_ms"] / max(1, v["launches"]), 3) for k, v in kernels.items()}}
 
 
+def bench_landmark(torch, hils, synth, W_, steps, warmup):
+    """Landmark compression (Prop. 3.1) forward and backward on the workload's
+    K, one landmark per (query head, chunk).  Algorithmic bytes: the forward
+    reads K and q' and writes k' and b'; the backward reads K, q', dk' and db'
+    and writes dq' and dK."""
+    p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=1, L=W_.L, d=W_.d, chunk=W_.chunk, topk=1, window=1,
+                    dtype=W_.dtype)
+    nc, Hl, e = p.L // p.chunk, p.Hq, 2 if p.dtype == "bf16" else 4
+    lq = synth.normal_device((p.B, Hl, nc, p.d), synth.seed_for(W_.wid, "lmk"), p.dtype, "cuda")
+    k = synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "k"), p.dtype, "cuda")
+    dl = synth.normal_device((p.B, Hl, nc, p.d), synth.seed_for(W_.wid, "dout"), p.dtype, "cuda")
+    db = synth.normal_device((p.B, Hl, nc), synth.seed_for(W_.wid, "bias"), "f32", "cuda")
+    lmk, bias = hils.hils_landmark_fwd(p, lq, k)
+    dlq, dk = hils.hils_landmark_bwd(p, lq, k, dl, db)
+    kb, lb, bb = p.B * p.Hkv * p.L * p.d * e, p.B * Hl * nc * p.d * e, p.B * Hl * nc * 4
+    out = {"workload": W_.name, "landmark_heads": Hl}
+    for name, fn, nbytes in (("fwd", lambda: hils.hils_landmark_fwd(p, lq, k, lmk, bias), kb + 2 * lb + bb),
+                             ("bwd", lambda: hils.hils_landmark_bwd(p, lq, k, dl, db, dlq, dk), 2 * kb + 3 * lb + bb)):
+        ms = Timer(torch).run(fn, steps, warmup)
+        out[name] = {"avg_ms": round(ms, 4), "bytes": nbytes, "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del lq, k, dl, db, lmk, bias, dlq, dk
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(W_, host, target_s=20.0):
     """The oracle (plain fp32 build, as it stands) on a bounded sample of query
     rows of the same workload, on all host cores; scaled to tokens/s."""
@@ -292,6 +318,7 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-train", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-landmark", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 1 GiB device-to-device (a plain copy kernel of known size, used to "
                          "calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -354,6 +381,8 @@ def main():
                                                  max(3, args.steps // 2), 2)
     if not args.no_train:
         res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], 3, 1)
+    if not args.no_landmark:
+        res["extra"]["landmark"] = bench_landmark(torch, hils, synth, Wp, args.steps, args.warmup)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(Wp, host)
     print(json.dumps(res), flush=True)

@@ -76,6 +76,11 @@ typedef enum {
  * are ignored; entries must be ascending. */
 #define HILS_FLAG_GIVEN_IDX 1u
 
+/* Landmark compression flag (hils_landmark_fwd/bwd only): the landmark-token-free
+ * variant of Sec. 4.1, one learnable landmark query per landmark head shared by
+ * every chunk of every sequence: lq and dlq are [Hl, d] instead of [B, Hl, L/S, d]. */
+#define HILS_FLAG_SHARED_LMK_QUERY 2u
+
 typedef enum { HILS_OP_PREFILL = 0, HILS_OP_DECODE = 1, HILS_OP_BWD = 2, HILS_OP_LANDMARK = 3 } hils_op;
 
 typedef struct {
@@ -175,8 +180,9 @@ int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* 
  *                              hl / (Hl / Hkv)
  *   lmk      [B, Hl, L/S, d]   written (dtype)
  *   lmk_bias [B, Hl, L/S] f32  written
- * Uses B, Hq, Hkv, Hl, L, d, chunk, scale and dtype of `p`; N, topk and window
- * are not used (they must still be >= 1).  No workspace.
+ * Uses B, Hq, Hkv, Hl, L, d, chunk, scale, dtype and flags of `p`; N, topk and
+ * window are not used (they must still be >= 1).  Under HILS_FLAG_SHARED_LMK_QUERY
+ * lq is [Hl, d]: q'_c is that head's one query for every chunk.  No workspace.
  */
 int hils_landmark_fwd(const hils_params* p, const void* lq, const void* k, void* lmk, float* lmk_bias, void* stream);
 
@@ -188,10 +194,16 @@ int hils_landmark_fwd(const hils_params* p, const void* lq, const void* k, void*
  *                        over the landmark heads of each KV group (every key
  *                        lies in a chunk, so every row is written); add it to
  *                        the attention's dk for the keys' total gradient.
- * Same parameter use as hils_landmark_fwd.  No workspace.  Deterministic.
+ * Same parameter use as hils_landmark_fwd.  Under HILS_FLAG_SHARED_LMK_QUERY, lq
+ * and dlq are [Hl, d] and dlq is the sum of the per-chunk gradients over every
+ * chunk and sequence; that sum needs a workspace of
+ * hils_workspace_size(p, HILS_OP_LANDMARK) bytes (B * Hl * L/S * d floats, caller
+ * owned, contents on entry ignored).  Without the flag the size is 0 and
+ * workspace may be NULL.  Deterministic (fixed summation order, no atomics).
  */
 int hils_landmark_bwd(const hils_params* p, const void* lq, const void* k, const void* dlmk,
-                      const float* dlmk_bias, void* dlq, void* dk, void* stream);
+                      const float* dlmk_bias, void* dlq, void* dk, void* workspace, size_t ws_bytes,
+                      void* stream);
 
 /*
  * Optional per-kernel timing, for profiling (not needed to use the operator).

@@ -214,12 +214,24 @@ def bwd(shape: Shape, dout, q, k, v, lmk, idx, bias=None, q_route=None, qpos=Non
     return {"dq": dq, "dk": dk, "dv": dv, "dlmk": dlmk, "dbias": dbias, "dq_route": dqr}
 
 
-def landmark_fwd(shape: Shape, lq, k, prec: str = "f64"):
-    """Landmark compression (Prop. 3.1): lq [B, Hl, L/S, d] landmark queries q'_c,
-    k [B, Hkv, L, d].  Returns dict(lmk = k'_c [B, Hl, L/S, d], bias = b'_c [B, Hl, L/S])."""
+def _shared_query(s: Shape, lq):
+    """The landmark-token-free variant (Sec. 4.1): one learnable query per
+    landmark head, [Hl, d], used as q'_c for every chunk of every sequence."""
+    lq = np.asarray(lq, np.float32)
+    if lq.shape != (s.Hl, s.d):
+        raise ValueError(f"shared landmark query: expected [{s.Hl}, {s.d}], got {list(lq.shape)}")
+    return np.ascontiguousarray(np.broadcast_to(lq[None, :, None, :], (s.B, s.Hl, s.L // s.chunk, s.d)))
+
+
+def landmark_fwd(shape: Shape, lq, k, prec: str = "f64", shared: bool = False):
+    """Landmark compression (Prop. 3.1): lq [B, Hl, L/S, d] landmark queries q'_c
+    (or [Hl, d] with shared=True: one query per head for all chunks), k [B, Hkv, L, d].
+    Returns dict(lmk = k'_c [B, Hl, L/S, d], bias = b'_c [B, Hl, L/S])."""
     lib = _lib(prec)
     R = _real(prec)
     s = shape
+    if shared:
+        lq = _shared_query(s, lq)
     lq, k = _f32(lq), _f32(k)
     _check(s, lmk=lq, k=k)
     nc = s.L // s.chunk
@@ -233,12 +245,16 @@ def landmark_fwd(shape: Shape, lq, k, prec: str = "f64"):
     return {"lmk": lmk, "bias": bias}
 
 
-def landmark_bwd(shape: Shape, lq, k, dlmk, dbias=None, prec: str = "f64"):
+def landmark_bwd(shape: Shape, lq, k, dlmk, dbias=None, prec: str = "f64", shared: bool = False):
     """Backward of the landmark compression for upstream dlmk (of k'_c) and
-    dbias (of b'_c, None = 0).  Returns dict(dlq [B, Hl, L/S, d], dk [B, Hkv, L, d])."""
+    dbias (of b'_c, None = 0).  Returns dict(dlq [B, Hl, L/S, d], dk [B, Hkv, L, d]).
+    With shared=True lq is [Hl, d] and dlq [Hl, d] is the sum of the per-chunk
+    gradients over every chunk and sequence that used the shared query."""
     lib = _lib(prec)
     R = _real(prec)
     s = shape
+    if shared:
+        lq = _shared_query(s, lq)
     lq, k, dlmk, dbias = _f32(lq), _f32(k), _f32(dlmk), _f32(dbias)
     _check(s, lmk=lq, k=k, bias=dbias)
     _check(s, lmk=dlmk)
@@ -250,6 +266,8 @@ def landmark_bwd(shape: Shape, lq, k, dlmk, dbias=None, prec: str = "f64"):
     sh = s.c()
     if fn(ctypes.byref(sh), _ptr(lq), _ptr(k), _ptr(dlmk), _ptr(dbias), _ptr(dlq), _ptr(dk)):
         raise ValueError("oracle landmark_bwd failed")
+    if shared:
+        dlq = dlq.sum(axis=(0, 2))
     return {"dlq": dlq, "dk": dk}
 
 

@@ -62,7 +62,12 @@ int check_params(const hils_params* p, int op) {
     if (p->L % p->chunk) return fail(HILS_ERR_INVALID, "L=%d is not a multiple of chunk=%d", p->L, p->chunk);
     if (p->dtype != HILS_F32 && p->dtype != HILS_BF16) return fail(HILS_ERR_INVALID, "unknown dtype %d", (int)p->dtype);
     if (!isfinite(p->scale)) return fail(HILS_ERR_INVALID, "scale is not finite");
-    if (p->flags & ~HILS_FLAG_GIVEN_IDX) return fail(HILS_ERR_INVALID, "unknown flags 0x%x", p->flags);
+    if (p->flags & ~(HILS_FLAG_GIVEN_IDX | HILS_FLAG_SHARED_LMK_QUERY))
+        return fail(HILS_ERR_INVALID, "unknown flags 0x%x", p->flags);
+    if ((p->flags & HILS_FLAG_SHARED_LMK_QUERY) && op != HILS_OP_LANDMARK)
+        return fail(HILS_ERR_INVALID, "HILS_FLAG_SHARED_LMK_QUERY applies to the landmark compression only");
+    if ((p->flags & HILS_FLAG_GIVEN_IDX) && op == HILS_OP_LANDMARK)
+        return fail(HILS_ERR_INVALID, "HILS_FLAG_GIVEN_IDX does not apply to the landmark compression");
     if (op == HILS_OP_DECODE && p->N != 1) return fail(HILS_ERR_INVALID, "decode needs N == 1 (got %d)", p->N);
     if (op != HILS_OP_DECODE && op != HILS_OP_LANDMARK && p->N > p->L)
         return fail(HILS_ERR_INVALID, "prefill/backward need N <= L (N=%d L=%d)", p->N, p->L);
@@ -84,7 +89,8 @@ int check_params(const hils_params* p, int op) {
 size_t ws_bytes_for(const hils_params* p, int op) {
     switch (op) {
         case HILS_OP_LANDMARK:
-            return 0;
+            return hils::landmark_workspace_bytes(p->B, p->Hl, p->L / p->chunk, p->d,
+                                                  (p->flags & HILS_FLAG_SHARED_LMK_QUERY) != 0);
         case HILS_OP_BWD:
             if (p->dtype == HILS_BF16)
                 return hils::bwd_mfma_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk);
@@ -257,6 +263,7 @@ static hils::LmkArgs lmk_args(const hils_params* p) {
     a.B = p->B; a.Hkv = p->Hkv; a.Hl = p->Hl; a.L = p->L; a.d = p->d;
     a.scale = p->scale;
     a.bf16 = p->dtype == HILS_BF16;
+    a.shared = (p->flags & HILS_FLAG_SHARED_LMK_QUERY) != 0;
     return a;
 }
 
@@ -271,12 +278,16 @@ int hils_landmark_fwd(const hils_params* p, const void* lq, const void* k, void*
 }
 
 int hils_landmark_bwd(const hils_params* p, const void* lq, const void* k, const void* dlmk,
-                      const float* dlmk_bias, void* dlq, void* dk, void* stream) {
+                      const float* dlmk_bias, void* dlq, void* dk, void* workspace, size_t ws_bytes,
+                      void* stream) {
     int rc = check_params(p, HILS_OP_LANDMARK);
     if (rc) return rc;
     REQUIRE(lq); REQUIRE(k); REQUIRE(dlmk); REQUIRE(dlq); REQUIRE(dk);
+    rc = check_ws(p, HILS_OP_LANDMARK, workspace, ws_bytes);
+    if (rc) return rc;
     hils::LmkArgs a = lmk_args(p);
     a.lq = lq; a.k = k; a.dlmk = dlmk; a.dbias = dlmk_bias; a.dlq = dlq; a.dk = dk;
+    a.ws = static_cast<float*>(workspace);
     return hip_status(hils::launch_landmark_bwd(a, (hipStream_t)stream), "hils_landmark_bwd launch");
 }
 

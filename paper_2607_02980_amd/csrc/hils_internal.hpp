@@ -54,17 +54,19 @@ struct BwdArgs {
 
 // Landmark compression (Prop. 3.1), forward and backward.
 struct LmkArgs {
-    const void* lq;      // landmark queries q'_c   [B, Hl, L/S, d]
+    const void* lq;      // landmark queries q'_c   [B, Hl, L/S, d] ([Hl, d] if shared)
     const void* k;       // keys                    [B, Hkv, L, d]
     void* lmk;           // fwd out: k'_c           [B, Hl, L/S, d]
     float* bias;         // fwd out: b'_c           [B, Hl, L/S]
     const void* dlmk;    // bwd in:  dL/dk'_c
     const float* dbias;  // bwd in:  dL/db'_c (nullable: 0)
-    void* dlq;           // bwd out: dL/dq'_c       [B, Hl, L/S, d]
+    void* dlq;           // bwd out: dL/dq'_c       [B, Hl, L/S, d] ([Hl, d] if shared)
     void* dk;            // bwd out: dL/dk          [B, Hkv, L, d]
+    float* ws;           // shared query: per-chunk dq' in fp32 [B, Hl, L/S, d]
     int B, Hkv, Hl, L, d;
     float scale;
     int bf16;
+    int shared;          // one landmark query per head for every chunk (Sec. 4.1)
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -121,6 +123,7 @@ hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s);  // fp32 storag
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_landmark_fwd(const LmkArgs& a, hipStream_t s);
 hipError_t launch_landmark_bwd(const LmkArgs& a, hipStream_t s);
+size_t landmark_workspace_bytes(int B, int Hl, int nC, int d, bool shared);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);       // fp32 storage
 hipError_t launch_bwd_mfma(const BwdArgs& a, hipStream_t s);  // bf16 storage
 size_t bwd_mfma_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K);

@@ -16,6 +16,11 @@
 // head when Hl == Hq, one when Hl == Hkv), one wave per head.  The work is a
 // single pass over K (16 KiB per chunk in bf16), so the kernels are organised
 // around that read; the arithmetic is a few dot products per key.
+//
+// Shared-query variant (the landmark-token-free alternative of Sec. 4.1): one
+// query per landmark head serves every chunk, lq is [Hl, D], and its gradient
+// is the sum of the per-chunk gradients: k_lmk_bwd leaves them in fp32 in the
+// workspace and k_lmk_dq_sum adds them up in a fixed order.
 #include "hils_device.hpp"
 #include "hils_dispatch.hpp"
 #include "hils_internal.hpp"
@@ -38,10 +43,12 @@ struct LmkSmem {
 };
 
 // Stage the chunk's keys and, per landmark head of the group, one D-vector
-// from each of up to two [B, Hl, L/S, D] tensors.
+// from each of up to two [B, Hl, L/S, D] tensors (x0 is [Hl, D] when
+// x0_shared: the shared landmark query).
 template <typename T, int D>
 __device__ __forceinline__ void stage(const LmkArgs& a, LmkSmem<T, D>& sm, int b, int g, int c, int nlh,
-                                      const void* x0, float (*s0)[D], const void* x1, float (*s1)[D]) {
+                                      const void* x0, bool x0_shared, float (*s0)[D], const void* x1,
+                                      float (*s1)[D]) {
     const int tid = threadIdx.x;
     const int nC = a.L / kChunk;
     const T* kb = as<T>(a.k) + (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
@@ -55,7 +62,8 @@ __device__ __forceinline__ void stage(const LmkArgs& a, LmkSmem<T, D>& sm, int b
     for (int e = tid; e < nlh * D; e += kBlock) {
         const int hh = e / D, dd = e % D;
         const size_t row = ((size_t)b * a.Hl + g * nlh + hh) * nC + c;
-        if (x0) s0[hh][dd] = to_f32(as<T>(x0)[row * D + dd]);
+        const size_t row0 = x0_shared ? (size_t)(g * nlh + hh) : row;
+        if (x0) s0[hh][dd] = to_f32(as<T>(x0)[row0 * D + dd]);
         if (x1) s1[hh][dd] = to_f32(as<T>(x1)[row * D + dd]);
     }
 }
@@ -76,7 +84,7 @@ __global__ __launch_bounds__(kBlock) void k_lmk_fwd(LmkArgs a) {
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int nlh = a.Hl / a.Hkv, nC = a.L / kChunk;
-    stage<T, D>(a, sm, b, g, c, nlh, a.lq, sm.q, nullptr, nullptr);
+    stage<T, D>(a, sm, b, g, c, nlh, a.lq, a.shared, sm.q, nullptr, nullptr);
     __syncthreads();
     for (int hh = wave; hh < nlh; hh += kBlock / kWave) {
         const float s = a.scale * key_dot<D>(sm.k, sm.q[hh], lane);  // lane = key (S = 64)
@@ -107,7 +115,7 @@ __global__ __launch_bounds__(kBlock) void k_lmk_bwd(LmkArgs a) {
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int nlh = a.Hl / a.Hkv, nC = a.L / kChunk;
-    stage<T, D>(a, sm, b, g, c, nlh, a.lq, sm.q, a.dlmk, sm.dk);
+    stage<T, D>(a, sm, b, g, c, nlh, a.lq, a.shared, sm.q, a.dlmk, sm.dk);
     if (tid < nlh) sm.db[tid] = a.dbias ? a.dbias[((size_t)b * a.Hl + g * nlh + tid) * nC + c] : 0.f;
     __syncthreads();
     for (int hh = wave; hh < nlh; hh += kBlock / kWave) {
@@ -123,14 +131,17 @@ __global__ __launch_bounds__(kBlock) void k_lmk_bwd(LmkArgs a) {
         sm.ds[hh][lane] = p * (gp - mean);
     }
     __syncthreads();
-    // dq'_c per head
+    // dq'_c per head (the shared query: the chunk's term, in fp32)
     for (int o = tid; o < nlh * D; o += kBlock) {
         const int hh = o / D, dd = o % D;
         float acc = 0.f;
 #pragma unroll 16
         for (int j = 0; j < kChunk; ++j) acc += sm.ds[hh][j] * sm.k[j][dd];
         const size_t row = ((size_t)b * a.Hl + g * nlh + hh) * nC + c;
-        as_mut<T>(a.dlq)[row * D + dd] = from_f32<T>(a.scale * acc);
+        if (a.shared)
+            a.ws[row * D + dd] = a.scale * acc;
+        else
+            as_mut<T>(a.dlq)[row * D + dd] = from_f32<T>(a.scale * acc);
     }
     // dk of the chunk's keys, summed over the group's landmark heads
     T* dkb = as_mut<T>(a.dk) + (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
@@ -142,20 +153,49 @@ __global__ __launch_bounds__(kBlock) void k_lmk_bwd(LmkArgs a) {
     }
 }
 
+// Shared query: dlq[hl] = sum over b, then c, of the chunk terms.  One block per
+// landmark head; thread t adds rows t / D, t / D + 256 / D, ... of column t % D,
+// then the 256 / D partial sums are added in thread order.
+template <typename T, int D>
+__global__ __launch_bounds__(kBlock) void k_lmk_dq_sum(LmkArgs a) {
+    constexpr int R = kBlock / D;
+    __shared__ float part[R][D];
+    const int hl = blockIdx.x, tid = threadIdx.x, dd = tid % D, r0 = tid / D;
+    const int nC = a.L / kChunk;
+    float acc = 0.f;
+    for (int b = 0; b < a.B; ++b) {
+        const float* src = a.ws + ((size_t)b * a.Hl + hl) * nC * D;
+        for (int c = r0; c < nC; c += R) acc += src[(size_t)c * D + dd];
+    }
+    part[r0][dd] = acc;
+    __syncthreads();
+    if (tid < D) {
+        float t = 0.f;
+#pragma unroll
+        for (int r = 0; r < R; ++r) t += part[r][tid];
+        as_mut<T>(a.dlq)[(size_t)hl * D + tid] = from_f32<T>(t);
+    }
+}
+
 template <bool BWD>
 struct LmkRun {
     template <typename T, int D, int G>
     static hipError_t run(const LmkArgs& a, hipStream_t s) {
         const dim3 grid(a.L / kChunk, a.Hkv, a.B);
-        if (BWD)
+        if (BWD) {
             HILS_LAUNCH("k_lmk_bwd", (k_lmk_bwd<T, D>), grid, dim3(kBlock), 0, s, a);
-        else
+            if (a.shared) HILS_LAUNCH("k_lmk_dq_sum", (k_lmk_dq_sum<T, D>), dim3(a.Hl), dim3(kBlock), 0, s, a);
+        } else
             HILS_LAUNCH("k_lmk_fwd", (k_lmk_fwd<T, D>), grid, dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }
 };
 
 }  // namespace
+
+size_t landmark_workspace_bytes(int B, int Hl, int nC, int d, bool shared) {
+    return shared ? (size_t)B * Hl * nC * d * sizeof(float) : 0;
+}
 
 // The kernels depend on (T, D) only; G = 1 picks one instantiation.
 hipError_t launch_landmark_fwd(const LmkArgs& a, hipStream_t s) { return dispatch<LmkRun<false>>(a.bf16, a.d, 1, a, s); }

@@ -22,6 +22,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhils.so
 HILS_F32, HILS_BF16 = 0, 1
 HILS_OK, HILS_ERR_INVALID, HILS_ERR_UNSUPPORTED, HILS_ERR_WORKSPACE, HILS_ERR_HIP = range(5)
 HILS_FLAG_GIVEN_IDX = 1
+HILS_FLAG_SHARED_LMK_QUERY = 2
 HILS_OP_PREFILL, HILS_OP_DECODE, HILS_OP_BWD, HILS_OP_LANDMARK = 0, 1, 2, 3
 
 
@@ -51,7 +52,7 @@ def _load():
     lib.hils_decode_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_bwd.argtypes = [P] + [vp] * 17 + [sz, vp]
     lib.hils_landmark_fwd.argtypes = [P, vp, vp, vp, vp, vp]
-    lib.hils_landmark_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
+    lib.hils_landmark_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_timing_enable.argtypes = [ctypes.c_int]
     lib.hils_timing_read.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(ctypes.c_float),
                                      ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
@@ -219,31 +220,40 @@ def hils_bwd(p: Params, dout, q, k, v, lmk, out, lse, idx, lmk_bias=None, q_rout
     return {"dq": dq, "dk": dk, "dv": dv, "dlmk": dlmk, "dlmk_bias": dbias, "dq_route": dqr}
 
 
+def _lq_shape(p: Params, S):
+    return (p.Hl or p.Hq, p.d) if p.flags & HILS_FLAG_SHARED_LMK_QUERY else S["lmk"]
+
+
 def hils_landmark_fwd(p: Params, lq, k, lmk=None, lmk_bias=None):
-    """Landmark compression (Prop. 3.1): lq [B, Hl, L/S, d] landmark queries and
-    k [B, Hkv, L, d] -> (lmk [B, Hl, L/S, d], lmk_bias [B, Hl, L/S] float32)."""
+    """Landmark compression (Prop. 3.1): lq [B, Hl, L/S, d] landmark queries (or
+    [Hl, d] under HILS_FLAG_SHARED_LMK_QUERY) and k [B, Hkv, L, d] ->
+    (lmk [B, Hl, L/S, d], lmk_bias [B, Hl, L/S] float32)."""
     S, dt = _shapes(p), p.torch_dtype
     dev = k.device
     lmk = torch.empty(S["lmk"], dtype=dt, device=dev) if lmk is None else lmk
     lmk_bias = torch.empty(S["bias"], dtype=torch.float32, device=dev) if lmk_bias is None else lmk_bias
     cp = p.c()
-    _check(LIB.hils_landmark_fwd(ctypes.byref(cp), _ptr(lq, "lq", S["lmk"], dt), _ptr(k, "k", S["kv"], dt),
+    _check(LIB.hils_landmark_fwd(ctypes.byref(cp), _ptr(lq, "lq", _lq_shape(p, S), dt), _ptr(k, "k", S["kv"], dt),
                                  _ptr(lmk, "lmk", S["lmk"], dt), _ptr(lmk_bias, "lmk_bias", S["bias"], torch.float32),
                                  _stream()))
     return lmk, lmk_bias
 
 
-def hils_landmark_bwd(p: Params, lq, k, dlmk, dlmk_bias=None, dlq=None, dk=None):
-    """Backward of hils_landmark_fwd -> (dlq [B, Hl, L/S, d], dk [B, Hkv, L, d])."""
+def hils_landmark_bwd(p: Params, lq, k, dlmk, dlmk_bias=None, dlq=None, dk=None, workspace=None):
+    """Backward of hils_landmark_fwd -> (dlq [B, Hl, L/S, d] (or [Hl, d] under
+    HILS_FLAG_SHARED_LMK_QUERY), dk [B, Hkv, L, d])."""
     S, dt = _shapes(p), p.torch_dtype
     dev = k.device
-    dlq = torch.empty(S["lmk"], dtype=dt, device=dev) if dlq is None else dlq
+    lqs = _lq_shape(p, S)
+    dlq = torch.empty(lqs, dtype=dt, device=dev) if dlq is None else dlq
     dk = torch.empty(S["kv"], dtype=dt, device=dev) if dk is None else dk
+    ws, n = _workspace(p, HILS_OP_LANDMARK, workspace)
     cp = p.c()
-    _check(LIB.hils_landmark_bwd(ctypes.byref(cp), _ptr(lq, "lq", S["lmk"], dt), _ptr(k, "k", S["kv"], dt),
+    _check(LIB.hils_landmark_bwd(ctypes.byref(cp), _ptr(lq, "lq", lqs, dt), _ptr(k, "k", S["kv"], dt),
                                  _ptr(dlmk, "dlmk", S["lmk"], dt),
                                  _ptr(dlmk_bias, "dlmk_bias", S["bias"], torch.float32, False),
-                                 _ptr(dlq, "dlq", S["lmk"], dt), _ptr(dk, "dk", S["kv"], dt), _stream()))
+                                 _ptr(dlq, "dlq", lqs, dt), _ptr(dk, "dk", S["kv"], dt), _ptr(ws, "workspace"), n,
+                                 _stream()))
     return dlq, dk
 
 

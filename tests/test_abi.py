@@ -173,12 +173,26 @@ def test_landmark_entry_points_validate_on_the_host(hils):
     assert "lmk" in hils.hils_last_error()
     assert hils.LIB.hils_landmark_fwd(ctypes.byref(cp), FAKE, FAKE, FAKE, None, None) == hils.HILS_ERR_INVALID
     assert "lmk_bias" in hils.hils_last_error()
-    assert hils.LIB.hils_landmark_bwd(ctypes.byref(cp), FAKE, FAKE, FAKE, None, FAKE, None, None) == \
+    assert hils.LIB.hils_landmark_bwd(ctypes.byref(cp), FAKE, FAKE, FAKE, None, FAKE, None, None, 0, None) == \
         hils.HILS_ERR_INVALID
     assert "dk" in hils.hils_last_error()
     bad = params(hils, L=200).c()
     assert hils.LIB.hils_landmark_fwd(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, None) == hils.HILS_ERR_INVALID
     assert "multiple of chunk" in hils.hils_last_error()
     odd = params(hils, d=96).c()
-    assert hils.LIB.hils_landmark_bwd(ctypes.byref(odd), FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == \
+    assert hils.LIB.hils_landmark_bwd(ctypes.byref(odd), FAKE, FAKE, FAKE, None, FAKE, FAKE, None, 0, None) == \
         hils.HILS_ERR_UNSUPPORTED
+    # the shared landmark query (one per head for every chunk) needs B*Hl*(L/S)*d floats
+    # to sum its per-chunk gradients, and is a landmark-only flag
+    sh = params(hils, B=2, Hq=8, Hkv=2, L=512, d=64, flags=hils.HILS_FLAG_SHARED_LMK_QUERY)
+    assert hils.hils_workspace_size(sh, hils.HILS_OP_LANDMARK) == 2 * 8 * 8 * 64 * 4
+    sc = sh.c()
+    assert hils.LIB.hils_landmark_bwd(ctypes.byref(sc), FAKE, FAKE, FAKE, None, FAKE, FAKE, None, 0, None) == \
+        hils.HILS_ERR_WORKSPACE
+    assert hils.LIB.hils_landmark_bwd(ctypes.byref(sc), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 100, None) == \
+        hils.HILS_ERR_WORKSPACE
+    for op in (hils.HILS_OP_PREFILL, hils.HILS_OP_DECODE, hils.HILS_OP_BWD):
+        with pytest.raises(hils.HilsError, match="landmark compression only"):
+            hils.hils_workspace_size(params(hils, N=1, flags=hils.HILS_FLAG_SHARED_LMK_QUERY), op)
+    gi = params(hils, flags=hils.HILS_FLAG_GIVEN_IDX).c()
+    assert hils.LIB.hils_landmark_fwd(ctypes.byref(gi), FAKE, FAKE, FAKE, FAKE, None) == hils.HILS_ERR_INVALID

@@ -22,10 +22,17 @@ CASES = {
 }
 
 
+def shared(p):
+    from paper_2607_02980_amd import hils
+
+    return bool(p.flags & hils.HILS_FLAG_SHARED_LMK_QUERY)
+
+
 def inputs(p, wid, sd_q=2.0):
     nc = p.L // p.chunk
     Hl = p.Hl or p.Hq
-    lq = synth.normal_device((p.B, Hl, nc, p.d), synth.seed_for(wid, "q"), p.dtype, "cuda")
+    lq_shape = (Hl, p.d) if shared(p) else (p.B, Hl, nc, p.d)
+    lq = synth.normal_device(lq_shape, synth.seed_for(wid, "q"), p.dtype, "cuda")
     lq = (lq.float() * sd_q).to(lq.dtype)  # sharper chunk attention than N(0,1)
     k = synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(wid, "k"), p.dtype, "cuda")
     dl = synth.normal_device((p.B, Hl, nc, p.d), synth.seed_for(wid, "dout"), p.dtype, "cuda")
@@ -41,32 +48,38 @@ def run(p, wid):
     dlq, dk = hils.hils_landmark_bwd(p, lq, k, dl, db)
     torch.cuda.synchronize()
     s = oshape(p)
-    ref = oracle.landmark_fwd(s, np32(lq), np32(k))
+    sh = shared(p)
+    ref = oracle.landmark_fwd(s, np32(lq), np32(k), shared=sh)
     check_close("lmk", np32(lmk), ref["lmk"], p.dtype)
     # b' is float32 output; inputs are exact on both sides, the sums differ in order only
     d = np.abs(np32(bias) - ref["bias"]).max()
     log(f"  bias: max|d|={d:.3e}")
     assert d < (2e-4 if p.dtype == "bf16" else 1e-4), d
-    g = oracle.landmark_bwd(s, np32(lq), np32(k), np32(dl), np32(db))
+    g = oracle.landmark_bwd(s, np32(lq), np32(k), np32(dl), np32(db), shared=sh)
     check_close("dlq", np32(dlq), g["dlq"], p.dtype, rel=True)
     check_close("dk", np32(dk), g["dk"], p.dtype, rel=True)
 
 
 @pytest.mark.parametrize("name", list(CASES))
-def test_landmark_matches_oracle(name):
+@pytest.mark.parametrize("query", ["per_chunk", "shared"])
+def test_landmark_matches_oracle(name, query):
     from paper_2607_02980_amd import hils
 
     kw, wid = CASES[name]
-    p = hils.Params(topk=1, window=1, **kw)
-    log(f"[landmark] case={name} params={kw}")
+    flags = hils.HILS_FLAG_SHARED_LMK_QUERY if query == "shared" else 0
+    p = hils.Params(topk=1, window=1, flags=flags, **kw)
+    log(f"[landmark] case={name} query={query} params={kw}")
     run(p, wid)
 
 
-def test_landmark_full_prefill_shape():
+@pytest.mark.parametrize("query", ["per_chunk", "shared"])
+def test_landmark_full_prefill_shape(query):
     from paper_2607_02980_amd import hils
 
     W = WORKLOADS["prefill_32k_bf16"]
-    p = hils.Params(B=W.B, Hq=W.Hq, Hkv=W.Hkv, N=1, L=W.L, d=W.d, chunk=W.chunk, topk=1, window=1, dtype=W.dtype)
+    flags = hils.HILS_FLAG_SHARED_LMK_QUERY if query == "shared" else 0
+    p = hils.Params(B=W.B, Hq=W.Hq, Hkv=W.Hkv, N=1, L=W.L, d=W.d, chunk=W.chunk, topk=1, window=1, dtype=W.dtype,
+                    flags=flags)
     log(f"[landmark] full shape of {W.name}: B={p.B} Hl={p.Hl or p.Hq} chunks={p.L // p.chunk} d={p.d}")
     run(p, 406)
 

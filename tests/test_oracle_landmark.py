@@ -174,3 +174,42 @@ def test_group_heads_sum_into_dk():
         dk[:, gg] += r["dk"][:, 0]
         np.testing.assert_allclose(g["dlq"][:, hl], r["dlq"][:, 0], rtol=0, atol=1e-12)
     np.testing.assert_allclose(g["dk"], dk, rtol=0, atol=1e-12)
+
+
+def test_shared_query_variant_matches_finite_differences():
+    # Sec. 4.1's landmark-token-free variant: one query per landmark head for every
+    # chunk; its gradient is checked by central differences of the loss in that query
+    rng = np.random.default_rng(18)
+    s = shape(B=2, Hq=4, Hkv=2, L=192, d=8)
+    nc = s.L // s.chunk
+    q = lambda *shp: np.round(rand(rng, *shp) * 64) / 64
+    lq, k = q(s.Hl, s.d), q(s.B, s.Hkv, s.L, s.d)
+    dl = rand(rng, s.B, s.Hl, nc, s.d).astype(np.float64)
+    db = rand(rng, s.B, s.Hl, nc).astype(np.float64)
+    r = oracle.landmark_fwd(s, lq, k, shared=True)
+    # forward: every chunk sees the same query, so chunk c of head hl matches the
+    # per-chunk attention of that one query (scipy's logsumexp route of Prop. 3.1)
+    for b in range(s.B):
+        for hl in range(s.Hl):
+            for c in range(nc):
+                K = chunk_keys(s, k, b, hl, c)
+                assert abs(s.scale * lq[hl].astype(np.float64) @ r["lmk"][b, hl, c] + r["bias"][b, hl, c]
+                           - logsumexp(s.scale * K @ lq[hl].astype(np.float64))) < 1e-12
+    g = oracle.landmark_bwd(s, lq, k, dl, db, shared=True)
+    assert g["dlq"].shape == (s.Hl, s.d)
+
+    def loss(x):
+        rr = oracle.landmark_fwd(s, x, k, shared=True)
+        return float((rr["lmk"] * dl).sum() + (rr["bias"] * db).sum())
+
+    h = 2.0 ** -12
+    for hl in range(s.Hl):
+        for dd in range(s.d):
+            xp, xm = lq.copy(), lq.copy()
+            xp[hl, dd] += h
+            xm[hl, dd] -= h
+            fd = (loss(xp) - loss(xm)) / (2 * h)
+            assert abs(fd - g["dlq"][hl, dd]) < 1e-5 * max(1.0, abs(fd)), (hl, dd, fd, g["dlq"][hl, dd])
+    # dk is the per-chunk backward's dk with the broadcast query
+    full = oracle.landmark_bwd(s, np.broadcast_to(lq[None, :, None], (s.B, s.Hl, nc, s.d)), k, dl, db)
+    np.testing.assert_array_equal(g["dk"], full["dk"])

@@ -271,6 +271,47 @@ def landmark_bwd(shape: Shape, lq, k, dlmk, dbias=None, prec: str = "f64", share
     return {"dlq": dlq, "dk": dk}
 
 
+def decode_positions(shape: Shape, seqlens=None):
+    """Positions [B, N] of the N new queries of each sequence in a decode step:
+    the N tokens that end the sequence (their k/v already in the cache), query n
+    of sequence b at len_b - N + n with len_b = seqlens[b] clamped into [N, L]
+    (None: L).  N = 1 is plain decode; N > 1 verifies N drafted tokens at once,
+    each attending causally up to its own position."""
+    s = shape
+    lens = np.full(s.B, s.L, np.int64) if seqlens is None else np.clip(np.asarray(seqlens, np.int64), s.N, s.L)
+    return (lens[:, None] - s.N + np.arange(s.N)[None, :]).astype(np.int32)
+
+
+def gather_pages(shape: Shape, block_table, k_pages, v_pages, lmk_pages, bias_pages=None):
+    """Per-sequence caches from a paged pool in which a page holds one chunk:
+    chunk c of sequence b is page block_table[b, c].  Pools: k/v [P, Hkv, S, d],
+    landmarks [P, Hl, d], bias [P, Hl].  Returns dense (k, v, lmk, bias) in the
+    [B, Hkv, L, d] / [B, Hl, L/S, d] / [B, Hl, L/S] layouts of fwd()."""
+    s = shape
+    nc = s.L // s.chunk
+    t = np.asarray(block_table, np.int64)
+    if t.shape != (s.B, nc):
+        raise ValueError(f"block_table has shape {t.shape}, expected {(s.B, nc)}")
+    # [B, nc, Hkv, S, d] -> [B, Hkv, nc, S, d] -> [B, Hkv, L, d]
+    k = np.asarray(k_pages)[t].transpose(0, 2, 1, 3, 4).reshape(s.B, s.Hkv, s.L, s.d)
+    v = np.asarray(v_pages)[t].transpose(0, 2, 1, 3, 4).reshape(s.B, s.Hkv, s.L, s.d)
+    lmk = np.asarray(lmk_pages)[t].transpose(0, 2, 1, 3)
+    bias = None if bias_pages is None else np.asarray(bias_pages)[t].transpose(0, 2, 1)
+    return (np.ascontiguousarray(k), np.ascontiguousarray(v), np.ascontiguousarray(lmk),
+            None if bias is None else np.ascontiguousarray(bias))
+
+
+def decode(shape: Shape, q, k, v, lmk, seqlens=None, bias=None, q_route=None, idx=None, rows=None,
+           prec: str = "f64", block_table=None):
+    """Decode step of N >= 1 new queries per sequence (q [B, Hq, N, d]) against
+    caches, contiguous ([B, Hkv, L, d], ...) or, with block_table, paged pools
+    (see gather_pages).  Returns fwd()'s dict."""
+    if block_table is not None:
+        k, v, lmk, bias = gather_pages(shape, block_table, k, v, lmk, bias)
+    return fwd(shape, q, k, v, lmk, bias=bias, q_route=q_route, qpos=decode_positions(shape, seqlens), rows=rows,
+               idx=idx, prec=prec)
+
+
 def n_candidates(i: int, chunk: int, window: int) -> int:
     """|C_i| = l(i)/S with l(i) clamped at 0 (Sec. 2.1)."""
     return max(0, (i - window + 1) // chunk)

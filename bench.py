@@ -79,15 +79,16 @@ def prefill_kernel_model(B, Hq, Hkv, N, L, d, S, K, W, elem=2):
     }
 
 
-def decode_bytes(B, Hq, Hkv, Hl, ctx, d, S, K, W, elem=2):
-    """Algorithmic HBM bytes of one decode step: landmark scan over C_i, the K
-    retrieved chunks' K/V, the local window's K/V, q in, out + lse out."""
-    i = ctx
+def decode_bytes(B, Hq, Hkv, Hl, ctx, d, S, K, W, elem=2, N=1):
+    """Algorithmic HBM bytes of one decode step of N new queries per sequence (the
+    last at position ctx + N - 1): landmark scan over C_i (once), the K retrieved
+    chunks' K/V of every query, the local window's K/V (once), q in, out + lse out."""
+    i = ctx + N - 1
     ncand = int(n_candidates(np.array(i), S, W))
     nloc = i - ncand * S + 1
     lmk = B * Hl * ncand * d * elem
-    kv = B * Hkv * (min(K, ncand) * S + nloc) * d * elem * 2
-    qo = B * Hq * d * elem * 2 + B * Hq * 4
+    kv = B * Hkv * (N * min(K, ncand) * S + nloc) * d * elem * 2
+    qo = N * (B * Hq * d * elem * 2 + B * Hq * 4)
     return lmk + kv + qo, dict(landmarks=lmk, kv=kv, q_out=qo)
 
 
@@ -166,20 +167,31 @@ def bench_prefill(torch, hils, synth, W_, steps, warmup):
     return p, host, ms, kernels
 
 
-def bench_decode(torch, hils, synth, W_, steps, warmup):
-    p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=1, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
+def bench_decode(torch, hils, synth, W_, steps, warmup, paged=False, N=1):
+    """One decode step of N new queries per sequence after W_.ctx cached tokens.
+    paged: the caches are pools of one-chunk pages in a seeded random order (a
+    random permutation as the page table)."""
+    p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
                     window=W_.window, dtype=W_.dtype)
     nc = p.L // p.chunk
+    if paged:
+        P = p.B * nc
+        gen = torch.Generator(device="cpu")
+        gen.manual_seed(synth.seed_for(W_.wid, "page_table"))
+        table = torch.randperm(P, generator=gen).to(torch.int32).reshape(p.B, nc).cuda()
+        kv_shape, lmk_shape = (P, p.Hkv, p.chunk, p.d), (P, p.Hq, p.d)
+    else:
+        kv_shape, lmk_shape = (p.B, p.Hkv, p.L, p.d), (p.B, p.Hq, nc, p.d)
     dev = {
-        "q": synth.normal_device((p.B, p.Hq, 1, p.d), synth.seed_for(W_.wid, "q"), p.dtype, "cuda"),
-        "k": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "k"), p.dtype, "cuda"),
-        "v": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "v"), p.dtype, "cuda"),
-        "lmk": synth.normal_device((p.B, p.Hq, nc, p.d), synth.seed_for(W_.wid, "lmk"), p.dtype, "cuda"),
+        "q": synth.normal_device((p.B, p.Hq, N, p.d), synth.seed_for(W_.wid, "q"), p.dtype, "cuda"),
+        "k": synth.normal_device(kv_shape, synth.seed_for(W_.wid, "k"), p.dtype, "cuda"),
+        "v": synth.normal_device(kv_shape, synth.seed_for(W_.wid, "v"), p.dtype, "cuda"),
+        "lmk": synth.normal_device(lmk_shape, synth.seed_for(W_.wid, "lmk"), p.dtype, "cuda"),
     }
-    seqlens = torch.full((p.B,), W_.ctx + 1, dtype=torch.int32, device="cuda")
-    out = torch.empty(p.B, p.Hq, 1, p.d, dtype=p.torch_dtype, device="cuda")
-    lse = torch.empty(p.B, p.Hq, 1, dtype=torch.float32, device="cuda")
-    idx = torch.empty(p.B, p.Hkv, 1, p.topk, dtype=torch.int32, device="cuda")
+    seqlens = torch.full((p.B,), W_.ctx + N, dtype=torch.int32, device="cuda")
+    out = torch.empty(p.B, p.Hq, N, p.d, dtype=p.torch_dtype, device="cuda")
+    lse = torch.empty(p.B, p.Hq, N, dtype=torch.float32, device="cuda")
+    idx = torch.empty(p.B, p.Hkv, N, p.topk, dtype=torch.int32, device="cuda")
     ws = torch.empty(max(1, hils.hils_workspace_size(p, hils.HILS_OP_DECODE)), dtype=torch.uint8, device="cuda")
     # reading 1 GiB between steps evicts L2 and MALL with clean lines, so the
     # timed step streams from HBM without paying for dirty write-backs
@@ -187,8 +199,12 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
     sink = torch.empty((), dtype=torch.float32, device="cuda")
 
     def step():
-        hils.hils_decode_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], seqlens=seqlens, out=out, lse=lse,
-                             idx=idx, workspace=ws)
+        if paged:
+            hils.hils_decode_paged_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], table, seqlens=seqlens, out=out,
+                                       lse=lse, idx=idx, workspace=ws)
+        else:
+            hils.hils_decode_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], seqlens=seqlens, out=out, lse=lse,
+                                 idx=idx, workspace=ws)
 
     for _ in range(warmup):
         step()
@@ -214,10 +230,11 @@ def bench_decode(torch, hils, synth, W_, steps, warmup):
     # launch to a ~0.2 ms step); a second, instrumented pass gives the breakdown
     ms, _ = timed(False)
     _, kernels = timed(True)
-    nbytes, parts = decode_bytes(p.B, p.Hq, p.Hkv, p.Hq, W_.ctx, p.d, p.chunk, p.topk, p.window)
+    nbytes, parts = decode_bytes(p.B, p.Hq, p.Hkv, p.Hq, W_.ctx, p.d, p.chunk, p.topk, p.window, N=N)
     del dev, flush, sink
     torch.cuda.empty_cache()
-    return {"workload": W_.name, "ms_per_step": round(ms, 4), "tokens_per_s": round(p.B / (ms * 1e-3), 1),
+    return {"workload": W_.name, "paged": paged, "new_tokens_per_seq": N, "ms_per_step": round(ms, 4),
+            "tokens_per_s": round(p.B * N / (ms * 1e-3), 1),
             "algorithmic_bytes": nbytes, "bytes_breakdown": parts,
             "hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
             "frac_hbm_peak": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -379,6 +396,10 @@ def main():
                                               max(3, args.steps // 2), 2)
         res["extra"]["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"],
                                                  max(3, args.steps // 2), 2)
+        res["extra"]["decode_paged"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
+                                                    max(3, args.steps // 2), 2, paged=True)
+        res["extra"]["decode_4_new_tokens"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
+                                                           max(3, args.steps // 2), 2, N=4)
     if not args.no_train:
         res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], 3, 1)
     if not args.no_landmark:

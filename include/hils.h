@@ -87,7 +87,8 @@ typedef struct {
     int B;          /* sequences */
     int Hq, Hkv;    /* query heads, KV heads; G = Hq / Hkv query heads share a KV head */
     int Hl;         /* landmark heads: Hq or Hkv */
-    int N;          /* queries per sequence (prefill, bwd: query n sits at position n; decode: 1) */
+    int N;          /* queries per sequence (prefill, bwd: query n sits at position n; decode: the
+                       new tokens, query n at seqlens[b] - N + n) */
     int L;          /* key positions per sequence (decode: cache capacity); multiple of `chunk` */
     int d;          /* head dimension */
     int chunk;      /* S, tokens per chunk */
@@ -132,19 +133,45 @@ int hils_prefill_fwd(const hils_params* p, const void* q, const void* k, const v
                      void* workspace, size_t ws_bytes, void* stream);
 
 /*
- * Decode forward: one new query per sequence (N == 1) against a KV cache.
- * The caller has already written the new token's k/v at position
- * seqlens[b] - 1, so the query sits at i = seqlens[b] - 1 and attends keys
- * j <= i.  Landmark rows exist for every complete chunk.
- *   seqlens  [B] int32 (device) valid tokens per sequence including the new one,
- *            or NULL for L; values are clamped into [1, L] by the kernels.
- * Other arguments as for hils_prefill_fwd with N = 1 (q, q_route, out [B,Hq,1,d];
- * lse [B,Hq,1]; idx [B,Hkv,1,K]; k, v, lmk, lmk_bias are the caches).
- * Windows above 4032 tokens return HILS_ERR_UNSUPPORTED.
+ * Decode forward: N >= 1 new queries per sequence against a KV cache (N = 1:
+ * one generated token; N > 1: drafted tokens verified together, as in
+ * speculative decoding, each attending causally up to its own position).
+ * The caller has already written the new tokens' k/v at the last N positions,
+ * so with len = seqlens[b] query n sits at i = len - N + n and attends keys
+ * j <= i; every query is computed as a decode row of its own (Eqs. (1), (9),
+ * (10) at position i).  Landmark rows exist for every complete chunk.
+ *   seqlens  [B] int32 (device) valid tokens per sequence including the new ones,
+ *            or NULL for L; values are clamped into [N, L] by the kernels.
+ * Other arguments as for hils_prefill_fwd (q, q_route, out [B,Hq,N,d];
+ * lse [B,Hq,N]; idx [B,Hkv,N,K]; k, v, lmk, lmk_bias are the caches).
+ * Requires N <= L and B * N <= 65535.  Windows above 4032 tokens return
+ * HILS_ERR_UNSUPPORTED.  The workspace (hils_workspace_size(p, HILS_OP_DECODE))
+ * grows with B * N.
  */
 int hils_decode_fwd(const hils_params* p, const void* q, const void* k_cache, const void* v_cache,
                     const void* lmk_cache, const float* lmk_bias, const void* q_route, const int32_t* seqlens,
                     void* out, float* lse, int32_t* idx, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Decode forward over a paged cache: a page holds one chunk (S tokens) of one
+ * sequence, for every KV head and landmark head, and chunk c of sequence b is
+ * page block_table[b, c]; pages may be shared between sequences (a common
+ * prefix) and need not be in any order.  Same computation and arguments as
+ * hils_decode_fwd, with the caches replaced by pools of num_pages pages:
+ *   k_pages, v_pages [num_pages, Hkv, S, d]  (dtype)
+ *   lmk_pages        [num_pages, Hl, d]      (dtype) landmark k'_c of the page's chunk
+ *   bias_pages       [num_pages, Hl] f32     landmark bias b'_c, or NULL
+ *   block_table      [B, L/S] int32 (device) page of each chunk; L = the logical
+ *                    capacity per sequence.  Entries of chunks at or past a
+ *                    sequence's length are not read; an entry outside
+ *                    [0, num_pages) is clamped into it (no out-of-bounds access,
+ *                    meaningless result).
+ * The workspace is hils_workspace_size(p, HILS_OP_DECODE).
+ */
+int hils_decode_paged_fwd(const hils_params* p, const void* q, const void* k_pages, const void* v_pages,
+                          const void* lmk_pages, const float* bias_pages, const void* q_route,
+                          const int32_t* block_table, int num_pages, const int32_t* seqlens, void* out, float* lse,
+                          int32_t* idx, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Backward of the prefill forward with the selection fixed to `idx`.

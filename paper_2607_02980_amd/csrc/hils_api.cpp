@@ -68,7 +68,10 @@ int check_params(const hils_params* p, int op) {
         return fail(HILS_ERR_INVALID, "HILS_FLAG_SHARED_LMK_QUERY applies to the landmark compression only");
     if ((p->flags & HILS_FLAG_GIVEN_IDX) && op == HILS_OP_LANDMARK)
         return fail(HILS_ERR_INVALID, "HILS_FLAG_GIVEN_IDX does not apply to the landmark compression");
-    if (op == HILS_OP_DECODE && p->N != 1) return fail(HILS_ERR_INVALID, "decode needs N == 1 (got %d)", p->N);
+    if (op == HILS_OP_DECODE && p->N > p->L)
+        return fail(HILS_ERR_INVALID, "decode needs N <= L new queries per sequence (N=%d L=%d)", p->N, p->L);
+    if (op == HILS_OP_DECODE && (long)p->B * p->N > 65535)
+        return fail(HILS_ERR_INVALID, "decode needs B * N <= 65535 (B=%d N=%d)", p->B, p->N);
     if (op != HILS_OP_DECODE && op != HILS_OP_LANDMARK && p->N > p->L)
         return fail(HILS_ERR_INVALID, "prefill/backward need N <= L (N=%d L=%d)", p->N, p->L);
     if (p->B > 65535 || p->Hkv > 65535) return fail(HILS_ERR_INVALID, "B and Hkv must be <= 65535");
@@ -96,7 +99,7 @@ size_t ws_bytes_for(const hils_params* p, int op) {
                 return hils::bwd_mfma_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk);
             return hils::bwd_workspace_layout(p->B, p->Hkv, p->N, p->L, p->topk).total;
         case HILS_OP_DECODE:
-            return hils::decode_workspace_bytes(p->B, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window);
+            return hils::decode_workspace_bytes(p->B, p->N, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window);
         default:
             return hils::prefill_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk,
                                                  p->dtype == HILS_BF16);
@@ -124,6 +127,7 @@ hils::FwdArgs fwd_args(const hils_params* p, const void* q, const void* k, const
                        int32_t* idx, void* ws, size_t ws_bytes, int decode) {
     hils::FwdArgs a;
     a.q = q; a.k = k; a.v = v; a.lmk = lmk; a.bias = bias; a.q_route = q_route; a.seqlens = seqlens;
+    a.block_table = nullptr; a.num_pages = 0;
     a.out = out; a.lse = lse; a.idx = idx;
     a.B = p->B; a.Hq = p->Hq; a.Hkv = p->Hkv; a.Hl = p->Hl; a.N = p->N; a.L = p->L; a.d = p->d;
     a.K = p->topk; a.W = p->window; a.scale = p->scale;
@@ -233,6 +237,24 @@ int hils_decode_fwd(const hils_params* p, const void* q, const void* k_cache, co
     const hils::FwdArgs a = fwd_args(p, q, k_cache, v_cache, lmk_cache, lmk_bias, q_route, seqlens, out, lse, idx,
                                      workspace, ws_bytes, 1);
     return hip_status(hils::launch_decode_fwd(a, (hipStream_t)stream), "hils_decode_fwd launch");
+}
+
+int hils_decode_paged_fwd(const hils_params* p, const void* q, const void* k_pages, const void* v_pages,
+                          const void* lmk_pages, const float* bias_pages, const void* q_route,
+                          const int32_t* block_table, int num_pages, const int32_t* seqlens, void* out, float* lse,
+                          int32_t* idx, void* workspace, size_t ws_bytes, void* stream) {
+    int rc = check_params(p, HILS_OP_DECODE);
+    if (rc) return rc;
+    REQUIRE(q); REQUIRE(k_pages); REQUIRE(v_pages); REQUIRE(lmk_pages); REQUIRE(block_table);
+    REQUIRE(out); REQUIRE(lse); REQUIRE(idx);
+    if (num_pages < 1) return fail(HILS_ERR_INVALID, "num_pages must be >= 1 (got %d)", num_pages);
+    rc = check_ws(p, HILS_OP_DECODE, workspace, ws_bytes);
+    if (rc) return rc;
+    hils::FwdArgs a = fwd_args(p, q, k_pages, v_pages, lmk_pages, bias_pages, q_route, seqlens, out, lse, idx,
+                               workspace, ws_bytes, 1);
+    a.block_table = block_table;
+    a.num_pages = num_pages;
+    return hip_status(hils::launch_decode_fwd(a, (hipStream_t)stream), "hils_decode_paged_fwd launch");
 }
 
 int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* k, const void* v, const void* lmk,

@@ -1,19 +1,27 @@
-// HiLS attention decode forward, gfx950.  One new query per sequence; the
-// work is a stream over HBM (landmark scan, then K/V gathers), so the kernels
-// are organised for coalesced, many-in-flight loads rather than for math.
+// HiLS attention decode forward, gfx950.  N >= 1 new queries per sequence (N > 1:
+// drafted tokens verified together, each at its own position); the work is a
+// stream over HBM (landmark scan, then K/V gathers), so the kernels are
+// organised for coalesced, many-in-flight loads rather than for math.
 //
-//   A  k_dec_scan     grid (nslices, Hkv, B): scores SLICE candidate chunks of one
+// Every (sequence b, new query n) is a row of its own: grids run over the
+// B * N rows, and workspace records, idx, out and lse are indexed by
+// rg = (b * Hkv + g) * N + n (the [B, Hkv, N, K] order of idx).  The caches are
+// contiguous ([B, Hkv, L, d] K/V, [B, Hl, L/S, d] landmarks, [B, Hl, L/S] bias)
+// or paged: with a page table, chunk c of sequence b is page block_table[b, c]
+// of pools [P, Hkv, S, d], [P, Hl, d] and [P, Hl] (a page holds one chunk).
+//
+//   A  k_dec_scan     grid (nslices, Hkv, B*N): scores SLICE candidate chunks of one
 //                     KV group (s^_hc for the G heads, max over heads, Eq. (9) /
 //                     App. C) and keeps the slice's top-K (exact wave radix select).
 //                     Small LDS, so many slices stream per CU while others select.
-//   B  k_dec_merge    grid (Hkv, B): top-K over the slices' survivors -> idx
-//   C  k_dec_parts    grid (K + nlocal, Hkv, B)
+//   B  k_dec_merge    grid (Hkv, B*N): top-K over the slices' survivors -> idx
+//   C  k_dec_parts    grid (K + nlocal, Hkv, B*N)
 //        x <  K     : the intra-chunk softmax of selected chunk x (Eq. (10)) and
 //                     its surrogate score s^_hc
 //        x >= K     : one 64-key piece of the local window [l(i), i] (Eq. (1))
 //                     (bf16: on MFMA, run_part_mfma)
 //   A part (chunk or piece) leaves per head its max, sum and unnormalised P.V.
-//   D  k_dec_combine  grid (Hkv, B): local pieces merged by online softmax,
+//   D  k_dec_combine  grid (Hkv, B*N): local pieces merged by online softmax,
 //                     then the fusion softmax over {s^_hc} U {log Z_swa} -> out, lse
 // Parts (local pieces and chunks) leave a record {m, l, s^, o[d]} per head.
 #include <type_traits>
@@ -38,31 +46,58 @@ struct DecLayout {
 
 __host__ __device__ inline int local_pieces_max(int W) { return (W + 62) / 64 + 1; }
 
-__host__ __device__ inline DecLayout dec_layout(int B, int Hkv, int G, int d, int L, int K, int W) {
+// R = B * N rows
+__host__ __device__ inline DecLayout dec_layout(int R, int Hkv, int G, int d, int L, int K, int W) {
     DecLayout o;
     o.nC = L / kChunk;
     o.nslices = (o.nC + kSlice - 1) / kSlice;
     o.nlocal = local_pieces_max(W);
     o.nparts = K + o.nlocal;
-    const size_t bg = (size_t)B * Hkv;
+    const size_t bg = (size_t)R * Hkv;
     o.cand = 0;
     o.parts = ((bg * o.nslices * K * 8) + 255) & ~(size_t)255;
     o.total = o.parts + ((bg * o.nparts * G * (4 + d) * 4 + 255) & ~(size_t)255);
     return o;
 }
 
-__device__ __forceinline__ int decode_position(const FwdArgs& a, int b) {
+// Query n of sequence b sits at len - N + n, len = seqlens[b] clamped into [N, L].
+__device__ __forceinline__ int decode_position(const FwdArgs& a, int b, int n) {
     int len = a.seqlens ? a.seqlens[b] : a.L;
-    len = len < 1 ? 1 : (len > a.L ? a.L : len);
-    return len - 1;
+    len = len < a.N ? a.N : (len > a.L ? a.L : len);
+    return len - a.N + n;
+}
+
+// Page of chunk c of sequence b; entries outside [0, P) are clamped (memory
+// safety only: such a table has no meaning).
+__device__ __forceinline__ int page_of(const FwdArgs& a, int nC, int b, int c) {
+    const int p = a.block_table[(size_t)b * nC + c];
+    return p < 0 ? 0 : (p >= a.num_pages ? a.num_pages - 1 : p);
+}
+
+// Element offset of the first K (or V) row of chunk c of sequence b, KV head g.
+__device__ __forceinline__ size_t kv_chunk_offset(const FwdArgs& a, int nC, int b, int g, int c, int D) {
+    if (a.block_table) return ((size_t)page_of(a, nC, b, c) * a.Hkv + g) * kChunk * D;
+    return (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
+}
+
+// Row of chunk c's landmark of head hl (times D: its element offset); the bias
+// of that landmark has the same index.
+__device__ __forceinline__ size_t lmk_row(const FwdArgs& a, int nC, int b, int hl, int c) {
+    if (a.block_table) return (size_t)page_of(a, nC, b, c) * a.Hl + hl;
+    return ((size_t)b * a.Hl + hl) * nC + c;
+}
+
+// Row of query head h, new query n of sequence b in q / out [B, Hq, N, D] and lse.
+__device__ __forceinline__ size_t q_row(const FwdArgs& a, int b, int h, int n) {
+    return ((size_t)b * a.Hq + h) * a.N + n;
 }
 
 // Record of one part for one head: m, l, s^, (pad), o[D] (unnormalised).
 template <int D>
-__device__ __forceinline__ float* part_record(const FwdArgs& a, const DecLayout& ly, int b, int g, int part, int hh,
+__device__ __forceinline__ float* part_record(const FwdArgs& a, const DecLayout& ly, size_t rg, int part, int hh,
                                               int G) {
     float* base = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.parts);
-    return base + ((((size_t)b * a.Hkv + g) * ly.nparts + part) * G + hh) * (4 + D);
+    return base + ((rg * ly.nparts + part) * G + hh) * (4 + D);
 }
 
 // Shared memory of a part: K and V of 64 keys (raw storage rows padded by 16 B), q, P.
@@ -110,15 +145,15 @@ __device__ __forceinline__ float2 lds_load2(const unsigned char* p, float) {
 // One 64-key part (a local-window piece or a retrieved chunk) of row (b, g):
 // per head m = max_j s_j, l = sum_j exp(s_j - m), o = sum_j exp(s_j - m) v_j.
 template <typename T, int D, int G>
-__device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G>& sm, int b, int g, int part, int c,
-                         int nk, bool is_chunk) {
+__device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G>& sm, int b, int n, int g,
+                         size_t rg, int part, int c, int nk, bool is_chunk) {
     constexpr int RB = PartSmem<T, D, G>::kRowBytes;
     constexpr int PIECES = D * (int)sizeof(T) / 16;  // 16-byte pieces per row
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
-    const size_t kv_off = (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
+    const size_t kv_off = kv_chunk_offset(a, ly.nC, b, g, c, D);
     const unsigned char* kg = reinterpret_cast<const unsigned char*>(as<T>(a.k) + kv_off);
     const unsigned char* vg = reinterpret_cast<const unsigned char*>(as<T>(a.v) + kv_off);
-    // All 64 rows lie inside the cache (c < L/64), so every load is in bounds;
+    // All 64 rows lie inside the cache or page (c < L/64), so every load is in bounds;
     // rows past the query position are loaded but never read back.
     constexpr int PPT = kChunk * PIECES / kBlock;  // pieces per thread per matrix
     uint4 xk[PPT], xv[PPT];
@@ -138,19 +173,18 @@ __device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G
         const int hh = wave + 4 * u;
         if (is_chunk && hh < G && 2 * lane < D) {
             const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-            const T* qr = as<T>(a.q_route ? a.q_route : a.q) + ((size_t)b * a.Hq + g * G + hh) * D + 2 * lane;
-            const T* lr = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * ly.nC + c) * D + 2 * lane;
+            const T* qr = as<T>(a.q_route ? a.q_route : a.q) + q_row(a, b, g * G + hh, n) * D + 2 * lane;
+            const T* lr = as<T>(a.lmk) + lmk_row(a, ly.nC, b, hl, c) * D + 2 * lane;
             qr2[u][0] = to_f32(qr[0]);
             qr2[u][1] = to_f32(qr[1]);
             lm2[u][0] = to_f32(lr[0]);
             lm2[u][1] = to_f32(lr[1]);
         }
     }
-    const T* q = as<T>(a.q) + ((size_t)b * a.Hq + g * G) * D;  // the group's G rows are contiguous
     constexpr int QV = G * D / 8;
     float qx[8];
     const int qe = tid * 8;
-    if (tid < QV) load8(q + qe, qx);
+    if (tid < QV) load8(as<T>(a.q) + q_row(a, b, g * G + qe / D, n) * D + qe % D, qx);
 #pragma unroll
     for (int u = 0; u < PPT; ++u) {
         const int e = tid + u * kBlock, j = e / PIECES, pc = e % PIECES;
@@ -187,10 +221,10 @@ __device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G
             const int u = (hh - wave) / 4;
             const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
             const float acc = wave_sum(qr2[u][0] * lm2[u][0] + qr2[u][1] * lm2[u][1]);
-            sh = a.scale * acc + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * ly.nC + c] : 0.f);
+            sh = a.scale * acc + (a.bias ? a.bias[lmk_row(a, ly.nC, b, hl, c)] : 0.f);
         }
         if (lane == 0) {
-            float* r = part_record<D>(a, ly, b, g, part, hh, G);
+            float* r = part_record<D>(a, ly, rg, part, hh, G);
             r[0] = m;
             r[1] = l;
             r[2] = sh;
@@ -216,7 +250,7 @@ __device__ void run_part(const FwdArgs& a, const DecLayout& ly, PartSmem<T, D, G
                 acc1 += pj * v.y;
             }
         }
-        float* r = part_record<D>(a, ly, b, g, part, hh, G);
+        float* r = part_record<D>(a, ly, rg, part, hh, G);
         r[4 + dd] = acc0;
         r[5 + dd] = acc1;
     }
@@ -236,19 +270,19 @@ struct PartSmemM {
 };
 
 template <int D, int G>
-__device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D, G>& sm, int b, int g, int part, int c,
-                              int nk, bool is_chunk) {
+__device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D, G>& sm, int b, int n, int g,
+                              size_t rg, int part, int c, int nk, bool is_chunk) {
     constexpr int KS = D / 32, DB = D / 16, VROW = D + 8;
     typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16, n16 = lane % 16;
-    const size_t kv_off = (((size_t)b * a.Hkv + g) * a.L + (size_t)c * kChunk) * D;
+    const size_t kv_off = kv_chunk_offset(a, ly.nC, b, g, c, D);
     const bf16* kg = as<bf16>(a.k) + kv_off;
     const bf16* vg = as<bf16>(a.v) + kv_off;
     // A operands: K rows 16w + l%16 (rows past the query position are loaded, in
     // bounds, and masked out of the softmax); B operands: q of head l%16 (< G)
     const int key = 16 * w + n16;
     bf16x8 kA[KS], qB[KS];
-    const bf16* qrow = as<bf16>(a.q) + ((size_t)b * a.Hq + g * G + min(n16, G - 1)) * D;
+    const bf16* qrow = as<bf16>(a.q) + q_row(a, b, g * G + min(n16, G - 1), n) * D;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
         kA[ks] = ld_bf16x8(kg + (size_t)key * D + ks * 32 + lg * 8);
@@ -277,12 +311,13 @@ __device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D
             float acc = 0.f;
             if (2 * lane < D) {
                 const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-                const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q) + ((size_t)b * a.Hq + g * G + hh) * D + 2 * lane;
-                const bf16* lr = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * ly.nC + c) * D + 2 * lane;
+                const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q) + q_row(a, b, g * G + hh, n) * D + 2 * lane;
+                const bf16* lr = as<bf16>(a.lmk) + lmk_row(a, ly.nC, b, hl, c) * D + 2 * lane;
                 acc = to_f32(qr[0]) * to_f32(lr[0]) + to_f32(qr[1]) * to_f32(lr[1]);
             }
             acc = wave_sum(acc);
-            sh[u] = a.scale * acc + (a.bias ? a.bias[((size_t)b * a.Hl + ((a.Hl == a.Hq) ? g * G + hh : g)) * ly.nC + c] : 0.f);
+            sh[u] = a.scale * acc +
+                    (a.bias ? a.bias[lmk_row(a, ly.nC, b, (a.Hl == a.Hq) ? g * G + hh : g, c)] : 0.f);
         }
     }
     // S^T (lane: head l%16, keys 16w + 4(l/16) + i)
@@ -323,7 +358,7 @@ __device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D
     __syncthreads();
     for (int e = tid; e < G * D; e += kBlock) {
         const int hh = e / D, dd = e % D;
-        float* r = part_record<D>(a, ly, b, g, part, hh, G);
+        float* r = part_record<D>(a, ly, rg, part, hh, G);
         r[4 + dd] = sm.o[0][hh][dd] + sm.o[1][hh][dd] + sm.o[2][hh][dd] + sm.o[3][hh][dd];
         if (dd == 0) {
             r[0] = (fmaxf(fmaxf(sm.m[0][hh], sm.m[1][hh]), fmaxf(sm.m[2][hh], sm.m[3][hh]))) * (1.f / kLog2e);
@@ -334,14 +369,14 @@ __device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D
 #pragma unroll
     for (int u = 0; u < HPW; ++u) {
         const int hh = w + 4 * u;
-        if (hh < G && lane == 0) part_record<D>(a, ly, b, g, part, hh, G)[2] = sh[u];
+        if (hh < G && lane == 0) part_record<D>(a, ly, rg, part, hh, G)[2] = sh[u];
     }
 }
 
 template <int D>
-__device__ void empty_part(const FwdArgs& a, const DecLayout& ly, int b, int g, int part, int G) {
+__device__ void empty_part(const FwdArgs& a, const DecLayout& ly, size_t rg, int part, int G) {
     for (int hh = threadIdx.x; hh < G; hh += kBlock) {
-        float* r = part_record<D>(a, ly, b, g, part, hh, G);
+        float* r = part_record<D>(a, ly, rg, part, hh, G);
         r[0] = -INFINITY;
         r[1] = 0.f;
         r[2] = -INFINITY;
@@ -349,26 +384,74 @@ __device__ void empty_part(const FwdArgs& a, const DecLayout& ly, int b, int g, 
 }
 
 // ---- A: landmark scan slices --------------------------------------------------
-template <typename T, int D, int G>
+// Scores of head hh of row (b, n) for the slice's chunks [c0, c0 + len) into
+// s_score[hh].  lanes_per_row lanes read one landmark row (16 B each), rows_per_step
+// rows per wave load.  Contiguous landmarks are rows c0 + r of one [L/S, D] slab;
+// paged ones are found through the slice's page ids (s_page).
+template <typename T, int D, bool PAGED>
+__device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly, int b, int n, int g, int G, int hh,
+                                          int c0, int len, const int* s_page, float* s_score) {
+    constexpr int LPR = D * (int)sizeof(T) / 16;
+    constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane per load
+    constexpr int RPS = kWave / LPR;
+    const int lane = threadIdx.x % kWave, sub = lane / LPR, seg = lane % LPR;
+    const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+    const T* qr = as<T>(a.q_route ? a.q_route : a.q) + q_row(a, b, g * G + hh, n) * D + seg * EPL;
+    float qv[EPL];
+#pragma unroll
+    for (int t = 0; t < EPL; ++t) qv[t] = to_f32(qr[t]);
+    const T* lm = as<T>(a.lmk) + seg * EPL;
+    const T* base = lm + (PAGED ? 0 : lmk_row(a, ly.nC, b, hl, c0) * D);
+    // NB independent 16-byte loads per lane are issued before any math; rows
+    // past the slice end re-read the last row (in bounds, result discarded).
+    constexpr int NB = 16;
+    for (int r0 = 0; r0 < len; r0 += RPS * NB) {
+        uint4 x[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int r = min(r0 + u * RPS + sub, len - 1);
+            const T* src = PAGED ? lm + ((size_t)s_page[r] * a.Hl + hl) * D : base + (size_t)r * D;
+            x[u] = *reinterpret_cast<const uint4*>(src);
+        }
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            float part;
+            if constexpr (sizeof(T) == 2) {
+                const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+                part = 0.f;
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    part += qv[2 * t] * __uint_as_float(w[t] << 16) + qv[2 * t + 1] * __uint_as_float(w[t] & 0xffff0000u);
+            } else {
+                part = qv[0] * __uint_as_float(x[u].x) + qv[1] * __uint_as_float(x[u].y) +
+                       qv[2] * __uint_as_float(x[u].z) + qv[3] * __uint_as_float(x[u].w);
+            }
+            part = group_sum<LPR>(part);
+            const int r = r0 + u * RPS + sub;
+            if (seg == 0 && r < len) s_score[r] = a.scale * part;
+        }
+    }
+}
+
+// PAGED is a kernel parameter so that the contiguous scan keeps its small
+// register footprint (the paged loads need a 64-bit address per row).
+template <typename T, int D, int G, bool PAGED>
 __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
-    const int b = blockIdx.z, g = blockIdx.y;
-    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
-    const int pos = decode_position(a, b);
+    const int b = blockIdx.z / a.N, n = blockIdx.z % a.N, g = blockIdx.y;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const int pos = decode_position(a, b, n);
     const int ncand = n_candidates(pos, a.W);
     __shared__ ScanSmem<G> ss;
     auto& s_score = ss.score;
     auto& s_sig = ss.sig;
     auto& s_id = ss.id;
-    auto& s_oid = ss.oid;
-    auto& s_tid = ss.tid;
-    auto& s_osc = ss.osc;
-    auto& s_tsc = ss.tsc;
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int c0 = blockIdx.x * kSlice;
     const int len = min(kSlice, ncand - c0);
     float* cand_sc = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.cand);
-    const size_t cbase = (((size_t)b * a.Hkv + g) * ly.nslices + blockIdx.x) * a.K;
-    int* cand_id = reinterpret_cast<int*>(cand_sc + (size_t)a.B * a.Hkv * ly.nslices * a.K);
+    const size_t cbase = (rg * ly.nslices + blockIdx.x) * a.K;
+    int* cand_id = reinterpret_cast<int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
     if (len <= 0) {
         for (int t = tid; t < a.K; t += kBlock) {
             cand_sc[cbase + t] = -INFINITY;
@@ -376,59 +459,24 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
         }
         return;
     }
-    // lanes_per_row lanes read one landmark row (16 B each); rows_per_step rows per wave load
-    constexpr int LPR = D * (int)sizeof(T) / 16;
-    constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane per load
-    constexpr int RPS = kWave / LPR;
-    const int sub = lane / LPR, seg = lane % LPR;
-    const T* qr = as<T>(a.q_route ? a.q_route : a.q);
-    for (int hh = wave; hh < G; hh += kBlock / kWave) {
-        const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-        float qv[EPL];
-#pragma unroll
-        for (int t = 0; t < EPL; ++t) qv[t] = to_f32(qr[((size_t)b * a.Hq + g * G + hh) * D + seg * EPL + t]);
-        const T* base = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * ly.nC + c0) * D + seg * EPL;
-        // NB independent 16-byte loads per lane are issued before any math; rows
-        // past the slice end re-read the last row (in bounds, result discarded).
-        constexpr int NB = 16;
-        for (int r0 = 0; r0 < len; r0 += RPS * NB) {
-            uint4 x[NB];
-#pragma unroll
-            for (int u = 0; u < NB; ++u) {
-                const int r = min(r0 + u * RPS + sub, len - 1);
-                x[u] = *reinterpret_cast<const uint4*>(base + (size_t)r * D);
-            }
-#pragma unroll
-            for (int u = 0; u < NB; ++u) {
-                float part;
-                if constexpr (sizeof(T) == 2) {
-                    const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-                    part = 0.f;
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        part += qv[2 * t] * __uint_as_float(w[t] << 16) +
-                                qv[2 * t + 1] * __uint_as_float(w[t] & 0xffff0000u);
-                } else {
-                    part = qv[0] * __uint_as_float(x[u].x) + qv[1] * __uint_as_float(x[u].y) +
-                           qv[2] * __uint_as_float(x[u].z) + qv[3] * __uint_as_float(x[u].w);
-                }
-                part = group_sum<LPR>(part);
-                const int r = r0 + u * RPS + sub;
-                if (seg == 0 && r < len) s_score[hh][r] = a.scale * part;
-            }
-        }
+    if constexpr (PAGED) {
+        // the slice's page ids (s_id is free until the selection pass)
+        for (int r = tid; r < len; r += kBlock) s_id[r] = page_of(a, ly.nC, b, c0 + r);
+        __syncthreads();
     }
+    for (int hh = wave; hh < G; hh += kBlock / kWave)
+        scan_head<T, D, PAGED>(a, ly, b, n, g, G, hh, c0, len, s_id, s_score[hh]);
     __syncthreads();
     for (int r = tid; r < len; r += kBlock) {
         float m = -INFINITY;
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
             const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-            const float bv = a.bias ? a.bias[((size_t)b * a.Hl + hl) * ly.nC + c0 + r] : 0.f;
+            const float bv = a.bias ? a.bias[PAGED ? (size_t)s_id[r] * a.Hl + hl : lmk_row(a, ly.nC, b, hl, c0 + r)]
+                                    : 0.f;
             m = fmaxf(m, s_score[hh][r] + bv);
         }
         s_sig[r] = m;
-        s_id[r] = c0 + r;
     }
     __syncthreads();
     if (wave == 0) {
@@ -441,12 +489,12 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
             const int e = r * kWave + lane;
             ok[r] = e < len;
             sc[r] = ok[r] ? s_sig[e] : 0.f;
-            id[r] = ok[r] ? s_id[e] : -1;
+            id[r] = ok[r] ? c0 + e : -1;
         }
-        const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, s_oid, s_osc, s_tid, s_tsc);  // ids c0 + e*64 + lane
+        const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, ss.oid, ss.osc, ss.tid, ss.tsc);  // ids c0 + e*64 + lane
         for (int t = lane; t < a.K; t += kWave) {
-            cand_sc[cbase + t] = t < m ? s_osc[t] : -INFINITY;
-            cand_id[cbase + t] = t < m ? s_oid[t] : -1;
+            cand_sc[cbase + t] = t < m ? ss.osc[t] : -INFINITY;
+            cand_id[cbase + t] = t < m ? ss.oid[t] : -1;
         }
     }
 }
@@ -463,11 +511,13 @@ __global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a) {
     __shared__ int s_wid[NW][64], s_tid[NW][64], s_bid[64];
     __shared__ float s_wsc[NW][64], s_tsc[NW][64], s_bsc[64];
     __shared__ int s_wn[NW];
-    const int b = blockIdx.y, g = blockIdx.x, tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
-    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+    const int b = blockIdx.y / a.N, n = blockIdx.y % a.N, g = blockIdx.x;
+    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
     const float* cand_sc = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.cand);
-    const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.Hkv * ly.nslices * a.K);
-    const size_t base = ((size_t)b * a.Hkv + g) * ly.nslices * a.K;
+    const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
+    const size_t base = rg * ly.nslices * a.K;
     const int total = ly.nslices * a.K;
     int nbest = 0;
     for (int r0 = 0; r0 < total; r0 += kBlock * kMergeE) {
@@ -503,7 +553,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a) {
         __syncthreads();
     }
     if (wave == 0) {
-        int32_t* orow = a.idx + ((size_t)b * a.Hkv + g) * a.K;
+        int32_t* orow = a.idx + rg * a.K;
         for (int t = lane; t < a.K; t += kWave) orow[t] = t < nbest ? s_bid[t] : -1;
     }
 }
@@ -515,33 +565,34 @@ __global__ __launch_bounds__(kBlock) void k_dec_parts(FwdArgs a) {
     typedef typename std::conditional<kMfma, PartSmemM<D, G>, PartSmem<T, D, G>>::type Smem;
     __shared__ Smem sm;
     __shared__ int s_c;
-    const int slot = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
-    const int pos = decode_position(a, b);
+    const int slot = blockIdx.x, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const int pos = decode_position(a, b, n);
     auto run = [&](int part, int c, int nk, bool is_chunk) {
         if constexpr (kMfma)
-            run_part_mfma<D, G>(a, ly, sm, b, g, part, c, nk, is_chunk);
+            run_part_mfma<D, G>(a, ly, sm, b, n, g, rg, part, c, nk, is_chunk);
         else
-            run_part<T, D, G>(a, ly, sm, b, g, part, c, nk, is_chunk);
+            run_part<T, D, G>(a, ly, sm, b, n, g, rg, part, c, nk, is_chunk);
     };
     if (slot >= a.K) {
         const int piece = slot - a.K;
         const int c = n_candidates(pos, a.W) + piece;
         if (c > pos / kChunk) {
-            empty_part<D>(a, ly, b, g, slot, G);
+            empty_part<D>(a, ly, rg, slot, G);
             return;
         }
         run(slot, c, min(kChunk, pos - c * kChunk + 1), false);
         return;
     }
     if (threadIdx.x == 0) {
-        const int32_t* irow = a.idx + ((size_t)b * a.Hkv + g) * a.K;
+        const int32_t* irow = a.idx + rg * a.K;
         s_c = idx_entry_valid(irow, slot, n_candidates(pos, a.W)) ? irow[slot] : -1;
     }
     __syncthreads();
     const int c = s_c;
     if (c < 0) {
-        empty_part<D>(a, ly, b, g, slot, G);
+        empty_part<D>(a, ly, rg, slot, G);
         return;
     }
     run(slot, c, kChunk, true);
@@ -556,13 +607,15 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
     constexpr int kMaxParts = 64 + kMaxLocalPieces;
     __shared__ float s_w[G][kMaxParts];  // weight of each part's unnormalised o
     __shared__ float s_lse[G];
-    const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
-    const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+    const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
+    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
     for (int hh = wave; hh < G; hh += kBlock / kWave) {
         // local pieces: lanes < nlocal
         float m = -INFINITY, l = 0.f;
         if (lane < ly.nlocal) {
-            const float* r = part_record<D>(a, ly, b, g, a.K + lane, hh, G);
+            const float* r = part_record<D>(a, ly, rg, a.K + lane, hh, G);
             m = r[0];
             l = r[1];
         }
@@ -572,7 +625,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
         // chunks: lanes < K
         float z = -INFINITY, lc = 0.f;
         if (lane < a.K) {
-            const float* r = part_record<D>(a, ly, b, g, lane, hh, G);
+            const float* r = part_record<D>(a, ly, rg, lane, hh, G);
             lc = r[1];
             z = lc > 0.f ? r[2] : -INFINITY;
         }
@@ -591,10 +644,10 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
 #pragma unroll 8
         for (int pt = 0; pt < ly.nparts; ++pt) {
             const float w = s_w[hh][pt];
-            const float v = part_record<D>(a, ly, b, g, pt, hh, G)[4 + dd];
+            const float v = part_record<D>(a, ly, rg, pt, hh, G)[4 + dd];
             acc += w != 0.f ? w * v : 0.f;
         }
-        const size_t row = (size_t)b * a.Hq + g * G + hh;
+        const size_t row = q_row(a, b, g * G + hh, n);
         as_mut<T>(a.out)[row * D + dd] = from_f32<T>(acc);
         if (dd == 0) a.lse[row] = s_lse[hh];
     }
@@ -603,21 +656,26 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
 struct DecRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
-        const DecLayout ly = dec_layout(a.B, a.Hkv, G, D, a.L, a.K, a.W);
+        const int R = a.B * a.N;  // rows (sequence, new query); the host keeps R <= 65535
+        const DecLayout ly = dec_layout(R, a.Hkv, G, D, a.L, a.K, a.W);
         if (!a.given_idx) {
-            HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G>), dim3(ly.nslices, a.Hkv, a.B), dim3(kBlock), 0, s, a);
-            HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
+            if (a.block_table)
+                HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, true>), dim3(ly.nslices, a.Hkv, R), dim3(kBlock), 0, s, a);
+            else
+                HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, false>), dim3(ly.nslices, a.Hkv, R), dim3(kBlock), 0, s,
+                            a);
+            HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         }
-        HILS_LAUNCH("k_dec_parts", (k_dec_parts<T, D, G>), dim3(a.K + ly.nlocal, a.Hkv, a.B), dim3(kBlock), 0, s, a);
-        HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, a.B), dim3(kBlock), 0, s, a);
+        HILS_LAUNCH("k_dec_parts", (k_dec_parts<T, D, G>), dim3(a.K + ly.nlocal, a.Hkv, R), dim3(kBlock), 0, s, a);
+        HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }
 };
 
 }  // namespace
 
-size_t decode_workspace_bytes(int B, int Hkv, int G, int d, int L, int K, int W) {
-    return dec_layout(B, Hkv, G, d, L, K, W).total;
+size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W) {
+    return dec_layout(B * N, Hkv, G, d, L, K, W).total;
 }
 
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s) {

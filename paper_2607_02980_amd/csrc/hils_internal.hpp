@@ -16,13 +16,15 @@ struct FwdArgs {
     const float* bias;      // nullable
     const void* q_route;    // nullable: q^ = q
     const int32_t* seqlens; // decode only, nullable: L
+    const int32_t* block_table; // decode only, nullable: contiguous caches; else [B, L/S] page ids
+    int num_pages;              // pages in the pools when paged
     void* out;
     float* lse;
     int32_t* idx;
     int B, Hq, Hkv, Hl, N, L, d, K, W;
     float scale;
     int bf16;      // storage dtype
-    int decode;    // 1: query n = 0 of sequence b sits at seqlens[b]-1
+    int decode;    // 1: query n of sequence b sits at len_b - N + n (len_b = seqlens[b] in [N, L])
     int given_idx; // 1: consume idx
     void* ws;
     size_t ws_bytes;
@@ -114,7 +116,7 @@ struct BwdWorkspace {
 };
 BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K);
 
-size_t decode_workspace_bytes(int B, int Hkv, int G, int d, int L, int K, int W);
+size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W);
 
 size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16);
 

@@ -50,6 +50,7 @@ def _load():
     lib.hils_workspace_size.argtypes = [P, ctypes.c_int, ctypes.POINTER(sz)]
     lib.hils_prefill_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_decode_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.hils_decode_paged_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_bwd.argtypes = [P] + [vp] * 17 + [sz, vp]
     lib.hils_landmark_fwd.argtypes = [P, vp, vp, vp, vp, vp]
     lib.hils_landmark_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -174,7 +175,8 @@ def hils_prefill_fwd(p: Params, q, k, v, lmk, lmk_bias=None, q_route=None, out=N
 
 def hils_decode_fwd(p: Params, q, k_cache, v_cache, lmk_cache, lmk_bias=None, q_route=None, seqlens=None,
                     out=None, lse=None, idx=None, workspace=None):
-    """Decode forward (N == 1).  Returns (out, lse, idx)."""
+    """Decode forward, N >= 1 new queries per sequence (query n at seqlens[b] - N + n).
+    Returns (out, lse, idx)."""
     S, dt = _shapes(p), p.torch_dtype
     if out is None:
         out = torch.empty(S["q"], dtype=dt, device=q.device)
@@ -190,6 +192,35 @@ def hils_decode_fwd(p: Params, q, k_cache, v_cache, lmk_cache, lmk_bias=None, q_
         ctypes.byref(cp), _ptr(q, "q", S["q"], dt), _ptr(k_cache, "k_cache", S["kv"], dt),
         _ptr(v_cache, "v_cache", S["kv"], dt), _ptr(lmk_cache, "lmk_cache", S["lmk"], dt),
         _ptr(lmk_bias, "lmk_bias", S["bias"], torch.float32, False), _ptr(q_route, "q_route", S["q"], dt, False),
+        _ptr(seqlens, "seqlens", (p.B,), torch.int32, False), _ptr(out, "out", S["q"], dt),
+        _ptr(lse, "lse", S["lse"], torch.float32), _ptr(idx, "idx", S["idx"], torch.int32),
+        _ptr(ws, "workspace"), n, _stream()))
+    return out, lse, idx
+
+
+def hils_decode_paged_fwd(p: Params, q, k_pages, v_pages, lmk_pages, block_table, bias_pages=None, q_route=None,
+                          seqlens=None, out=None, lse=None, idx=None, workspace=None):
+    """Decode forward over paged pools (one chunk per page): k/v_pages [P, Hkv, S, d],
+    lmk_pages [P, Hl, d], bias_pages [P, Hl] f32, block_table [B, L/S] int32.
+    Returns (out, lse, idx)."""
+    S, dt = _shapes(p), p.torch_dtype
+    P = k_pages.shape[0]
+    Hl = p.Hl or p.Hq
+    if out is None:
+        out = torch.empty(S["q"], dtype=dt, device=q.device)
+    if lse is None:
+        lse = torch.empty(S["lse"], dtype=torch.float32, device=q.device)
+    if idx is None:
+        if p.flags & HILS_FLAG_GIVEN_IDX:
+            raise ValueError("HILS_FLAG_GIVEN_IDX needs idx")
+        idx = torch.empty(S["idx"], dtype=torch.int32, device=q.device)
+    ws, n = _workspace(p, HILS_OP_DECODE, workspace)
+    cp = p.c()
+    _check(LIB.hils_decode_paged_fwd(
+        ctypes.byref(cp), _ptr(q, "q", S["q"], dt), _ptr(k_pages, "k_pages", (P, p.Hkv, p.chunk, p.d), dt),
+        _ptr(v_pages, "v_pages", (P, p.Hkv, p.chunk, p.d), dt), _ptr(lmk_pages, "lmk_pages", (P, Hl, p.d), dt),
+        _ptr(bias_pages, "bias_pages", (P, Hl), torch.float32, False), _ptr(q_route, "q_route", S["q"], dt, False),
+        _ptr(block_table, "block_table", (p.B, p.L // p.chunk), torch.int32), P,
         _ptr(seqlens, "seqlens", (p.B,), torch.int32, False), _ptr(out, "out", S["q"], dt),
         _ptr(lse, "lse", S["lse"], torch.float32), _ptr(idx, "idx", S["idx"], torch.int32),
         _ptr(ws, "workspace"), n, _stream()))

@@ -11,7 +11,7 @@ from __future__ import annotations
 
 import torch
 
-TENSOR_IDS = {"q": 1, "k": 2, "v": 3, "lmk": 4, "bias": 5, "dout": 6, "q_route": 7}
+TENSOR_IDS = {"q": 1, "k": 2, "v": 3, "lmk": 4, "bias": 5, "dout": 6, "q_route": 7, "page_table": 8}
 
 
 def seed_for(workload_id: int, tensor: str, slab: int = 0) -> int:

@@ -95,11 +95,11 @@ def test_params_null_and_bad_dtype_and_scale(hils):
     assert "scale" in hils.hils_last_error()
 
 
-def test_decode_requires_single_query(hils):
-    p = params(hils, N=2).c()
+def test_decode_needs_N_at_most_L(hils):
+    p = params(hils, N=300, L=256).c()
     rc = hils.LIB.hils_decode_fwd(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, FAKE, FAKE,
                                   None, 0, None)
-    assert rc == hils.HILS_ERR_INVALID and "N == 1" in hils.hils_last_error()
+    assert rc == hils.HILS_ERR_INVALID and "N <= L" in hils.hils_last_error()
 
 
 def test_workspace_sizes_and_workspace_errors(hils):
@@ -196,3 +196,25 @@ def test_landmark_entry_points_validate_on_the_host(hils):
             hils.hils_workspace_size(params(hils, N=1, flags=hils.HILS_FLAG_SHARED_LMK_QUERY), op)
     gi = params(hils, flags=hils.HILS_FLAG_GIVEN_IDX).c()
     assert hils.LIB.hils_landmark_fwd(ctypes.byref(gi), FAKE, FAKE, FAKE, FAKE, None) == hils.HILS_ERR_INVALID
+
+
+def test_paged_and_multi_token_decode_validate_on_the_host(hils):
+    p1 = params(hils, B=4, N=1, L=4096, window=512)
+    p4 = params(hils, B=4, N=4, L=4096, window=512)
+    w1 = hils.hils_workspace_size(p1, hils.HILS_OP_DECODE)
+    w4 = hils.hils_workspace_size(p4, hils.HILS_OP_DECODE)
+    assert w4 > 3 * w1  # one set of records per (sequence, new query)
+    with pytest.raises(hils.HilsError, match="N <= L"):
+        hils.hils_workspace_size(params(hils, N=300, L=256), hils.HILS_OP_DECODE)
+    with pytest.raises(hils.HilsError, match="B \\* N"):
+        hils.hils_workspace_size(params(hils, B=300, N=256, L=256), hils.HILS_OP_DECODE)
+    cp = p4.c()
+    F = FAKE
+    # (p, q, k_pages, v_pages, lmk_pages, bias_pages, q_route, block_table, num_pages, seqlens,
+    #  out, lse, idx, workspace, ws_bytes, stream)
+    rc = hils.LIB.hils_decode_paged_fwd(ctypes.byref(cp), F, F, F, F, None, None, None, 10, None, F, F, F, F, w4, None)
+    assert rc == hils.HILS_ERR_INVALID and "block_table" in hils.hils_last_error()
+    rc = hils.LIB.hils_decode_paged_fwd(ctypes.byref(cp), F, F, F, F, None, None, F, 0, None, F, F, F, F, w4, None)
+    assert rc == hils.HILS_ERR_INVALID and "num_pages" in hils.hils_last_error()
+    rc = hils.LIB.hils_decode_paged_fwd(ctypes.byref(cp), F, F, F, F, None, None, F, 10, None, F, F, F, F, w1, None)
+    assert rc == hils.HILS_ERR_WORKSPACE

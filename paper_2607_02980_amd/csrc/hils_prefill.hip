@@ -106,6 +106,10 @@ __device__ __forceinline__ bf16x8 vt_operand(const bf16* s_v, int db, int t, int
 }
 
 // B operand of O^T = V^T P^T from exponentiated S^T accumulators of key blocks 2t, 2t+1.
+__device__ __forceinline__ bf16x8 p_operand(const f32x4& e0, const f32x4& e1) {
+    float x[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
+    return pack_bf16x8(x);
+}
 __device__ __forceinline__ bf16x8 p_operand(const float* e0, const float* e1) {
     float x[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
     return pack_bf16x8(x);
@@ -274,14 +278,23 @@ __global__ __launch_bounds__(kWave) void k_pf_ref_given(FwdArgs a, float* ref_ou
 // Units of work are (16 entries, head) pairs; wave w takes units w, w + 4, ...
 // K and V^T of the chunk are held in registers as MFMA operands for the whole
 // block, and the next unit's rows are fetched while the current one computes.
+// K and V of the chunk, and the landmark rows of the group's heads, stay in LDS
+// and every unit reads its MFMA operands from there, so that a wave holds only
+// one unit's state and the prefetched operands of the next: four waves per
+// SIMD keep the gathers of many units in flight (the kernel waits on memory,
+// not on the matrix cores).  K rows are padded by 8 elements (16-byte row reads
+// without bank conflicts), V rows by 16 (transposing 8-byte reads without
+// conflicts).
 template <int D, int G, bool ROUTE>
-__global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offsets, const int* list,
-                                                      const int4* work, const int* nwork, const float* ref,
-                                                      bf16* part, float* wgt) {
+__global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, const int* offsets, const int* list,
+                                                                    const int4* work, const int* nwork,
+                                                                    const float* ref, bf16* part, float* wgt) {
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
-    constexpr int HW = G > 4 ? 2 : 1;  // heads a wave visits
-    __shared__ __align__(16) bf16 s_k[kChunk * Tiles<D>::KROW];
-    __shared__ __align__(16) bf16 s_v[kChunk * Tiles<D>::KROW];
+    constexpr int KROW = Tiles<D>::KROW, VROW = D + 16;
+    __shared__ __align__(16) bf16 s_k[kChunk * KROW];
+    __shared__ __align__(16) bf16 s_v[kChunk * VROW];
+    __shared__ __align__(16) bf16 s_l[G][D];
+    __shared__ float s_bias[G];
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
     if ((int)blockIdx.x >= *nwork) return;
@@ -293,30 +306,25 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
     const int len = min(kInvSeg, offsets[bg * (nC + 1) + c + 1] - beg);
     if (len <= 0) return;
     const int* seg = list + bg * a.N * a.K + beg;
-    store_block<D>(s_k, load_block<D>(as<bf16>(a.k) + (bg * a.L + (size_t)c * kChunk) * D));
-    store_block<D>(s_v, load_block<D>(as<bf16>(a.v) + (bg * a.L + (size_t)c * kChunk) * D));
-    __syncthreads();
-    bf16x8 kA[4][KS], vA[DB][2];
+    {
+        const KVRegs<D> kr = load_block<D>(as<bf16>(a.k) + (bg * a.L + (size_t)c * kChunk) * D);
+        const KVRegs<D> vr = load_block<D>(as<bf16>(a.v) + (bg * a.L + (size_t)c * kChunk) * D);
+        if (tid < G * D / 8) {
+            const int hh = tid / (D / 8), d8 = (tid % (D / 8)) * 8;
+            const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+            const size_t lrow = ((size_t)b * a.Hl + hl) * nC + c;
+            *reinterpret_cast<uint4*>(&s_l[hh][d8]) =
+                *reinterpret_cast<const uint4*>(as<bf16>(a.lmk) + lrow * D + d8);
+            if (d8 == 0) s_bias[hh] = a.bias ? a.bias[lrow] : 0.f;
+        }
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kA[kb][ks] = k_operand<D>(s_k, kb, ks, lane);
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int t = 0; t < 2; ++t) vA[db][t] = vt_operand<D>(s_v, db, t, lane);
-    // landmark rows of the wave's heads as the A operand of s^ (row 0 of the tile)
-    bf16x8 aL[HW][KS];
-    float bias_h[HW];
-#pragma unroll
-    for (int x = 0; x < HW; ++x) {
-        const int hh = (w + 4 * x) % G, h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
-        const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            aL[x][ks] = (lane % 16 == 0) ? ld_bf16x8(lrow + ks * 32 + lg * 8) : as_bf16x8(make_uint4(0, 0, 0, 0));
-        bias_h[x] = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
+        for (int u = 0; u < Tiles<D>::PPT; ++u) {
+            const int e = tid + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            *reinterpret_cast<uint4*>(s_k + j * KROW + d8) = kr.x[u];
+            *reinterpret_cast<uint4*>(s_v + j * VROW + d8) = vr.x[u];
+        }
     }
+    __syncthreads();
     const float c1 = a.scale * kLog2e;
     const bf16* qbase = as<bf16>(a.q);
     const bf16* rbase = as<bf16>(a.q_route);
@@ -341,9 +349,10 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
         }
         x.rf = ref[bg * a.N + (ent >> 6)];
     };
+    // a wave's units are u = w, w + 4, ...; the operands of the next two are in flight
     auto unit = [&](int u, const Ops& cur, Ops& nxt) {
-        load_ops(u + 4, nxt);
-        const int hh = u % G, x = HW > 1 ? (u / 4) % 2 : 0;
+        load_ops(u + 8, nxt);
+        const int hh = u % G;
         const bool qv = cur.ent >= 0;
         const int n = cur.ent >> 6, slot = cur.ent & 63;
         const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + (qv ? n : 0);
@@ -351,57 +360,69 @@ __global__ __launch_bounds__(kBlock) void k_pf_chunks(FwdArgs a, const int* offs
         f32x4 sh4 = zero4();
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 lrow = ld_bf16x8(&s_l[hh][ks * 32 + lg * 8]);
+            const bf16x8 aL = (lane % 16 == 0) ? lrow : as_bf16x8(make_uint4(0, 0, 0, 0));
             if constexpr (ROUTE)
-                sh4 = mfma16x16x32(aL[x][ks], as_bf16x8(cur.qr[ks]), sh4);
+                sh4 = mfma16x16x32(aL, as_bf16x8(cur.qr[ks]), sh4);
             else
-                sh4 = mfma16x16x32(aL[x][ks], as_bf16x8(cur.q[ks]), sh4);
+                sh4 = mfma16x16x32(aL, as_bf16x8(cur.q[ks]), sh4);
         }
-        const float shat = a.scale * group0_bcast(sh4[0]) + bias_h[x];
+        const float shat = a.scale * group0_bcast(sh4[0]) + s_bias[hh];
         // S^T = K_c Q^T and the intra-chunk softmax p_j = exp(s_j - lse_c)
+        // (scheduling barriers keep the operand reads of one key block, or of two
+        // dim blocks below, live at a time: that is what fits four waves per SIMD)
         f32x4 st[4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
             st[kb] = zero4();
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(kA[kb][ks], as_bf16x8(cur.q[ks]), st[kb]);
+            for (int ks = 0; ks < KS; ++ks)
+                st[kb] = mfma16x16x32(k_operand<D>(s_k, kb, ks, lane), as_bf16x8(cur.q[ks]), st[kb]);
+            __builtin_amdgcn_sched_barrier(0);
         }
         float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) mx = fmaxf(mx, fmaxf(fmaxf(st[kb][0], st[kb][1]), fmaxf(st[kb][2], st[kb][3])));
         mx = group4_max(mx);
         const float m2 = mx * c1;
-        float ex[4][4], sum = 0.f;
+        // unnormalised exp in (0, 1] as the P operand; 1/sum is applied to O^T
+        float sum = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                ex[kb][i] = fexp2(fmaf(st[kb][i], c1, -m2));
-                sum += ex[kb][i];
+                st[kb][i] = fexp2(fmaf(st[kb][i], c1, -m2));
+                sum += st[kb][i];
             }
+        const bf16x8 pb0 = p_operand(st[0], st[1]);
+        const bf16x8 pb1 = p_operand(st[2], st[3]);
         sum = group4_sum(sum);
         const float inv = 1.f / sum;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) ex[kb][i] *= inv;
-        const bf16x8 pb0 = p_operand(ex[0], ex[1]);
-        const bf16x8 pb1 = p_operand(ex[2], ex[3]);
         f32x4 o[DB];
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-            o[db] = mfma16x16x32(vA[db][0], pb0, zero4());
-            o[db] = mfma16x16x32(vA[db][1], pb1, o[db]);
+            o[db] = mfma16x16x32(tr_operand_perm(s_v, VROW, 0, db * 16, lane), pb0, zero4());
+            o[db] = mfma16x16x32(tr_operand_perm(s_v, VROW, 32, db * 16, lane), pb1, o[db]);
+            if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
         }
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[db][i] *= inv;
         if (qv) {
             store_lane_order<D>(part + (qrow * a.K + slot) * D, o, lg);
             if (lane < 16) wgt[qrow * a.K + slot] = fexp2((shat - cur.rf) * kLog2e);
         }
     };
-    Ops opa, opb;
+    Ops opa, opb, opc;
     load_ops(w, opa);
-    for (int u = w; u < nunits; u += 8) {
-        unit(u, opa, opb);
-        if (u + 4 < nunits) unit(u + 4, opb, opa);
+    load_ops(w + 4, opb);
+    for (int u = w; u < nunits; u += 12) {
+        unit(u, opa, opc);
+        if (u + 4 >= nunits) break;
+        unit(u + 4, opb, opa);
+        if (u + 8 >= nunits) break;
+        unit(u + 8, opc, opb);
     }
 }
 

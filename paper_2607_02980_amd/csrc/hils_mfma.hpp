@@ -70,9 +70,11 @@ __device__ __forceinline__ bf16x8 tr_operand_perm(const E* X, int ld, int k0, in
 
 // "Lane order" of a D-vector held as O^T accumulators (DB = D/16 blocks, lane
 // group lg = l/16 holding d = 16 db + 4 lg + i): element d is stored at position
-// lg * D/4 + 4 db + i, so that the four lanes of a row move 64 contiguous bytes
-// each (D = 128) with 16-byte accesses.  Used for the per-slot partial vectors
-// that one kernel writes and another reads in the same lane layout.
+// 32 (db / 2) + 8 lg + 4 (db % 2) + i.  A lane moves its 32 values as D/32
+// 16-byte pieces, and piece t of the four lanes of a row is one contiguous
+// 64-byte span (positions 32 t .. 32 t + 31), so every access instruction covers
+// whole 64-byte runs of each row.  Used for the per-slot partial vectors that
+// one kernel writes and another reads in the same lane layout.
 template <int D>
 __device__ __forceinline__ void store_lane_order(bf16* row, const f32x4* o, int lg) {
     uint32_t w[D / 8];
@@ -85,7 +87,7 @@ __device__ __forceinline__ void store_lane_order(bf16* row, const f32x4* o, int 
 #pragma unroll
     for (int t = 0; t < D / 32; ++t) {
         const u32x4 v = {w[4 * t], w[4 * t + 1], w[4 * t + 2], w[4 * t + 3]};
-        reinterpret_cast<u32x4*>(row + lg * (D / 4))[t] = v;
+        *reinterpret_cast<u32x4*>(row + 32 * t + 8 * lg) = v;
     }
 }
 
@@ -93,7 +95,7 @@ __device__ __forceinline__ void store_lane_order(bf16* row, const f32x4* o, int 
 template <int D>
 __device__ __forceinline__ void load_lane_order(const bf16* row, int lg, uint4* x) {
 #pragma unroll
-    for (int t = 0; t < D / 32; ++t) x[t] = reinterpret_cast<const uint4*>(row + lg * (D / 4))[t];
+    for (int t = 0; t < D / 32; ++t) x[t] = *reinterpret_cast<const uint4*>(row + 32 * t + 8 * lg);
 }
 // (ok = false adds nothing, whatever bits x holds.)
 template <int D>

@@ -695,8 +695,8 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
                 const float xv = dshat[row * a.K + k];
                 xk[u] = ok ? a.scale * xv : 0.f;
                 okk[u] = ok;
-                const int kk = ok ? k : 0, ck = ok ? cc : 0;
-                load_lane_order<D>(dqp + (row * a.K + kk) * D, lg, pv[u]);
+                const int ck = ok ? cc : 0;
+                load_lane_order<D>(dqp + (row * a.K + k) * D, lg, pv[u]);  // masked by okk if invalid
                 const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + ck) * D;
 #pragma unroll
                 for (int db = 0; db < DB; ++db) lv[u][db] = *reinterpret_cast<const uint2*>(lrow + db * 16 + lg * 4);

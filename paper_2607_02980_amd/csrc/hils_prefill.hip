@@ -12,10 +12,11 @@
 //                    exp(s^ - ref) (float).  A chunk's rows are scattered over the
 //                    sequence, so per-slot partials replace atomics (float atomics on
 //                    gfx950 sustain ~0.3 G-ops/ms, 7 ms for the 32K workload).
-//   P2 k_pf_local    flash-style local window [l(i), i] (Eq. (1)) per 16*QB-query
-//                    tile, then the fusion (Eq. (10)) with the row's slots summed in
-//                    slot order: acc = sum_k w_k o_k, zsum = sum_k w_k, M = max(log Z_swa, ref),
-//                    out = (e^{log Z_swa - M} o_swa + e^{ref - M} acc) / (e^{log Z_swa - M} + e^{ref - M} zsum),
+//   P2 k_pf_local    flash-style local window [l(i), i] (Eq. (1)) per tile of 16*8/G
+//                    queries x G heads (8 waves), then the fusion (Eq. (10)) with the
+//                    row's slots summed in slot order: M = max(log Z_swa, ref),
+//                    out = (e^{log Z_swa - M} o_swa + e^{ref - M} sum_k w_k o_k)
+//                          / (e^{log Z_swa - M} + e^{ref - M} sum_k w_k),
 //                    lse = M + log(denominator).
 //
 // MFMA orientation: attention tiles compute S^T = K Q^T (keys on the M side,
@@ -429,20 +430,31 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
 // ---------------------------------------------------------------------------
 // P2: local window (flash style) + fusion epilogue
 // ---------------------------------------------------------------------------
+// One block of 8 waves per tile of QT = 16 * 8 / G queries of one KV group:
+// wave w owns the item (head w / QB, 16-query block w % QB), i.e. 16 rows of
+// one head.  The 64-key blocks of K and V that the tile's windows cover are
+// double-buffered in LDS: block j + 1 is fetched into registers while block j
+// is used and stored into the other buffer afterwards, one barrier per block.
+// After the window, the row's retrieved-chunk slots are added into the same
+// accumulators (fusion, Eq. (10)): with M = max(log Z_swa, ref),
+//   out = (e^{log Z_swa - M} o_swa + e^{ref - M} sum_k w_k o_k) / (e^{log Z_swa - M} + e^{ref - M} sum_k w_k).
 template <int G>
 struct LocalCfg {
-    static constexpr int QB = G >= 4 ? 1 : 4 / G;  // 16-query blocks per tile
+    static constexpr int QB = 8 / G;   // 16-query blocks per tile
     static constexpr int QT = 16 * QB;
-    static constexpr int ITEMS = G * QB;           // (head, query block) items
-    static constexpr int IPW = (ITEMS + 3) / 4;    // items per wave
+    static constexpr int NT = 8 * kWave;
 };
 
 template <int D, int G>
-__global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref, const bf16* part, const float* wgt) {
+__global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, const float* ref, const bf16* part,
+                                                                const float* wgt) {
     using C = LocalCfg<G>;
-    constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB, IPW = C::IPW;
-    __shared__ __align__(16) bf16 s_k[kChunk * Tiles<D>::KROW];
-    __shared__ __align__(16) bf16 s_v[kChunk * Tiles<D>::KROW];
+    constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
+    constexpr int KROW = Tiles<D>::KROW, VROW = D + 16;
+    constexpr int PPT = kChunk * D / 8 / C::NT;  // 16-byte pieces per thread of a K or V block
+    static_assert(PPT >= 1 && kChunk * D / 8 == PPT * C::NT, "K/V blocks split evenly over the threads");
+    __shared__ __align__(16) bf16 s_k[2][kChunk * KROW];
+    __shared__ __align__(16) bf16 s_v[2][kChunk * VROW];
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int ntiles = (a.N + C::QT - 1) / C::QT;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
@@ -454,157 +466,163 @@ __global__ __launch_bounds__(kBlock) void k_pf_local(FwdArgs a, const float* ref
     const bf16* kbase = as<bf16>(a.k) + bg * a.L * D;
     const bf16* vbase = as<bf16>(a.v) + bg * a.L * D;
     const float c1 = a.scale * kLog2e;
+    const int hh = w / C::QB, qb = w % C::QB;
+    const int nq_raw = q0 + qb * 16 + lane % 16;
+    const int nq = min(nq_raw, a.N - 1);
+    const size_t row = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
 
-    KVRegs<D> nk = load_block<D>(kbase + (size_t)kbeg * D);
-    KVRegs<D> nv = load_block<D>(vbase + (size_t)kbeg * D);
-
-    bf16x8 bq[IPW][KS];
-    f32x4 o[IPW][DB];
-    float m[IPW], l[IPW];  // running max (log2 units) and sum
+    struct KV {
+        uint4 k[PPT], v[PPT];
+    };
+    auto fetch = [&](int j0) {
+        KV x;
 #pragma unroll
-    for (int it = 0; it < IPW; ++it) {
-        const int item = w + 4 * it;
-        m[it] = -INFINITY;
-        l[it] = 0.f;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) o[it][db] = zero4();
-        if (item < C::ITEMS) {
-            const int hh = item / C::QB, qb = item % C::QB;
-            const int nq = min(q0 + qb * 16 + lane % 16, a.N - 1);
-            const bf16* qrow = as<bf16>(a.q) + (((size_t)b * a.Hq + g * G + hh) * a.N + nq) * D;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) bq[it][ks] = ld_bf16x8(qrow + ks * 32 + lg * 8);
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * C::NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            x.k[u] = *reinterpret_cast<const uint4*>(kbase + (size_t)(j0 + j) * D + d8);
+            x.v[u] = *reinterpret_cast<const uint4*>(vbase + (size_t)(j0 + j) * D + d8);
         }
-    }
+        return x;
+    };
+    auto stage = [&](int buf, const KV& x) {
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * C::NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            *reinterpret_cast<uint4*>(&s_k[buf][j * KROW + d8]) = x.k[u];
+            *reinterpret_cast<uint4*>(&s_v[buf][j * VROW + d8]) = x.v[u];
+        }
+    };
 
-    for (int j0 = kbeg; j0 <= qlast; j0 += kChunk) {
-        __syncthreads();
-        store_block<D>(s_k, nk);
-        store_block<D>(s_v, nv);
-        __syncthreads();
-        if (j0 + kChunk <= qlast) {  // the next key block, fetched during this one
-            nk = load_block<D>(kbase + (size_t)(j0 + kChunk) * D);
-            nv = load_block<D>(vbase + (size_t)(j0 + kChunk) * D);
+    bf16x8 bq[KS];
+    {
+        const bf16* qrow = as<bf16>(a.q) + row * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) bq[ks] = ld_bf16x8(qrow + ks * 32 + lg * 8);
+    }
+    f32x4 o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = zero4();
+    float m = -INFINITY, l = 0.f;  // running max (log2 units) and sum
+    const int ell = n_candidates(nq, a.W) * kChunk;
+
+    KV nx = fetch(kbeg);
+    stage(0, nx);
+    __syncthreads();
+    int buf = 0;
+    for (int j0 = kbeg; j0 <= qlast; j0 += kChunk, buf ^= 1) {
+        const bool more = j0 + kChunk <= qlast;  // uniform over the block
+        if (more) nx = fetch(j0 + kChunk);
+        const bf16* tk = s_k[buf];
+        const bf16* tv = s_v[buf];
+        // S^T for the wave's 16 rows (scheduling barriers keep one key block's
+        // operands live at a time)
+        f32x4 st[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            st[kb] = zero4();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                st[kb] = mfma16x16x32(ld_bf16x8(tk + (kb * 16 + lane % 16) * KROW + ks * 32 + lg * 8), bq[ks], st[kb]);
+            __builtin_amdgcn_sched_barrier(0);
         }
         // ...and below every row of the tile: such blocks need no mask
         const bool full = j0 >= kfull && j0 + kChunk - 1 <= q0;
-#pragma unroll
-        for (int it = 0; it < IPW; ++it) {
-            const int item = w + 4 * it;
-            if (item >= C::ITEMS) continue;
-            const int qb = item % C::QB;
-            const int nq = q0 + qb * 16 + lane % 16;
-            f32x4 st[4];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                st[kb] = zero4();
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(k_operand<D>(s_k, kb, ks, lane), bq[it][ks], st[kb]);
-            }
-            float mx = -INFINITY;
-            if (full) {
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        st[kb][i] *= c1;
-                        mx = fmaxf(mx, st[kb][i]);
-                    }
-            } else {
-                const int ell = n_candidates(nq, a.W) * kChunk;
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int j = j0 + kb * 16 + lg * 4 + i;
-                        const bool valid = nq < a.N && j <= nq && j >= ell;
-                        st[kb][i] = valid ? st[kb][i] * c1 : -INFINITY;
-                        mx = fmaxf(mx, st[kb][i]);
-                    }
-            }
-            mx = group4_max(mx);
-            const float mnew = fmaxf(m[it], mx);
-            const float muse = mnew == -INFINITY ? 0.f : mnew;
-            const float alpha = fexp2(m[it] - muse);
-            float ex[4][4], psum = 0.f;
+        float mx = -INFINITY;
+        if (full) {
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    ex[kb][i] = fexp2(st[kb][i] - muse);
-                    psum += ex[kb][i];
+                    st[kb][i] *= c1;
+                    mx = fmaxf(mx, st[kb][i]);
                 }
-            psum = group4_sum(psum);
-            l[it] = l[it] * alpha + psum;
-            m[it] = mnew;
-            const bf16x8 pb0 = p_operand(ex[0], ex[1]);
-            const bf16x8 pb1 = p_operand(ex[2], ex[3]);
+        } else {
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                o[it][db] *= alpha;
-                o[it][db] = mfma16x16x32(vt_operand<D>(s_v, db, 0, lane), pb0, o[it][db]);
-                o[it][db] = mfma16x16x32(vt_operand<D>(s_v, db, 1, lane), pb1, o[it][db]);
-            }
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int j = j0 + kb * 16 + lg * 4 + i;
+                    const bool valid = nq_raw < a.N && j <= nq && j >= ell;
+                    st[kb][i] = valid ? st[kb][i] * c1 : -INFINITY;
+                    mx = fmaxf(mx, st[kb][i]);
+                }
         }
+        mx = group4_max(mx);
+        const float mnew = fmaxf(m, mx);
+        const float muse = mnew == -INFINITY ? 0.f : mnew;
+        const float alpha = fexp2(m - muse);
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                st[kb][i] = fexp2(st[kb][i] - muse);
+                psum += st[kb][i];
+            }
+        const bf16x8 pb0 = p_operand(st[0], st[1]);
+        const bf16x8 pb1 = p_operand(st[2], st[3]);
+        psum = group4_sum(psum);
+        l = l * alpha + psum;
+        m = mnew;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            o[db] *= alpha;
+            o[db] = mfma16x16x32(tr_operand_perm(tv, VROW, 0, db * 16, lane), pb0, o[db]);
+            o[db] = mfma16x16x32(tr_operand_perm(tv, VROW, 32, db * 16, lane), pb1, o[db]);
+            if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
+        }
+        if (more) stage(buf ^ 1, nx);
+        __syncthreads();
     }
 
     // fusion epilogue (lane: row l%16 of the item, dims 16 db + 4 lg + i)
-    constexpr int SB = D >= 128 ? 4 : 8;  // slots whose loads are in flight together
-    bf16* out = as_mut<bf16>(a.out);
+    const float lam0 = (m + __log2f(l)) * (1.f / kLog2e);  // local log-sum-exp (l >= 1: key nq is in the window)
+    const float rf = ref[bg * a.N + nq];                 // best selected group score, or -inf
+    const float M = fmaxf(lam0, rf);
+    const float wl = fexp(lam0 - M) / l;
+    const float wc = fexp(rf - M);
 #pragma unroll
-    for (int it = 0; it < IPW; ++it) {
-        const int item = w + 4 * it;
-        if (item >= C::ITEMS) continue;
-        const int hh = item / C::QB, qb = item % C::QB;
-        const int nq = min(q0 + qb * 16 + lane % 16, a.N - 1);
-        const bool rowv = q0 + qb * 16 + lane % 16 < a.N;
-        const size_t row = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
-        const float lam0 = (m[it] + __log2f(l[it])) * (1.f / kLog2e);  // local log-sum-exp
-        const float rf = ref[bg * a.N + nq];
-        // the row's retrieved chunks: slots in idx order, valid entries only
-        const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
-        const int ncand = n_candidates(nq, a.W);
-        float zs = 0.f;
-        f32x4 av[DB];
+    for (int db = 0; db < DB; ++db) o[db] *= wl;
+    // the row's retrieved chunks: slots in idx order, valid entries only
+    constexpr int SB = D >= 128 ? 2 : 4;  // slots whose loads are in flight together
+    const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
+    const int ncand = n_candidates(nq, a.W);
+    float zs = 0.f;
+    int prev = -1;
+    for (int k0 = 0; k0 < a.K; k0 += SB) {
+        float wk[SB];
+        bool okk[SB];
+        uint4 pv[SB][D / 32];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) av[db] = zero4();
-        int prev = -1;
-        for (int k0 = 0; k0 < a.K; k0 += SB) {
-            float wk[SB];
-            bool okk[SB];
-            uint4 pv[SB][D / 32];
-#pragma unroll
-            for (int u = 0; u < SB; ++u) {
-                const int k = min(k0 + u, a.K - 1);
-                const int cc = irow[k];
-                const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
-                prev = cc;  // idx_entry_valid compares with the previous entry as written
-                const float wv = wgt[row * a.K + k];
-                wk[u] = ok ? wv : 0.f;
-                okk[u] = ok;
-                load_lane_order<D>(part + (row * a.K + (ok ? k : 0)) * D, lg, pv[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < SB; ++u) {
-                zs += wk[u];
-                fma_lane_order<D>(pv[u], wk[u], okk[u], av);
-            }
+        for (int u = 0; u < SB; ++u) {
+            const int k = min(k0 + u, a.K - 1);
+            const int cc = irow[k];
+            const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
+            prev = cc;  // idx_entry_valid compares with the previous entry as written
+            const float wv = wgt[row * a.K + k];
+            wk[u] = ok ? wv : 0.f;
+            okk[u] = ok;
+            // (address independent of idx, so these loads issue with the idx loads;
+            // an invalid slot's bits are masked by fma_lane_order)
+            load_lane_order<D>(part + (row * a.K + k) * D, lg, pv[u]);
         }
-        const float M = fmaxf(lam0, rf);
-        const float wl = fexp(lam0 - M) / l[it];
-        const float wc = zs > 0.f ? fexp(rf - M) : 0.f;
-        const float Z = fexp(lam0 - M) + wc * zs;
-        const float inv = 1.f / Z;
-        if (rowv) {
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d0 = db * 16 + lg * 4;
-                const f32x4 r = (wl * o[it][db] + wc * av[db]) * inv;
-                *reinterpret_cast<uint2*>(out + row * D + d0) =
-                    make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
-            }
-            if (lane < 16) a.lse[row] = M + __logf(Z);
+        for (int u = 0; u < SB; ++u) {
+            zs += wk[u];
+            fma_lane_order<D>(pv[u], wc * wk[u], okk[u], o);
         }
+    }
+    const float Z = fexp(lam0 - M) + wc * zs;
+    const float inv = 1.f / Z;
+    if (nq_raw < a.N) {
+        bf16* out = as_mut<bf16>(a.out);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const int d0 = db * 16 + lg * 4;
+            const f32x4 r = o[db] * inv;
+            *reinterpret_cast<uint2*>(out + row * D + d0) = make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+        }
+        if (lane < 16) a.lse[row] = M + __logf(Z);
     }
 }
 
@@ -635,7 +653,7 @@ struct PfRun {
             HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
                         offsets, list, work, nwork, (const float*)ref, part, wgt);
         HILS_LAUNCH("k_pf_local", (k_pf_local<D, G>), dim3((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B),
-                           dim3(kBlock), 0, s, a, (const float*)ref, (const bf16*)part, (const float*)wgt);
+                           dim3(LocalCfg<G>::NT), 0, s, a, (const float*)ref, (const bf16*)part, (const float*)wgt);
         return hipGetLastError();
     }
 };

@@ -250,6 +250,18 @@ __device__ inline int wave_topk(const float* sc, const int* id, int n, int K, in
 // the compaction position is then the ascending rank and out_* are written
 // directly.
 constexpr int kTopkUnordered = -2, kTopkNatural = -1;
+
+// m-th largest value of one 32-bit key per lane (0 if fewer than m lanes hold
+// a key >= 1): the bits of the threshold from the top, one ballot each.
+__device__ __forceinline__ uint32_t wave_kth_key(uint32_t x, int m) {
+    uint32_t T = 0;
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t t = T | (1u << bit);
+        if (popc64(__ballot(x >= t)) >= m) T = t;
+    }
+    return T;
+}
+
 template <int E, int FIRST = kTopkUnordered>
 __device__ inline int wave_topk_reg(const float (&sc)[E], const int (&id)[E], const bool (&valid)[E], int K,
                                     int* out_id, float* out_sc, int* tmp_id, float* tmp_sc) {
@@ -275,6 +287,86 @@ __device__ inline int wave_topk_reg(const float (&sc)[E], const int (&id)[E], co
     };
     uint32_t T = 0, id_thr = 0x7fffffffu;
     const bool all = (n <= K);
+    constexpr bool kOrdered = FIRST != kTopkUnordered;
+    if (!all && E > 1) {
+        // Fast path.  The m-th largest of the lane maxima, T0, is a lower bound of
+        // the m-th largest key (m lanes hold a key >= T0), so the m best entries
+        // are among the survivors key >= T0.  When they fit one per lane they are
+        // compacted in visiting order and selected with one-register passes.
+        uint32_t lmax = 0;
+#pragma unroll
+        for (int r = 0; r < E; ++r) lmax = key[r] > lmax ? key[r] : lmax;
+        uint32_t T0 = wave_kth_key(lmax, m);
+        T0 = T0 ? T0 : 1u;
+        const int c = count_ge(T0);
+        if (c <= kWave) {
+            int w = 0;
+#pragma unroll
+            for (int q = 0; q < E; ++q) {
+                const int r = FIRST >= 0 ? (q == 0 ? FIRST : (q - 1 < FIRST ? q - 1 : q)) : q;
+                const bool pr = key[r] >= T0;
+                const uint64_t bal = __ballot(pr);
+                if (pr) {
+                    const int pos = w + popc64(bal & ((1ull << lane) - 1ull));
+                    tmp_id[pos] = id[r];
+                    tmp_sc[pos] = sc[r];
+                }
+                w += popc64(bal);
+            }
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            const bool have = lane < c;
+            const int i1 = have ? tmp_id[lane] : 0;
+            const float s1 = have ? tmp_sc[lane] : 0.f;
+            uint32_t k1 = 0;
+            if (have) {
+                const uint32_t k = ordered_key(s1);
+                k1 = k ? k : 1u;
+            }
+            const uint32_t T1 = wave_kth_key(k1, m);  // >= T0 >= 1
+            const int cnt_gt = (T1 == 0xffffffffu) ? 0 : popc64(__ballot(k1 > T1));
+            const int need = m - cnt_gt;
+            const int ties = popc64(__ballot(k1 == T1));
+            uint32_t thr = 0x7fffffffu;
+            if (ties > need) {
+                uint32_t x = 0;
+                for (int bit = 30; bit >= 0; --bit) {
+                    const uint32_t y = x | (1u << bit);
+                    if (popc64(__ballot(k1 == T1 && (uint32_t)i1 < y)) < need) x = y;
+                }
+                thr = x;
+            }
+            const bool pr = k1 > T1 || (k1 == T1 && (uint32_t)i1 <= thr);
+            const uint64_t bal = __ballot(pr);
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            const int pos = popc64(bal & ((1ull << lane) - 1ull));
+            if (kOrdered) {
+                // survivors ascend by id over the lanes: the compaction is the order
+                if (pr) {
+                    out_id[pos] = i1;
+                    out_sc[pos] = s1;
+                }
+            } else {
+                if (pr) {
+                    tmp_id[pos] = i1;
+                    tmp_sc[pos] = s1;
+                }
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                if (lane < m) {
+                    const int my = tmp_id[lane];
+                    int rk = 0;
+                    for (int t = 0; t < m; ++t) rk += tmp_id[t] < my;
+                    out_id[rk] = my;
+                    out_sc[rk] = tmp_sc[lane];
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            return m;
+        }
+    }
     if (!all) {
         for (int bit = 31; bit >= 0; --bit) {
             const uint32_t t = T | (1u << bit);
@@ -296,7 +388,6 @@ __device__ inline int wave_topk_reg(const float (&sc)[E], const int (&id)[E], co
             id_thr = x;
         }
     }
-    constexpr bool kOrdered = FIRST != kTopkUnordered;
     int* dst_id = kOrdered ? out_id : tmp_id;
     float* dst_sc = kOrdered ? out_sc : tmp_sc;
     int w = 0;

@@ -296,6 +296,7 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
     __shared__ __align__(16) bf16 s_v[kChunk * VROW];
     __shared__ __align__(16) bf16 s_l[G][D];
     __shared__ float s_bias[G];
+    __shared__ int s_ent[kInvSeg];  // the segment's entries (row << 6 | slot)
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
     if ((int)blockIdx.x >= *nwork) return;
@@ -307,6 +308,8 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
     const int len = min(kInvSeg, offsets[bg * (nC + 1) + c + 1] - beg);
     if (len <= 0) return;
     const int* seg = list + bg * a.N * a.K + beg;
+    static_assert(kInvSeg <= kBlock, "one entry per thread");
+    if (tid < len) s_ent[tid] = seg[tid];
     {
         const KVRegs<D> kr = load_block<D>(as<bf16>(a.k) + (bg * a.L + (size_t)c * kChunk) * D);
         const KVRegs<D> vr = load_block<D>(as<bf16>(a.v) + (bg * a.L + (size_t)c * kChunk) * D);
@@ -340,7 +343,7 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
     auto load_ops = [&](int u, Ops& x) {
         const int grp = u / G, hh = u % G;
         const int e = min(grp * 16 + lane % 16, len - 1);
-        const int ent = seg[e];
+        const int ent = s_ent[e];
         x.ent = (u < nunits && grp * 16 + lane % 16 < len) ? ent : -1;
         const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + (ent >> 6);
 #pragma unroll

@@ -41,7 +41,8 @@ def build(verbose: bool = False) -> None:
 class _Shape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int), ("Hq", ctypes.c_int), ("Hkv", ctypes.c_int), ("Hl", ctypes.c_int),
                 ("N", ctypes.c_int), ("L", ctypes.c_int), ("d", ctypes.c_int), ("chunk", ctypes.c_int),
-                ("topk", ctypes.c_int), ("window", ctypes.c_int), ("scale", ctypes.c_double)]
+                ("topk", ctypes.c_int), ("window", ctypes.c_int), ("scale", ctypes.c_double),
+                ("head_norm", ctypes.c_int)]
 
 
 @dataclass
@@ -57,10 +58,11 @@ class Shape:
     topk: int
     window: int
     scale: float
+    head_norm: bool = False  # rank by per-head normalised scores (Sec. 4.1 variant)
 
     def c(self) -> _Shape:
         return _Shape(self.B, self.Hq, self.Hkv, self.Hl, self.N, self.L, self.d, self.chunk, self.topk,
-                      self.window, float(self.scale))
+                      self.window, float(self.scale), int(self.head_norm))
 
 
 _loaded: dict[str, ctypes.CDLL] = {}

@@ -92,6 +92,7 @@ typedef struct {
     int topk;   /* K */
     int window; /* W */
     double scale;
+    int head_norm; /* 1: rank by per-head normalised scores (Sec. 4.1 variant) */
 } hils_oracle_shape;
 
 /* ---- small helpers --------------------------------------------------- */
@@ -172,18 +173,23 @@ static REAL surrogate_score(const inputs* in, int b, int h, int n, long c) {
     return (REAL)p->scale * dot_f(QHAT(in, b, h, n), LMK(in, b, hl, c), p->d) + BIAS(in, b, hl, c);
 }
 
-/* Appendix C: group score = max over the G heads of group g. */
+/* Appendix C: group score = max over the G heads of group g.
+ * head_norm (the wording of Sec. 4.1, "normalized chunk weights" per head before
+ * the maximum): each head's scores are first turned into log-weights over the
+ * candidates, s^_hc - log sum_{c' in C_i} exp(s^_hc'), so that a head whose
+ * scores are all large does not outrank a head with one decisive chunk. */
 static void group_scores(const inputs* in, int b, int g, int n, long ncand, REAL* sigma) {
     const hils_oracle_shape* p = in->p;
     int G = p->Hq / p->Hkv;
-    for (long c = 0; c < ncand; ++c) {
-        REAL m = -INFINITY;
-        for (int hh = 0; hh < G; ++hh) {
-            REAL s = surrogate_score(in, b, g * G + hh, n, c);
-            if (s > m) m = s;
-        }
-        sigma[c] = m;
+    REAL* sh = (REAL*)malloc(sizeof(REAL) * (ncand > 0 ? ncand : 1));
+    for (long c = 0; c < ncand; ++c) sigma[c] = -INFINITY;
+    for (int hh = 0; hh < G; ++hh) {
+        for (long c = 0; c < ncand; ++c) sh[c] = surrogate_score(in, b, g * G + hh, n, c);
+        const REAL lse = p->head_norm && ncand > 0 ? logsumexp(sh, ncand) : 0;
+        for (long c = 0; c < ncand; ++c)
+            if (sh[c] - lse > sigma[c]) sigma[c] = sh[c] - lse;
     }
+    free(sh);
 }
 
 /* Eq. (9): I_i = {c in C_i : rank_desc(sigma_c) < K}.  Ties go to the smaller

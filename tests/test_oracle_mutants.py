@@ -2,19 +2,22 @@
 that at least one pin fails.  This is evidence that the pins constrain every
 step: the group max, the window edge, the local mass, the bias, the scale, the
 routing query, tie-breaking, the backward's chunk and score terms, and the
-landmark compression's entropy, head-to-group map and both backward terms."""
+landmark compression's entropy, head-to-group map and both backward terms, and
+the per-head normalisation of the selection variant."""
 import os
 
 import pytest
 
 import oracle
+from tests import test_oracle_headnorm as hnorm
 from tests import test_oracle_landmark as lmk
 from tests import test_oracle_pins as pins
 
 SRC = open(oracle._SRC).read()
 
 MUTANTS = {
-    "group_score_first_head_only": ("if (s > m) m = s;", "if (hh == 0) m = s;",
+    "group_score_first_head_only": ("if (sh[c] - lse > sigma[c]) sigma[c] = sh[c] - lse;",
+                                    "if (hh == 0) sigma[c] = sh[c] - lse;",
                                     [pins.test_hand_worked_example]),
     "window_edge_off_by_one": ("long lc = floor_div(i - W + 1, S);", "long lc = floor_div(i - W, S);",
                                [pins.test_hand_worked_example]),
@@ -33,6 +36,11 @@ MUTANTS = {
                                 [lambda: pins.test_p7_backward_matches_finite_differences(True, True, True)]),
     "bwd_score_grad_drops_u": ("REAL dshat = a * (uc - ubar);", "REAL dshat = a * uc;",
                                [lambda: pins.test_p7_backward_matches_finite_differences(False, False, True)]),
+    # per-head normalised selection (Sec. 4.1 variant)
+    "head_norm_skipped": ("const REAL lse = p->head_norm && ncand > 0 ? logsumexp(sh, ncand) : 0;",
+                          "const REAL lse = 0;",
+                          [hnorm.test_hand_worked_example,
+                           hnorm.test_a_shift_of_one_heads_scores_changes_only_the_raw_selection]),
     # landmark compression (Prop. 3.1)
     "lmk_entropy_sign": ("ent -= pj * logp;", "ent += pj * logp;", [lmk.test_entropy_range_and_uniform_regime]),
     "lmk_group_map": ("return hl / (p->Hl / p->Hkv);", "return hl % p->Hkv;",

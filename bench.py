@@ -131,11 +131,12 @@ class Timer:
         return e0.elapsed_time(e1) / steps  # ms
 
 
-def bench_prefill(torch, hils, synth, W_, steps, warmup):
-    """Times `steps` prefill calls (HIP events on the library's stream) with
-    per-kernel timing enabled; returns (params, host inputs, ms/step, kernels)."""
+def bench_prefill(torch, hils, synth, W_, steps, warmup, flags=0):
+    """Times `steps` prefill calls (HIP events on the library's stream, no
+    per-kernel events), then a second pass with per-kernel timing for the
+    breakdown; returns (params, host inputs, ms/step, kernels)."""
     p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=W_.N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
-                    window=W_.window, dtype=W_.dtype)
+                    window=W_.window, dtype=W_.dtype, flags=flags)
     nc = p.L // p.chunk
     dt = p.torch_dtype
     host = {
@@ -153,11 +154,9 @@ def bench_prefill(torch, hils, synth, W_, steps, warmup):
     def step():
         hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], out=out, lse=lse, idx=idx, workspace=ws)
 
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
+    ms = Timer(torch).run(step, steps, warmup)
     hils.hils_timing_enable(True)
-    ms = Timer(torch).run(step, steps, 0)
+    Timer(torch).run(step, steps, 0)
     kernels = hils.hils_timing_read()
     hils.hils_timing_enable(False)
     for k in kernels.values():
@@ -167,12 +166,12 @@ def bench_prefill(torch, hils, synth, W_, steps, warmup):
     return p, host, ms, kernels
 
 
-def bench_decode(torch, hils, synth, W_, steps, warmup, paged=False, N=1):
+def bench_decode(torch, hils, synth, W_, steps, warmup, paged=False, N=1, flags=0):
     """One decode step of N new queries per sequence after W_.ctx cached tokens.
     paged: the caches are pools of one-chunk pages in a seeded random order (a
     random permutation as the page table)."""
     p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
-                    window=W_.window, dtype=W_.dtype)
+                    window=W_.window, dtype=W_.dtype, flags=flags)
     nc = p.L // p.chunk
     if paged:
         P = p.B * nc
@@ -336,6 +335,7 @@ def main():
     ap.add_argument("--no-train", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-landmark", action="store_true")
+    ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 1 GiB device-to-device (a plain copy kernel of known size, used to "
                          "calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -404,6 +404,17 @@ def main():
         res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], 3, 1)
     if not args.no_landmark:
         res["extra"]["landmark"] = bench_landmark(torch, hils, synth, Wp, args.steps, args.warmup)
+    if not args.no_variants:
+        # selection variants: per-head normalised ranking, and one query head per KV head (MHA)
+        for name, W_, fl in (("prefill_head_norm", Wp, hils.HILS_FLAG_HEAD_NORM_SELECT),
+                             ("prefill_mha_G1", Wp.with_(Hkv=Wp.Hq), 0)):
+            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, max(3, args.steps // 2), 1, flags=fl)
+            res["extra"][name] = {"ms_per_step": round(msv, 4), "tokens_per_s": round(pv.B * pv.N / (msv * 1e-3), 1),
+                                  "Hq": pv.Hq, "Hkv": pv.Hkv,
+                                  "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kv.items()}}
+        res["extra"]["decode_head_norm"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
+                                                        max(3, args.steps // 2), 2,
+                                                        flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(Wp, host)
     print(json.dumps(res), flush=True)

@@ -81,6 +81,14 @@ typedef enum {
  * every chunk of every sequence: lq and dlq are [Hl, d] instead of [B, Hl, L/S, d]. */
 #define HILS_FLAG_SHARED_LMK_QUERY 2u
 
+/* Forward flag (prefill, decode): rank the chunks by per-head normalised scores,
+ * the wording of Sec. 4.1 (each query head's chunk weights are normalised before
+ * the maximum over the group's heads): the group score of chunk c becomes
+ * max_h (s^_hc - log sum_{c' in C_i} exp(s^_hc')) instead of max_h s^_hc.  Only
+ * the selection changes; the fusion weights use the raw s^_hc.  Costs a second
+ * pass over the landmark scores.  Ignored by hils_bwd (the selection is given). */
+#define HILS_FLAG_HEAD_NORM_SELECT 4u
+
 typedef enum { HILS_OP_PREFILL = 0, HILS_OP_DECODE = 1, HILS_OP_BWD = 2, HILS_OP_LANDMARK = 3 } hils_op;
 
 typedef struct {

@@ -62,8 +62,10 @@ int check_params(const hils_params* p, int op) {
     if (p->L % p->chunk) return fail(HILS_ERR_INVALID, "L=%d is not a multiple of chunk=%d", p->L, p->chunk);
     if (p->dtype != HILS_F32 && p->dtype != HILS_BF16) return fail(HILS_ERR_INVALID, "unknown dtype %d", (int)p->dtype);
     if (!isfinite(p->scale)) return fail(HILS_ERR_INVALID, "scale is not finite");
-    if (p->flags & ~(HILS_FLAG_GIVEN_IDX | HILS_FLAG_SHARED_LMK_QUERY))
+    if (p->flags & ~(HILS_FLAG_GIVEN_IDX | HILS_FLAG_SHARED_LMK_QUERY | HILS_FLAG_HEAD_NORM_SELECT))
         return fail(HILS_ERR_INVALID, "unknown flags 0x%x", p->flags);
+    if ((p->flags & HILS_FLAG_HEAD_NORM_SELECT) && op == HILS_OP_LANDMARK)
+        return fail(HILS_ERR_INVALID, "HILS_FLAG_HEAD_NORM_SELECT does not apply to the landmark compression");
     if ((p->flags & HILS_FLAG_SHARED_LMK_QUERY) && op != HILS_OP_LANDMARK)
         return fail(HILS_ERR_INVALID, "HILS_FLAG_SHARED_LMK_QUERY applies to the landmark compression only");
     if ((p->flags & HILS_FLAG_GIVEN_IDX) && op == HILS_OP_LANDMARK)
@@ -134,6 +136,7 @@ hils::FwdArgs fwd_args(const hils_params* p, const void* q, const void* k, const
     a.bf16 = p->dtype == HILS_BF16;
     a.decode = decode;
     a.given_idx = (p->flags & HILS_FLAG_GIVEN_IDX) ? 1 : 0;
+    a.head_norm = (p->flags & HILS_FLAG_HEAD_NORM_SELECT) ? 1 : 0;
     a.ws = ws; a.ws_bytes = ws_bytes;
     return a;
 }

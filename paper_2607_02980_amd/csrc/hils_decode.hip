@@ -41,7 +41,7 @@ constexpr int kMaxLocalPieces = 64;  // local window pieces per row (W <= 4032)
 
 struct DecLayout {
     int nC, nslices, nlocal, nparts;  // nparts = K + nlocal records per (b, g)
-    size_t cand, parts, total;        // byte offsets
+    size_t cand, parts, lse, total;   // byte offsets
 };
 
 __host__ __device__ inline int local_pieces_max(int W) { return (W + 62) / 64 + 1; }
@@ -56,7 +56,9 @@ __host__ __device__ inline DecLayout dec_layout(int R, int Hkv, int G, int d, in
     const size_t bg = (size_t)R * Hkv;
     o.cand = 0;
     o.parts = ((bg * o.nslices * K * 8) + 255) & ~(size_t)255;
-    o.total = o.parts + ((bg * o.nparts * G * (4 + d) * 4 + 255) & ~(size_t)255);
+    // per-head (max, sum of exp) of each slice's scores, for the normalised ranking
+    o.lse = o.parts + ((bg * o.nparts * G * (4 + d) * 4 + 255) & ~(size_t)255);
+    o.total = o.lse + ((bg * o.nslices * G * 2 * 4 + 255) & ~(size_t)255);
     return o;
 }
 
@@ -435,8 +437,13 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
 
 // PAGED is a kernel parameter so that the contiguous scan keeps its small
 // register footprint (the paged loads need a 64-bit address per row).
+// mode kScanSelect: group scores and the slice's top-K.  For the per-head
+// normalised ranking the scan runs twice: kScanLse leaves each head's (max, sum
+// of exp) over the slice, kScanNormSelect subtracts each head's log-sum-exp over
+// all of C_i (from those partials) before the maximum over the heads.
+constexpr int kScanSelect = 0, kScanLse = 1, kScanNormSelect = 2;
 template <typename T, int D, int G, bool PAGED>
-__global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
+__global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
     const int b = blockIdx.z / a.N, n = blockIdx.z % a.N, g = blockIdx.y;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
     const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
@@ -452,12 +459,32 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
     float* cand_sc = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.cand);
     const size_t cbase = (rg * ly.nslices + blockIdx.x) * a.K;
     int* cand_id = reinterpret_cast<int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
+    float* lse_part = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.lse) + (rg * ly.nslices) * G * 2;
     if (len <= 0) {
+        if (mode == kScanLse) {
+            for (int t = tid; t < G; t += kBlock) {
+                lse_part[(blockIdx.x * G + t) * 2] = -INFINITY;
+                lse_part[(blockIdx.x * G + t) * 2 + 1] = 0.f;
+            }
+            return;
+        }
         for (int t = tid; t < a.K; t += kBlock) {
             cand_sc[cbase + t] = -INFINITY;
             cand_id[cbase + t] = -1;
         }
         return;
+    }
+    __shared__ float s_lse[G];
+    if (mode == kScanNormSelect && tid < G) {
+        // log-sum-exp of head tid over all candidates, from the slices' partials
+        float m = -INFINITY;
+        for (int sl = 0; sl < ly.nslices; ++sl) m = fmaxf(m, lse_part[(sl * G + tid) * 2]);
+        float sum = 0.f;
+        for (int sl = 0; sl < ly.nslices; ++sl) {
+            const float pm = lse_part[(sl * G + tid) * 2], ps = lse_part[(sl * G + tid) * 2 + 1];
+            sum += ps > 0.f ? ps * fexp(pm - m) : 0.f;
+        }
+        s_lse[tid] = m + __logf(sum);
     }
     if constexpr (PAGED) {
         // the slice's page ids (s_id is free until the selection pass)
@@ -467,15 +494,34 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a) {
     for (int hh = wave; hh < G; hh += kBlock / kWave)
         scan_head<T, D, PAGED>(a, ly, b, n, g, G, hh, c0, len, s_id, s_score[hh]);
     __syncthreads();
+    if (a.bias) {
+        for (int e = tid; e < G * len; e += kBlock) {
+            const int hh = e / len, r = e % len;
+            const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+            s_score[hh][r] += a.bias[PAGED ? (size_t)s_id[r] * a.Hl + hl : lmk_row(a, ly.nC, b, hl, c0 + r)];
+        }
+        __syncthreads();
+    }
+    if (mode == kScanLse) {
+        for (int hh = wave; hh < G; hh += kBlock / kWave) {
+            float m = -INFINITY;
+            for (int r = lane; r < len; r += kWave) m = fmaxf(m, s_score[hh][r]);
+            m = wave_max(m);
+            float sum = 0.f;
+            for (int r = lane; r < len; r += kWave) sum += fexp(s_score[hh][r] - m);
+            sum = wave_sum(sum);
+            if (lane == 0) {
+                lse_part[(blockIdx.x * G + hh) * 2] = m;
+                lse_part[(blockIdx.x * G + hh) * 2 + 1] = sum;
+            }
+        }
+        return;
+    }
     for (int r = tid; r < len; r += kBlock) {
         float m = -INFINITY;
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-            const float bv = a.bias ? a.bias[PAGED ? (size_t)s_id[r] * a.Hl + hl : lmk_row(a, ly.nC, b, hl, c0 + r)]
-                                    : 0.f;
-            m = fmaxf(m, s_score[hh][r] + bv);
-        }
+        for (int hh = 0; hh < G; ++hh)
+            m = fmaxf(m, s_score[hh][r] - (mode == kScanNormSelect ? s_lse[hh] : 0.f));
         s_sig[r] = m;
     }
     __syncthreads();
@@ -659,11 +705,19 @@ struct DecRun {
         const int R = a.B * a.N;  // rows (sequence, new query); the host keeps R <= 65535
         const DecLayout ly = dec_layout(R, a.Hkv, G, D, a.L, a.K, a.W);
         if (!a.given_idx) {
-            if (a.block_table)
-                HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, true>), dim3(ly.nslices, a.Hkv, R), dim3(kBlock), 0, s, a);
-            else
-                HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, false>), dim3(ly.nslices, a.Hkv, R), dim3(kBlock), 0, s,
-                            a);
+            const dim3 grid(ly.nslices, a.Hkv, R);
+            auto scan = [&](int mode) {
+                if (a.block_table)
+                    HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, true>), grid, dim3(kBlock), 0, s, a, mode);
+                else
+                    HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, false>), grid, dim3(kBlock), 0, s, a, mode);
+            };
+            if (a.head_norm) {
+                scan(kScanLse);
+                scan(kScanNormSelect);
+            } else {
+                scan(kScanSelect);
+            }
             HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         }
         HILS_LAUNCH("k_dec_parts", (k_dec_parts<T, D, G>), dim3(a.K + ly.nlocal, a.Hkv, R), dim3(kBlock), 0, s, a);

@@ -53,28 +53,50 @@ __global__ __launch_bounds__(kBlock) void k_score_topk_rows(FwdArgs a) {
     }
     __builtin_amdgcn_wave_barrier();
 
+    // s^ of head hh for chunk c (Eq. (9) with Eq. (11))
+    auto score = [&](int hh, int c) {
+        const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+        const T* lr = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
+        float acc = 0.f;
+#pragma unroll 4
+        for (int dd = 0; dd < D; dd += 8) {
+            float x[8];
+            load8(lr + dd, x);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) acc += s_q[wave][hh][dd + t] * x[t];
+        }
+        float sv = a.scale * acc;
+        if (a.bias) sv += a.bias[((size_t)b * a.Hl + hl) * nC + c];
+        return sv;
+    };
+    // per-head normalised ranking: each head's log-sum-exp over C_i first
+    float lse[G];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) lse[hh] = 0.f;
+    if (a.head_norm && ncand > 0) {
+#pragma unroll 1
+        for (int hh = 0; hh < G; ++hh) {
+            float m = -INFINITY, sum = 0.f;
+            for (int c = lane; c < ncand; c += kWave) {
+                const float sv = score(hh, c);
+                const float nm = fmaxf(m, sv);
+                sum = sum * fexp(m - nm) + fexp(sv - nm);
+                m = nm;
+            }
+            const float M = wave_max(m);
+            const float S = wave_sum(m == -INFINITY ? 0.f : sum * fexp(m - M));
+            lse[hh] = M + __logf(S);
+        }
+    }
+
     int nbest = 0;
     for (int s0 = 0; s0 < ncand; s0 += kSlice) {
         const int len = min(kSlice, ncand - s0);
         for (int e = lane; e < len; e += kWave) {
             const int c = s0 + e;
             float best = -INFINITY;
-#pragma unroll 1
-            for (int hh = 0; hh < G; ++hh) {
-                const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-                const T* lr = as<T>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
-                float acc = 0.f;
-#pragma unroll 4
-                for (int dd = 0; dd < D; dd += 8) {
-                    float x[8];
-                    load8(lr + dd, x);
 #pragma unroll
-                    for (int t = 0; t < 8; ++t) acc += s_q[wave][hh][dd + t] * x[t];
-                }
-                float sv = a.scale * acc;
-                if (a.bias) sv += a.bias[((size_t)b * a.Hl + hl) * nC + c];
-                best = fmaxf(best, sv);
-            }
+            for (int hh = 0; hh < G; ++hh) best = fmaxf(best, score(hh, c) - lse[hh]);
             s_sc[wave][e] = best;
             s_id[wave][e] = c;
         }

@@ -119,7 +119,24 @@ __device__ __forceinline__ bf16x8 p_operand(const float* e0, const float* e1) {
 // ---------------------------------------------------------------------------
 // P1: scores, group max, top-K
 // ---------------------------------------------------------------------------
-template <int D, int G>
+// (max, sum of exp) pairs merged over each aligned group of 16 lanes.
+__device__ __forceinline__ void lse16_merge(float& m, float& s) {
+    auto step = [&](float om, float os) {
+        const float nm = fmaxf(m, om);
+        s = (m == -INFINITY ? 0.f : s * fexp(m - nm)) + (om == -INFINITY ? 0.f : os * fexp(om - nm));
+        m = nm;
+    };
+    step(dpp<0xB1>(m), dpp<0xB1>(s));
+    step(dpp<0x4E>(m), dpp<0x4E>(s));
+    step(dpp<0x141>(m), dpp<0x141>(s));
+    step(dpp<0x140>(m), dpp<0x140>(s));
+}
+
+// NORM: rank by per-head normalised scores.  A first pass over the candidates
+// gives each (row, head) its log-sum-exp over C_i; the second subtracts it
+// before the maximum over the group's heads.  ref is then the largest of the
+// row's per-head log-sum-exps (>= every raw s^ of the row).
+template <int D, int G, bool NORM>
 __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) {
     constexpr int KS = Tiles<D>::KS;
     constexpr int NCB = kSL / 16;
@@ -127,6 +144,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
     __shared__ float s_sig[kSQ][kSL + 1];
     __shared__ int s_tid[4][64], s_oid[4][64];
     __shared__ float s_tsc[4][64], s_osc[4][64];
+    __shared__ float s_lse[NORM ? G : 1][kSQ];
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
     const int ntiles = (a.N + kSQ - 1) / kSQ;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
@@ -146,13 +164,101 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
         bid[r] = -1;
         nb[r] = 0;
     }
+    constexpr int NJ = NCB / 4, NT = kSQ / 16;
+    if constexpr (NORM) {
+        // pass 1: per (row, head) log-sum-exp of s^ over the row's candidates; the
+        // per-wave partials live in s_sig until the slices need it
+        float* s_pm = &s_sig[0][0];     // [4 waves][G][kSQ]
+        float* s_ps = s_pm + 4 * G * kSQ;
+        const int lg = lane / 16;
+        for (int hh = 0; hh < G; ++hh) {
+            const int h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
+            const bf16* lbase = lmk + ((size_t)b * a.Hl + hl) * nC * D;
+            float rm[NT][4], rs[NT][4];
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    rm[t][i] = -INFINITY;
+                    rs[t][i] = 0.f;
+                }
+            for (int s0 = 0; s0 < nct; s0 += kSL) {
+                bf16x8 bl[NJ][KS];
+                float bv[NJ];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const int c = min(s0 + (w + 4 * j) * 16 + lane % 16, nC - 1);
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) bl[j][ks] = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + lg * 8);
+                    bv[j] = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
+                }
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const int qa = min(q0 + 16 * t + lane % 16, a.N - 1);
+                    bf16x8 aq[KS];
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks)
+                        aq[ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + h) * a.N + qa) * D + ks * 32 + lg * 8);
+                    float x[NJ][4];
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+                        f32x4 acc4 = zero4();
+#pragma unroll
+                        for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[ks], bl[j][ks], acc4);
+                        const int c = s0 + (w + 4 * j) * 16 + lane % 16;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int n = q0 + 16 * t + lg * 4 + i;
+                            x[j][i] = (n < a.N && c < n_candidates(n, a.W)) ? a.scale * acc4[i] + bv[j] : -INFINITY;
+                        }
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        float mx = rm[t][i];
+#pragma unroll
+                        for (int j = 0; j < NJ; ++j) mx = fmaxf(mx, x[j][i]);
+                        if (mx == -INFINITY) continue;
+                        float sum = rs[t][i] * fexp(rm[t][i] - mx);
+#pragma unroll
+                        for (int j = 0; j < NJ; ++j) sum += fexp(x[j][i] - mx);
+                        rm[t][i] = mx;
+                        rs[t][i] = sum;
+                    }
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    lse16_merge(rm[t][i], rs[t][i]);
+                    if (lane % 16 == 0) {
+                        s_pm[(w * G + hh) * kSQ + 16 * t + lg * 4 + i] = rm[t][i];
+                        s_ps[(w * G + hh) * kSQ + 16 * t + lg * 4 + i] = rs[t][i];
+                    }
+                }
+        }
+        __syncthreads();
+        for (int e = tid; e < G * kSQ; e += kBlock) {
+            const int hh = e / kSQ, row = e % kSQ;
+            float m = -INFINITY;
+#pragma unroll
+            for (int ww = 0; ww < 4; ++ww) m = fmaxf(m, s_pm[(ww * G + hh) * kSQ + row]);
+            float sum = 0.f;
+#pragma unroll
+            for (int ww = 0; ww < 4; ++ww) {
+                const float pm = s_pm[(ww * G + hh) * kSQ + row];
+                sum += pm == -INFINITY ? 0.f : s_ps[(ww * G + hh) * kSQ + row] * fexp(pm - m);
+            }
+            s_lse[hh][row] = m == -INFINITY ? -INFINITY : m + __logf(sum);
+        }
+        __syncthreads();
+    }
     for (int s0 = 0; s0 < nct; s0 += kSL) {
         const int len = min(kSL, nct - s0);
         const int ncb = (len + 15) / 16;
         // Wave w scores chunk blocks cb = w + 4j (j < NCB/4) against all kSQ rows of the
         // tile (4 row tiles), so each landmark operand it loads feeds 4 MFMAs; all of a
         // head's landmark loads are issued before its MFMAs.
-        constexpr int NJ = NCB / 4, NT = kSQ / 16;
         f32x4 sig[NT][NJ];
 #pragma unroll
         for (int t = 0; t < NT; ++t)
@@ -181,13 +287,16 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks)
                     aq[ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + h) * a.N + qa) * D + ks * 32 + (lane / 16) * 8);
+                float sub[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sub[i] = NORM ? s_lse[hh][16 * t + (lane / 16) * 4 + i] : 0.f;
 #pragma unroll
                 for (int j = 0; j < NJ; ++j) {
                     f32x4 acc4 = zero4();
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[ks], bl[j][ks], acc4);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) sig[t][j][i] = fmaxf(sig[t][j][i], a.scale * acc4[i] + bv[j]);
+                    for (int i = 0; i < 4; ++i) sig[t][j][i] = fmaxf(sig[t][j][i], a.scale * acc4[i] + bv[j] - sub[i]);
                 }
             }
         }
@@ -236,7 +345,13 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
         if (n >= a.N) break;
         int32_t* orow = a.idx + (((size_t)b * a.Hkv + g) * a.N + n) * a.K;
         if (lane < a.K) orow[lane] = lane < nb[r] ? bid[r] : -1;
-        const float top = wave_max(lane < nb[r] ? bsc[r] : -INFINITY);
+        float top = wave_max(lane < nb[r] ? bsc[r] : -INFINITY);
+        if constexpr (NORM) {
+            float lm = -INFINITY;
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) lm = fmaxf(lm, s_lse[hh][16 * w + r]);
+            top = nb[r] > 0 ? lm : -INFINITY;
+        }
         if (lane == 0) ref_out[((size_t)b * a.Hkv + g) * a.N + n] = top;
     }
 }
@@ -640,8 +755,11 @@ struct PfRun {
         if (a.given_idx) {
             HILS_LAUNCH("k_pf_ref_given", (k_pf_ref_given<D, G>), dim3(a.N, a.Hkv, a.B), dim3(kWave), 0, s, a, ref);
         } else {
-            HILS_LAUNCH("k_pf_score", (k_pf_score<D, G>), dim3((a.N + kSQ - 1) / kSQ, a.Hkv, a.B), dim3(kBlock), 0, s, a,
-                               ref);
+            const dim3 grid((a.N + kSQ - 1) / kSQ, a.Hkv, a.B);
+            if (a.head_norm)
+                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kBlock), 0, s, a, ref);
+            else
+                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kBlock), 0, s, a, ref);
         }
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
         launch_inverse_index(ia, ly.inv, a.ws, s);

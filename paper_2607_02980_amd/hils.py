@@ -23,6 +23,7 @@ HILS_F32, HILS_BF16 = 0, 1
 HILS_OK, HILS_ERR_INVALID, HILS_ERR_UNSUPPORTED, HILS_ERR_WORKSPACE, HILS_ERR_HIP = range(5)
 HILS_FLAG_GIVEN_IDX = 1
 HILS_FLAG_SHARED_LMK_QUERY = 2
+HILS_FLAG_HEAD_NORM_SELECT = 4
 HILS_OP_PREFILL, HILS_OP_DECODE, HILS_OP_BWD, HILS_OP_LANDMARK = 0, 1, 2, 3
 
 

@@ -34,9 +34,12 @@ def log(msg: str):
 
 
 def oshape(p, N=None) -> oracle.Shape:
+    from paper_2607_02980_amd.hils import HILS_FLAG_HEAD_NORM_SELECT
+
     return oracle.Shape(B=p.B, Hq=p.Hq, Hkv=p.Hkv, Hl=p.Hl or p.Hq, N=p.N if N is None else N, L=p.L, d=p.d,
                         chunk=p.chunk, topk=p.topk, window=p.window,
-                        scale=float(np.float32(p.scale if p.scale is not None else p.d ** -0.5)))
+                        scale=float(np.float32(p.scale if p.scale is not None else p.d ** -0.5)),
+                        head_norm=bool(p.flags & HILS_FLAG_HEAD_NORM_SELECT))
 
 
 def host_inputs(p, wid: int, bias=None, route=False, dout=False, bias_shift=0.0):

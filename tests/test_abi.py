@@ -63,7 +63,7 @@ def call_prefill(hils, p, **override):
     (dict(topk=0), 1, ">= 1"),
     (dict(window=0), 1, ">= 1"),
     (dict(B=0), 1, ">= 1"),
-    (dict(flags=4), 1, "unknown flags"),
+    (dict(flags=8), 1, "unknown flags"),
     (dict(chunk=32), 2, "chunk 64"),
     (dict(d=96), 2, "d in {64, 128}"),
     (dict(Hq=6, Hkv=2), 2, "G=3"),
@@ -218,3 +218,12 @@ def test_paged_and_multi_token_decode_validate_on_the_host(hils):
     assert rc == hils.HILS_ERR_INVALID and "num_pages" in hils.hils_last_error()
     rc = hils.LIB.hils_decode_paged_fwd(ctypes.byref(cp), F, F, F, F, None, None, F, 10, None, F, F, F, F, w1, None)
     assert rc == hils.HILS_ERR_WORKSPACE
+
+
+def test_head_normalised_selection_flag(hils):
+    f = hils.HILS_FLAG_HEAD_NORM_SELECT
+    assert hils.hils_workspace_size(params(hils, flags=f), hils.HILS_OP_PREFILL) >= 0
+    assert hils.hils_workspace_size(params(hils, N=1, flags=f), hils.HILS_OP_DECODE) >= 0
+    assert hils.hils_workspace_size(params(hils, flags=f), hils.HILS_OP_BWD) >= 0  # ignored there
+    with pytest.raises(hils.HilsError, match="landmark compression"):
+        hils.hils_workspace_size(params(hils, flags=f), hils.HILS_OP_LANDMARK)

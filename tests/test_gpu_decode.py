@@ -22,11 +22,11 @@ CASES = {
 }
 
 
-def run_case(name, forced=False):
+def run_case(name, forced=False, flags=0):
     from paper_2607_02980_amd import hils
 
     kw, wid, bias, route, seqlens = CASES[name]
-    p = hils.Params(**kw)
+    p = hils.Params(flags=flags, **kw)
     log(f"[decode] case={name} forced={forced} seqlens={seqlens} params={kw}")
     host = host_inputs(p, wid, bias=bias, route=route)
     dev = to_device(host, p)
@@ -37,7 +37,7 @@ def run_case(name, forced=False):
                      bias=np32(host.get("bias")), q_route=np32(host.get("q_route")), qpos=qpos)
     idx_in = None
     if forced:
-        p.flags = hils.HILS_FLAG_GIVEN_IDX
+        p.flags = hils.HILS_FLAG_GIVEN_IDX | flags
         idx_in = torch.from_numpy(ref["idx"]).cuda()
     out, lse, idx = hils.hils_decode_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], dev.get("bias"),
                                          dev.get("q_route"), sl_dev, idx=idx_in)
@@ -59,3 +59,10 @@ def test_decode_matches_oracle(name):
 
 def test_decode_forced_index():
     run_case("bf16_ragged_lengths", forced=True)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_decode_head_normalised_selection(name):
+    from paper_2607_02980_amd import hils
+
+    run_case(name, flags=hils.HILS_FLAG_HEAD_NORM_SELECT)

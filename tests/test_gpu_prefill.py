@@ -35,19 +35,19 @@ CASES = {
 }
 
 
-def run_case(name, forced=False):
+def run_case(name, forced=False, flags=0):
     from paper_2607_02980_amd import hils
 
     kw, wid, bias, route, shift = CASES[name]
-    p = hils.Params(**kw)
-    log(f"[prefill] case={name} forced={forced} params={kw}")
+    p = hils.Params(flags=flags, **kw)
+    log(f"[prefill] case={name} forced={forced} flags={flags} params={kw}")
     host = host_inputs(p, wid, bias=bias, route=route, bias_shift=shift)
     dev = to_device(host, p)
     s = oshape(p)
     ref = oracle.fwd(s, np32(host["q"]), np32(host["k"]), np32(host["v"]), np32(host["lmk"]),
                      bias=np32(host.get("bias")), q_route=np32(host.get("q_route")))
     if forced:
-        p.flags = hils.HILS_FLAG_GIVEN_IDX
+        p.flags = hils.HILS_FLAG_GIVEN_IDX | flags
         idx_in = torch.from_numpy(ref["idx"]).cuda()
         out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], dev.get("bias"),
                                               dev.get("q_route"), idx=idx_in)
@@ -73,6 +73,16 @@ def test_prefill_matches_oracle(name):
 @pytest.mark.parametrize("name", ["bf16_ragged_multi_tile", "f32_route_bias_G2"])
 def test_prefill_forced_index(name):
     run_case(name, forced=True)
+
+
+@pytest.mark.parametrize("name", ["tiny_2k_f32_full_config", "bf16_ragged_multi_tile", "bf16_bias_boosted",
+                                  "bf16_route_Hl_eq_Hkv", "f32_route_bias_G2", "bf16_mha_G1", "bf16_G8_d128",
+                                  "bf16_topk_exceeds_candidates"])
+def test_prefill_head_normalised_selection(name):
+    # the per-head normalised ranking (Sec. 4.1 wording), against the oracle's
+    from paper_2607_02980_amd import hils
+
+    run_case(name, flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
 
 
 def test_prefill_is_deterministic():

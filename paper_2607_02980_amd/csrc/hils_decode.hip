@@ -375,6 +375,161 @@ __device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D
     }
 }
 
+// One part per wavefront (bf16): no block barriers.  S^T = K Q^T for the 64 keys
+// (K rows and q straight from HBM as MFMA operands), the softmax per head over the
+// four lane groups with permlane swaps, and O^T = V^T P^T with V^T from the
+// wave's own LDS tile (transposing reads); the record is written by the lanes
+// that hold it.  Keys at or past nk are masked.
+template <int D>
+struct PartWaveSmem {
+    static constexpr int VROW = D + 16;  // conflict-free transposing reads
+    bf16 v[kChunk * VROW];
+};
+
+// B operand of O^T = V^T P^T from the exponentiated S^T blocks 2t, 2t + 1.
+__device__ __forceinline__ bf16x8 pack_bf16x8_4x2(const f32x4& e0, const f32x4& e1) {
+    const float x[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
+    return pack_bf16x8(x);
+}
+
+template <int D, int G>
+__device__ void run_part_wave(const FwdArgs& a, const DecLayout& ly, bf16* sv, int b, int n, int g, size_t rg,
+                              int part, int c, int nk, bool is_chunk) {
+    constexpr int KS = D / 32, DB = D / 16, VROW = PartWaveSmem<D>::VROW;
+    const int lane = threadIdx.x % kWave, lg = lane / 16, n16 = lane % 16;
+    const size_t kv_off = kv_chunk_offset(a, ly.nC, b, g, c, D);
+    const bf16* kg = as<bf16>(a.k) + kv_off;
+    const bf16* vg = as<bf16>(a.v) + kv_off;
+    // V rows into the wave's tile (all 64 rows lie in the cache or page; rows at or
+    // past nk are zeroed so that they add nothing)
+    {
+        constexpr int PR = D / 8;  // 16-byte pieces per row
+        uint4 x[kChunk * PR / kWave];
+#pragma unroll
+        for (int u = 0; u < kChunk * PR / kWave; ++u) {
+            const int e = lane + u * kWave, r = e / PR, pc = e % PR;
+            x[u] = *reinterpret_cast<const uint4*>(vg + (size_t)r * D + pc * 8);
+        }
+        bf16x8 kA[4][KS];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) kA[kb][ks] = ld_bf16x8(kg + (size_t)(kb * 16 + n16) * D + ks * 32 + lg * 8);
+        bf16x8 qB[KS];
+        const bf16* qrow = as<bf16>(a.q) + q_row(a, b, g * G + min(n16, G - 1), n) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 qq = ld_bf16x8(qrow + ks * 32 + lg * 8);
+            qB[ks] = n16 < G ? qq : as_bf16x8(make_uint4(0, 0, 0, 0));
+        }
+        // s^ of the retrieved chunk for head n16: q^ . k' over the lane's 8 dims per
+        // k-step, summed over the four lane groups
+        float sh = -INFINITY;
+        if (is_chunk) {
+            const int hh = min(n16, G - 1);
+            const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+            const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q) + q_row(a, b, g * G + hh, n) * D;
+            const bf16* lr = as<bf16>(a.lmk) + lmk_row(a, ly.nC, b, hl, c) * D;
+            float acc = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 x1 = ld_bf16x8(qr + ks * 32 + lg * 8), y1 = ld_bf16x8(lr + ks * 32 + lg * 8);
+#pragma unroll
+                for (int t = 0; t < 8; ++t) acc += (float)x1[t] * (float)y1[t];
+            }
+            sh = a.scale * group4_sum(acc) + (a.bias ? a.bias[lmk_row(a, ly.nC, b, hl, c)] : 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < kChunk * PR / kWave; ++u) {
+            const int e = lane + u * kWave, r = e / PR, pc = e % PR;
+            *reinterpret_cast<uint4*>(sv + r * VROW + pc * 8) = r < nk ? x[u] : make_uint4(0, 0, 0, 0);
+        }
+        // S^T (lane: head n16, keys 16 kb + 4 lg + i), in log2 units
+        const float c1 = a.scale * kLog2e;
+        f32x4 st[4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            st[kb] = zero4();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(kA[kb][ks], qB[ks], st[kb]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                st[kb][i] = kb * 16 + lg * 4 + i < nk ? st[kb][i] * c1 : -INFINITY;
+                mx = fmaxf(mx, st[kb][i]);
+            }
+        }
+        mx = group4_max(mx);
+        float ls = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                st[kb][i] = fexp2(st[kb][i] - mx);
+                ls += st[kb][i];
+            }
+        ls = group4_sum(ls);
+        const bf16x8 pb0 = pack_bf16x8_4x2(st[0], st[1]);
+        const bf16x8 pb1 = pack_bf16x8_4x2(st[2], st[3]);
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        // O^T (lane: head n16, dims 16 db + 4 lg + i), unnormalised
+        if (n16 < G) {
+            float* r = part_record<D>(a, ly, rg, part, n16, G);
+            if (lg == 0) {
+                r[0] = mx * (1.f / kLog2e);
+                r[1] = ls;
+                r[2] = sh;
+            }
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            f32x4 o = mfma16x16x32(tr_operand_perm(sv, VROW, 0, db * 16, lane), pb0, zero4());
+            o = mfma16x16x32(tr_operand_perm(sv, VROW, 32, db * 16, lane), pb1, o);
+            if (n16 < G) *reinterpret_cast<f32x4*>(part_record<D>(a, ly, rg, part, n16, G) + 4 + db * 16 + lg * 4) = o;
+        }
+    }
+}
+
+// bf16 parts: four parts per block, one per wave.
+template <int D, int G>
+__global__ __launch_bounds__(kBlock) void k_dec_parts_w(FwdArgs a) {
+    __shared__ __align__(16) PartWaveSmem<D> sm[kBlock / kWave];
+    const int w = wave_id();
+    const int part = blockIdx.x * (kBlock / kWave) + w, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    if (part >= ly.nparts) return;  // whole wave; no block barriers in this kernel
+    const int pos = decode_position(a, b, n);
+    const int lane = threadIdx.x % kWave;
+    if (part >= a.K) {
+        const int c = n_candidates(pos, a.W) + (part - a.K);
+        if (c > pos / kChunk) {
+            if (lane < G) {
+                float* r = part_record<D>(a, ly, rg, part, lane, G);
+                r[0] = -INFINITY;
+                r[1] = 0.f;
+                r[2] = -INFINITY;
+            }
+            return;
+        }
+        run_part_wave<D, G>(a, ly, sm[w].v, b, n, g, rg, part, c, min(kChunk, pos - c * kChunk + 1), false);
+        return;
+    }
+    const int32_t* irow = a.idx + rg * a.K;
+    const int c = __builtin_amdgcn_readfirstlane(idx_entry_valid(irow, part, n_candidates(pos, a.W)) ? irow[part] : -1);
+    if (c < 0) {
+        if (lane < G) {
+            float* r = part_record<D>(a, ly, rg, part, lane, G);
+            r[0] = -INFINITY;
+            r[1] = 0.f;
+            r[2] = -INFINITY;
+        }
+        return;
+    }
+    run_part_wave<D, G>(a, ly, sm[w].v, b, n, g, rg, part, c, kChunk, true);
+}
+
 template <int D>
 __device__ void empty_part(const FwdArgs& a, const DecLayout& ly, size_t rg, int part, int G) {
     for (int hh = threadIdx.x; hh < G; hh += kBlock) {
@@ -720,7 +875,13 @@ struct DecRun {
             }
             HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         }
-        HILS_LAUNCH("k_dec_parts", (k_dec_parts<T, D, G>), dim3(a.K + ly.nlocal, a.Hkv, R), dim3(kBlock), 0, s, a);
+        if constexpr (sizeof(T) == 2) {
+            constexpr int WPB = kBlock / kWave;
+            HILS_LAUNCH("k_dec_parts", (k_dec_parts_w<D, G>), dim3((ly.nparts + WPB - 1) / WPB, a.Hkv, R), dim3(kBlock),
+                        0, s, a);
+        } else {
+            HILS_LAUNCH("k_dec_parts", (k_dec_parts<T, D, G>), dim3(a.K + ly.nlocal, a.Hkv, R), dim3(kBlock), 0, s, a);
+        }
         HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }

@@ -48,8 +48,14 @@ struct BwLayout {
     size_t total;
 };
 
-// u [B, Hq, N] f32 | dq partials [B, Hq, N, K, d] bf16 | ds^ [B, Hq, N, K] f32 |
+// u [B, Hq, N] f32 | dq partials [B, Hkv, N, K, G, d] bf16 | ds^ [B, Hkv, N, K, G] f32 |
+// (the G heads of a (row, slot) adjacent: one workgroup's waves write them together)
 // sorted lists [B, Hkv, N*K] i32 | inverse index
+// Element offset of the per-slot value of (row n, slot, head hh) of KV group bg.
+__device__ __forceinline__ size_t slot_offset(size_t bg, int N, int n, int K, int slot, int G, int hh, int D) {
+    return (((bg * N + n) * K + slot) * G + hh) * (size_t)D;
+}
+
 BwLayout bw_layout(int B, int Hq, int Hkv, int N, int L, int d, int K) {
     BwLayout w;
     w.u = 0;
@@ -433,7 +439,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                     ds[kb][i] = pw[kb][i] * (gv4[kb][i] - uc);
                 }
             const float dsh = al * (uc - cur.u);
-            if (qv && lane < 16) dshat[qrow * a.K + slot] = dsh;
+            if (qv && lane < 16) dshat[slot_offset(bg, a.N, qn, a.K, slot, G, hh, 1)] = dsh;
             // H row of the pair: ds^ split into a bf16 head and its bf16 residual, in
             // columns m and 8 + m of its landmark head m (the product then keeps ds^ to
             // about fp32 accuracy)
@@ -472,7 +478,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                 od[db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 0, db * 16, lane), b0, zero4());
                 od[db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, od[db]);
             }
-            if (qv) store_lane_order<D>(dqp + (qrow * a.K + slot) * D, od, lg);
+            if (qv) store_lane_order<D>(dqp + slot_offset(bg, a.N, qn, a.K, slot, G, hh, D), od, lg);
         }
         __syncthreads();
         // ---- phase 2: keys [32kh, 32kh + 32) x head-dim blocks of dh, over the 64 pairs ----
@@ -692,11 +698,11 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
                 const int cc = irow[k];
                 const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
                 prev = cc;  // idx_entry_valid compares with the previous entry as written
-                const float xv = dshat[row * a.K + k];
+                const float xv = dshat[slot_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
                 xk[u] = ok ? a.scale * xv : 0.f;
                 okk[u] = ok;
                 const int ck = ok ? cc : 0;
-                load_lane_order<D>(dqp + (row * a.K + k) * D, lg, pv[u]);  // masked by okk if invalid
+                load_lane_order<D>(dqp + slot_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, pv[u]);  // masked by okk if invalid
                 const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + ck) * D;
 #pragma unroll
                 for (int db = 0; db < DB; ++db) lv[u][db] = *reinterpret_cast<const uint2*>(lrow + db * 16 + lg * 4);

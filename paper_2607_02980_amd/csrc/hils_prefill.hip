@@ -47,8 +47,15 @@ struct PfLayout {
     size_t total;
 };
 
-// part [B, Hq, N, K, d] bf16 (each d-vector in lane order), wgt [B, Hq, N, K] f32,
+// part [B, Hkv, N, K, G, d] bf16 (each d-vector in lane order; the G heads of a
+// (row, slot) are adjacent, so the heads' chunk outputs, written by the waves of
+// one workgroup, form one contiguous run), wgt [B, Hkv, N, K, G] f32,
 // ref [B, Hkv, N] f32, inverse index
+// Element offset of the partial of (row n, slot, head hh) of KV group bg = b * Hkv + g.
+__device__ __forceinline__ size_t part_offset(size_t bg, int N, int n, int K, int slot, int G, int hh, int D) {
+    return (((bg * N + n) * K + slot) * G + hh) * (size_t)D;
+}
+
 PfLayout pf_layout(int B, int Hq, int Hkv, int N, int L, int d, int K) {
     PfLayout w;
     w.part = 0;
@@ -474,7 +481,6 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
         const int hh = u % G;
         const bool qv = cur.ent >= 0;
         const int n = cur.ent >> 6, slot = cur.ent & 63;
-        const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + (qv ? n : 0);
         // surrogate score s^ = q^ . k'_c: the landmark row is row 0 of the A tile
         f32x4 sh4 = zero4();
 #pragma unroll
@@ -529,8 +535,8 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
 #pragma unroll
             for (int i = 0; i < 4; ++i) o[db][i] *= inv;
         if (qv) {
-            store_lane_order<D>(part + (qrow * a.K + slot) * D, o, lg);
-            if (lane < 16) wgt[qrow * a.K + slot] = fexp2((shat - cur.rf) * kLog2e);
+            store_lane_order<D>(part + part_offset(bg, a.N, n, a.K, slot, G, hh, D), o, lg);
+            if (lane < 16) wgt[part_offset(bg, a.N, n, a.K, slot, G, hh, 1)] = fexp2((shat - cur.rf) * kLog2e);
         }
     };
     Ops opa, opb, opc;
@@ -717,12 +723,12 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
             const int cc = irow[k];
             const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
             prev = cc;  // idx_entry_valid compares with the previous entry as written
-            const float wv = wgt[row * a.K + k];
+            const float wv = wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
             wk[u] = ok ? wv : 0.f;
             okk[u] = ok;
             // (address independent of idx, so these loads issue with the idx loads;
             // an invalid slot's bits are masked by fma_lane_order)
-            load_lane_order<D>(part + (row * a.K + k) * D, lg, pv[u]);
+            load_lane_order<D>(part + part_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, pv[u]);
         }
 #pragma unroll
         for (int u = 0; u < SB; ++u) {

@@ -568,25 +568,31 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
 // ---------------------------------------------------------------------------
 // Query-major dq: local window, then the row's retrieved-chunk partials
 // ---------------------------------------------------------------------------
+// One block of 8 waves per tile of 16 * 8 / G rows of one KV group; wave w owns
+// the item (head w / QB, 16-row block w % QB).  The window's 64-key blocks of K
+// and V are double-buffered in LDS (the next block is fetched into registers
+// while the current one is used), one barrier per block.
 template <int G>
 struct DqCfg {
     static constexpr int QB = 8 / G;          // 16-row blocks per workgroup
     static constexpr int QT = 16 * QB;        // rows per workgroup
-    static constexpr int ITEMS = G * QB;      // (head, 16-row block) items: 8
-    static constexpr int IPW = ITEMS / 4;     // items per wave: 2
+    static constexpr int NT = 8 * kWave;      // threads
 };
 
 template <int D>
 struct DqSmem {
     static constexpr int KROW = BT<D>::KROW;
-    bf16 k[kChunk * KROW];
-    bf16 v[kChunk * KROW];
+    bf16 k[2][kChunk * KROW];
+    bf16 v[2][kChunk * KROW];
 };
 
 template <int D, int G>
-__global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, const bf16* dqp, const float* dshat) {
+__global__ __launch_bounds__(DqCfg<G>::NT, 4) void k_bwd_dq(BwdArgs a, const float* u, const bf16* dqp,
+                                                           const float* dshat) {
     using C = DqCfg<G>;
-    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, IPW = C::IPW;
+    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW;
+    constexpr int PPT = kChunk * D / 8 / C::NT;  // 16-byte pieces per thread of a K or V block
+    static_assert(PPT >= 1 && kChunk * D / 8 == PPT * C::NT, "K/V blocks split evenly over the threads");
     __shared__ __align__(16) DqSmem<D> sm;
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int ntiles = (a.N + C::QT - 1) / C::QT;
@@ -598,139 +604,142 @@ __global__ __launch_bounds__(kBlock) void k_bwd_dq(BwdArgs a, const float* u, co
     const int nC = a.L / kChunk;
     const bf16* kbase = as<bf16>(a.k) + bg * a.L * D;
     const bf16* vbase = as<bf16>(a.v) + bg * a.L * D;
+    const int hh = w / C::QB, qb = w % C::QB;
+    const int nq_raw = q0 + qb * 16 + lane % 16;
+    const int nq = min(nq_raw, a.N - 1);
+    const int h = g * G + hh;
+    const size_t qrow = ((size_t)b * a.Hq + h) * a.N + nq;
 
-    Rows<D> xk = load_rows<D>(kbase + (size_t)kbeg * D);
-    Rows<D> xv = load_rows<D>(vbase + (size_t)kbeg * D);
-
-    bf16x8 bq[IPW][KS], bo[IPW][KS];
-    f32x4 dq[IPW][DB];
-    float Lr[IPW], ub[IPW];
+    struct KV {
+        uint4 k[PPT], v[PPT];
+    };
+    auto fetch = [&](int j0) {
+        KV x;
 #pragma unroll
-    for (int it = 0; it < IPW; ++it) {
-        const int item = w + 4 * it;
-        const int hh = item / C::QB, qb = item % C::QB;
-        const int nq = min(q0 + qb * 16 + lane % 16, a.N - 1);
-        const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            bq[it][ks] = ld_bf16x8(as<bf16>(a.q) + qrow * D + ks * 32 + lg * 8);
-            bo[it][ks] = ld_bf16x8(as<bf16>(a.dout) + qrow * D + ks * 32 + lg * 8);
+        for (int t = 0; t < PPT; ++t) {
+            const int e = tid + t * C::NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            x.k[t] = *reinterpret_cast<const uint4*>(kbase + (size_t)(j0 + j) * D + d8);
+            x.v[t] = *reinterpret_cast<const uint4*>(vbase + (size_t)(j0 + j) * D + d8);
         }
+        return x;
+    };
+    auto stage = [&](int buf, const KV& x) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db) dq[it][db] = zero4();
-        Lr[it] = a.lse[qrow];
-        ub[it] = u[qrow];
+        for (int t = 0; t < PPT; ++t) {
+            const int e = tid + t * C::NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            *reinterpret_cast<uint4*>(&sm.k[buf][j * KROW + d8]) = x.k[t];
+            *reinterpret_cast<uint4*>(&sm.v[buf][j * KROW + d8]) = x.v[t];
+        }
+    };
+
+    bf16x8 bq[KS], bo[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        bq[ks] = ld_bf16x8(as<bf16>(a.q) + qrow * D + ks * 32 + lg * 8);
+        bo[ks] = ld_bf16x8(as<bf16>(a.dout) + qrow * D + ks * 32 + lg * 8);
     }
-    for (int j0 = kbeg; j0 <= qlast; j0 += kChunk) {
+    f32x4 dq[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dq[db] = zero4();
+    const float Lr = a.lse[qrow], ub = u[qrow];
+    const int ell = n_candidates(nq, a.W) * kChunk;
+
+    KV nx = fetch(kbeg);
+    stage(0, nx);
+    __syncthreads();
+    int buf = 0;
+    for (int j0 = kbeg; j0 <= qlast; j0 += kChunk, buf ^= 1) {
+        const bool more = j0 + kChunk <= qlast;  // uniform over the block
+        if (more) nx = fetch(j0 + kChunk);
+        const bf16* tk = sm.k[buf];
+        const bf16* tv = sm.v[buf];
+        f32x4 s4[4], gv4[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            s4[kb] = zero4();
+            gv4[kb] = zero4();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                s4[kb] = mfma16x16x32(row_operand<KROW>(tk, kb * 16, ks * 32, lane), bq[ks], s4[kb]);
+                gv4[kb] = mfma16x16x32(row_operand<KROW>(tv, kb * 16, ks * 32, lane), bo[ks], gv4[kb]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        float ds[4][4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = j0 + kb * 16 + lg * 4 + i;
+                const bool valid = nq_raw < a.N && j <= nq && j >= ell;
+                const float wgt = valid ? fexp(a.scale * s4[kb][i] - Lr) : 0.f;
+                ds[kb][i] = wgt * (gv4[kb][i] - ub);
+            }
+        const bf16x8 b0 = pack_perm(ds[0], ds[1]);
+        const bf16x8 b1 = pack_perm(ds[2], ds[3]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            dq[db] = mfma16x16x32(tr_operand_perm(tk, KROW, 0, db * 16, lane), b0, dq[db]);
+            dq[db] = mfma16x16x32(tr_operand_perm(tk, KROW, 32, db * 16, lane), b1, dq[db]);
+            if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
+        }
+        if (more) stage(buf ^ 1, nx);
         __syncthreads();
-        store_rows<D>(sm.k, xk);
-        store_rows<D>(sm.v, xv);
-        __syncthreads();
-        if (j0 + kChunk <= qlast) {  // the next key tile, fetched during this one
-            xk = load_rows<D>(kbase + (size_t)(j0 + kChunk) * D);
-            xv = load_rows<D>(vbase + (size_t)(j0 + kChunk) * D);
+    }
+    // epilogue (lane: row l%16 of the item, dims 16db + (l/16)*4 + {0..3})
+    if (nq_raw >= a.N) return;  // no barriers below
+    const int hl = (a.Hl == a.Hq) ? h : g;
+    const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
+    const int ncand = n_candidates(nq, a.W);
+    f32x4 accr[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) accr[db] = zero4();
+    // the row's slots, SB at a time with every load in flight before use
+    constexpr int SB = D >= 128 ? 1 : 4;
+    int prev = -1;
+    for (int k0 = 0; k0 < a.K; k0 += SB) {
+        float xk[SB];
+        bool okk[SB];
+        uint4 pv[SB][D / 32];
+        uint2 lv[SB][DB];
+#pragma unroll
+        for (int t = 0; t < SB; ++t) {
+            const int k = min(k0 + t, a.K - 1);
+            const int cc = irow[k];
+            const bool ok = k0 + t < a.K && cc >= 0 && cc < ncand && cc > prev;
+            prev = cc;  // idx_entry_valid compares with the previous entry as written
+            const float xv = dshat[slot_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
+            xk[t] = ok ? a.scale * xv : 0.f;
+            okk[t] = ok;
+            const int ck = ok ? cc : 0;
+            load_lane_order<D>(dqp + slot_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, pv[t]);  // masked by okk if invalid
+            const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + ck) * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) lv[t][db] = *reinterpret_cast<const uint2*>(lrow + db * 16 + lg * 4);
         }
 #pragma unroll
-        for (int it = 0; it < IPW; ++it) {
-            const int item = w + 4 * it;
-            const int qb = item % C::QB;
-            const int nq = q0 + qb * 16 + lane % 16;
-            const int ell = n_candidates(nq, a.W) * kChunk;
-            f32x4 s4[4], gv4[4];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                s4[kb] = zero4();
-                gv4[kb] = zero4();
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    s4[kb] = mfma16x16x32(row_operand<KROW>(sm.k, kb * 16, ks * 32, lane), bq[it][ks], s4[kb]);
-                    gv4[kb] = mfma16x16x32(row_operand<KROW>(sm.v, kb * 16, ks * 32, lane), bo[it][ks], gv4[kb]);
-                }
-            }
-            float ds[4][4];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int j = j0 + kb * 16 + lg * 4 + i;
-                    const bool valid = nq < a.N && j <= nq && j >= ell;
-                    const float wgt = valid ? fexp(a.scale * s4[kb][i] - Lr[it]) : 0.f;
-                    ds[kb][i] = wgt * (gv4[kb][i] - ub[it]);
-                }
-            const bf16x8 b0 = pack_perm(ds[0], ds[1]);
-            const bf16x8 b1 = pack_perm(ds[2], ds[3]);
+        for (int t = 0; t < SB; ++t) {
+            fma_lane_order<D>(pv[t], 1.f, okk[t], dq);
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                dq[it][db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 0, db * 16, lane), b0, dq[it][db]);
-                dq[it][db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, dq[it][db]);
+                accr[db][0] += xk[t] * bf_lo(lv[t][db].x);
+                accr[db][1] += xk[t] * bf_hi(lv[t][db].x);
+                accr[db][2] += xk[t] * bf_lo(lv[t][db].y);
+                accr[db][3] += xk[t] * bf_hi(lv[t][db].y);
             }
         }
     }
-    // epilogue (lane: row l%16 of the block, dims 16db + (l/16)*4 + {0..3})
+    bf16* dqo = as_mut<bf16>(a.dq) + qrow * D;
+    bf16* dqr = a.dq_route ? as_mut<bf16>(a.dq_route) + qrow * D : nullptr;
 #pragma unroll
-    for (int it = 0; it < IPW; ++it) {
-        const int item = w + 4 * it;
-        const int hh = item / C::QB, qb = item % C::QB;
-        const int nq = q0 + qb * 16 + lane % 16;
-        if (nq >= a.N) continue;
-        const int h = g * G + hh;
-        const int hl = (a.Hl == a.Hq) ? h : g;
-        const size_t row = ((size_t)b * a.Hq + h) * a.N + nq;
-        const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
-        const int ncand = n_candidates(nq, a.W);
-        f32x4 acc[DB], accr[DB];
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-            acc[db] = dq[it][db];
-            accr[db] = zero4();
-        }
-        // the row's slots, SB at a time with every load in flight before use
-        constexpr int SB = D >= 128 ? 4 : 8;
-        int prev = -1;
-        for (int k0 = 0; k0 < a.K; k0 += SB) {
-            float xk[SB];
-            bool okk[SB];
-            uint4 pv[SB][D / 32];
-            uint2 lv[SB][DB];
-#pragma unroll
-            for (int u = 0; u < SB; ++u) {
-                const int k = min(k0 + u, a.K - 1);
-                const int cc = irow[k];
-                const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
-                prev = cc;  // idx_entry_valid compares with the previous entry as written
-                const float xv = dshat[slot_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
-                xk[u] = ok ? a.scale * xv : 0.f;
-                okk[u] = ok;
-                const int ck = ok ? cc : 0;
-                load_lane_order<D>(dqp + slot_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, pv[u]);  // masked by okk if invalid
-                const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + ck) * D;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) lv[u][db] = *reinterpret_cast<const uint2*>(lrow + db * 16 + lg * 4);
-            }
-#pragma unroll
-            for (int u = 0; u < SB; ++u) {
-                fma_lane_order<D>(pv[u], 1.f, okk[u], acc);
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    accr[db][0] += xk[u] * bf_lo(lv[u][db].x);
-                    accr[db][1] += xk[u] * bf_hi(lv[u][db].x);
-                    accr[db][2] += xk[u] * bf_lo(lv[u][db].y);
-                    accr[db][3] += xk[u] * bf_hi(lv[u][db].y);
-                }
-            }
-        }
-        bf16* dqo = as_mut<bf16>(a.dq) + row * D;
-        bf16* dqr = a.dq_route ? as_mut<bf16>(a.dq_route) + row * D : nullptr;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-            const int d0 = db * 16 + lg * 4;
-            f32x4 x = acc[db] * a.scale;
-            if (!dqr) x += accr[db];
-            *reinterpret_cast<uint2*>(dqo + d0) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
-            if (dqr)
-                *reinterpret_cast<uint2*>(dqr + d0) = make_uint2(pack_bf16x2(accr[db][0], accr[db][1]),
-                                                                 pack_bf16x2(accr[db][2], accr[db][3]));
-        }
+    for (int db = 0; db < DB; ++db) {
+        const int d0 = db * 16 + lg * 4;
+        f32x4 x = dq[db] * a.scale;
+        if (!dqr) x += accr[db];
+        *reinterpret_cast<uint2*>(dqo + d0) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+        if (dqr)
+            *reinterpret_cast<uint2*>(dqr + d0) = make_uint2(pack_bf16x2(accr[db][0], accr[db][1]),
+                                                             pack_bf16x2(accr[db][2], accr[db][3]));
     }
 }
 
@@ -758,7 +767,7 @@ struct BwRun {
             HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, false>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a, offsets,
                         (const int*)sorted, (const float*)u, dqp, dsh);
         HILS_LAUNCH("k_bwd_dq", (k_bwd_dq<D, G>), dim3((a.N + DqCfg<G>::QT - 1) / DqCfg<G>::QT, a.Hkv, a.B),
-                    dim3(kBlock), 0, s, a, (const float*)u, (const bf16*)dqp, (const float*)dsh);
+                    dim3(DqCfg<G>::NT), 0, s, a, (const float*)u, (const bf16*)dqp, (const float*)dsh);
         return hipGetLastError();
     }
 };

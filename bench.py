@@ -131,7 +131,20 @@ class Timer:
         return e0.elapsed_time(e1) / steps  # ms
 
 
-def bench_prefill(torch, hils, synth, W_, steps, warmup, flags=0):
+def chunk_overlap(idx, M=16):
+    """Normalised chunk overlap of blocks of M adjacent queries, (M K - |union|) / ((M - 1) K),
+    over the blocks whose rows all hold K chunks (a statistic of the inputs)."""
+    B, Hkv, N, K = idx.shape
+    n0 = (N // M) * M
+    blk = idx[:, :, :n0].reshape(B, Hkv, n0 // M, M * K)
+    full = (blk >= 0).all(axis=-1)
+    srt = np.sort(blk, axis=-1)
+    uniq = 1 + (np.diff(srt, axis=-1) != 0).sum(axis=-1)
+    vals = (M * K - uniq[full]) / ((M - 1) * K)
+    return float(vals.mean()) if vals.size else float("nan")
+
+
+def bench_prefill(torch, hils, synth, W_, steps, warmup, flags=0, rho=None):
     """Times `steps` prefill calls (HIP events on the library's stream, no
     per-kernel events), then a second pass with per-kernel timing for the
     breakdown; returns (params, host inputs, ms/step, kernels)."""
@@ -146,6 +159,9 @@ def bench_prefill(torch, hils, synth, W_, steps, warmup, flags=0):
         "lmk": synth.normal_host((p.B, p.Hq, nc, p.d), synth.seed_for(W_.wid, "lmk"), p.dtype),
     }
     dev = {k: v.to("cuda", dt).contiguous() for k, v in host.items()}
+    if rho is not None:  # queries correlated along the sequence (the locality inputs)
+        dev["q"] = synth.ar1_host((p.B, p.Hq, p.N, p.d), synth.seed_for(W_.wid, "q"), p.dtype, rho=rho,
+                                  device="cuda").to(dt).contiguous()
     out = torch.empty(p.B, p.Hq, p.N, p.d, dtype=dt, device="cuda")
     lse = torch.empty(p.B, p.Hq, p.N, dtype=torch.float32, device="cuda")
     idx = torch.empty(p.B, p.Hkv, p.N, p.topk, dtype=torch.int32, device="cuda")
@@ -161,6 +177,7 @@ def bench_prefill(torch, hils, synth, W_, steps, warmup, flags=0):
     hils.hils_timing_enable(False)
     for k in kernels.values():
         k["avg_ms"] = k["total_ms"] / max(1, k["launches"])
+    p.overlap16 = chunk_overlap(idx.cpu().numpy(), 16)
     del dev, ws
     torch.cuda.empty_cache()
     return p, host, ms, kernels
@@ -406,11 +423,16 @@ def main():
         res["extra"]["landmark"] = bench_landmark(torch, hils, synth, Wp, args.steps, args.warmup)
     if not args.no_variants:
         # selection variants: per-head normalised ranking, and one query head per KV head (MHA)
-        for name, W_, fl in (("prefill_head_norm", Wp, hils.HILS_FLAG_HEAD_NORM_SELECT),
-                             ("prefill_mha_G1", Wp.with_(Hkv=Wp.Hq), 0)):
-            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, max(3, args.steps // 2), 1, flags=fl)
+        U = hils.HILS_FLAG_UNION_PACKING
+        for name, W_, fl, rho in (("prefill_head_norm", Wp, hils.HILS_FLAG_HEAD_NORM_SELECT, None),
+                                  ("prefill_mha_G1", Wp.with_(Hkv=Wp.Hq), 0, None),
+                                  ("prefill_union_packing", Wp, U, None),
+                                  ("prefill_locality_chunk_major", Wp, 0, 0.97),
+                                  ("prefill_locality_union_packing", Wp, U, 0.97)):
+            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, max(3, args.steps // 2), 1, flags=fl, rho=rho)
             res["extra"][name] = {"ms_per_step": round(msv, 4), "tokens_per_s": round(pv.B * pv.N / (msv * 1e-3), 1),
-                                  "Hq": pv.Hq, "Hkv": pv.Hkv,
+                                  "Hq": pv.Hq, "Hkv": pv.Hkv, "query_rho": rho,
+                                  "chunk_overlap_16": round(pv.overlap16, 4),
                                   "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kv.items()}}
         res["extra"]["decode_head_norm"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
                                                         max(3, args.steps // 2), 2,

@@ -89,6 +89,15 @@ typedef enum {
  * pass over the landmark scores.  Ignored by hils_bwd (the selection is given). */
 #define HILS_FLAG_HEAD_NORM_SELECT 4u
 
+/* Prefill flag (bf16): compute the retrieved-chunk terms by union packing, the
+ * one-load-multiple-compute scheme of Sec. 4.2 — each tile of adjacent queries
+ * loads the union of their selected chunks once and computes every chunk for
+ * all of its rows (rows that did not select a chunk get weight 0).  Same
+ * results as the default chunk-major pass; faster when adjacent queries select
+ * overlapping chunks (as trained models do), slower when they do not.  Ignored
+ * with HILS_FLAG_GIVEN_IDX, by the fp32 path, decode and the backward. */
+#define HILS_FLAG_UNION_PACKING 8u
+
 typedef enum { HILS_OP_PREFILL = 0, HILS_OP_DECODE = 1, HILS_OP_BWD = 2, HILS_OP_LANDMARK = 3 } hils_op;
 
 typedef struct {

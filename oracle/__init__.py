@@ -314,6 +314,26 @@ def decode(shape: Shape, q, k, v, lmk, seqlens=None, bias=None, q_route=None, id
                idx=idx, prec=prec)
 
 
+def chunk_overlap(idx, M: int) -> float:
+    """Normalised chunk-overlap ratio of blocks of M adjacent queries (the
+    measure of the kernel-design section, Sec. 4.2): (M K - |union of their top-K
+    sets|) / ((M - 1) K), averaged over every block of M consecutive rows (per
+    sequence and KV group) whose rows all hold K valid entries.  1 means the M
+    queries retrieve the same chunks, 0 that they share none.  idx [B, Hkv, N, K]."""
+    idx = np.asarray(idx)
+    B, Hkv, N, K = idx.shape
+    vals = []
+    for b in range(B):
+        for g in range(Hkv):
+            for n0 in range(0, N - M + 1, M):
+                blk = idx[b, g, n0:n0 + M]
+                if (blk < 0).any():
+                    continue
+                u = len(np.unique(blk))
+                vals.append((M * K - u) / ((M - 1) * K))
+    return float(np.mean(vals)) if vals else float("nan")
+
+
 def n_candidates(i: int, chunk: int, window: int) -> int:
     """|C_i| = l(i)/S with l(i) clamped at 0 (Sec. 2.1)."""
     return max(0, (i - window + 1) // chunk)

@@ -62,7 +62,8 @@ int check_params(const hils_params* p, int op) {
     if (p->L % p->chunk) return fail(HILS_ERR_INVALID, "L=%d is not a multiple of chunk=%d", p->L, p->chunk);
     if (p->dtype != HILS_F32 && p->dtype != HILS_BF16) return fail(HILS_ERR_INVALID, "unknown dtype %d", (int)p->dtype);
     if (!isfinite(p->scale)) return fail(HILS_ERR_INVALID, "scale is not finite");
-    if (p->flags & ~(HILS_FLAG_GIVEN_IDX | HILS_FLAG_SHARED_LMK_QUERY | HILS_FLAG_HEAD_NORM_SELECT))
+    if (p->flags & ~(HILS_FLAG_GIVEN_IDX | HILS_FLAG_SHARED_LMK_QUERY | HILS_FLAG_HEAD_NORM_SELECT |
+                     HILS_FLAG_UNION_PACKING))
         return fail(HILS_ERR_INVALID, "unknown flags 0x%x", p->flags);
     if ((p->flags & HILS_FLAG_HEAD_NORM_SELECT) && op == HILS_OP_LANDMARK)
         return fail(HILS_ERR_INVALID, "HILS_FLAG_HEAD_NORM_SELECT does not apply to the landmark compression");
@@ -137,6 +138,7 @@ hils::FwdArgs fwd_args(const hils_params* p, const void* q, const void* k, const
     a.decode = decode;
     a.given_idx = (p->flags & HILS_FLAG_GIVEN_IDX) ? 1 : 0;
     a.head_norm = (p->flags & HILS_FLAG_HEAD_NORM_SELECT) ? 1 : 0;
+    a.union_pack = (p->flags & HILS_FLAG_UNION_PACKING) ? 1 : 0;
     a.ws = ws; a.ws_bytes = ws_bytes;
     return a;
 }

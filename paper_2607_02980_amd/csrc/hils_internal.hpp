@@ -27,6 +27,7 @@ struct FwdArgs {
     int decode;    // 1: query n of sequence b sits at len_b - N + n (len_b = seqlens[b] in [N, L])
     int given_idx; // 1: consume idx
     int head_norm; // 1: rank by per-head normalised scores
+    int union_pack; // 1: prefill chunk terms by the union of each tile's selections
     void* ws;
     size_t ws_bytes;
 };

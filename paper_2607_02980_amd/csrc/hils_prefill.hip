@@ -569,7 +569,16 @@ struct LocalCfg {
     static constexpr int NT = 8 * kWave;
 };
 
-template <int D, int G>
+// UNION (the paper's one-load-multiple-compute, Sec. 4.2, on MFMA): instead of
+// reading per-slot partials, the tile loads the union of its rows' selected
+// chunks once each (ascending, double-buffered like the window) and computes
+// every chunk for all of its rows; a row that did not select the chunk gets
+// weight 0, and a wave none of whose rows selected it skips the chunk's MFMAs.
+// With adjacent queries that retrieve overlapping chunks the union is small and
+// no partials go through HBM.  The union is built in LDS from the rows' idx: a
+// bitmap over the chunks, then the set bits in order (dynamic LDS: the bitmap,
+// the rows' valid entries, the union list).
+template <int D, int G, bool UNION, bool ROUTE>
 __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, const float* ref, const bf16* part,
                                                                 const float* wgt) {
     using C = LocalCfg<G>;
@@ -594,6 +603,50 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     const int nq_raw = q0 + qb * 16 + lane % 16;
     const int nq = min(nq_raw, a.N - 1);
     const size_t row = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
+
+    // union of the tile's selections (UNION only)
+    extern __shared__ int s_dyn[];
+    __shared__ int s_nu;
+    const int nC = a.L / kChunk, nwords = (nC + 31) / 32;
+    int* s_bits = s_dyn;
+    int* s_idx = s_bits + nwords;              // [QT][K] the rows' valid entries, then INT_MAX
+    int* s_list = s_idx + C::QT * a.K;         // the union, ascending
+    if constexpr (UNION) {
+        for (int i = tid; i < nwords; i += C::NT) s_bits[i] = 0;
+        __syncthreads();
+        for (int e = tid; e < C::QT * a.K; e += C::NT) {
+            const int r = e / a.K, n = q0 + r;
+            int v = INT_MAX;
+            if (n < a.N) {
+                const int raw = a.idx[(bg * a.N + n) * a.K + e % a.K];
+                if (raw >= 0 && raw < n_candidates(n, a.W)) v = raw;
+            }
+            s_idx[e] = v;
+            if (v != INT_MAX) atomicOr(reinterpret_cast<unsigned*>(&s_bits[v >> 5]), 1u << (v & 31));
+        }
+        __syncthreads();
+        if (w == 0) {
+            int base = 0;
+            for (int w0 = 0; w0 < nwords; w0 += kWave) {
+                unsigned word = w0 + lane < nwords ? (unsigned)s_bits[w0 + lane] : 0u;
+                const int cnt = __popc(word);
+                int incl = cnt;
+#pragma unroll
+                for (int o2 = 1; o2 < kWave; o2 <<= 1) {
+                    const int y = __shfl_up(incl, o2, kWave);
+                    if (lane >= o2) incl += y;
+                }
+                int pos = base + incl - cnt;
+                while (word) {
+                    s_list[pos++] = (w0 + lane) * 32 + __ffs(word) - 1;
+                    word &= word - 1u;
+                }
+                base += __shfl(incl, kWave - 1, kWave);
+            }
+            if (lane == 0) s_nu = base;
+        }
+        // (the barrier before the window's first block orders these writes)
+    }
 
     struct KV {
         uint4 k[PPT], v[PPT];
@@ -707,11 +760,91 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     const float wc = fexp(rf - M);
 #pragma unroll
     for (int db = 0; db < DB; ++db) o[db] *= wl;
+    float zs = 0.f;
+    if constexpr (UNION) {
+        // the union's chunks, each for all rows of the tile
+        const int U = s_nu;
+        const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
+        const bf16* lbase = as<bf16>(a.lmk) + ((size_t)b * a.Hl + hl) * nC * D;
+        bf16x8 bqr[ROUTE ? KS : 1];
+        if constexpr (ROUTE) {
+            const bf16* rrow = as<bf16>(a.q_route) + row * D;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) bqr[ks] = ld_bf16x8(rrow + ks * 32 + lg * 8);
+        }
+        const int* myidx = s_idx + (qb * 16 + lane % 16) * a.K;
+        int ptr = 0;
+        if (U > 0) {
+            nx = fetch(s_list[0] * kChunk);
+            stage(0, nx);
+        }
+        __syncthreads();
+        buf = 0;
+        for (int u = 0; u < U; ++u, buf ^= 1) {
+            const bool more = u + 1 < U;
+            if (more) nx = fetch(s_list[u + 1] * kChunk);
+            const int c = s_list[u];
+            const bool sel = nq_raw < a.N && myidx[min(ptr, a.K - 1)] == c && ptr < a.K;
+            ptr += sel ? 1 : 0;
+            if (__ballot(sel) != 0ull) {
+                const bf16* tk = s_k[buf];
+                const bf16* tv = s_v[buf];
+                // s^ of the rows for chunk c: the landmark row is row 0 of the A tile
+                f32x4 sh4 = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    const bf16x8 lrow = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + lg * 8);
+                    const bf16x8 aL = (lane % 16 == 0) ? lrow : as_bf16x8(make_uint4(0, 0, 0, 0));
+                    sh4 = mfma16x16x32(aL, ROUTE ? bqr[ks] : bq[ks], sh4);
+                }
+                const float shat = a.scale * group0_bcast(sh4[0]) + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f);
+                f32x4 st[4];
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb) {
+                    st[kb] = zero4();
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks)
+                        st[kb] = mfma16x16x32(ld_bf16x8(tk + (kb * 16 + lane % 16) * KROW + ks * 32 + lg * 8), bq[ks],
+                                              st[kb]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                float mx = -INFINITY;
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[kb][i]);
+                mx = group4_max(mx) * c1;
+                float psum = 0.f;
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        st[kb][i] = fexp2(fmaf(st[kb][i], c1, -mx));
+                        psum += st[kb][i];
+                    }
+                const bf16x8 pb0 = p_operand(st[0], st[1]);
+                const bf16x8 pb1 = p_operand(st[2], st[3]);
+                psum = group4_sum(psum);
+                // weight of the chunk for this row: exp(s^ - ref) if it selected c, else 0
+                const float wk = sel ? fexp2((shat - rf) * kLog2e) : 0.f;
+                zs += wk;
+                const float f = wc * wk / psum;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    f32x4 oc = mfma16x16x32(tr_operand_perm(tv, VROW, 0, db * 16, lane), pb0, zero4());
+                    oc = mfma16x16x32(tr_operand_perm(tv, VROW, 32, db * 16, lane), pb1, oc);
+                    o[db] += f * oc;
+                    if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+            if (more) stage(buf ^ 1, nx);
+            __syncthreads();
+        }
+    } else {
     // the row's retrieved chunks: slots in idx order, valid entries only
     constexpr int SB = D >= 128 ? 2 : 4;  // slots whose loads are in flight together
     const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
     const int ncand = n_candidates(nq, a.W);
-    float zs = 0.f;
     int prev = -1;
     for (int k0 = 0; k0 < a.K; k0 += SB) {
         float wk[SB];
@@ -735,6 +868,7 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
             zs += wk[u];
             fma_lane_order<D>(pv[u], wc * wk[u], okk[u], o);
         }
+    }
     }
     const float Z = fexp(lam0 - M) + wc * zs;
     const float inv = 1.f / Z;
@@ -767,6 +901,20 @@ struct PfRun {
             else
                 HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kBlock), 0, s, a, ref);
         }
+        const dim3 lgrid((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B);
+        if (a.union_pack && !a.given_idx) {
+            // one-load-multiple-compute: no inverse index, no per-slot partials
+            const int nC = a.L / kChunk;
+            const int qk = LocalCfg<G>::QT * a.K;
+            const size_t dyn = (size_t)((nC + 31) / 32 + qk + min(nC, qk)) * sizeof(int);
+            if (a.q_route)
+                HILS_LAUNCH("k_pf_union", (k_pf_local<D, G, true, true>), lgrid, dim3(LocalCfg<G>::NT), dyn, s, a,
+                            (const float*)ref, (const bf16*)part, (const float*)wgt);
+            else
+                HILS_LAUNCH("k_pf_union", (k_pf_local<D, G, true, false>), lgrid, dim3(LocalCfg<G>::NT), dyn, s, a,
+                            (const float*)ref, (const bf16*)part, (const float*)wgt);
+            return hipGetLastError();
+        }
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
         launch_inverse_index(ia, ly.inv, a.ws, s);
         const int* offsets = reinterpret_cast<const int*>(ws + ly.inv.offsets);
@@ -779,8 +927,8 @@ struct PfRun {
         else
             HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
                         offsets, list, work, nwork, (const float*)ref, part, wgt);
-        HILS_LAUNCH("k_pf_local", (k_pf_local<D, G>), dim3((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B),
-                           dim3(LocalCfg<G>::NT), 0, s, a, (const float*)ref, (const bf16*)part, (const float*)wgt);
+        HILS_LAUNCH("k_pf_local", (k_pf_local<D, G, false, false>), lgrid, dim3(LocalCfg<G>::NT), 0, s, a,
+                    (const float*)ref, (const bf16*)part, (const float*)wgt);
         return hipGetLastError();
     }
 };

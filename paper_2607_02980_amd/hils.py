@@ -24,6 +24,7 @@ HILS_OK, HILS_ERR_INVALID, HILS_ERR_UNSUPPORTED, HILS_ERR_WORKSPACE, HILS_ERR_HI
 HILS_FLAG_GIVEN_IDX = 1
 HILS_FLAG_SHARED_LMK_QUERY = 2
 HILS_FLAG_HEAD_NORM_SELECT = 4
+HILS_FLAG_UNION_PACKING = 8
 HILS_OP_PREFILL, HILS_OP_DECODE, HILS_OP_BWD, HILS_OP_LANDMARK = 0, 1, 2, 3
 
 

@@ -63,7 +63,7 @@ def call_prefill(hils, p, **override):
     (dict(topk=0), 1, ">= 1"),
     (dict(window=0), 1, ">= 1"),
     (dict(B=0), 1, ">= 1"),
-    (dict(flags=8), 1, "unknown flags"),
+    (dict(flags=16), 1, "unknown flags"),
     (dict(chunk=32), 2, "chunk 64"),
     (dict(d=96), 2, "d in {64, 128}"),
     (dict(Hq=6, Hkv=2), 2, "G=3"),

@@ -75,6 +75,43 @@ def test_prefill_forced_index(name):
     run_case(name, forced=True)
 
 
+@pytest.mark.parametrize("name", ["bf16_ragged_multi_tile", "bf16_window1", "bf16_bias_boosted", "bf16_route_Hl_eq_Hkv",
+                                  "bf16_mha_G1", "bf16_G8_d128", "bf16_topk_exceeds_candidates", "bf16_all_local"])
+def test_prefill_union_packing(name):
+    # the one-load-multiple-compute chunk terms (tiles load the union of their
+    # rows' chunks) on i.i.d. inputs, against the oracle
+    from paper_2607_02980_amd import hils
+
+    run_case(name, flags=hils.HILS_FLAG_UNION_PACKING)
+
+
+@pytest.mark.parametrize("G", [4, 1])
+def test_prefill_union_packing_on_locality_inputs(G):
+    # queries correlated along the sequence (adjacent queries share most chunks):
+    # the union path and the chunk-major path against the oracle
+    from paper_2607_02980_amd import hils, synth
+
+    p = hils.Params(B=1, Hq=8, Hkv=8 // G, N=3072, L=3072, d=128, topk=16, window=512)
+    host = host_inputs(p, 120)
+    host["q"] = synth.ar1_host((p.B, p.Hq, p.N, p.d), synth.seed_for(120, "q"), "bf16", rho=0.97)
+    dev = to_device(host, p)
+    s = oshape(p)
+    ref = oracle.fwd(s, np32(host["q"]), np32(host["k"]), np32(host["v"]), np32(host["lmk"]))
+    ov = oracle.chunk_overlap(ref["idx"], 16)
+    log(f"[prefill-union] G={G} chunk overlap of 16 adjacent queries: {ov:.3f}")
+    assert ov > 0.7
+    for flags in (hils.HILS_FLAG_UNION_PACKING, 0):
+        p.flags = flags
+        out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"])
+        torch.cuda.synchronize()
+        gidx = idx.cpu().numpy()
+        ndiff = check_selection(p, host, gidx, ref["idx"])
+        r = ref if not ndiff else oracle.fwd(s, np32(host["q"]), np32(host["k"]), np32(host["v"]),
+                                            np32(host["lmk"]), idx=gidx)
+        check_close("out", np32(out), r["out"], p.dtype)
+        check_lse(np32(lse), r["lse"], p.dtype)
+
+
 @pytest.mark.parametrize("name", ["tiny_2k_f32_full_config", "bf16_ragged_multi_tile", "bf16_bias_boosted",
                                   "bf16_route_Hl_eq_Hkv", "f32_route_bias_G2", "bf16_mha_G1", "bf16_G8_d128",
                                   "bf16_topk_exceeds_candidates"])

@@ -143,3 +143,18 @@ def test_lengths_are_clamped_into_N_to_L():
     pos = oracle.decode_positions(s, [0, 2, 3, 1000])
     np.testing.assert_array_equal(pos, [[0, 1, 2], [0, 1, 2], [0, 1, 2], [61, 62, 63]])
     np.testing.assert_array_equal(oracle.decode_positions(s), [[61, 62, 63]] * 4)
+
+
+def test_chunk_overlap_measure():
+    # the overlap ratio of the kernel-design section: identical sets -> 1, disjoint -> 0,
+    # and a hand-computed block: M = 2, K = 3, sets {1, 2, 3} and {2, 3, 7}: union 4,
+    # (6 - 4) / 3 = 2/3
+    same = np.tile(np.array([[1, 2, 3]]), (4, 1))[None, None]
+    assert oracle.chunk_overlap(same, 4) == 1.0
+    disjoint = np.arange(12).reshape(4, 3)[None, None]
+    assert oracle.chunk_overlap(disjoint, 4) == 0.0
+    ex = np.array([[1, 2, 3], [2, 3, 7]])[None, None]
+    assert abs(oracle.chunk_overlap(ex, 2) - 2 / 3) < 1e-12
+    # blocks with padded (-1) entries are skipped
+    pad = np.array([[1, 2, -1], [1, 2, 3]])[None, None]
+    assert np.isnan(oracle.chunk_overlap(pad, 2))

@@ -607,6 +607,8 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     // union of the tile's selections (UNION only)
     extern __shared__ int s_dyn[];
     __shared__ int s_nu;
+    __shared__ __align__(16) bf16 s_lm[UNION ? 2 : 1][UNION ? G * D : 8];  // the chunk's landmark rows
+    __shared__ float s_lb[UNION ? 2 : 1][UNION ? G : 1];                  // and biases
     const int nC = a.L / kChunk, nwords = (nC + 31) / 32;
     int* s_bits = s_dyn;
     int* s_idx = s_bits + nwords;              // [QT][K] the rows' valid entries, then INT_MAX
@@ -774,15 +776,43 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
         }
         const int* myidx = s_idx + (qb * 16 + lane % 16) * a.K;
         int ptr = 0;
+        // two chunks in flight: chunk u + 1 waits in registers (nx) while chunk u + 2
+        // is being fetched (nx2) and chunk u is computed from LDS; the chunk's G
+        // landmark rows and biases travel with its K/V (threads < G * D / 8)
+        const bool lm_thread = tid < G * D / 8;
+        const int lm_h = tid / (D / 8), lm_d8 = (tid % (D / 8)) * 8;
+        const int lm_hl = (a.Hl == a.Hq) ? g * G + min(lm_h, G - 1) : g;
+        const bf16* lm_base = as<bf16>(a.lmk) + ((size_t)b * a.Hl + lm_hl) * nC * D + lm_d8;
+        auto fetch_lm = [&](int cc) { return lm_thread ? *reinterpret_cast<const uint4*>(lm_base + (size_t)cc * D) : make_uint4(0, 0, 0, 0); };
+        auto fetch_lb = [&](int cc) { return (lm_thread && lm_d8 == 0 && a.bias) ? a.bias[((size_t)b * a.Hl + lm_hl) * nC + cc] : 0.f; };
+        auto stage_lm = [&](int bb, uint4 x, float bv) {
+            if (lm_thread) {
+                *reinterpret_cast<uint4*>(&s_lm[bb][lm_h * D + lm_d8]) = x;
+                if (lm_d8 == 0) s_lb[bb][lm_h] = bv;
+            }
+        };
+        KV nx2;
+        uint4 lx = make_uint4(0, 0, 0, 0), lx2 = lx;
+        float bx = 0.f, bx2 = 0.f;
         if (U > 0) {
             nx = fetch(s_list[0] * kChunk);
             stage(0, nx);
+            stage_lm(0, fetch_lm(s_list[0]), fetch_lb(s_list[0]));
+            if (U > 1) {
+                nx = fetch(s_list[1] * kChunk);
+                lx = fetch_lm(s_list[1]);
+                bx = fetch_lb(s_list[1]);
+            }
         }
         __syncthreads();
         buf = 0;
         for (int u = 0; u < U; ++u, buf ^= 1) {
             const bool more = u + 1 < U;
-            if (more) nx = fetch(s_list[u + 1] * kChunk);
+            if (u + 2 < U) {
+                nx2 = fetch(s_list[u + 2] * kChunk);
+                lx2 = fetch_lm(s_list[u + 2]);
+                bx2 = fetch_lb(s_list[u + 2]);
+            }
             const int c = s_list[u];
             const bool sel = nq_raw < a.N && myidx[min(ptr, a.K - 1)] == c && ptr < a.K;
             ptr += sel ? 1 : 0;
@@ -793,11 +823,11 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
                 f32x4 sh4 = zero4();
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    const bf16x8 lrow = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + lg * 8);
+                    const bf16x8 lrow = ld_bf16x8(&s_lm[buf][hh * D + ks * 32 + lg * 8]);
                     const bf16x8 aL = (lane % 16 == 0) ? lrow : as_bf16x8(make_uint4(0, 0, 0, 0));
                     sh4 = mfma16x16x32(aL, ROUTE ? bqr[ks] : bq[ks], sh4);
                 }
-                const float shat = a.scale * group0_bcast(sh4[0]) + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f);
+                const float shat = a.scale * group0_bcast(sh4[0]) + s_lb[buf][hh];
                 f32x4 st[4];
 #pragma unroll
                 for (int kb = 0; kb < 4; ++kb) {
@@ -837,7 +867,13 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
                     if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
                 }
             }
-            if (more) stage(buf ^ 1, nx);
+            if (more) {
+                stage(buf ^ 1, nx);
+                stage_lm(buf ^ 1, lx, bx);
+            }
+            nx = nx2;
+            lx = lx2;
+            bx = bx2;
             __syncthreads();
         }
     } else {

@@ -245,7 +245,18 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
     __shared__ __align__(16) KeySmem<D, ROUTE> sm;
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
-    const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    // Workgroups go round-robin over the 8 XCDs.  With nC a multiple of 32 the chunk
+    // order below gives each XCD runs of 4 neighbouring chunks (whose local windows
+    // overlap, so their rows meet in that XCD's L2), the runs spread over the whole
+    // chunk range and dealt to the XCDs in alternating directions (early chunks are
+    // retrieved by more rows: one contiguous range per XCD would load the XCDs
+    // unevenly).
+    int c = blockIdx.x;
+    if (nC % 32 == 0) {
+        const int x = c % 8, blk = c / 32;
+        c = 4 * (blk % 2 ? 7 - x : x) + 32 * blk + (c / 8) % 4;
+    }
+    const int g = blockIdx.y, b = blockIdx.z;
     const size_t bg = (size_t)b * a.Hkv + g;
     const int j0 = c * kChunk;
     const bool per_head_lmk = (a.Hl == a.Hq);

@@ -12,19 +12,21 @@
 //   k_bwd_u        u per (row, head)
 //   inverse index  the rows that retrieved each (b, g, chunk); k_inv_sort puts every
 //                  list in ascending row order so that the sums below have one order
-//   k_bwd_keys     one block per (b, g, chunk c), 64 (row, head) pairs per step: first
-//                  the rows whose local window covers keys of c, then the rows that
-//                  retrieved c.  Phase 1, one 16-pair tile per wave: S^T = K Q^T and
-//                  GV^T = V dO^T on MFMA, the softmax terms, ds; for retrieving rows also
-//                  s^_c (one more MFMA against the landmark rows), the chunk's share of
-//                  dq (K^T ds^T / scale, a bf16 partial of the row's slot) and ds^_c.
-//                  K and V stay in registers as the phase-1 operands.  Phase 2, 32 keys
-//                  x half the head dim per wave: dK and dV as MFMA reductions over the
-//                  step's 64 pairs, and dk' as one more (heads x pairs) product, with
+//   k_bwd_keys     one block of 8 waves per (b, g, chunk c), 64 (row, head) pairs per
+//                  step: first the rows whose local window covers keys of c, then the
+//                  rows that retrieved c.  Phase 1, one 16-pair tile per two waves, each
+//                  against half the chunk's keys (its K and V held in registers as A
+//                  operands): S^T = K Q^T and GV^T = V dO^T on MFMA, the softmax terms
+//                  (for retrieving rows the two halves' max / sum meet in LDS), ds; for
+//                  retrieving rows also s^_c (one more MFMA against the landmark rows)
+//                  and ds^_c.  Phase 2, 16 keys x half the head dim per wave: dK and dV
+//                  as MFMA reductions over the step's 64 pairs, dk' as one more
+//                  (heads x pairs) product, and for retrieving rows the chunk's share
+//                  of dq (K^T ds^T / scale, a bf16 partial of the row's slot), with
 //                  operands read back from row-major LDS tiles by transposing reads
-//                  (ds_read_b64_tr_b16).  The next step's rows are fetched while the
-//                  current step computes.  dk, dv, dk', db' of chunk c
-//                  are written once (no atomics).
+//                  (ds_read_b64_tr_b16).  The q / dO tiles are double-buffered: the
+//                  next step's rows are fetched and staged while the current step
+//                  computes.  dk, dv, dk', db' of chunk c are written once (no atomics).
 //   k_bwd_dq       query-major: dq over the local window (the forward's local tile with
 //                  ds in place of p), plus the row's slot partials and scale ds^ k'.
 #include "hils_device.hpp"
@@ -87,32 +89,6 @@ __device__ __forceinline__ int in_vgpr(int x) {
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// 64 rows of D bf16 (K or V of one chunk) held in registers, and their store
-// into a padded row-major LDS tile.
-template <int D>
-struct Rows {
-    static constexpr int PPT = kChunk * D / 8 / kBlock;
-    uint4 x[PPT];
-};
-template <int D>
-__device__ __forceinline__ Rows<D> load_rows(const bf16* src) {
-    Rows<D> r;
-#pragma unroll
-    for (int u = 0; u < Rows<D>::PPT; ++u) {
-        const int e = threadIdx.x + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
-        r.x[u] = *reinterpret_cast<const uint4*>(src + (size_t)j * D + d8);
-    }
-    return r;
-}
-template <int D>
-__device__ __forceinline__ void store_rows(bf16* tile, const Rows<D>& r) {
-#pragma unroll
-    for (int u = 0; u < Rows<D>::PPT; ++u) {
-        const int e = threadIdx.x + u * kBlock, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
-        *reinterpret_cast<uint4*>(tile + j * BT<D>::KROW + d8) = r.x[u];
-    }
-}
 
 // Operand read from a padded row-major tile: rows r0 + l%16, the 8 consecutive
 // columns k0 + (l/16)*8 ...
@@ -212,36 +188,61 @@ __global__ __launch_bounds__(kBlock) void k_inv_sort(const int* offsets, const i
 // ---------------------------------------------------------------------------
 // Key-major pass: dK, dV, dK', db' of one chunk and the retrieved chunks' dq partials
 // ---------------------------------------------------------------------------
+// One block of 8 waves per (b, g, chunk c), two waves per SIMD.  A step takes 64
+// (row, head) pairs, four tiles of 16.  Phase 1: wave w holds K and V of the key
+// half 32 (w % 2) ... of the chunk in registers and works on pair tile w / 2, so
+// that the two waves of a tile share its softmax terms through LDS (retrieved
+// chunks: the max, sum and sum of p gv over each half).  Phase 2: wave w owns keys
+// 16 (w % 4) ... x head-dim half w / 2 / 2 of dK and dV, head-dim block w of dK'
+// and, for retrieving rows, head-dim half w % 2 of pair tile w / 2's dq partial.
+constexpr int kKeyWaves = 8;
+constexpr int kKeyThreads = kKeyWaves * kWave;
+
+// Tiles k, q, g, qr, p, ds are staggered (st_off), rows of D or 64 bf16.
 template <int D, bool ROUTE>
 struct KeySmem {
-    static constexpr int KROW = BT<D>::KROW, PROW = BT<D>::PROW, HROW = BT<D>::HROW;
-    bf16 k[kChunk * KROW];                  // K of the chunk, row-major (K^T operands of dq)
-    bf16 q[kPairs * KROW];                  // q of the step's pairs, row-major [pair][d]
-    bf16 g[kPairs * KROW];                  // dO
-    bf16 qr[ROUTE ? kPairs * KROW : 8];     // q^ (routing queries given)
-    bf16 p[kPairs * PROW];                  // dV weights [pair][key]
-    bf16 ds[kPairs * PROW];                 // ds [pair][key]
-    bf16 h[kPairs * HROW];                  // ds^_c in the columns of the pair's landmark head
+    static constexpr int KROW = BT<D>::KROW, TD = st_size<D>(64), TP = st_size<kChunk>(kPairs);
+    bf16 k[TD];                       // K of the chunk [key][d] (K^T operands of dq)
+    bf16 q[2][TD];                    // q of a step's pairs [pair][d], two steps in flight
+    bf16 g[2][TD];                    // dO
+    bf16 qr[ROUTE ? 2 : 1][ROUTE ? TD : 8];  // q^ (routing queries given)
+    bf16 p[TP];                       // dV weights [pair][key]
+    bf16 ds[TP];                      // ds [pair][key]
+    bf16 h[kPairs * 16];                             // ds^_c in the columns of the pair's landmark head
+    bf16 lm[8 * KROW];                               // landmark rows of the group's heads (or its one)
+    float red[2][kPairs][3];                            // per key half: max, sum, sum of p gv of each pair
     float db[4][16];
 };
 
-// The per-pair operands of one step: row entry (n << 6 | slot, or -1), q, dO, q^,
-// L * log2(e) (+inf for an empty pair, which zeroes all its weights) and u.
+// What a wave fetches for its pair tile's next step: q (key half 0) or dO (key
+// half 1) rows, q^ (key half 0, routing queries given), and per pair the row entry
+// (n << 6 | slot, or -1), L * log2(e) (+inf for an empty pair, which zeroes all of
+// its weights) and u.
 template <int KS, bool ROUTE>
 struct PairOps {
-    uint4 q[KS], o[KS], qr[ROUTE ? KS : 1];
+    bf16x8 x[KS], y[ROUTE ? KS : 1];
     float L2, u;
     int ent;
 };
 
+// Head-dim half `half` (blocks half * D/32 ...) of a lane-order vector.
+template <int D>
+__device__ __forceinline__ void store_lane_order_half(bf16* row, const f32x4* o, int lg, int half) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int t = 0; t < D / 64; ++t) {
+        const u32x4 v = {pack_bf16x2(o[2 * t][0], o[2 * t][1]), pack_bf16x2(o[2 * t][2], o[2 * t][3]),
+                         pack_bf16x2(o[2 * t + 1][0], o[2 * t + 1][1]), pack_bf16x2(o[2 * t + 1][2], o[2 * t + 1][3])};
+        *reinterpret_cast<u32x4*>(row + 32 * (half * (D / 64) + t) + 8 * lg) = v;
+    }
+}
+
 template <int D, int G, bool ROUTE>
-__global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offsets, const int* sorted, const float* u,
-                                                     bf16* dqp, float* dshat) {
-    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW, PROW = BT<D>::PROW, HROW = BT<D>::HROW;
-    constexpr int R = kPairs / G;              // rows per step
-    constexpr int HT = G > 4 ? G / 4 : 1;      // heads in one wave's 16-pair tile
-    constexpr int DH = DB / 2;                 // phase 2: head-dim blocks per wave
-    constexpr int DBW = DB / 4;                // dk' head-dim blocks per wave
+__global__ __launch_bounds__(kKeyThreads) void k_bwd_keys(BwdArgs a, const int* offsets, const int* sorted,
+                                                          const float* u, bf16* dqp, float* dshat) {
+    constexpr int KS = BT<D>::KS, DB = BT<D>::DB, KROW = BT<D>::KROW;
+    constexpr int R = kPairs / G;  // rows per step
+    constexpr int DH = DB / 2;     // phase 2: head-dim blocks per wave
     __shared__ __align__(16) KeySmem<D, ROUTE> sm;
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
@@ -260,64 +261,60 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
     const size_t bg = (size_t)b * a.Hkv + g;
     const int j0 = c * kChunk;
     const bool per_head_lmk = (a.Hl == a.Hq);
+    const int nLH = per_head_lmk ? G : 1;
     const bf16* qb = as<bf16>(a.q);
     const bf16* gob = as<bf16>(a.dout);
     const bf16* rb = as<bf16>(a.q_route);
     const float c1 = a.scale * kLog2e;
+    const int kh = w % 2, pt = w / 2;   // phase 1: key half, pair tile
+    const int kb2 = w % 4, dh = w / 4;  // phase 2: 16-key block, head-dim half of dK / dV
 
-    // K and V of the chunk as phase-1 A operands, in registers for the whole block
-    // (lane: key kb*16 + l%16, dims ks*32 + (l/16)*8 ...); wave w also stores key block w
-    // of K into LDS for the K^T operands of the dq partials
-    bf16x8 kA[4][KS], vA[4][KS];
+    // K and V of the key half as phase-1 A operands (lane: key 32 kh + 16 kb + l%16,
+    // dims 32 ks + (l/16)*8 ...); waves of pair tiles 0 and 1 also store their first
+    // or second 16 keys into LDS for the K^T operands of the dq partials
+    bf16x8 kA[2][KS], vA[2][KS];
     {
         const bf16* kb0 = as<bf16>(a.k) + (bg * a.L + j0) * D;
         const bf16* vb0 = as<bf16>(a.v) + (bg * a.L + j0) * D;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const size_t off = (size_t)(kb * 16 + lane % 16) * D + ks * 32 + lg * 8;
+                const size_t off = (size_t)(32 * kh + kb * 16 + lane % 16) * D + ks * 32 + lg * 8;
                 kA[kb][ks] = ld_bf16x8(kb0 + off);
                 vA[kb][ks] = ld_bf16x8(vb0 + off);
             }
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-            if (kb == w)
+        for (int kb = 0; kb < 2; ++kb)
+            if (kb == pt)
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks)
-                    *reinterpret_cast<bf16x8*>(sm.k + (kb * 16 + lane % 16) * KROW + ks * 32 + lg * 8) = kA[kb][ks];
+                    *reinterpret_cast<bf16x8*>(sm.k + st_off<D>(32 * kh + kb * 16 + lane % 16, ks * 32 + lg * 8)) =
+                        kA[kb][ks];
+        for (int e = tid; e < nLH * (D / 8); e += kKeyThreads) {
+            const int m = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            const int hlm = per_head_lmk ? g * G + m : g;
+            *reinterpret_cast<uint4*>(sm.lm + m * KROW + d8) =
+                *reinterpret_cast<const uint4*>(as<bf16>(a.lmk) + (((size_t)b * a.Hl + hlm) * nC + c) * D + d8);
+        }
     }
 
     // this lane's pair in phase 1
-    const int pair = w * 16 + lane % 16;
+    const int pair = pt * 16 + lane % 16;
     const int hh = pair / R, r = pair % R;
     const int h = g * G + hh;
-    const int hfirst = (w * 16) / R;
+    const int hfirst = (pt * 16) / R;
     const int hl = per_head_lmk ? h : g;
-    // landmark rows as the A operand of s^: row m = head hfirst + m of the tile (per-head
-    // landmarks) or the group's one landmark (m = 0)
-    bf16x8 aL[KS];
-    {
-        const int m = lane % 16;
-        const bool has = per_head_lmk ? m < HT : m == 0;
-        const int hlm = per_head_lmk ? g * G + hfirst + m : g;
-        const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + (has ? hlm : 0)) * nC + c) * D;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            aL[ks] = has ? ld_bf16x8(lrow + ks * 32 + lg * 8) : as_bf16x8(make_uint4(0, 0, 0, 0));
-    }
+    // row of the landmark tile in A-operand row m = l%16 of s^: head hfirst + m of the
+    // tile (per-head landmarks; rows past the group's heads repeat its last one and
+    // are not used) or the group's one landmark
+    const int lrow = per_head_lmk ? min(hfirst + lane % 16, G - 1) : 0;
     const int hloc = per_head_lmk ? hh - hfirst : 0;
     const float bias_h = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
 
-    // phase 2 ownership: keys [32 kh, 32 kh + 32) x head-dim blocks [dh DH, dh DH + DH)
-    const int kh = w % 2, dh = w / 2;
-    f32x4 dk[2][DH], dv[2][DH], dkl[DBW];
+    f32x4 dk[DH], dv[DH], dkl = zero4();
 #pragma unroll
-    for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-        for (int dl = 0; dl < DH; ++dl) dk[kb2][dl] = dv[kb2][dl] = zero4();
-#pragma unroll
-    for (int t = 0; t < DBW; ++t) dkl[t] = zero4();
+    for (int dl = 0; dl < DH; ++dl) dk[dl] = dv[dl] = zero4();
     float dbl = 0.f;
 
     const int n_lo = j0, n_hi = min(a.N - 1, j0 + kChunk + a.W - 2);
@@ -341,94 +338,106 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
         const int ent = loc ? (n_lo + e) << 6 : got;
         return (s < nst && e < lim) ? ent : -1;
     };
-    // An empty pair (ent < 0) reads row 0 and gets L = +inf, so that every weight
-    // and gradient term it produces is exactly zero.
-    auto load_ops = [&](int ent, PairOps<KS, ROUTE>& x) {
+    // An empty pair (ent < 0) reads row 0 and gets L = +inf.
+    const bf16* src = kh ? gob : qb;
+    auto load_ops = [&](int ent) {
+        PairOps<KS, ROUTE> x;
         x.ent = ent;
         const bool ok = ent >= 0;
         const size_t row = ((size_t)b * a.Hq + h) * a.N + (ok ? (ent >> 6) : 0);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             const int d0 = ks * 32 + lg * 8;
-            x.q[ks] = *reinterpret_cast<const uint4*>(qb + row * D + d0);
-            x.o[ks] = *reinterpret_cast<const uint4*>(gob + row * D + d0);
-            if constexpr (ROUTE) x.qr[ks] = *reinterpret_cast<const uint4*>(rb + row * D + d0);
+            x.x[ks] = ld_bf16x8(src + row * D + d0);
+            if constexpr (ROUTE) x.y[ks] = ld_bf16x8(rb + row * D + d0);
         }
         const float L = a.lse[row];
         x.L2 = ok ? L * kLog2e : INFINITY;
         x.u = u[row];
+        return x;
     };
-
-    // one step: compute with `cur` while `nxt` (the following step) and the entry after
-    // it are fetched
-    auto step = [&](int st, const PairOps<KS, ROUTE>& cur, PairOps<KS, ROUTE>& nxt, int& ent_next) {
-        const bool retrieval = st >= nsl;
-        const int ent_after = entry_of(st + 2);
-        load_ops(ent_next, nxt);
-        ent_next = ent_after;
-
-        const bool qv = cur.ent >= 0;
-        const int qn = cur.ent >> 6, slot = cur.ent & 63;
-        const size_t qrow = ((size_t)b * a.Hq + h) * a.N + (qv ? qn : 0);
-        __syncthreads();  // the previous step's tiles are consumed
+    auto stage_ops = [&](int buf, const PairOps<KS, ROUTE>& x) {
+        bf16* dst = kh ? sm.g[buf] : sm.q[buf];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const int d0 = ks * 32 + lg * 8;
-            *reinterpret_cast<uint4*>(sm.q + pair * KROW + d0) = cur.q[ks];
-            *reinterpret_cast<uint4*>(sm.g + pair * KROW + d0) = cur.o[ks];
+            const int o = st_off<D>(pair, ks * 32 + lg * 8);
+            *reinterpret_cast<bf16x8*>(dst + o) = x.x[ks];
             if constexpr (ROUTE)
-                if (retrieval) *reinterpret_cast<uint4*>(sm.qr + pair * KROW + d0) = cur.qr[ks];
+                if (kh == 0) *reinterpret_cast<bf16x8*>(sm.qr[buf] + o) = x.y[ks];
         }
+    };
 
-        // ---- phase 1: this wave's 16 pairs against the 64 keys ----
-        f32x4 s4[4], gv4[4];
+    PairOps<KS, ROUTE> nxt = load_ops(entry_of(0));
+    float curL2 = nxt.L2, curU = nxt.u;
+    int curEnt = nxt.ent;
+    stage_ops(0, nxt);
+    nxt = load_ops(entry_of(1));
+    int ent_next = entry_of(2);
+
+    for (int st = 0; st < nst; ++st) {
+        const int buf = st & 1;
+        const bool retrieval = st >= nsl;
+        const bool qv = curEnt >= 0;
+        const int qn = curEnt >> 6, slot = curEnt & 63;
+        __syncthreads();  // step st's tiles are staged; step st - 1's phase 2 is done
+
+        // ---- phase 1: pair tile pt against the 32 keys of half kh ----
+        bf16x8 bq[KS], bo[KS];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
+        for (int ks = 0; ks < KS; ++ks) {
+            bq[ks] = row_operand_st<D>(sm.q[buf], pt * 16, ks * 32, lane);
+            bo[ks] = row_operand_st<D>(sm.g[buf], pt * 16, ks * 32, lane);
+        }
+        f32x4 s4[2], gv4[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
             s4[kb] = zero4();
             gv4[kb] = zero4();
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                s4[kb] = mfma16x16x32(kA[kb][ks], as_bf16x8(cur.q[ks]), s4[kb]);
-                gv4[kb] = mfma16x16x32(vA[kb][ks], as_bf16x8(cur.o[ks]), gv4[kb]);
+                s4[kb] = mfma16x16x32(kA[kb][ks], bq[ks], s4[kb]);
+                gv4[kb] = mfma16x16x32(vA[kb][ks], bo[ks], gv4[kb]);
             }
         }
-        float pw[4][4], ds[4][4];
+        float pw[2][4], ds[2][4];
         if (!retrieval) {
             // rows of the step below j0 + 63 see only part of the chunk (j <= n)
             const bool diag = st * R < kChunk - 1;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    float x = fmaf(s4[kb][i], c1, -cur.L2);
-                    if (diag && j0 + kb * 16 + lg * 4 + i > qn) x = -INFINITY;
+                    float x = fmaf(s4[kb][i], c1, -curL2);
+                    if (diag && j0 + 32 * kh + kb * 16 + lg * 4 + i > qn) x = -INFINITY;
                     const float wgt = fexp2(x);
                     pw[kb][i] = wgt;
-                    ds[kb][i] = wgt * (gv4[kb][i] - cur.u);
+                    ds[kb][i] = wgt * (gv4[kb][i] - curU);
                 }
         } else {
             // s^_c of the pair: landmark rows (A) against the pair's q^ (B)
             f32x4 sh4 = zero4();
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 al = ld_bf16x8(sm.lm + lrow * KROW + ks * 32 + lg * 8);
                 if constexpr (ROUTE)
-                    sh4 = mfma16x16x32(aL[ks], as_bf16x8(cur.qr[ks]), sh4);
+                    sh4 = mfma16x16x32(al, row_operand_st<D>(sm.qr[buf], pt * 16, ks * 32, lane), sh4);
                 else
-                    sh4 = mfma16x16x32(aL[ks], as_bf16x8(cur.q[ks]), sh4);
+                    sh4 = mfma16x16x32(al, bq[ks], sh4);
             }
             float mine = sh4[0];
 #pragma unroll
             for (int i = 1; i < 4; ++i)
                 if (hloc == i) mine = sh4[i];
             const float shat = a.scale * group0_bcast(mine) + bias_h;
+            // softmax terms over this half's 32 keys
             float mx = -INFINITY;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb) mx = fmaxf(mx, fmaxf(fmaxf(s4[kb][0], s4[kb][1]), fmaxf(s4[kb][2], s4[kb][3])));
+            for (int kb = 0; kb < 2; ++kb) mx = fmaxf(mx, fmaxf(fmaxf(s4[kb][0], s4[kb][1]), fmaxf(s4[kb][2], s4[kb][3])));
             mx = group4_max(mx);
             const float m2 = mx * c1;
             float sum = 0.f, ue = 0.f;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const float e = fexp2(fmaf(s4[kb][i], c1, -m2));
@@ -438,138 +447,144 @@ __global__ __launch_bounds__(kBlock) void k_bwd_keys(BwdArgs a, const int* offse
                 }
             sum = group4_sum(sum);
             ue = group4_sum(ue);
-            const float inv = 1.f / sum;
-            const float uc = ue * inv;
-            const float al = qv ? fexp2(fmaf(shat, kLog2e, -cur.L2)) : 0.f;
-            const float f = al * inv;
+            if (lg == 0) {
+                sm.red[kh][pair][0] = mx;
+                sm.red[kh][pair][1] = sum;
+                sm.red[kh][pair][2] = ue;
+            }
+            __syncthreads();
+            // both halves, combined in the same order by the two waves of the tile
+            const float mo = sm.red[kh ^ 1][pair][0], so = sm.red[kh ^ 1][pair][1], uo = sm.red[kh ^ 1][pair][2];
+            const float m0 = kh ? mo : mx, m1 = kh ? mx : mo;
+            const float s0 = kh ? so : sum, s1 = kh ? sum : so;
+            const float u0 = kh ? uo : ue, u1 = kh ? ue : uo;
+            const float M = fmaxf(m0, m1);
+            const float f0 = fexp2((m0 - M) * c1), f1 = fexp2((m1 - M) * c1);
+            const float tot = s0 * f0 + s1 * f1;
+            const float inv = 1.f / tot;
+            const float uc = (u0 * f0 + u1 * f1) * inv;
+            const float al = qv ? fexp2(fmaf(shat, kLog2e, -curL2)) : 0.f;
+            const float f = al * inv * (kh ? f1 : f0);
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     pw[kb][i] *= f;
                     ds[kb][i] = pw[kb][i] * (gv4[kb][i] - uc);
                 }
-            const float dsh = al * (uc - cur.u);
-            if (qv && lane < 16) dshat[slot_offset(bg, a.N, qn, a.K, slot, G, hh, 1)] = dsh;
-            // H row of the pair: ds^ split into a bf16 head and its bf16 residual, in
-            // columns m and 8 + m of its landmark head m (the product then keeps ds^ to
-            // about fp32 accuracy)
-            if (lane < 16) {
-                const int col = per_head_lmk ? hh : 0;
-                const float hi = to_f32(from_f32<bf16>(dsh)), lo = dsh - hi;
-                float hv[16];
+            const float dsh = al * (uc - curU);
+            if (kh == 0) {
+                if (qv && lane < 16) dshat[slot_offset(bg, a.N, qn, a.K, slot, G, hh, 1)] = dsh;
+                // H row of the pair: ds^ split into a bf16 head and its bf16 residual, in
+                // columns m and 8 + m of its landmark head m (the product then keeps ds^
+                // to about fp32 accuracy)
+                if (lane < 16) {
+                    const int col = per_head_lmk ? hh : 0;
+                    const float hi = to_f32(from_f32<bf16>(dsh)), lo = dsh - hi;
+                    float hv[16];
 #pragma unroll
-                for (int t = 0; t < 16; ++t) hv[t] = t == col ? hi : (t == col + 8 ? lo : 0.f);
-                uint32_t wds[8];
+                    for (int t = 0; t < 16; ++t) hv[t] = t == col ? hi : (t == col + 8 ? lo : 0.f);
+                    uint32_t wds[8];
 #pragma unroll
-                for (int t = 0; t < 8; ++t) wds[t] = pack_bf16x2(hv[2 * t], hv[2 * t + 1]);
-                *reinterpret_cast<uint4*>(sm.h + pair * HROW) = make_uint4(wds[0], wds[1], wds[2], wds[3]);
-                *reinterpret_cast<uint4*>(sm.h + pair * HROW + 8) = make_uint4(wds[4], wds[5], wds[6], wds[7]);
+                    for (int t = 0; t < 8; ++t) wds[t] = pack_bf16x2(hv[2 * t], hv[2 * t + 1]);
+                    *reinterpret_cast<uint4*>(sm.h + pair * 16) = make_uint4(wds[0], wds[1], wds[2], wds[3]);
+                    *reinterpret_cast<uint4*>(sm.h + pair * 16 + 8) = make_uint4(wds[4], wds[5], wds[6], wds[7]);
+                }
+                // db': sum ds^ over the pairs of each head of the tile
+                const float hs = (R >= 16) ? group_sum<16>(dsh) : group_sum<8>(dsh);
+                if (lane < 16 && (lane % (R >= 16 ? 16 : 8)) == 0) dbl += hs;
             }
-            // db': sum ds^ over the pairs of each head of the tile
-            const float hs = (R >= 16) ? group_sum<16>(dsh) : group_sum<8>(dsh);
-            if (lane < 16 && (lane % (R >= 16 ? 16 : 8)) == 0) dbl += hs;
         }
         // dV weights and ds, row-major [pair][key]
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            const int key = kb * 16 + lg * 4;
-            *reinterpret_cast<uint2*>(sm.p + pair * PROW + key) =
+        for (int kb = 0; kb < 2; ++kb) {
+            const int key = 32 * kh + kb * 16 + lg * 4;
+            *reinterpret_cast<uint2*>(sm.p + st_off<kChunk>(pair, key)) =
                 make_uint2(pack_bf16x2(pw[kb][0], pw[kb][1]), pack_bf16x2(pw[kb][2], pw[kb][3]));
-            *reinterpret_cast<uint2*>(sm.ds + pair * PROW + key) =
+            *reinterpret_cast<uint2*>(sm.ds + st_off<kChunk>(pair, key)) =
                 make_uint2(pack_bf16x2(ds[kb][0], ds[kb][1]), pack_bf16x2(ds[kb][2], ds[kb][3]));
         }
-        if (retrieval) {
-            // the chunk's share of dq / scale: K^T ds^T, into the row's slot partial
-            const bf16x8 b0 = pack_perm(ds[0], ds[1]);
-            const bf16x8 b1 = pack_perm(ds[2], ds[3]);
-            f32x4 od[DB];
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                od[db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 0, db * 16, lane), b0, zero4());
-                od[db] = mfma16x16x32(tr_operand_perm(sm.k, KROW, 32, db * 16, lane), b1, od[db]);
-            }
-            if (qv) store_lane_order<D>(dqp + slot_offset(bg, a.N, qn, a.K, slot, G, hh, D), od, lg);
-        }
+        // stage step st + 1 into the other buffers (read last by step st - 1's phase 2)
+        // and fetch step st + 2
+        const float nL2 = nxt.L2, nU = nxt.u;
+        const int nEnt = nxt.ent;
+        if (st + 1 < nst) stage_ops(buf ^ 1, nxt);
+        const int ent_after = entry_of(st + 3);
+        nxt = load_ops(ent_next);
+        ent_next = ent_after;
         __syncthreads();
-        // ---- phase 2: keys [32kh, 32kh + 32) x head-dim blocks of dh, over the 64 pairs ----
-        bf16x8 ads[2][2], ap[2][2], ah[2];
+
+        // ---- phase 2: keys 16 kb2 ... x head-dim half dh, over the 64 pairs ----
+        bf16x8 ads[2], ap[2];
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                ads[kb2][t] = tr_operand(sm.ds, PROW, t * 32, (2 * kh + kb2) * 16, lane);
-                ap[kb2][t] = tr_operand(sm.p, PROW, t * 32, (2 * kh + kb2) * 16, lane);
-            }
-        if (retrieval)
-#pragma unroll
-            for (int t = 0; t < 2; ++t) ah[t] = tr_operand(sm.h, HROW, t * 32, 0, lane);
+        for (int t = 0; t < 2; ++t) {
+            ads[t] = tr_operand_st<kChunk>(sm.ds, t * 32, kb2 * 16, lane);
+            ap[t] = tr_operand_st<kChunk>(sm.p, t * 32, kb2 * 16, lane);
+        }
 #pragma unroll
         for (int dl = 0; dl < DH; ++dl) {
             const int db = dh * DH + dl;
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                const bf16x8 bq = tr_operand(sm.q, KROW, t * 32, db * 16, lane);
-                const bf16x8 bgo = tr_operand(sm.g, KROW, t * 32, db * 16, lane);
-#pragma unroll
-                for (int kb2 = 0; kb2 < 2; ++kb2) {
-                    dk[kb2][dl] = mfma16x16x32(ads[kb2][t], bq, dk[kb2][dl]);
-                    dv[kb2][dl] = mfma16x16x32(ap[kb2][t], bgo, dv[kb2][dl]);
-                }
-                if (retrieval && dl / DBW == kh) {
-                    if constexpr (ROUTE)
-                        dkl[dl % DBW] = mfma16x16x32(ah[t], tr_operand(sm.qr, KROW, t * 32, db * 16, lane), dkl[dl % DBW]);
-                    else
-                        dkl[dl % DBW] = mfma16x16x32(ah[t], bq, dkl[dl % DBW]);
-                }
+                dk[dl] = mfma16x16x32(ads[t], tr_operand_st<D>(sm.q[buf], t * 32, db * 16, lane), dk[dl]);
+                dv[dl] = mfma16x16x32(ap[t], tr_operand_st<D>(sm.g[buf], t * 32, db * 16, lane), dv[dl]);
             }
         }
-    };
-
-    PairOps<KS, ROUTE> opa, opb;
-    load_ops(entry_of(0), opa);
-    int ent_next = entry_of(1);
-    for (int st = 0; st < nst; st += 2) {
-        step(st, opa, opb, ent_next);
-        if (st + 1 < nst) step(st + 1, opb, opa, ent_next);
+        if (retrieval) {
+            // dk': the H tile against q^ (or q), head-dim block w
+            if (w < DB)
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    dkl = mfma16x16x32(tr_operand(sm.h, 16, t * 32, 0, lane),
+                                       tr_operand_st<D>(ROUTE ? sm.qr[buf] : sm.q[buf], t * 32, w * 16, lane), dkl);
+            // the chunk's share of dq / scale for pair tile pt, head-dim half kh: K^T ds^T
+            const bf16x8 b0 = row_operand_st<kChunk>(sm.ds, pt * 16, 0, lane);
+            const bf16x8 b1 = row_operand_st<kChunk>(sm.ds, pt * 16, 32, lane);
+            f32x4 od[DB / 2];
+#pragma unroll
+            for (int dl = 0; dl < DB / 2; ++dl) {
+                const int db = kh * (DB / 2) + dl;
+                od[dl] = mfma16x16x32(tr_operand_st<D>(sm.k, 0, db * 16, lane), b0, zero4());
+                od[dl] = mfma16x16x32(tr_operand_st<D>(sm.k, 32, db * 16, lane), b1, od[dl]);
+            }
+            if (qv) store_lane_order_half<D>(dqp + slot_offset(bg, a.N, qn, a.K, slot, G, hh, D), od, lg, kh);
+        }
+        curL2 = nL2;
+        curU = nU;
+        curEnt = nEnt;
     }
 
-    // ---- dK, dV of the chunk (lane: key 16(2kh + kb2) + (l/16)*4 + i, dim 16 db + l%16) ----
+    // ---- dK, dV of the chunk (lane: key 16 kb2 + (l/16)*4 + i, dim 16 db + l%16) ----
     bf16* dkp = as_mut<bf16>(a.dk) + (bg * a.L + j0) * D;
     bf16* dvp = as_mut<bf16>(a.dv) + (bg * a.L + j0) * D;
 #pragma unroll
-    for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-        for (int dl = 0; dl < DH; ++dl)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key = (2 * kh + kb2) * 16 + lg * 4 + i, d = (dh * DH + dl) * 16 + lane % 16;
-                dkp[key * D + d] = from_f32<bf16>(a.scale * dk[kb2][dl][i]);
-                dvp[key * D + d] = from_f32<bf16>(dv[kb2][dl][i]);
-            }
-    // ---- dK' (lane: rows (l/16)*4 + i = head m and its residual row m + 8 in lane l ^ 32,
-    // dim 16(dh DH + kh DBW + t) + l%16) ----
-    const int nLH = per_head_lmk ? G : 1;
-#pragma unroll
-    for (int t = 0; t < DBW; ++t)
+    for (int dl = 0; dl < DH; ++dl)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float v = dkl[t][i] + __shfl_xor(dkl[t][i], 32, kWave);
-            const int m = lg * 4 + i, d = (dh * DH + kh * DBW + t) * 16 + lane % 16;
-            if (lg < 2 && m < nLH) {
-                const int hl_out = per_head_lmk ? g * G + m : g;
-                as_mut<bf16>(a.dlmk)[(((size_t)b * a.Hl + hl_out) * nC + c) * D + d] = from_f32<bf16>(a.scale * v);
-            }
+            const int key = kb2 * 16 + lg * 4 + i, d = (dh * DH + dl) * 16 + lane % 16;
+            dkp[key * D + d] = from_f32<bf16>(a.scale * dk[dl][i]);
+            dvp[key * D + d] = from_f32<bf16>(dv[dl][i]);
         }
-    // ---- db': per-lane head sums of the four waves ----
+    // ---- dK' (lane: rows (l/16)*4 + i = head m and its residual row m + 8 in lane
+    // l ^ 32, dim 16 w + l%16) ----
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float v = dkl[i] + __shfl_xor(dkl[i], 32, kWave);
+        const int m = lg * 4 + i, d = w * 16 + lane % 16;
+        if (w < DB && lg < 2 && m < nLH) {
+            const int hl_out = per_head_lmk ? g * G + m : g;
+            as_mut<bf16>(a.dlmk)[(((size_t)b * a.Hl + hl_out) * nC + c) * D + d] = from_f32<bf16>(a.scale * v);
+        }
+    }
+    // ---- db': per-lane head sums of the pair tiles ----
     if (a.dbias) {
-        if (lane < 16) sm.db[w][lane] = dbl;
+        if (kh == 0 && lane < 16) sm.db[pt][lane] = dbl;
         __syncthreads();
         if (tid < nLH) {
             float v = 0.f;
-            for (int ww = 0; ww < 4; ++ww)
+            for (int tt = 0; tt < 4; ++tt)
                 for (int l = 0; l < 16; ++l)
-                    if (!per_head_lmk || (ww * 16 + l) / R == tid) v += sm.db[ww][l];
+                    if (!per_head_lmk || (tt * 16 + l) / R == tid) v += sm.db[tt][l];
             const int hl_out = per_head_lmk ? g * G + tid : g;
             a.dbias[((size_t)b * a.Hl + hl_out) * nC + c] = v;
         }
@@ -772,10 +787,10 @@ struct BwRun {
         HILS_LAUNCH("k_inv_sort", k_inv_sort, dim3(nC, a.B * a.Hkv), dim3(kBlock), 0, s, offsets,
                     reinterpret_cast<const int*>(ws + ly.inv.list), sorted, a.N, a.K, nC, a.W);
         if (a.q_route)
-            HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, true>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a, offsets,
+            HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, true>), dim3(nC, a.Hkv, a.B), dim3(kKeyThreads), 0, s, a, offsets,
                         (const int*)sorted, (const float*)u, dqp, dsh);
         else
-            HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, false>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a, offsets,
+            HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, false>), dim3(nC, a.Hkv, a.B), dim3(kKeyThreads), 0, s, a, offsets,
                         (const int*)sorted, (const float*)u, dqp, dsh);
         HILS_LAUNCH("k_bwd_dq", (k_bwd_dq<D, G>), dim3((a.N + DqCfg<G>::QT - 1) / DqCfg<G>::QT, a.Hkv, a.B),
                     dim3(DqCfg<G>::NT), 0, s, a, (const float*)u, (const bf16*)dqp, (const float*)dsh);

@@ -68,6 +68,39 @@ __device__ __forceinline__ bf16x8 tr_operand_perm(const E* X, int ld, int k0, in
     return __builtin_bit_cast(bf16x8, c);
 }
 
+// Staggered LDS tiles: rows of W = 64 or 128 bf16 at a stride of W + 16, rows with
+// r % 8 >= 4 shifted by 8 more.  Relative to the 128-byte LDS bank cycle (32 banks
+// of 4 bytes) rows r = 0..7 then start at 16-byte slots 0, 2, 4, 6, 1, 3, 5, 7, so
+// that row-wise 16-byte operand reads (8 lanes = 8 rows per cycle) and transposing
+// reads (16 lanes = 4 rows x 32 bytes per cycle) are both free of bank conflicts,
+// which no uniform row padding gives (+8 suits the first, +16 the second); unlike
+// an XOR swizzle, offsets along a row stay linear, so that the column steps of
+// unrolled loops fold into the instruction offsets.
+template <int W>
+__device__ __forceinline__ int st_off(int r, int c) {
+    return r * (W + 16) + 8 * ((r >> 2) & 1) + c;
+}
+template <int W>
+constexpr int st_size(int rows) {
+    return rows * (W + 16) + 8;
+}
+// row_operand / tr_operand of a staggered tile (tr: k0 a multiple of 8)
+template <int W>
+__device__ __forceinline__ bf16x8 row_operand_st(const bf16* X, int r0, int k0, int lane) {
+    return ld_bf16x8(X + st_off<W>(r0 + lane % 16, k0 + (lane / 16) * 8));
+}
+template <int W>
+__device__ __forceinline__ bf16x8 tr_operand_st(const bf16* X, int k0, int n0, int lane) {
+    const int g = lane / 16, s = lane % 16;
+    // rows k0 + 8g + s/4 have r % 8 < 4; the second read's rows (+4) have r % 8 >= 4
+    const bf16* p = X + (k0 + g * 8 + s / 4) * (W + 16) + n0 + 4 * (s % 4);
+    const v4i16 a = lds_read_tr16(p);
+    const v4i16 b = lds_read_tr16(p + 4 * (W + 16) + 8);
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
 // "Lane order" of a D-vector held as O^T accumulators (DB = D/16 blocks, lane
 // group lg = l/16 holding d = 16 db + 4 lg + i): element d is stored at position
 // 32 (db / 2) + 8 lg + 4 (db % 2) + i.  A lane moves its 32 values as D/32

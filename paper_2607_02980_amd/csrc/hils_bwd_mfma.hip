@@ -400,6 +400,7 @@ __global__ __launch_bounds__(kKeyThreads) void k_bwd_keys(BwdArgs a, const int* 
             }
         }
         float pw[2][4], ds[2][4];
+        float dsh = 0.f;  // ds^_c of the lane's pair (retrieving rows)
         if (!retrieval) {
             // rows of the step below j0 + 63 see only part of the chunk (j <= n)
             const bool diag = st * R < kChunk - 1;
@@ -472,9 +473,9 @@ __global__ __launch_bounds__(kKeyThreads) void k_bwd_keys(BwdArgs a, const int* 
                     pw[kb][i] *= f;
                     ds[kb][i] = pw[kb][i] * (gv4[kb][i] - uc);
                 }
-            const float dsh = al * (uc - curU);
+            dsh = al * (uc - curU);
             if (kh == 0) {
-                if (qv && lane < 16) dshat[slot_offset(bg, a.N, qn, a.K, slot, G, hh, 1)] = dsh;
+                if (ROUTE && qv && lane < 16) dshat[slot_offset(bg, a.N, qn, a.K, slot, G, hh, 1)] = dsh;
                 // H row of the pair: ds^ split into a bf16 head and its bf16 residual, in
                 // columns m and 8 + m of its landmark head m (the product then keeps ds^
                 // to about fp32 accuracy)
@@ -537,14 +538,20 @@ __global__ __launch_bounds__(kKeyThreads) void k_bwd_keys(BwdArgs a, const int* 
                 for (int t = 0; t < 2; ++t)
                     dkl = mfma16x16x32(tr_operand(sm.h, 16, t * 32, 0, lane),
                                        tr_operand_st<D>(ROUTE ? sm.qr[buf] : sm.q[buf], t * 32, w * 16, lane), dkl);
-            // the chunk's share of dq / scale for pair tile pt, head-dim half kh: K^T ds^T
+            // the chunk's share of dq / scale for pair tile pt, head-dim half kh: K^T ds^T,
+            // and without routing queries also ds^_c k'_c (lane: dims 16 db + (l/16)*4 + i)
             const bf16x8 b0 = row_operand_st<kChunk>(sm.ds, pt * 16, 0, lane);
             const bf16x8 b1 = row_operand_st<kChunk>(sm.ds, pt * 16, 32, lane);
             f32x4 od[DB / 2];
 #pragma unroll
             for (int dl = 0; dl < DB / 2; ++dl) {
                 const int db = kh * (DB / 2) + dl;
-                od[dl] = mfma16x16x32(tr_operand_st<D>(sm.k, 0, db * 16, lane), b0, zero4());
+                f32x4 o0 = zero4();
+                if constexpr (!ROUTE) {
+                    const uint2 lw = *reinterpret_cast<const uint2*>(sm.lm + (per_head_lmk ? hh : 0) * KROW + db * 16 + lg * 4);
+                    o0 = f32x4{dsh * bf_lo(lw.x), dsh * bf_hi(lw.x), dsh * bf_lo(lw.y), dsh * bf_hi(lw.y)};
+                }
+                od[dl] = mfma16x16x32(tr_operand_st<D>(sm.k, 0, db * 16, lane), b0, o0);
                 od[dl] = mfma16x16x32(tr_operand_st<D>(sm.k, 32, db * 16, lane), b1, od[dl]);
             }
             if (qv) store_lane_order_half<D>(dqp + slot_offset(bg, a.N, qn, a.K, slot, G, hh, D), od, lg, kh);
@@ -608,11 +615,24 @@ struct DqCfg {
 template <int D>
 struct DqSmem {
     static constexpr int KROW = BT<D>::KROW;
-    bf16 k[2][kChunk * KROW];
+    bf16 k[2][st_size<D>(kChunk)];  // staggered: row-wise and transposing reads
     bf16 v[2][kChunk * KROW];
 };
 
-template <int D, int G>
+// acc (O^T layout) += x * the bf16 row held as lv (dims 16 db + (l/16)*4 ...)
+template <int DB>
+__device__ __forceinline__ void fma_lmk(f32x4* acc, const uint2* lv, float x) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        acc[db][0] += x * bf_lo(lv[db].x);
+        acc[db][1] += x * bf_hi(lv[db].x);
+        acc[db][2] += x * bf_lo(lv[db].y);
+        acc[db][3] += x * bf_hi(lv[db].y);
+    }
+}
+
+// ROUTE: routing queries given, so that scale ds^ k' goes to dq^ instead of dq.
+template <int D, int G, bool ROUTE>
 __global__ __launch_bounds__(DqCfg<G>::NT, 4) void k_bwd_dq(BwdArgs a, const float* u, const bf16* dqp,
                                                            const float* dshat) {
     using C = DqCfg<G>;
@@ -653,7 +673,7 @@ __global__ __launch_bounds__(DqCfg<G>::NT, 4) void k_bwd_dq(BwdArgs a, const flo
 #pragma unroll
         for (int t = 0; t < PPT; ++t) {
             const int e = tid + t * C::NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
-            *reinterpret_cast<uint4*>(&sm.k[buf][j * KROW + d8]) = x.k[t];
+            *reinterpret_cast<uint4*>(&sm.k[buf][st_off<D>(j, d8)]) = x.k[t];
             *reinterpret_cast<uint4*>(&sm.v[buf][j * KROW + d8]) = x.v[t];
         }
     };
@@ -679,93 +699,99 @@ __global__ __launch_bounds__(DqCfg<G>::NT, 4) void k_bwd_dq(BwdArgs a, const flo
         if (more) nx = fetch(j0 + kChunk);
         const bf16* tk = sm.k[buf];
         const bf16* tv = sm.v[buf];
-        f32x4 s4[4], gv4[4];
+        // keys in two halves of 32 (fewer live accumulators); dq takes the halves in order
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            s4[kb] = zero4();
-            gv4[kb] = zero4();
+        for (int hf = 0; hf < 2; ++hf) {
+            f32x4 s4[2], gv4[2];
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                s4[kb] = mfma16x16x32(row_operand<KROW>(tk, kb * 16, ks * 32, lane), bq[ks], s4[kb]);
-                gv4[kb] = mfma16x16x32(row_operand<KROW>(tv, kb * 16, ks * 32, lane), bo[ks], gv4[kb]);
+            for (int k2 = 0; k2 < 2; ++k2) {
+                const int kb = 2 * hf + k2;
+                s4[k2] = zero4();
+                gv4[k2] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    s4[k2] = mfma16x16x32(row_operand_st<D>(tk, kb * 16, ks * 32, lane), bq[ks], s4[k2]);
+                    gv4[k2] = mfma16x16x32(row_operand<KROW>(tv, kb * 16, ks * 32, lane), bo[ks], gv4[k2]);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        float ds[4][4];
+            float ds[2][4];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+            for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int j = j0 + kb * 16 + lg * 4 + i;
-                const bool valid = nq_raw < a.N && j <= nq && j >= ell;
-                const float wgt = valid ? fexp(a.scale * s4[kb][i] - Lr) : 0.f;
-                ds[kb][i] = wgt * (gv4[kb][i] - ub);
+                for (int i = 0; i < 4; ++i) {
+                    const int j = j0 + (2 * hf + k2) * 16 + lg * 4 + i;
+                    const bool valid = nq_raw < a.N && j <= nq && j >= ell;
+                    const float wgt = valid ? fexp(a.scale * s4[k2][i] - Lr) : 0.f;
+                    ds[k2][i] = wgt * (gv4[k2][i] - ub);
+                }
+            const bf16x8 bh = pack_perm(ds[0], ds[1]);
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                dq[db] = mfma16x16x32(tr_operand_perm_st<D>(tk, 32 * hf, db * 16, lane), bh, dq[db]);
+                if (db % 4 == 3) __builtin_amdgcn_sched_barrier(0);
             }
-        const bf16x8 b0 = pack_perm(ds[0], ds[1]);
-        const bf16x8 b1 = pack_perm(ds[2], ds[3]);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-            dq[db] = mfma16x16x32(tr_operand_perm(tk, KROW, 0, db * 16, lane), b0, dq[db]);
-            dq[db] = mfma16x16x32(tr_operand_perm(tk, KROW, 32, db * 16, lane), b1, dq[db]);
-            if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
         }
         if (more) stage(buf ^ 1, nx);
         __syncthreads();
     }
-    // epilogue (lane: row l%16 of the item, dims 16db + (l/16)*4 + {0..3})
+    // epilogue (lane: row l%16 of the item, dims 16db + (l/16)*4 + {0..3}): the row's
+    // slot partials and scale ds^ k', one slot ahead in flight (the slot's chunk id,
+    // which the landmark row's address needs, two ahead)
     if (nq_raw >= a.N) return;  // no barriers below
     const int hl = (a.Hl == a.Hq) ? h : g;
     const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
     const int ncand = n_candidates(nq, a.W);
-    f32x4 accr[DB];
+    f32x4 accr[ROUTE ? DB : 1];
 #pragma unroll
-    for (int db = 0; db < DB; ++db) accr[db] = zero4();
-    // the row's slots, SB at a time with every load in flight before use
-    constexpr int SB = D >= 128 ? 1 : 4;
-    int prev = -1;
-    for (int k0 = 0; k0 < a.K; k0 += SB) {
-        float xk[SB];
-        bool okk[SB];
-        uint4 pv[SB][D / 32];
-        uint2 lv[SB][DB];
-#pragma unroll
-        for (int t = 0; t < SB; ++t) {
-            const int k = min(k0 + t, a.K - 1);
-            const int cc = irow[k];
-            const bool ok = k0 + t < a.K && cc >= 0 && cc < ncand && cc > prev;
-            prev = cc;  // idx_entry_valid compares with the previous entry as written
-            const float xv = dshat[slot_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
-            xk[t] = ok ? a.scale * xv : 0.f;
-            okk[t] = ok;
-            const int ck = ok ? cc : 0;
-            load_lane_order<D>(dqp + slot_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, pv[t]);  // masked by okk if invalid
+    for (int db = 0; db < (ROUTE ? DB : 1); ++db) accr[db] = zero4();
+    // a slot's inputs: the lane-order partial (which, without routing queries, holds
+    // ds^_c k'_c too) and, with routing queries, ds^ and the landmark row k'_c
+    struct SlotIn {
+        uint4 pv[D / 32];
+        uint2 lv[ROUTE ? DB : 1];
+        float x;
+    };
+    auto fetch_slot = [&](int k, int cc) {
+        SlotIn r;
+        load_lane_order<D>(dqp + slot_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, r.pv);
+        if constexpr (ROUTE) {
+            const int ck = (cc >= 0 && cc < ncand) ? cc : 0;
+            r.x = dshat[slot_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
             const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + ck) * D;
 #pragma unroll
-            for (int db = 0; db < DB; ++db) lv[t][db] = *reinterpret_cast<const uint2*>(lrow + db * 16 + lg * 4);
+            for (int db = 0; db < DB; ++db) r.lv[db] = *reinterpret_cast<const uint2*>(lrow + db * 16 + lg * 4);
         }
-#pragma unroll
-        for (int t = 0; t < SB; ++t) {
-            fma_lane_order<D>(pv[t], 1.f, okk[t], dq);
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                accr[db][0] += xk[t] * bf_lo(lv[t][db].x);
-                accr[db][1] += xk[t] * bf_hi(lv[t][db].x);
-                accr[db][2] += xk[t] * bf_lo(lv[t][db].y);
-                accr[db][3] += xk[t] * bf_hi(lv[t][db].y);
-            }
+        return r;
+    };
+    if (a.K > 0) {
+        int c_prev = -1, c_cur = irow[0], c_nxt = irow[min(1, a.K - 1)];
+        SlotIn cur = fetch_slot(0, c_cur);
+        for (int k = 0; k < a.K; ++k) {
+            const int c_after = irow[min(k + 2, a.K - 1)];
+            const SlotIn nx = fetch_slot(min(k + 1, a.K - 1), c_nxt);
+            // idx_entry_valid: a candidate chunk, above the previous entry as written
+            const bool ok = c_cur >= 0 && c_cur < ncand && c_cur > c_prev;
+            fma_lane_order<D>(cur.pv, 1.f, ok, dq);
+            // ds^ unscaled: dq^ is scaled at the end
+            if constexpr (ROUTE) fma_lmk<DB>(accr, cur.lv, ok ? cur.x : 0.f);
+            c_prev = c_cur;
+            c_cur = c_nxt;
+            c_nxt = c_after;
+            cur = nx;
         }
     }
     bf16* dqo = as_mut<bf16>(a.dq) + qrow * D;
-    bf16* dqr = a.dq_route ? as_mut<bf16>(a.dq_route) + qrow * D : nullptr;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
         const int d0 = db * 16 + lg * 4;
-        f32x4 x = dq[db] * a.scale;
-        if (!dqr) x += accr[db];
+        const f32x4 x = dq[db] * a.scale;
         *reinterpret_cast<uint2*>(dqo + d0) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
-        if (dqr)
-            *reinterpret_cast<uint2*>(dqr + d0) = make_uint2(pack_bf16x2(accr[db][0], accr[db][1]),
-                                                             pack_bf16x2(accr[db][2], accr[db][3]));
+        if constexpr (ROUTE) {
+            const f32x4 y = accr[db] * a.scale;
+            *reinterpret_cast<uint2*>(as_mut<bf16>(a.dq_route) + qrow * D + d0) =
+                make_uint2(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]));
+        }
     }
 }
 
@@ -792,8 +818,13 @@ struct BwRun {
         else
             HILS_LAUNCH("k_bwd_keys", (k_bwd_keys<D, G, false>), dim3(nC, a.Hkv, a.B), dim3(kKeyThreads), 0, s, a, offsets,
                         (const int*)sorted, (const float*)u, dqp, dsh);
-        HILS_LAUNCH("k_bwd_dq", (k_bwd_dq<D, G>), dim3((a.N + DqCfg<G>::QT - 1) / DqCfg<G>::QT, a.Hkv, a.B),
-                    dim3(DqCfg<G>::NT), 0, s, a, (const float*)u, (const bf16*)dqp, (const float*)dsh);
+        const dim3 dgrid((a.N + DqCfg<G>::QT - 1) / DqCfg<G>::QT, a.Hkv, a.B);
+        if (a.dq_route)
+            HILS_LAUNCH("k_bwd_dq", (k_bwd_dq<D, G, true>), dgrid, dim3(DqCfg<G>::NT), 0, s, a, (const float*)u,
+                        (const bf16*)dqp, (const float*)dsh);
+        else
+            HILS_LAUNCH("k_bwd_dq", (k_bwd_dq<D, G, false>), dgrid, dim3(DqCfg<G>::NT), 0, s, a, (const float*)u,
+                        (const bf16*)dqp, (const float*)dsh);
         return hipGetLastError();
     }
 };

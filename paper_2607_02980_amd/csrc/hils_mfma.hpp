@@ -84,10 +84,11 @@ template <int W>
 constexpr int st_size(int rows) {
     return rows * (W + 16) + 8;
 }
-// row_operand / tr_operand of a staggered tile (tr: k0 a multiple of 8)
+// row_operand / tr_operand of a staggered tile (r0, k0 multiples of 8: the shift of
+// a row then depends on the lane alone, and the compiler keeps one address per lane)
 template <int W>
 __device__ __forceinline__ bf16x8 row_operand_st(const bf16* X, int r0, int k0, int lane) {
-    return ld_bf16x8(X + st_off<W>(r0 + lane % 16, k0 + (lane / 16) * 8));
+    return ld_bf16x8(X + (r0 + lane % 16) * (W + 16) + 8 * ((lane >> 2) & 1) + k0 + (lane / 16) * 8);
 }
 template <int W>
 __device__ __forceinline__ bf16x8 tr_operand_st(const bf16* X, int k0, int n0, int lane) {
@@ -96,6 +97,18 @@ __device__ __forceinline__ bf16x8 tr_operand_st(const bf16* X, int k0, int n0, i
     const bf16* p = X + (k0 + g * 8 + s / 4) * (W + 16) + n0 + 4 * (s % 4);
     const v4i16 a = lds_read_tr16(p);
     const v4i16 b = lds_read_tr16(p + 4 * (W + 16) + 8);
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+// tr_operand_perm of a staggered tile (k0 a multiple of 8)
+template <int W>
+__device__ __forceinline__ bf16x8 tr_operand_perm_st(const bf16* X, int k0, int n0, int lane) {
+    const int g = lane / 16, s = lane % 16;
+    // rows k0 + 4g + s/4: r % 8 >= 4 for odd g
+    const bf16* p = X + (k0 + g * 4 + s / 4) * (W + 16) + 8 * (g & 1) + n0 + 4 * (s % 4);
+    const v4i16 a = lds_read_tr16(p);
+    const v4i16 b = lds_read_tr16(p + 16 * (W + 16));  // rows + 16: the same r % 8
     typedef short v8i16 __attribute__((ext_vector_type(8)));
     const v8i16 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(bf16x8, v);

@@ -104,22 +104,23 @@ __device__ __forceinline__ bf16x8 pack_perm(const float* e0, const float* e1) {
 }
 
 // ---------------------------------------------------------------------------
-// u = dO . out, one wave per (row, head)
+// u = dO . out: D/8 lanes per (row, head), 16 bytes of each per lane
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_bwd_u(BwdArgs a, float* u) {
+    constexpr int LPR = D / 8;  // lanes per row
     const size_t rows = (size_t)a.B * a.Hq * a.N;
-    const size_t r = (size_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
-    const int lane = threadIdx.x % kWave;
-    if (r >= rows) return;
-    float acc = 0.f;
-    for (int d = lane * 2; d < D; d += 2 * kWave) {
-        const uint32_t go = *reinterpret_cast<const uint32_t*>(as<bf16>(a.dout) + r * D + d);
-        const uint32_t oo = *reinterpret_cast<const uint32_t*>(as<bf16>(a.out) + r * D + d);
-        acc += bf_lo(go) * bf_lo(oo) + bf_hi(go) * bf_hi(oo);
-    }
-    acc = wave_sum(acc);
-    if (lane == 0) u[r] = acc;
+    const size_t r = (size_t)blockIdx.x * (kBlock / LPR) + threadIdx.x / LPR;
+    const int d0 = (threadIdx.x % LPR) * 8;
+    const size_t rr = r < rows ? r : rows - 1;  // every lane reaches the group sum below
+    const uint4 go = *reinterpret_cast<const uint4*>(as<bf16>(a.dout) + rr * D + d0);
+    const uint4 oo = *reinterpret_cast<const uint4*>(as<bf16>(a.out) + rr * D + d0);
+    float acc = bf_lo(go.x) * bf_lo(oo.x) + bf_hi(go.x) * bf_hi(oo.x);
+    acc += bf_lo(go.y) * bf_lo(oo.y) + bf_hi(go.y) * bf_hi(oo.y);
+    acc += bf_lo(go.z) * bf_lo(oo.z) + bf_hi(go.z) * bf_hi(oo.z);
+    acc += bf_lo(go.w) * bf_lo(oo.w) + bf_hi(go.w) * bf_hi(oo.w);
+    acc = group_sum<LPR>(acc);
+    if (r < rows && d0 == 0) u[r] = acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -807,7 +808,8 @@ struct BwRun {
         const int* offsets = reinterpret_cast<const int*>(ws + ly.inv.offsets);
         const int nC = a.L / kChunk;
         const size_t rows = (size_t)a.B * a.Hq * a.N;
-        HILS_LAUNCH("k_bwd_u", (k_bwd_u<D>), dim3((unsigned)((rows + 3) / 4)), dim3(kBlock), 0, s, a, u);
+        constexpr int upb = kBlock / (D / 8);  // rows per k_bwd_u block
+        HILS_LAUNCH("k_bwd_u", (k_bwd_u<D>), dim3((unsigned)((rows + upb - 1) / upb)), dim3(kBlock), 0, s, a, u);
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
         launch_inverse_index(ia, ly.inv, a.ws, s, false);
         HILS_LAUNCH("k_inv_sort", k_inv_sort, dim3(nC, a.B * a.Hkv), dim3(kBlock), 0, s, offsets,

@@ -14,7 +14,10 @@
 //                     KV group (s^_hc for the G heads, max over heads, Eq. (9) /
 //                     App. C) and keeps the slice's top-K (exact wave radix select).
 //                     Small LDS, so many slices stream per CU while others select.
-//   B  k_dec_merge    grid (Hkv, B*N): top-K over the slices' survivors -> idx
+//   B  merge          top-K over the slices' survivors -> idx: for bf16 at the start
+//                     of C, in each workgroup of a row's retrieved chunks (no launch
+//                     and no round trip through idx in between); fp32: k_dec_merge,
+//                     grid (Hkv, B*N)
 //   C  k_dec_parts    grid (K + nlocal, Hkv, B*N)
 //        x <  K     : the intra-chunk softmax of selected chunk x (Eq. (10)) and
 //                     its surrogate score s^_hc
@@ -375,6 +378,64 @@ __device__ void run_part_mfma(const FwdArgs& a, const DecLayout& ly, PartSmemM<D
     }
 }
 
+// ---- B: merge the slices' survivors into the final top-K --------------------
+// By a workgroup of NW waves for row rg.  Per round each wave selects the top-K of
+// its 64*E survivors from registers (all loads in flight together); wave 0 then
+// merges the NW lists with the running best.  E (8 or 16) is chosen so that one
+// round covers all the slices' survivors where it can.  The result, ascending
+// chunk ids, is left in ms.bid[0, ms.nbest).
+template <int NW>
+struct MergeSmem {
+    int wid[NW][64], tid[NW][64], bid[64];
+    float wsc[NW][64], tsc[NW][64], bsc[64];
+    int wn[NW], nbest;
+};
+template <int E, int NW>
+__device__ void merge_row(const FwdArgs& a, const DecLayout& ly, size_t rg, MergeSmem<NW>& ms) {
+    constexpr int NT = NW * kWave;
+    constexpr int E2 = NW + 1;  // NW wave lists + running best, <= 64 each
+    const int wave = wave_id(), lane = threadIdx.x % kWave;
+    const float* cand_sc = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.cand);
+    const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
+    const size_t base = rg * ly.nslices * a.K;
+    const int total = ly.nslices * a.K;
+    int nbest = 0;
+    for (int r0 = 0; r0 < total; r0 += NT * E) {
+        float sc[E];
+        int id[E];
+        bool ok[E];
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const int e = r0 + (wave * E + r) * kWave + lane;
+            id[r] = e < total ? cand_id[base + e] : -1;
+            sc[r] = e < total ? cand_sc[base + e] : 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < E; ++r) ok[r] = id[r] >= 0;
+        const int nw = wave_topk_reg<E>(sc, id, ok, a.K, ms.wid[wave], ms.wsc[wave], ms.tid[wave], ms.tsc[wave]);
+        if (lane == 0) ms.wn[wave] = nw;
+        __syncthreads();
+        if (wave == 0) {
+            float sc2[E2];
+            int id2[E2];
+            bool ok2[E2];
+#pragma unroll
+            for (int r = 0; r < E2; ++r) {
+                const int list = r;  // lane indexes the entry inside list r
+                const int cnt = list < NW ? ms.wn[list] : nbest;
+                ok2[r] = lane < cnt;
+                id2[r] = ok2[r] ? (list < NW ? ms.wid[list][lane] : ms.bid[lane]) : -1;
+                sc2[r] = ok2[r] ? (list < NW ? ms.wsc[list][lane] : ms.bsc[lane]) : 0.f;
+            }
+            __builtin_amdgcn_wave_barrier();
+            nbest = wave_topk_reg<E2>(sc2, id2, ok2, a.K, ms.bid, ms.bsc, ms.tid[0], ms.tsc[0]);
+        }
+        __syncthreads();
+    }
+    if (wave == 0 && lane == 0) ms.nbest = nbest;
+    __syncthreads();
+}
+
 // One part per wavefront (bf16): no block barriers.  S^T = K Q^T for the 64 keys
 // (K rows and q straight from HBM as MFMA operands), the softmax per head over the
 // four lane groups with permlane swaps, and O^T = V^T P^T with V^T from the
@@ -491,33 +552,44 @@ __device__ void run_part_wave(const FwdArgs& a, const DecLayout& ly, bf16* sv, i
     }
 }
 
-// bf16 parts: four parts per block, one per wave.
-template <int D, int G>
+// bf16, few rows: four parts per block, one per wave, the fusion a pass of its own.
+// E > 0: the workgroups of a row's retrieved chunks first merge the scan's
+// survivors themselves (the same result in each; the first writes the row of
+// idx), so that no launch and no round trip through idx separate the selection
+// from the gathers; E = 0: idx given.
+template <int D, int G, int E>
 __global__ __launch_bounds__(kBlock) void k_dec_parts_w(FwdArgs a) {
-    __shared__ __align__(16) PartWaveSmem<D> sm[kBlock / kWave];
+    constexpr int NW = kBlock / kWave;
+    __shared__ __align__(16) PartWaveSmem<D> sm[NW];
+    __shared__ MergeSmem<NW> ms;
     const int w = wave_id();
-    const int part = blockIdx.x * (kBlock / kWave) + w, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
+    const int part = blockIdx.x * NW + w, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
     const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
-    if (part >= ly.nparts) return;  // whole wave; no block barriers in this kernel
     const int pos = decode_position(a, b, n);
     const int lane = threadIdx.x % kWave;
-    if (part >= a.K) {
-        const int c = n_candidates(pos, a.W) + (part - a.K);
-        if (c > pos / kChunk) {
-            if (lane < G) {
-                float* r = part_record<D>(a, ly, rg, part, lane, G);
-                r[0] = -INFINITY;
-                r[1] = 0.f;
-                r[2] = -INFINITY;
-            }
-            return;
+    int csel = -1;  // this wave's chunk if part < K
+    if constexpr (E > 0) {
+        if ((int)blockIdx.x * NW < a.K) {  // uniform over the workgroup
+            merge_row<E, NW>(a, ly, rg, ms);
+            const int nb = ms.nbest;
+            if (blockIdx.x == 0)
+                for (int t = threadIdx.x; t < a.K; t += kBlock) a.idx[rg * a.K + t] = t < nb ? ms.bid[t] : -1;
+            if (part < a.K) csel = part < nb ? ms.bid[part] : -1;
         }
-        run_part_wave<D, G>(a, ly, sm[w].v, b, n, g, rg, part, c, min(kChunk, pos - c * kChunk + 1), false);
-        return;
+    } else {
+        if (part < a.K) {
+            const int32_t* irow = a.idx + rg * a.K;
+            csel = idx_entry_valid(irow, part, n_candidates(pos, a.W)) ? irow[part] : -1;
+        }
     }
-    const int32_t* irow = a.idx + rg * a.K;
-    const int c = __builtin_amdgcn_readfirstlane(idx_entry_valid(irow, part, n_candidates(pos, a.W)) ? irow[part] : -1);
+    if (part >= ly.nparts) return;  // whole wave; no block barriers below
+    int c = __builtin_amdgcn_readfirstlane(csel), nk = kChunk;
+    if (part >= a.K) {
+        c = n_candidates(pos, a.W) + (part - a.K);
+        nk = min(kChunk, pos - c * kChunk + 1);
+        if (c > pos / kChunk) c = -1;
+    }
     if (c < 0) {
         if (lane < G) {
             float* r = part_record<D>(a, ly, rg, part, lane, G);
@@ -527,7 +599,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_parts_w(FwdArgs a) {
         }
         return;
     }
-    run_part_wave<D, G>(a, ly, sm[w].v, b, n, g, rg, part, c, kChunk, true);
+    run_part_wave<D, G>(a, ly, sm[w].v, b, n, g, rg, part, c, nk, part < a.K);
 }
 
 template <int D>
@@ -700,63 +772,15 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
     }
 }
 
-// ---- B: merge the slices' survivors into the final top-K --------------------
-// One 256-thread block per (b, g).  Per round each wave selects the top-K of
-// its 64*kMergeE survivors from registers (all loads in flight together);
-// wave 0 then merges the four lists with the running best.
-constexpr int kMergeE = 8;
-template <int G, int D>
-__global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a) {
-    constexpr int NW = kBlock / kWave;
-    constexpr int E2 = (NW + 1) * 64 / kWave;  // 4 wave lists + running best, <= 64 each
-    __shared__ int s_wid[NW][64], s_tid[NW][64], s_bid[64];
-    __shared__ float s_wsc[NW][64], s_tsc[NW][64], s_bsc[64];
-    __shared__ int s_wn[NW];
+// fp32 path: the merge as its own pass (one workgroup per row) before k_dec_parts.
+template <int E>
+__global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a, int G, int D) {
+    __shared__ MergeSmem<kBlock / kWave> ms;
     const int b = blockIdx.y / a.N, n = blockIdx.y % a.N, g = blockIdx.x;
-    const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
     const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
-    const float* cand_sc = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.cand);
-    const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
-    const size_t base = rg * ly.nslices * a.K;
-    const int total = ly.nslices * a.K;
-    int nbest = 0;
-    for (int r0 = 0; r0 < total; r0 += kBlock * kMergeE) {
-        float sc[kMergeE];
-        int id[kMergeE];
-        bool ok[kMergeE];
-#pragma unroll
-        for (int r = 0; r < kMergeE; ++r) {
-            const int e = r0 + (wave * kMergeE + r) * kWave + lane;
-            id[r] = e < total ? cand_id[base + e] : -1;
-            sc[r] = e < total ? cand_sc[base + e] : 0.f;
-        }
-#pragma unroll
-        for (int r = 0; r < kMergeE; ++r) ok[r] = id[r] >= 0;
-        const int nw = wave_topk_reg<kMergeE>(sc, id, ok, a.K, s_wid[wave], s_wsc[wave], s_tid[wave], s_tsc[wave]);
-        if (lane == 0) s_wn[wave] = nw;
-        __syncthreads();
-        if (wave == 0) {
-            float sc2[E2];
-            int id2[E2];
-            bool ok2[E2];
-#pragma unroll
-            for (int r = 0; r < E2; ++r) {
-                const int list = r;  // lane indexes the entry inside list r
-                const int cnt = list < NW ? s_wn[list] : nbest;
-                ok2[r] = lane < cnt;
-                id2[r] = ok2[r] ? (list < NW ? s_wid[list][lane] : s_bid[lane]) : -1;
-                sc2[r] = ok2[r] ? (list < NW ? s_wsc[list][lane] : s_bsc[lane]) : 0.f;
-            }
-            __builtin_amdgcn_wave_barrier();
-            nbest = wave_topk_reg<E2>(sc2, id2, ok2, a.K, s_bid, s_bsc, s_tid[0], s_tsc[0]);
-        }
-        __syncthreads();
-    }
-    if (wave == 0) {
-        int32_t* orow = a.idx + rg * a.K;
-        for (int t = lane; t < a.K; t += kWave) orow[t] = t < nbest ? s_bid[t] : -1;
-    }
+    merge_row<E, kBlock / kWave>(a, ly, rg, ms);
+    for (int t = threadIdx.x; t < a.K; t += kBlock) a.idx[rg * a.K + t] = t < ms.nbest ? ms.bid[t] : -1;
 }
 
 // ---- C: one selected chunk or one local-window piece per workgroup -----------
@@ -800,19 +824,32 @@ __global__ __launch_bounds__(kBlock) void k_dec_parts(FwdArgs a) {
 }
 
 // ---- D: fusion -----------------------------------------------------------------
-template <typename T, int D, int G>
-__global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
-    // Per head: local pieces merge into (lambda0 = log Z_swa, o0); then the fusion
-    // weights are exp(z_t - L) over z = {lambda0} U {s^_c}, L = LSE(z), and each
-    // retrieved chunk contributes exp(s^_c - L) * o_c with o_c its own softmax output.
-    constexpr int kMaxParts = 64 + kMaxLocalPieces;
-    __shared__ float s_w[G][kMaxParts];  // weight of each part's unnormalised o
-    __shared__ float s_lse[G];
-    const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
+// Per head: local pieces merge into (lambda0 = log Z_swa, o0); then the fusion
+// weights are exp(z_t - L) over z = {lambda0} U {s^_c}, L = LSE(z), and each
+// retrieved chunk contributes exp(s^_c - L) * o_c with o_c its own softmax output.
+// Run by all NT threads of a workgroup once row rg's part records are written.
+constexpr int kMaxParts = 64 + kMaxLocalPieces;
+template <int G>
+struct CombineSmem {
+    float w[G][kMaxParts];  // weight of each part's unnormalised o
+    float lse[G];
+};
+template <typename T, int D, int G, int NT>
+__device__ void combine_row(const FwdArgs& a, const DecLayout& ly, CombineSmem<G>& cs, int b, int n, int g,
+                            size_t rg) {
+    constexpr int NW = NT / kWave;
+    constexpr int OPT = (G * D + NT - 1) / NT;  // outputs per thread (o = tid + t NT < G D)
+    constexpr int CH = 48;                      // parts whose values are loaded ahead of the weights
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
-    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
-    for (int hh = wave; hh < G; hh += kBlock / kWave) {
+    // the first CH parts' values of this thread's outputs, in flight with the headers below
+    float v0[OPT][CH];
+#pragma unroll
+    for (int t = 0; t < OPT; ++t) {
+        const int o = min(tid + t * NT, G * D - 1), hh = o / D, dd = o % D;
+#pragma unroll
+        for (int j = 0; j < CH; ++j) v0[t][j] = part_record<D>(a, ly, rg, min(j, ly.nparts - 1), hh, G)[4 + dd];
+    }
+    for (int hh = wave; hh < G; hh += NW) {
         // local pieces: lanes < nlocal
         float m = -INFINITY, l = 0.f;
         if (lane < ly.nlocal) {
@@ -834,24 +871,110 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
         const float Z = wave_sum(lc > 0.f ? fexp(z - M) : 0.f) + fexp(lam0 - M);
         const float L = M + __logf(Z);
         const float a0 = fexp(lam0 - L) / l0;  // applied to each piece as exp(m - m0)
-        if (lane < ly.nlocal) s_w[hh][a.K + lane] = l > 0.f ? a0 * fexp(m - m0) : 0.f;
-        if (lane < a.K) s_w[hh][lane] = lc > 0.f ? fexp(z - L) / lc : 0.f;
-        if (lane == 0) s_lse[hh] = L;
+        if (lane < ly.nlocal) cs.w[hh][a.K + lane] = l > 0.f ? a0 * fexp(m - m0) : 0.f;
+        if (lane < a.K) cs.w[hh][lane] = lc > 0.f ? fexp(z - L) / lc : 0.f;
+        if (lane == 0) cs.lse[hh] = L;
     }
     __syncthreads();
-    for (int o = tid; o < G * D; o += kBlock) {
-        const int hh = o / D, dd = o % D;
+#pragma unroll
+    for (int t = 0; t < OPT; ++t) {
+        const int o = tid + t * NT, hh = o / D, dd = o % D;
+        if (o >= G * D) break;
         float acc = 0.f;
-#pragma unroll 8
-        for (int pt = 0; pt < ly.nparts; ++pt) {
-            const float w = s_w[hh][pt];
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+            const float w = j < ly.nparts ? cs.w[hh][j] : 0.f;
+            acc += w != 0.f ? w * v0[t][j] : 0.f;
+        }
+        for (int pt = CH; pt < ly.nparts; ++pt) {
+            const float w = cs.w[hh][pt];
             const float v = part_record<D>(a, ly, rg, pt, hh, G)[4 + dd];
             acc += w != 0.f ? w * v : 0.f;
         }
         const size_t row = q_row(a, b, g * G + hh, n);
         as_mut<T>(a.out)[row * D + dd] = from_f32<T>(acc);
-        if (dd == 0) a.lse[row] = s_lse[hh];
+        if (dd == 0) a.lse[row] = cs.lse[hh];
     }
+}
+
+// fp32 path: the fusion as its own pass, one workgroup per row.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
+    __shared__ CombineSmem<G> cs;
+    const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    combine_row<T, D, G, kBlock>(a, ly, cs, b, n, g, rg);
+}
+
+// ---- bf16: one workgroup of kRowWaves waves per row ----------------------------
+// Selection (E > 0: the merge of the scan's survivors, which also writes the row
+// of idx; E = 0: idx given), then the row's parts, wave w taking parts w, w + 8,
+// ... (one at a time, run_part_wave), then the fusion: one launch after the scan,
+// and the records only cross between waves of one workgroup (a barrier orders
+// them), never between workgroups.
+constexpr int kRowWaves = 8;
+// Rows (b, g, n) from which the one-workgroup-per-row pass is used: with fewer,
+// it would leave most CUs idle, and the parts spread over workgroups instead.
+constexpr int kRowPassMinRows = 256;
+template <int D, int G, int E>
+__global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
+    constexpr int NT = kRowWaves * kWave;
+    constexpr int kTileBytes = (int)sizeof(PartWaveSmem<D>) * kRowWaves;
+    static_assert(sizeof(MergeSmem<kRowWaves>) <= (size_t)kTileBytes, "the merge scratch fits in the part tiles");
+    // the waves' part tiles; before the parts, the merge's scratch in the same bytes
+    __shared__ __align__(16) unsigned char s_raw[kTileBytes];
+    __shared__ CombineSmem<G> cs;
+    __shared__ int s_sel[64];
+    auto& ms = *reinterpret_cast<MergeSmem<kRowWaves>*>(s_raw);
+    bf16* tiles = reinterpret_cast<bf16*>(s_raw);
+    const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const int pos = decode_position(a, b, n);
+    const int ncand = n_candidates(pos, a.W);
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
+    if constexpr (E > 0) {
+        merge_row<E, kRowWaves>(a, ly, rg, ms);
+        if (tid < a.K) {
+            const int v = tid < ms.nbest ? ms.bid[tid] : -1;
+            s_sel[tid] = v;
+            a.idx[rg * a.K + tid] = v;
+        }
+    } else {
+        if (tid < a.K) {
+            const int32_t* irow = a.idx + rg * a.K;
+            s_sel[tid] = idx_entry_valid(irow, tid, ncand) ? irow[tid] : -1;
+        }
+    }
+    __syncthreads();  // s_sel is set; the merge scratch is free for the tiles
+    bf16* sv = tiles + (size_t)w * (sizeof(PartWaveSmem<D>) / sizeof(bf16));
+    for (int part = w; part < ly.nparts; part += kRowWaves) {
+        int c, nk;
+        bool is_chunk;
+        if (part >= a.K) {
+            c = ncand + (part - a.K);
+            nk = min(kChunk, pos - c * kChunk + 1);
+            is_chunk = false;
+            if (c > pos / kChunk) c = -1;
+        } else {
+            c = s_sel[part];
+            nk = kChunk;
+            is_chunk = true;
+        }
+        if (c < 0) {
+            if (lane < G) {
+                float* r = part_record<D>(a, ly, rg, part, lane, G);
+                r[0] = -INFINITY;
+                r[1] = 0.f;
+                r[2] = -INFINITY;
+            }
+        } else {
+            run_part_wave<D, G>(a, ly, sv, b, n, g, rg, part, c, nk, is_chunk);
+        }
+    }
+    __syncthreads();  // every record of the row is written
+    combine_row<bf16, D, G, NT>(a, ly, cs, b, n, g, rg);
 }
 
 struct DecRun {
@@ -873,16 +996,42 @@ struct DecRun {
             } else {
                 scan(kScanSelect);
             }
-            HILS_LAUNCH("k_dec_merge", (k_dec_merge<G, D>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         }
         if constexpr (sizeof(T) == 2) {
-            constexpr int WPB = kBlock / kWave;
-            HILS_LAUNCH("k_dec_parts", (k_dec_parts_w<D, G>), dim3((ly.nparts + WPB - 1) / WPB, a.Hkv, R), dim3(kBlock),
-                        0, s, a);
+            const int surv = ly.nslices * a.K;  // the scan's survivors per row
+            if (R * a.Hkv >= kRowPassMinRows) {
+                // a workgroup per row; one merge round covers kRowWaves * 64 * E survivors
+                const dim3 rgrid(a.Hkv, R), rblock(kRowWaves * kWave);
+                if (a.given_idx)
+                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 0>), rgrid, rblock, 0, s, a);
+                else if (surv <= kRowWaves * kWave * 4)
+                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 4>), rgrid, rblock, 0, s, a);
+                else if (surv <= kRowWaves * kWave * 8)
+                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 8>), rgrid, rblock, 0, s, a);
+                else
+                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 16>), rgrid, rblock, 0, s, a);
+            } else {
+                // few rows: a workgroup per four parts, then the fusion
+                constexpr int WPB = kBlock / kWave;
+                const dim3 pgrid((ly.nparts + WPB - 1) / WPB, a.Hkv, R);
+                if (a.given_idx)
+                    HILS_LAUNCH("k_dec_parts", (k_dec_parts_w<D, G, 0>), pgrid, dim3(kBlock), 0, s, a);
+                else if (surv <= kBlock * 8)
+                    HILS_LAUNCH("k_dec_parts", (k_dec_parts_w<D, G, 8>), pgrid, dim3(kBlock), 0, s, a);
+                else
+                    HILS_LAUNCH("k_dec_parts", (k_dec_parts_w<D, G, 16>), pgrid, dim3(kBlock), 0, s, a);
+                HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
+            }
         } else {
+            if (!a.given_idx) {
+                if (ly.nslices * a.K <= kBlock * 8)
+                    HILS_LAUNCH("k_dec_merge", (k_dec_merge<8>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a, G, D);
+                else
+                    HILS_LAUNCH("k_dec_merge", (k_dec_merge<16>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a, G, D);
+            }
             HILS_LAUNCH("k_dec_parts", (k_dec_parts<T, D, G>), dim3(a.K + ly.nlocal, a.Hkv, R), dim3(kBlock), 0, s, a);
+            HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         }
-        HILS_LAUNCH("k_dec_combine", (k_dec_combine<T, D, G>), dim3(a.Hkv, R), dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }
 };

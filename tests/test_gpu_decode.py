@@ -2,7 +2,8 @@
 
 Covers unequal sequence lengths in one batch (including a single-token
 sequence and a full cache), seqlens = NULL (full capacity), Q-Cal routing and
-bias, Hl = Hkv, and forced-index mode."""
+bias, Hl = Hkv, forced-index mode, and both bf16 decode layouts (a workgroup per
+row from 256 rows up, per-part workgroups below)."""
 import numpy as np
 import pytest
 import torch
@@ -19,6 +20,10 @@ CASES = {
     "f32_route_bias_Hl_eq_Hkv": (dict(B=3, Hq=8, Hkv=1, Hl=1, N=1, L=3072, d=64, topk=32, window=100, dtype="f32"),
                                  203, True, True, [3072, 3000, 65]),
     "bf16_window1_G2": (dict(B=2, Hq=4, Hkv=2, N=1, L=2048, d=64, topk=5, window=1), 204, True, False, [2048, 2047]),
+    # 256 (sequence, KV group) rows: the one-workgroup-per-row pass (fewer rows take
+    # the per-part workgroups and a separate fusion pass)
+    "bf16_many_rows_ragged": (dict(B=64, Hq=16, Hkv=4, N=1, L=1024, d=128, topk=8, window=256), 205, True, False,
+                              [1024 - 13 * i for i in range(63)] + [1]),
 }
 
 
@@ -59,6 +64,10 @@ def test_decode_matches_oracle(name):
 
 def test_decode_forced_index():
     run_case("bf16_ragged_lengths", forced=True)
+
+
+def test_decode_forced_index_many_rows():
+    run_case("bf16_many_rows_ragged", forced=True)
 
 
 @pytest.mark.parametrize("name", list(CASES))

@@ -41,6 +41,10 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kSlice = 256;       // candidate chunks per scan workgroup
 constexpr int kMaxLocalPieces = 64;  // local window pieces per row (W <= 4032)
+constexpr int kRowWaves = 8;         // waves of a k_dec_row workgroup
+// Rows (b, g, n) from which the one-workgroup-per-row pass is used: with fewer,
+// it would leave most CUs idle, and the parts spread over workgroups instead.
+constexpr int kRowPassMinRows = 256;
 
 struct DecLayout {
     int nC, nslices, nlocal, nparts;  // nparts = K + nlocal records per (b, g)
@@ -907,17 +911,188 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
     combine_row<T, D, G, kBlock>(a, ly, cs, b, n, g, rg);
 }
 
+// The parts of row rg taken by this wave (w, w + kRowWaves, ...), each as in
+// run_part_wave, with the next part's K, V and landmark rows loaded while the
+// current one computes: each operand's registers are refilled as soon as the
+// current part is done with them (V once staged in LDS, the landmark rows once
+// s^ is formed, K once S is).  The loads are the same in every iteration (past
+// the wave's last part every lane reads one 16-byte piece), so that the
+// compiler counts the outstanding loads exactly.  q and q^ of the row are loaded
+// once; s^ is the diagonal of the landmark rows x q^ MFMA.
+struct RowPart {
+    int c, nk, chunk;  // chunk (c < 0: nothing to attend), its first nk keys, retrieved or local
+};
+template <int D, int G, bool ROUTE>
+__device__ void row_parts(const FwdArgs& a, const DecLayout& ly, bf16* sv, const int* s_sel, int b, int n, int g,
+                          size_t rg, int pos, int ncand) {
+    constexpr int KS = D / 32, DB = D / 16, VROW = PartWaveSmem<D>::VROW, PV = kChunk * D / 8 / kWave;
+    const int lane = threadIdx.x % kWave, lg = lane / 16, n16 = lane % 16, w = wave_id();
+    const float c1 = a.scale * kLog2e;
+    const bf16x8 zero8 = as_bf16x8(make_uint4(0, 0, 0, 0));
+    auto part_of = [&](int part) {
+        RowPart r;
+        if (part >= a.K) {
+            r.c = ncand + (part - a.K);
+            r.nk = min(kChunk, pos - r.c * kChunk + 1);
+            r.chunk = 0;
+            if (r.c > pos / kChunk) r.c = -1;
+        } else {
+            r.c = s_sel[part];
+            r.nk = kChunk;
+            r.chunk = 1;
+        }
+        return r;
+    };
+    // q and q^ of the row's G heads as B operands (head l%16; zero past G)
+    bf16x8 qB[KS], qR[ROUTE ? KS : 1];
+    {
+        const int hh = min(n16, G - 1);
+        const bf16* qrow = as<bf16>(a.q) + q_row(a, b, g * G + hh, n) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 qq = ld_bf16x8(qrow + ks * 32 + lg * 8);
+            qB[ks] = n16 < G ? qq : zero8;
+        }
+        if constexpr (ROUTE) {
+            const bf16* rrow = as<bf16>(a.q_route) + q_row(a, b, g * G + hh, n) * D;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 qq = ld_bf16x8(rrow + ks * 32 + lg * 8);
+                qR[ks] = n16 < G ? qq : zero8;
+            }
+        }
+    }
+    const int hl = (a.Hl == a.Hq) ? g * G + min(n16, G - 1) : g;  // landmark head of lane l%16
+    struct KOp {
+        bf16x8 k[4][KS];
+    };
+    struct VOp {
+        bf16x8 v[PV];
+    };
+    struct LOp {
+        bf16x8 l[KS];
+    };
+    auto load_k = [&](const RowPart& p, bool real) {
+        KOp x;
+        const bf16* kg = as<bf16>(a.k) + kv_chunk_offset(a, ly.nC, b, g, p.c < 0 ? 0 : p.c, D);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                x.k[kb][ks] = ld_bf16x8(kg + (real ? (size_t)(kb * 16 + n16) * D + ks * 32 + lg * 8 : 0));
+        return x;
+    };
+    auto load_v = [&](const RowPart& p, bool real) {
+        VOp x;
+        const bf16* vg = as<bf16>(a.v) + kv_chunk_offset(a, ly.nC, b, g, p.c < 0 ? 0 : p.c, D);
+#pragma unroll
+        for (int u = 0; u < PV; ++u) {
+            const int e = lane + u * kWave, r = e / (D / 8), pc = e % (D / 8);
+            x.v[u] = ld_bf16x8(vg + (real ? (size_t)r * D + pc * 8 : 0));
+        }
+        return x;
+    };
+    auto load_l = [&](const RowPart& p, bool real) {
+        LOp x;
+        const bf16* lr = as<bf16>(a.lmk) + lmk_row(a, ly.nC, b, hl, p.c < 0 ? 0 : p.c) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) x.l[ks] = ld_bf16x8(lr + (real ? ks * 32 + lg * 8 : 0));
+        return x;
+    };
+    RowPart p = part_of(w);
+    VOp vx = load_v(p, true);
+    LOp lx = load_l(p, true);
+    KOp kx = load_k(p, true);
+    for (int part = w; part < ly.nparts; part += kRowWaves) {
+        const bool real = part + kRowWaves < ly.nparts;  // uniform over the wave
+        const RowPart pn = part_of(real ? part + kRowWaves : part);
+        const int nk = p.nk;
+        // V rows into the wave's tile (rows at or past nk zeroed); the next V
+#pragma unroll
+        for (int u = 0; u < PV; ++u) {
+            const int e = lane + u * kWave, r = e / (D / 8), pc = e % (D / 8);
+            *reinterpret_cast<bf16x8*>(sv + r * VROW + pc * 8) = r < nk ? vx.v[u] : zero8;
+        }
+        vx = load_v(pn, real);
+        // s^ of a retrieved chunk for head n16: the diagonal (m = n = n16) of the
+        // landmark rows (A, row m = head m) x q^ (B, column n = head n), held by lane
+        // group n16 / 4; the next landmark rows
+        f32x4 s4 = zero4();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) s4 = mfma16x16x32(lx.l[ks], ROUTE ? qR[ks] : qB[ks], s4);
+        lx = load_l(pn, real);
+        float dg = s4[0];
+#pragma unroll
+        for (int i = 1; i < 4; ++i)
+            if (n16 % 4 == i) dg = s4[i];
+        const float sdiag = __shfl(dg, n16 + 16 * (n16 / 4), kWave);
+        // (branch-free: without a bias the load reads the landmark cache's first word)
+        const float* bsrc = a.bias ? a.bias + lmk_row(a, ly.nC, b, hl, p.c < 0 ? 0 : p.c)
+                                   : reinterpret_cast<const float*>(a.lmk);
+        const float bv = *bsrc;
+        const float sh = p.chunk && p.c >= 0 ? a.scale * sdiag + (a.bias ? bv : 0.f) : -INFINITY;
+        // S^T (lane: head n16, keys 16 kb + 4 lg + i), in log2 units; the next K
+        f32x4 st[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            st[kb] = zero4();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(kx.k[kb][ks], qB[ks], st[kb]);
+        }
+        kx = load_k(pn, real);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                st[kb][i] = kb * 16 + lg * 4 + i < nk ? st[kb][i] * c1 : -INFINITY;
+                mx = fmaxf(mx, st[kb][i]);
+            }
+        mx = group4_max(mx);
+        float ls = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                st[kb][i] = fexp2(st[kb][i] - mx);
+                ls += st[kb][i];
+            }
+        ls = group4_sum(ls);
+        const bf16x8 pb0 = pack_bf16x8_4x2(st[0], st[1]);
+        const bf16x8 pb1 = pack_bf16x8_4x2(st[2], st[3]);
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        // the record (an empty one when there is nothing to attend: l = 0, and the
+        // fusion never reads its o); O^T (lane: head n16, dims 16 db + 4 lg + i)
+        const bool empty = p.c < 0;
+        if (n16 < G) {
+            float* r = part_record<D>(a, ly, rg, part, n16, G);
+            if (lg == 0) {
+                r[0] = empty ? -INFINITY : mx * (1.f / kLog2e);
+                r[1] = empty ? 0.f : ls;
+                r[2] = empty ? -INFINITY : sh;
+            }
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            f32x4 o = mfma16x16x32(tr_operand_perm(sv, VROW, 0, db * 16, lane), pb0, zero4());
+            o = mfma16x16x32(tr_operand_perm(sv, VROW, 32, db * 16, lane), pb1, o);
+            if (n16 < G) *reinterpret_cast<f32x4*>(part_record<D>(a, ly, rg, part, n16, G) + 4 + db * 16 + lg * 4) = o;
+        }
+        // the tile is rewritten by the next part: its reads above must be complete
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        p = pn;
+    }
+}
+
 // ---- bf16: one workgroup of kRowWaves waves per row ----------------------------
 // Selection (E > 0: the merge of the scan's survivors, which also writes the row
 // of idx; E = 0: idx given), then the row's parts, wave w taking parts w, w + 8,
 // ... (one at a time, run_part_wave), then the fusion: one launch after the scan,
 // and the records only cross between waves of one workgroup (a barrier orders
 // them), never between workgroups.
-constexpr int kRowWaves = 8;
-// Rows (b, g, n) from which the one-workgroup-per-row pass is used: with fewer,
-// it would leave most CUs idle, and the parts spread over workgroups instead.
-constexpr int kRowPassMinRows = 256;
-template <int D, int G, int E>
+template <int D, int G, int E, bool ROUTE>
 __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     constexpr int NT = kRowWaves * kWave;
     constexpr int kTileBytes = (int)sizeof(PartWaveSmem<D>) * kRowWaves;
@@ -948,31 +1123,8 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
         }
     }
     __syncthreads();  // s_sel is set; the merge scratch is free for the tiles
-    bf16* sv = tiles + (size_t)w * (sizeof(PartWaveSmem<D>) / sizeof(bf16));
-    for (int part = w; part < ly.nparts; part += kRowWaves) {
-        int c, nk;
-        bool is_chunk;
-        if (part >= a.K) {
-            c = ncand + (part - a.K);
-            nk = min(kChunk, pos - c * kChunk + 1);
-            is_chunk = false;
-            if (c > pos / kChunk) c = -1;
-        } else {
-            c = s_sel[part];
-            nk = kChunk;
-            is_chunk = true;
-        }
-        if (c < 0) {
-            if (lane < G) {
-                float* r = part_record<D>(a, ly, rg, part, lane, G);
-                r[0] = -INFINITY;
-                r[1] = 0.f;
-                r[2] = -INFINITY;
-            }
-        } else {
-            run_part_wave<D, G>(a, ly, sv, b, n, g, rg, part, c, nk, is_chunk);
-        }
-    }
+    if (w < ly.nparts) row_parts<D, G, ROUTE>(a, ly, tiles + (size_t)w * (sizeof(PartWaveSmem<D>) / sizeof(bf16)), s_sel,
+                                              b, n, g, rg, pos, ncand);
     __syncthreads();  // every record of the row is written
     combine_row<bf16, D, G, NT>(a, ly, cs, b, n, g, rg);
 }
@@ -1002,14 +1154,21 @@ struct DecRun {
             if (R * a.Hkv >= kRowPassMinRows) {
                 // a workgroup per row; one merge round covers kRowWaves * 64 * E survivors
                 const dim3 rgrid(a.Hkv, R), rblock(kRowWaves * kWave);
+                auto row = [&](auto e_tag) {
+                    constexpr int EE = decltype(e_tag)::value;
+                    if (a.q_route)
+                        HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, EE, true>), rgrid, rblock, 0, s, a);
+                    else
+                        HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, EE, false>), rgrid, rblock, 0, s, a);
+                };
                 if (a.given_idx)
-                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 0>), rgrid, rblock, 0, s, a);
+                    row(std::integral_constant<int, 0>{});
                 else if (surv <= kRowWaves * kWave * 4)
-                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 4>), rgrid, rblock, 0, s, a);
+                    row(std::integral_constant<int, 4>{});
                 else if (surv <= kRowWaves * kWave * 8)
-                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 8>), rgrid, rblock, 0, s, a);
+                    row(std::integral_constant<int, 8>{});
                 else
-                    HILS_LAUNCH("k_dec_row", (k_dec_row<D, G, 16>), rgrid, rblock, 0, s, a);
+                    row(std::integral_constant<int, 16>{});
             } else {
                 // few rows: a workgroup per four parts, then the fusion
                 constexpr int WPB = kBlock / kWave;

@@ -637,6 +637,7 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
     const T* base = lm + (PAGED ? 0 : lmk_row(a, ly.nC, b, hl, c0) * D);
     // NB independent 16-byte loads per lane are issued before any math; rows
     // past the slice end re-read the last row (in bounds, result discarded).
+    // The landmarks are read once per step: non-temporal loads.
     constexpr int NB = 16;
     for (int r0 = 0; r0 < len; r0 += RPS * NB) {
         uint4 x[NB];
@@ -644,7 +645,7 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
         for (int u = 0; u < NB; ++u) {
             const int r = min(r0 + u * RPS + sub, len - 1);
             const T* src = PAGED ? lm + ((size_t)s_page[r] * a.Hl + hl) * D : base + (size_t)r * D;
-            x[u] = *reinterpret_cast<const uint4*>(src);
+            x[u] = ld_stream16(src);
         }
 #pragma unroll
         for (int u = 0; u < NB; ++u) {

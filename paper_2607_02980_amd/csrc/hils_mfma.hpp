@@ -24,6 +24,18 @@ __device__ __forceinline__ bf16x8 ld_bf16x8(const void* p) { return *reinterpret
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
+// 16-byte global load marked non-temporal (data streamed once: it is not kept in
+// the caches at the expense of data that is reused).
+__device__ __forceinline__ uint4 ld_stream16(const void* p) {
+    typedef unsigned v4u __attribute__((ext_vector_type(4)));
+    const v4u t = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p));
+    return make_uint4(t[0], t[1], t[2], t[3]);
+}
+__device__ __forceinline__ bf16x8 ld_stream_bf16x8(const void* p) {
+    typedef unsigned v4u __attribute__((ext_vector_type(4)));
+    return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p)));
+}
+
 // Round 8 floats to bf16 (nearest-even) into one MFMA operand.
 __device__ __forceinline__ bf16x8 pack_bf16x8(const float* x) {
     bf16x8 r;

@@ -42,9 +42,11 @@ constexpr int kBlock = 256;
 constexpr int kSlice = 256;       // candidate chunks per scan workgroup
 constexpr int kMaxLocalPieces = 64;  // local window pieces per row (W <= 4032)
 constexpr int kRowWaves = 8;         // waves of a k_dec_row workgroup
-// Rows (b, g, n) from which the one-workgroup-per-row pass is used: with fewer,
-// it would leave most CUs idle, and the parts spread over workgroups instead.
-constexpr int kRowPassMinRows = 256;
+// The one-workgroup-per-row pass is used for kRowPassMinRows..(CUs of the device)
+// rows (b, g, n): with fewer it would leave CUs idle, with more its workgroups run
+// in rounds that each wait out a selection and a fusion; otherwise the parts
+// spread over per-part workgroups.
+constexpr int kRowPassMinRows = 128;
 
 struct DecLayout {
     int nC, nslices, nlocal, nparts;  // nparts = K + nlocal records per (b, g)
@@ -621,7 +623,7 @@ __device__ void empty_part(const FwdArgs& a, const DecLayout& ly, size_t rg, int
 // s_score[hh].  lanes_per_row lanes read one landmark row (16 B each), rows_per_step
 // rows per wave load.  Contiguous landmarks are rows c0 + r of one [L/S, D] slab;
 // paged ones are found through the slice's page ids (s_page).
-template <typename T, int D, bool PAGED>
+template <typename T, int D, bool PAGED, bool STREAM>
 __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly, int b, int n, int g, int G, int hh,
                                           int c0, int len, const int* s_page, float* s_score) {
     constexpr int LPR = D * (int)sizeof(T) / 16;
@@ -637,7 +639,9 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
     const T* base = lm + (PAGED ? 0 : lmk_row(a, ly.nC, b, hl, c0) * D);
     // NB independent 16-byte loads per lane are issued before any math; rows
     // past the slice end re-read the last row (in bounds, result discarded).
-    // The landmarks are read once per step: non-temporal loads.
+    // STREAM (one new query per sequence): the landmarks are read once per step,
+    // with non-temporal loads; with several, each query row rescans them, and the
+    // later rows find them in the caches.
     constexpr int NB = 16;
     for (int r0 = 0; r0 < len; r0 += RPS * NB) {
         uint4 x[NB];
@@ -645,7 +649,7 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
         for (int u = 0; u < NB; ++u) {
             const int r = min(r0 + u * RPS + sub, len - 1);
             const T* src = PAGED ? lm + ((size_t)s_page[r] * a.Hl + hl) * D : base + (size_t)r * D;
-            x[u] = ld_stream16(src);
+            x[u] = STREAM ? ld_stream16(src) : *reinterpret_cast<const uint4*>(src);
         }
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
@@ -724,7 +728,10 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
         __syncthreads();
     }
     for (int hh = wave; hh < G; hh += kBlock / kWave)
-        scan_head<T, D, PAGED>(a, ly, b, n, g, G, hh, c0, len, s_id, s_score[hh]);
+        if (a.N == 1)
+            scan_head<T, D, PAGED, true>(a, ly, b, n, g, G, hh, c0, len, s_id, s_score[hh]);
+        else
+            scan_head<T, D, PAGED, false>(a, ly, b, n, g, G, hh, c0, len, s_id, s_score[hh]);
     __syncthreads();
     if (a.bias) {
         for (int e = tid; e < G * len; e += kBlock) {
@@ -1130,6 +1137,19 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     combine_row<bf16, D, G, NT>(a, ly, cs, b, n, g, rg);
 }
 
+// Compute units of the current device (queried once per device).
+int device_cus() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
+}
+
 struct DecRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
@@ -1152,7 +1172,8 @@ struct DecRun {
         }
         if constexpr (sizeof(T) == 2) {
             const int surv = ly.nslices * a.K;  // the scan's survivors per row
-            if (R * a.Hkv >= kRowPassMinRows) {
+            const int rows = R * a.Hkv;
+            if (rows >= kRowPassMinRows && rows <= device_cus()) {
                 // a workgroup per row; one merge round covers kRowWaves * 64 * E survivors
                 const dim3 rgrid(a.Hkv, R), rblock(kRowWaves * kWave);
                 auto row = [&](auto e_tag) {

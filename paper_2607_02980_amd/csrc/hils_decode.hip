@@ -120,13 +120,14 @@ struct PartSmem {
     float p[G][kChunk];
 };
 
-template <int G>
+// NQ: new queries of one sequence scored together (one landmark read for all).
+template <int G, int NQ>
 struct ScanSmem {
-    float score[G][kSlice];
-    float sig[kSlice];
+    float score[NQ][G][kSlice];
+    float sig[NQ][kSlice];
     int id[kSlice];
-    int oid[64], tid[64];
-    float osc[64], tsc[64];
+    int oid[NQ][64], tid[NQ][64];
+    float osc[NQ][64], tsc[NQ][64];
 };
 
 // 8 consecutive elements of an LDS row as floats (one 16-byte read for bf16).
@@ -619,30 +620,34 @@ __device__ void empty_part(const FwdArgs& a, const DecLayout& ly, size_t rg, int
 }
 
 // ---- A: landmark scan slices --------------------------------------------------
-// Scores of head hh of row (b, n) for the slice's chunks [c0, c0 + len) into
-// s_score[hh].  lanes_per_row lanes read one landmark row (16 B each), rows_per_step
-// rows per wave load.  Contiguous landmarks are rows c0 + r of one [L/S, D] slab;
-// paged ones are found through the slice's page ids (s_page).
-template <typename T, int D, bool PAGED, bool STREAM>
-__device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly, int b, int n, int g, int G, int hh,
-                                          int c0, int len, const int* s_page, float* s_score) {
+// Scores of head hh of the nq query rows (b, n0 + q) for the slice's chunks
+// [c0, c0 + len) into s_score[q][hh].  LPR lanes read one landmark row (16 B
+// each), RPS rows per wave load; each row read is scored against all nq queries.
+// Contiguous landmarks are rows c0 + r of one [L/S, D] slab; paged ones are found
+// through the slice's page ids (s_page).
+template <typename T, int D, int G, int NQ, bool PAGED, bool STREAM>
+__device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly, int b, int n0, int nq, int g,
+                                          int hh, int c0, int len, const int* s_page, float (*s_score)[G][kSlice]) {
     constexpr int LPR = D * (int)sizeof(T) / 16;
     constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane per load
     constexpr int RPS = kWave / LPR;
     const int lane = threadIdx.x % kWave, sub = lane / LPR, seg = lane % LPR;
     const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-    const T* qr = as<T>(a.q_route ? a.q_route : a.q) + q_row(a, b, g * G + hh, n) * D + seg * EPL;
-    float qv[EPL];
+    float qv[NQ][EPL];
 #pragma unroll
-    for (int t = 0; t < EPL; ++t) qv[t] = to_f32(qr[t]);
+    for (int q = 0; q < NQ; ++q) {
+        const T* qr = as<T>(a.q_route ? a.q_route : a.q) + q_row(a, b, g * G + hh, n0 + min(q, nq - 1)) * D + seg * EPL;
+#pragma unroll
+        for (int t = 0; t < EPL; ++t) qv[q][t] = to_f32(qr[t]);
+    }
     const T* lm = as<T>(a.lmk) + seg * EPL;
     const T* base = lm + (PAGED ? 0 : lmk_row(a, ly.nC, b, hl, c0) * D);
     // NB independent 16-byte loads per lane are issued before any math; rows
     // past the slice end re-read the last row (in bounds, result discarded).
-    // STREAM (one new query per sequence): the landmarks are read once per step,
-    // with non-temporal loads; with several, each query row rescans them, and the
-    // later rows find them in the caches.
-    constexpr int NB = 16;
+    // STREAM (the sequence's new queries all in this workgroup): the landmarks
+    // are read once per step, with non-temporal loads; otherwise other query
+    // groups rescan them and find them in the caches.
+    constexpr int NB = NQ == 1 ? 16 : 8;
     for (int r0 = 0; r0 < len; r0 += RPS * NB) {
         uint4 x[NB];
 #pragma unroll
@@ -653,20 +658,29 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
         }
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            float part;
+            float xf[EPL];
             if constexpr (sizeof(T) == 2) {
                 const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-                part = 0.f;
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    part += qv[2 * t] * __uint_as_float(w[t] << 16) + qv[2 * t + 1] * __uint_as_float(w[t] & 0xffff0000u);
+                for (int t = 0; t < 4; ++t) {
+                    xf[2 * t] = __uint_as_float(w[t] << 16);
+                    xf[2 * t + 1] = __uint_as_float(w[t] & 0xffff0000u);
+                }
             } else {
-                part = qv[0] * __uint_as_float(x[u].x) + qv[1] * __uint_as_float(x[u].y) +
-                       qv[2] * __uint_as_float(x[u].z) + qv[3] * __uint_as_float(x[u].w);
+                xf[0] = __uint_as_float(x[u].x);
+                xf[1] = __uint_as_float(x[u].y);
+                xf[2] = __uint_as_float(x[u].z);
+                xf[3] = __uint_as_float(x[u].w);
             }
-            part = group_sum<LPR>(part);
             const int r = r0 + u * RPS + sub;
-            if (seg == 0 && r < len) s_score[r] = a.scale * part;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                float part = 0.f;
+#pragma unroll
+                for (int t = 0; t < EPL; ++t) part += qv[q][t] * xf[t];
+                part = group_sum<LPR>(part);
+                if (seg == 0 && r < len) s_score[q][hh][r] = a.scale * part;
+            }
         }
     }
 }
@@ -677,109 +691,134 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
 // normalised ranking the scan runs twice: kScanLse leaves each head's (max, sum
 // of exp) over the slice, kScanNormSelect subtracts each head's log-sum-exp over
 // all of C_i (from those partials) before the maximum over the heads.
+// NQ new queries of one sequence share a workgroup (grid z = B x ceil(N / NQ)):
+// the landmark rows are read once for all of them; wave q selects for query q.
+// Each query row keeps its own candidate count (its own position).
 constexpr int kScanSelect = 0, kScanLse = 1, kScanNormSelect = 2;
-template <typename T, int D, int G, bool PAGED>
+template <typename T, int D, int G, int NQ, bool PAGED>
 __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
-    const int b = blockIdx.z / a.N, n = blockIdx.z % a.N, g = blockIdx.y;
-    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    static_assert(NQ <= kBlock / kWave, "one selecting wave per query");
+    const int ngrp = (a.N + NQ - 1) / NQ;
+    const int b = blockIdx.z / ngrp, n0 = (blockIdx.z % ngrp) * NQ, g = blockIdx.y;
+    const int nq = min(NQ, a.N - n0);
     const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
-    const int pos = decode_position(a, b, n);
-    const int ncand = n_candidates(pos, a.W);
-    __shared__ ScanSmem<G> ss;
-    auto& s_score = ss.score;
-    auto& s_sig = ss.sig;
-    auto& s_id = ss.id;
+    __shared__ ScanSmem<G, NQ> ss;
+    __shared__ float s_lse[NQ][G];
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int c0 = blockIdx.x * kSlice;
-    const int len = min(kSlice, ncand - c0);
     float* cand_sc = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.cand);
-    const size_t cbase = (rg * ly.nslices + blockIdx.x) * a.K;
     int* cand_id = reinterpret_cast<int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
-    float* lse_part = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.lse) + (rg * ly.nslices) * G * 2;
-    if (len <= 0) {
+    // per query: its row, its slice length (0 if the slice is past its candidates)
+    auto row_of = [&](int q) { return ((size_t)b * a.Hkv + g) * a.N + n0 + q; };
+    auto len_of = [&](int q) {
+        return q < nq ? max(0, min(kSlice, n_candidates(decode_position(a, b, n0 + q), a.W) - c0)) : 0;
+    };
+    int len = 0;  // the longest of the queries' slices (the last query's)
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) len = max(len, len_of(q));
+    // rows whose slice is empty: empty survivors (or lse partials) now
+    for (int q = 0; q < nq; ++q) {
+        if (len_of(q) > 0) continue;
+        const size_t rg = row_of(q);
         if (mode == kScanLse) {
+            float* lp = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.lse) + (rg * ly.nslices) * G * 2;
             for (int t = tid; t < G; t += kBlock) {
-                lse_part[(blockIdx.x * G + t) * 2] = -INFINITY;
-                lse_part[(blockIdx.x * G + t) * 2 + 1] = 0.f;
+                lp[(blockIdx.x * G + t) * 2] = -INFINITY;
+                lp[(blockIdx.x * G + t) * 2 + 1] = 0.f;
             }
-            return;
+        } else {
+            const size_t cbase = (rg * ly.nslices + blockIdx.x) * a.K;
+            for (int t = tid; t < a.K; t += kBlock) {
+                cand_sc[cbase + t] = -INFINITY;
+                cand_id[cbase + t] = -1;
+            }
         }
-        for (int t = tid; t < a.K; t += kBlock) {
-            cand_sc[cbase + t] = -INFINITY;
-            cand_id[cbase + t] = -1;
-        }
-        return;
     }
-    __shared__ float s_lse[G];
-    if (mode == kScanNormSelect && tid < G) {
-        // log-sum-exp of head tid over all candidates, from the slices' partials
+    if (len <= 0) return;
+    if (mode == kScanNormSelect && tid < nq * G) {
+        // log-sum-exp of head hh of query q over all its candidates, from the slices' partials
+        const int q = tid / G, hh = tid % G;
+        const float* lp = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.lse) +
+                          (row_of(q) * ly.nslices) * G * 2;
         float m = -INFINITY;
-        for (int sl = 0; sl < ly.nslices; ++sl) m = fmaxf(m, lse_part[(sl * G + tid) * 2]);
+        for (int sl = 0; sl < ly.nslices; ++sl) m = fmaxf(m, lp[(sl * G + hh) * 2]);
         float sum = 0.f;
         for (int sl = 0; sl < ly.nslices; ++sl) {
-            const float pm = lse_part[(sl * G + tid) * 2], ps = lse_part[(sl * G + tid) * 2 + 1];
+            const float pm = lp[(sl * G + hh) * 2], ps = lp[(sl * G + hh) * 2 + 1];
             sum += ps > 0.f ? ps * fexp(pm - m) : 0.f;
         }
-        s_lse[tid] = m + __logf(sum);
+        s_lse[q][hh] = m + __logf(sum);
     }
     if constexpr (PAGED) {
         // the slice's page ids (s_id is free until the selection pass)
-        for (int r = tid; r < len; r += kBlock) s_id[r] = page_of(a, ly.nC, b, c0 + r);
+        for (int r = tid; r < len; r += kBlock) ss.id[r] = page_of(a, ly.nC, b, c0 + r);
         __syncthreads();
     }
+    const bool stream = a.N <= NQ;
     for (int hh = wave; hh < G; hh += kBlock / kWave)
-        if (a.N == 1)
-            scan_head<T, D, PAGED, true>(a, ly, b, n, g, G, hh, c0, len, s_id, s_score[hh]);
+        if (stream)
+            scan_head<T, D, G, NQ, PAGED, true>(a, ly, b, n0, nq, g, hh, c0, len, ss.id, ss.score);
         else
-            scan_head<T, D, PAGED, false>(a, ly, b, n, g, G, hh, c0, len, s_id, s_score[hh]);
+            scan_head<T, D, G, NQ, PAGED, false>(a, ly, b, n0, nq, g, hh, c0, len, ss.id, ss.score);
     __syncthreads();
     if (a.bias) {
         for (int e = tid; e < G * len; e += kBlock) {
             const int hh = e / len, r = e % len;
             const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-            s_score[hh][r] += a.bias[PAGED ? (size_t)s_id[r] * a.Hl + hl : lmk_row(a, ly.nC, b, hl, c0 + r)];
+            const float bv = a.bias[PAGED ? (size_t)ss.id[r] * a.Hl + hl : lmk_row(a, ly.nC, b, hl, c0 + r)];
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) ss.score[q][hh][r] += bv;
         }
         __syncthreads();
     }
     if (mode == kScanLse) {
-        for (int hh = wave; hh < G; hh += kBlock / kWave) {
+        for (int e = wave; e < nq * G; e += kBlock / kWave) {
+            const int q = e / G, hh = e % G, lq = len_of(q);
+            if (lq <= 0) continue;
             float m = -INFINITY;
-            for (int r = lane; r < len; r += kWave) m = fmaxf(m, s_score[hh][r]);
+            for (int r = lane; r < lq; r += kWave) m = fmaxf(m, ss.score[q][hh][r]);
             m = wave_max(m);
             float sum = 0.f;
-            for (int r = lane; r < len; r += kWave) sum += fexp(s_score[hh][r] - m);
+            for (int r = lane; r < lq; r += kWave) sum += fexp(ss.score[q][hh][r] - m);
             sum = wave_sum(sum);
             if (lane == 0) {
-                lse_part[(blockIdx.x * G + hh) * 2] = m;
-                lse_part[(blockIdx.x * G + hh) * 2 + 1] = sum;
+                float* lp = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.lse) + (row_of(q) * ly.nslices) * G * 2;
+                lp[(blockIdx.x * G + hh) * 2] = m;
+                lp[(blockIdx.x * G + hh) * 2 + 1] = sum;
             }
         }
         return;
     }
-    for (int r = tid; r < len; r += kBlock) {
+    for (int e = tid; e < NQ * len; e += kBlock) {
+        const int q = e / len, r = e % len;
         float m = -INFINITY;
 #pragma unroll
         for (int hh = 0; hh < G; ++hh)
-            m = fmaxf(m, s_score[hh][r] - (mode == kScanNormSelect ? s_lse[hh] : 0.f));
-        s_sig[r] = m;
+            m = fmaxf(m, ss.score[q][hh][r] - (mode == kScanNormSelect ? s_lse[q][hh] : 0.f));
+        ss.sig[q][r] = m;
     }
     __syncthreads();
-    if (wave == 0) {
-        constexpr int E = kSlice / kWave;
-        float sc[E];
-        int id[E];
-        bool ok[E];
+    if (wave < nq) {
+        const int q = wave, lq = len_of(q);
+        if (lq > 0) {
+            constexpr int E = kSlice / kWave;
+            float sc[E];
+            int id[E];
+            bool ok[E];
 #pragma unroll
-        for (int r = 0; r < E; ++r) {
-            const int e = r * kWave + lane;
-            ok[r] = e < len;
-            sc[r] = ok[r] ? s_sig[e] : 0.f;
-            id[r] = ok[r] ? c0 + e : -1;
-        }
-        const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, ss.oid, ss.osc, ss.tid, ss.tsc);  // ids c0 + e*64 + lane
-        for (int t = lane; t < a.K; t += kWave) {
-            cand_sc[cbase + t] = t < m ? ss.osc[t] : -INFINITY;
-            cand_id[cbase + t] = t < m ? ss.oid[t] : -1;
+            for (int r = 0; r < E; ++r) {
+                const int e = r * kWave + lane;
+                ok[r] = e < lq;
+                sc[r] = ok[r] ? ss.sig[q][e] : 0.f;
+                id[r] = ok[r] ? c0 + e : -1;
+            }
+            const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, ss.oid[q], ss.osc[q], ss.tid[q],
+                                                         ss.tsc[q]);  // ids c0 + e*64 + lane
+            const size_t cbase = (row_of(q) * ly.nslices + blockIdx.x) * a.K;
+            for (int t = lane; t < a.K; t += kWave) {
+                cand_sc[cbase + t] = t < m ? ss.osc[q][t] : -INFINITY;
+                cand_id[cbase + t] = t < m ? ss.oid[q][t] : -1;
+            }
         }
     }
 }
@@ -1156,12 +1195,22 @@ struct DecRun {
         const int R = a.B * a.N;  // rows (sequence, new query); the host keeps R <= 65535
         const DecLayout ly = dec_layout(R, a.Hkv, G, D, a.L, a.K, a.W);
         if (!a.given_idx) {
-            const dim3 grid(ly.nslices, a.Hkv, R);
+            // one new query per sequence: a workgroup per (slice, group, row); several:
+            // the sequence's queries four at a time share each landmark read
             auto scan = [&](int mode) {
-                if (a.block_table)
-                    HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, true>), grid, dim3(kBlock), 0, s, a, mode);
-                else
-                    HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, false>), grid, dim3(kBlock), 0, s, a, mode);
+                if (a.N == 1) {
+                    const dim3 grid(ly.nslices, a.Hkv, R);
+                    if (a.block_table)
+                        HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, 1, true>), grid, dim3(kBlock), 0, s, a, mode);
+                    else
+                        HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, 1, false>), grid, dim3(kBlock), 0, s, a, mode);
+                } else {
+                    const dim3 grid(ly.nslices, a.Hkv, a.B * ((a.N + 3) / 4));
+                    if (a.block_table)
+                        HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, 4, true>), grid, dim3(kBlock), 0, s, a, mode);
+                    else
+                        HILS_LAUNCH("k_dec_scan", (k_dec_scan<T, D, G, 4, false>), grid, dim3(kBlock), 0, s, a, mode);
+                }
             };
             if (a.head_norm) {
                 scan(kScanLse);

@@ -68,11 +68,11 @@ def make_pool(p, host, rng):
     return pools, table, contiguous
 
 
-def run_case(name):
+def run_case(name, flags=0):
     from paper_2607_02980_amd import hils
 
     kw, wid, bias, route, seqlens, paged = CASES[name]
-    p = hils.Params(**kw)
+    p = hils.Params(flags=flags, **kw)
     log(f"[decode-paged] case={name} seqlens={seqlens} params={kw}")
     host = host_inputs(p, wid, bias=bias, route=route)
     s = oshape(p)
@@ -110,6 +110,14 @@ def run_case(name):
 @pytest.mark.parametrize("name", list(CASES))
 def test_decode_paged_and_multi_token(name):
     run_case(name)
+
+
+@pytest.mark.parametrize("name", ["bf16_multi_token_ragged", "bf16_paged_window1_G1"])
+def test_decode_multi_token_head_normalised(name):
+    # the two-pass scan with several new queries per sequence sharing its workgroups
+    from paper_2607_02980_amd import hils
+
+    run_case(name, flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
 
 
 def test_paged_equals_contiguous_bitwise():

@@ -1176,17 +1176,13 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     combine_row<bf16, D, G, NT>(a, ly, cs, b, n, g, rg);
 }
 
-// Compute units of the current device (queried once per device).
+// Compute units of the current device (a host-side attribute query; nothing cached).
 int device_cus() {
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cached[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cached[dev] = n;
-    }
-    return cached[dev];
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        return 256;
+    return n;
 }
 
 struct DecRun {

@@ -338,9 +338,18 @@ def cpu_baseline(W_, host, target_s=20.0):
         if dt * threads >= target_s or nrows >= W_.N:
             break
         nrows = min(W_.N, int(nrows * max(2.0, min(16.0, target_s / max(dt * threads, 1e-3)))))
+    model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": round(nrows / dt, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{nrows} query rows evenly spaced over the {W_.N}-token sequence (all {W_.Hq} heads), "
-                      f"fp32 oracle, {dt:.2f} s wall on {threads} threads"}
+                      f"fp32 oracle, {dt:.2f} s wall on {threads} threads of a {model}"}
 
 
 def main():

@@ -47,16 +47,20 @@ constexpr int kRowWaves = 8;         // waves of a k_dec_row workgroup
 // in rounds that each wait out a selection and a fusion; otherwise the parts
 // spread over per-part workgroups.
 constexpr int kRowPassMinRows = 128;
+constexpr int kMqMaxUnion = 256;  // union chunks of a multi-query workgroup (larger: per-part path)
 
 struct DecLayout {
     int nC, nslices, nlocal, nparts;  // nparts = K + nlocal records per (b, g)
-    size_t cand, parts, lse, total;   // byte offsets
+    int mq_umax;                      // union chunks per multi-query workgroup (at most)
+    size_t cand, parts, lse, mq, total;  // byte offsets
 };
 
 __host__ __device__ inline int local_pieces_max(int W) { return (W + 62) / 64 + 1; }
 
-// R = B * N rows
-__host__ __device__ inline DecLayout dec_layout(int R, int Hkv, int G, int d, int L, int K, int W) {
+// R = B * N rows; with N > 1 also the records of the multi-query pass
+// (k_dec_mq: per workgroup mq_umax union chunks x 16 tile rows)
+__host__ __device__ inline DecLayout dec_layout(int B, int N, int Hkv, int G, int d, int L, int K, int W) {
+    const int R = B * N;
     DecLayout o;
     o.nC = L / kChunk;
     o.nslices = (o.nC + kSlice - 1) / kSlice;
@@ -67,7 +71,11 @@ __host__ __device__ inline DecLayout dec_layout(int R, int Hkv, int G, int d, in
     o.parts = ((bg * o.nslices * K * 8) + 255) & ~(size_t)255;
     // per-head (max, sum of exp) of each slice's scores, for the normalised ranking
     o.lse = o.parts + ((bg * o.nparts * G * (4 + d) * 4 + 255) & ~(size_t)255);
-    o.total = o.lse + ((bg * o.nslices * G * 2 * 4 + 255) & ~(size_t)255);
+    o.mq = o.lse + ((bg * o.nslices * G * 2 * 4 + 255) & ~(size_t)255);
+    const int nq = 16 / G < 8 ? 16 / G : 8;  // queries per multi-query workgroup
+    o.mq_umax = nq * K + o.nlocal + 1;
+    const size_t mq_groups = N > 1 ? (size_t)B * ((N + nq - 1) / nq) * Hkv : 0;
+    o.total = o.mq + ((mq_groups * o.mq_umax * 16 * (4 + d) * 4 + 255) & ~(size_t)255);
     return o;
 }
 
@@ -397,11 +405,13 @@ struct MergeSmem {
     float wsc[NW][64], tsc[NW][64], bsc[64];
     int wn[NW], nbest;
 };
+// (wave: the caller's wave index within the NW waves that share ms; every wave of
+// the workgroup calls merge_row the same number of times: it holds block barriers)
 template <int E, int NW>
-__device__ void merge_row(const FwdArgs& a, const DecLayout& ly, size_t rg, MergeSmem<NW>& ms) {
+__device__ void merge_row(const FwdArgs& a, const DecLayout& ly, size_t rg, MergeSmem<NW>& ms, int wave) {
     constexpr int NT = NW * kWave;
     constexpr int E2 = NW + 1;  // NW wave lists + running best, <= 64 each
-    const int wave = wave_id(), lane = threadIdx.x % kWave;
+    const int lane = threadIdx.x % kWave;
     const float* cand_sc = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.cand);
     const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
     const size_t base = rg * ly.nslices * a.K;
@@ -572,13 +582,13 @@ __global__ __launch_bounds__(kBlock) void k_dec_parts_w(FwdArgs a) {
     const int w = wave_id();
     const int part = blockIdx.x * NW + w, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
     const int pos = decode_position(a, b, n);
     const int lane = threadIdx.x % kWave;
     int csel = -1;  // this wave's chunk if part < K
     if constexpr (E > 0) {
         if ((int)blockIdx.x * NW < a.K) {  // uniform over the workgroup
-            merge_row<E, NW>(a, ly, rg, ms);
+            merge_row<E, NW>(a, ly, rg, ms, w);
             const int nb = ms.nbest;
             if (blockIdx.x == 0)
                 for (int t = threadIdx.x; t < a.K; t += kBlock) a.idx[rg * a.K + t] = t < nb ? ms.bid[t] : -1;
@@ -701,7 +711,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
     const int ngrp = (a.N + NQ - 1) / NQ;
     const int b = blockIdx.z / ngrp, n0 = (blockIdx.z % ngrp) * NQ, g = blockIdx.y;
     const int nq = min(NQ, a.N - n0);
-    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
     __shared__ ScanSmem<G, NQ> ss;
     __shared__ float s_lse[NQ][G];
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
@@ -829,8 +839,8 @@ __global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a, int G, int D) {
     __shared__ MergeSmem<kBlock / kWave> ms;
     const int b = blockIdx.y / a.N, n = blockIdx.y % a.N, g = blockIdx.x;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
-    merge_row<E, kBlock / kWave>(a, ly, rg, ms);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    merge_row<E, kBlock / kWave>(a, ly, rg, ms, wave_id());
     for (int t = threadIdx.x; t < a.K; t += kBlock) a.idx[rg * a.K + t] = t < ms.nbest ? ms.bid[t] : -1;
 }
 
@@ -843,7 +853,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_parts(FwdArgs a) {
     __shared__ int s_c;
     const int slot = blockIdx.x, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
     const int pos = decode_position(a, b, n);
     auto run = [&](int part, int c, int nk, bool is_chunk) {
         if constexpr (kMfma)
@@ -954,7 +964,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
     __shared__ CombineSmem<G> cs;
     const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
     combine_row<T, D, G, kBlock>(a, ly, cs, b, n, g, rg);
 }
 
@@ -1152,12 +1162,12 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     bf16* tiles = reinterpret_cast<bf16*>(s_raw);
     const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B * a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
     const int pos = decode_position(a, b, n);
     const int ncand = n_candidates(pos, a.W);
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
     if constexpr (E > 0) {
-        merge_row<E, kRowWaves>(a, ly, rg, ms);
+        merge_row<E, kRowWaves>(a, ly, rg, ms, w);
         if (tid < a.K) {
             const int v = tid < ms.nbest ? ms.bid[tid] : -1;
             s_sel[tid] = v;
@@ -1176,6 +1186,387 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     combine_row<bf16, D, G, NT>(a, ly, cs, b, n, g, rg);
 }
 
+// ---- bf16, several new queries per sequence: one workgroup per query group -----
+// The sequence's new queries are taken NQ = min(8, 16 / G) at a time, and the
+// NQ x G (query, head) rows fill the 16 rows of one MFMA tile (row r: query r / G,
+// head r % G).  Each workgroup selects for its queries (merge_row, 8 / NQ waves per
+// query), builds the union of their chunks in LDS (the retrieved ones and the local
+// windows' chunks, each flagged per query), computes every union chunk once for all
+// 16 rows -- row r keeps the whole chunk if its query retrieved it, the keys up to
+// its query's position if the chunk is in that query's window, nothing otherwise --
+// and then fuses each row's parts.  A chunk that several of the queries use is read
+// from HBM once; drafted tokens of one sequence share their window entirely.
+template <int G>
+struct MqCfg {
+    static constexpr int NQ = 16 / G < 8 ? 16 / G : 8;  // queries per workgroup
+    static constexpr int WPQ = kRowWaves / NQ;            // merge waves per query
+};
+
+template <int D, int G, int E, bool ROUTE>
+__global__ __launch_bounds__(kRowWaves * kWave) void k_dec_mq(FwdArgs a) {
+    using C = MqCfg<G>;
+    constexpr int NQ = C::NQ, WPQ = C::WPQ, NT = kRowWaves * kWave;
+    constexpr int KS = D / 32, DB = D / 16, VROW = PartWaveSmem<D>::VROW, PV = kChunk * D / 8 / kWave;
+    constexpr int kTileBytes = (int)sizeof(PartWaveSmem<D>) * kRowWaves;
+    constexpr int RECF = 4 + D;  // floats per record
+    static_assert(NQ * sizeof(MergeSmem<WPQ>) <= (size_t)kTileBytes, "the merge scratch fits in the part tiles");
+    static_assert(16 * kMqMaxUnion * sizeof(float) <= (size_t)kTileBytes, "the fusion weights fit in the part tiles");
+    // part tiles; before the parts the merges' scratch and the union bitmap, after them
+    // the fusion weights, in the same bytes
+    __shared__ __align__(16) unsigned char s_raw[kTileBytes];
+    __shared__ int s_sel[NQ][64];
+    __shared__ int s_nsel[NQ];
+    __shared__ int s_u[kMqMaxUnion];       // union chunk ids, ascending
+    __shared__ unsigned s_flag[kMqMaxUnion];  // bit q: in query q's window; bit 16 + q: retrieved by query q
+    __shared__ int s_nu;
+    __shared__ float s_lse[16];
+    const int ngrp = (a.N + NQ - 1) / NQ;
+    const int g = blockIdx.x, b = blockIdx.y / ngrp, n0 = (blockIdx.y % ngrp) * NQ;
+    const int nq = min(NQ, a.N - n0);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16, n16 = lane % 16;
+    auto row_of = [&](int q) { return ((size_t)b * a.Hkv + g) * a.N + n0 + q; };
+
+    // ---- selection for each query ----
+    {
+        const int q = w / WPQ, qc = min(q, nq - 1);
+        if constexpr (E > 0) {
+            MergeSmem<WPQ>& ms = reinterpret_cast<MergeSmem<WPQ>*>(s_raw)[q];
+            merge_row<E, WPQ>(a, ly, row_of(qc), ms, w % WPQ);  // every wave: the same barriers
+            if (w % WPQ == 0 && q < nq) {
+                for (int t = lane; t < a.K; t += kWave) {
+                    const int v = t < ms.nbest ? ms.bid[t] : -1;
+                    if (t < 64) s_sel[q][t] = v;
+                    a.idx[row_of(q) * a.K + t] = v;
+                }
+                if (lane == 0) s_nsel[q] = ms.nbest;
+            }
+        } else {
+            if (w % WPQ == 0 && q < nq) {
+                // the valid entries of the given row, in order
+                const int32_t* irow = a.idx + row_of(q) * a.K;
+                const int ncand = n_candidates(decode_position(a, b, n0 + q), a.W);
+                const bool ok = lane < a.K && idx_entry_valid(irow, lane, ncand);
+                const uint64_t bal = __ballot(ok);
+                if (ok) s_sel[q][popc64(bal & ((1ull << lane) - 1ull))] = irow[lane];
+                if (lane == 0) s_nsel[q] = popc64(bal);
+            }
+        }
+    }
+    __syncthreads();
+    // ---- the union of the queries' chunks: a bitmap over the chunks, then its set bits ----
+    unsigned* bits = reinterpret_cast<unsigned*>(s_raw);
+    const int nwords = (ly.nC + 31) / 32;
+    for (int i = tid; i < nwords; i += NT) bits[i] = 0u;
+    __syncthreads();
+    for (int e = tid; e < NQ * 64; e += NT) {
+        const int q = e / 64, t = e % 64;
+        if (q < nq && t < s_nsel[q]) {
+            const int c = s_sel[q][t];
+            atomicOr(&bits[c >> 5], 1u << (c & 31));
+        }
+    }
+    for (int e = tid; e < NQ * kMaxLocalPieces; e += NT) {
+        const int q = e / kMaxLocalPieces, piece = e % kMaxLocalPieces;
+        if (q >= nq || piece >= ly.nlocal) continue;
+        const int pos = decode_position(a, b, n0 + q);
+        const int c = n_candidates(pos, a.W) + piece;
+        if (c <= pos / kChunk) atomicOr(&bits[c >> 5], 1u << (c & 31));
+    }
+    __syncthreads();
+    if (w == 0) {
+        int base = 0;
+        for (int w0 = 0; w0 < nwords; w0 += kWave) {
+            unsigned word = w0 + lane < nwords ? bits[w0 + lane] : 0u;
+            const int cnt = __popc(word);
+            int incl = cnt;
+#pragma unroll
+            for (int o2 = 1; o2 < kWave; o2 <<= 1) {
+                const int y = __shfl_up(incl, o2, kWave);
+                if (lane >= o2) incl += y;
+            }
+            int pos = base + incl - cnt;
+            while (word) {
+                if (pos < kMqMaxUnion) s_u[pos] = (w0 + lane) * 32 + __ffs(word) - 1;
+                ++pos;
+                word &= word - 1u;
+            }
+            base += __shfl(incl, kWave - 1, kWave);
+        }
+        if (lane == 0) s_nu = min(base, kMqMaxUnion);  // the host keeps the union within kMqMaxUnion
+    }
+    __syncthreads();
+    const int U = s_nu;
+    for (int i = tid; i < U; i += NT) {
+        const int c = s_u[i];
+        unsigned f = 0u;
+        for (int q = 0; q < nq; ++q) {
+            const int pos = decode_position(a, b, n0 + q);
+            if (c >= n_candidates(pos, a.W) && c <= pos / kChunk) f |= 1u << q;
+        }
+        s_flag[i] = f;
+    }
+    __syncthreads();
+    for (int e = tid; e < NQ * 64; e += NT) {
+        const int q = e / 64, t = e % 64;
+        if (q < nq && t < s_nsel[q]) {
+            const int c = s_sel[q][t];
+            int lo = 0, hi = U - 1;  // c is in the union: binary search
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (s_u[mid] < c) lo = mid + 1;
+                else hi = mid;
+            }
+            atomicOr(&s_flag[lo], 1u << (16 + q));
+        }
+    }
+    __syncthreads();  // the union is set; the bitmap's bytes are free for the tiles
+
+    // ---- the parts: union chunk u by wave u % 8, for all 16 rows ----
+    float* recs = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.mq) +
+                  ((size_t)(blockIdx.y * gridDim.x + blockIdx.x) * ly.mq_umax) * 16 * RECF;
+    {
+        const int rq = n16 / G, rh = n16 % G;             // the lane's tile row: query, head
+        const bool rvalid = rq < nq;
+        const int rpos = decode_position(a, b, n0 + min(rq, nq - 1));
+        bf16* sv = reinterpret_cast<bf16*>(s_raw) + (size_t)w * (sizeof(PartWaveSmem<D>) / sizeof(bf16));
+        const float c1 = a.scale * kLog2e;
+        const bf16x8 zero8 = as_bf16x8(make_uint4(0, 0, 0, 0));
+        bf16x8 qB[KS], qR[ROUTE ? KS : 1];
+        {
+            const size_t qrow = q_row(a, b, g * G + rh, n0 + min(rq, nq - 1));
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 x = ld_bf16x8(as<bf16>(a.q) + qrow * D + ks * 32 + lg * 8);
+                qB[ks] = rvalid ? x : zero8;
+                if constexpr (ROUTE) {
+                    const bf16x8 y = ld_bf16x8(as<bf16>(a.q_route) + qrow * D + ks * 32 + lg * 8);
+                    qR[ks] = rvalid ? y : zero8;
+                }
+            }
+        }
+        const int hl = (a.Hl == a.Hq) ? g * G + rh : g;  // landmark head of the lane's row
+        struct KOp {
+            bf16x8 k[4][KS];
+        };
+        struct VOp {
+            bf16x8 v[PV];
+        };
+        struct LOp {
+            bf16x8 l[KS];
+        };
+        auto load_k = [&](int c, bool real) {
+            KOp x;
+            const bf16* kg = as<bf16>(a.k) + kv_chunk_offset(a, ly.nC, b, g, c, D);
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    x.k[kb][ks] = ld_bf16x8(kg + (real ? (size_t)(kb * 16 + n16) * D + ks * 32 + lg * 8 : 0));
+            return x;
+        };
+        auto load_v = [&](int c, bool real) {
+            VOp x;
+            const bf16* vg = as<bf16>(a.v) + kv_chunk_offset(a, ly.nC, b, g, c, D);
+#pragma unroll
+            for (int u = 0; u < PV; ++u) {
+                const int e = lane + u * kWave, r = e / (D / 8), pc = e % (D / 8);
+                x.v[u] = ld_bf16x8(vg + (real ? (size_t)r * D + pc * 8 : 0));
+            }
+            return x;
+        };
+        auto load_l = [&](int c, bool real) {
+            LOp x;
+            const bf16* lr = as<bf16>(a.lmk) + lmk_row(a, ly.nC, b, hl, c) * D;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) x.l[ks] = ld_bf16x8(lr + (real ? ks * 32 + lg * 8 : 0));
+            return x;
+        };
+        if (w < U) {
+            int c = s_u[w];
+            VOp vx = load_v(c, true);
+            LOp lx = load_l(c, true);
+            KOp kx = load_k(c, true);
+            for (int u = w; u < U; u += kRowWaves) {
+                const bool real = u + kRowWaves < U;  // uniform over the wave
+                const int cn = s_u[real ? u + kRowWaves : u];
+                const unsigned f = s_flag[u];
+                const bool loc = rvalid && ((f >> rq) & 1u), ret = rvalid && ((f >> (16 + rq)) & 1u);
+                // keys of the chunk the lane's row attends to
+                const int nk = ret ? kChunk : (loc ? min(kChunk, rpos - c * kChunk + 1) : 0);
+                // V rows into the wave's tile; rows no tile row attends to are zeroed
+                const int nkmax = (int)wave_max((float)nk);
+#pragma unroll
+                for (int uu = 0; uu < PV; ++uu) {
+                    const int e = lane + uu * kWave, r = e / (D / 8), pc = e % (D / 8);
+                    *reinterpret_cast<bf16x8*>(sv + r * VROW + pc * 8) = r < nkmax ? vx.v[uu] : zero8;
+                }
+                vx = load_v(cn, real);
+                // s^ of the chunk for row n16 (diagonal of landmark rows x q^)
+                f32x4 s4 = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) s4 = mfma16x16x32(lx.l[ks], ROUTE ? qR[ks] : qB[ks], s4);
+                lx = load_l(cn, real);
+                float dg = s4[0];
+#pragma unroll
+                for (int i = 1; i < 4; ++i)
+                    if (n16 % 4 == i) dg = s4[i];
+                const float sdiag = __shfl(dg, n16 + 16 * (n16 / 4), kWave);
+                const float* bsrc = a.bias ? a.bias + lmk_row(a, ly.nC, b, hl, c) : reinterpret_cast<const float*>(a.lmk);
+                const float bv = *bsrc;
+                const float sh = a.scale * sdiag + (a.bias ? bv : 0.f);
+                // S^T (lane: row n16, keys 16 kb + 4 lg + i), in log2 units
+                f32x4 st[4];
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb) {
+                    st[kb] = zero4();
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) st[kb] = mfma16x16x32(kx.k[kb][ks], qB[ks], st[kb]);
+                }
+                kx = load_k(cn, real);
+                float mx = -INFINITY;
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        st[kb][i] = kb * 16 + lg * 4 + i < nk ? st[kb][i] * c1 : -INFINITY;
+                        mx = fmaxf(mx, st[kb][i]);
+                    }
+                mx = group4_max(mx);
+                const float muse = mx == -INFINITY ? 0.f : mx;
+                float ls = 0.f;
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        st[kb][i] = fexp2(st[kb][i] - muse);
+                        ls += st[kb][i];
+                    }
+                ls = group4_sum(ls);
+                const bf16x8 pb0 = pack_bf16x8_4x2(st[0], st[1]);
+                const bf16x8 pb1 = pack_bf16x8_4x2(st[2], st[3]);
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                // the record of (u, row n16): m, l (0: the row does not use the chunk), s^, o
+                // (rows that do not use the chunk write nothing; the fusion reads only
+                // the records its flags name)
+                float* rec = recs + ((size_t)u * 16 + n16) * RECF;
+                if (lg == 0 && nk > 0) {
+                    rec[0] = mx * (1.f / kLog2e);
+                    rec[1] = ls;
+                    rec[2] = ret ? sh : -INFINITY;
+                }
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    f32x4 o = mfma16x16x32(tr_operand_perm(sv, VROW, 0, db * 16, lane), pb0, zero4());
+                    o = mfma16x16x32(tr_operand_perm(sv, VROW, 32, db * 16, lane), pb1, o);
+                    if (nk > 0) *reinterpret_cast<f32x4*>(rec + 4 + db * 16 + lg * 4) = o;
+                }
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                c = cn;
+            }
+        }
+    }
+    __syncthreads();  // every record written; the tiles' bytes now hold the fusion weights
+
+    // ---- fusion, per tile row r (query r / G, head r % G) ----
+    // wave w takes rows w and w + 8: the headers {m, l, s^} of the row's parts (lane
+    // l: union entries l, l + 64, ...; at most kMqMaxUnion / 64 per lane) are read once,
+    // and the row's parts with a nonzero weight are listed in LDS (entry, weight)
+    constexpr int UPL = kMqMaxUnion / kWave;
+    float* s_wt = reinterpret_cast<float*>(s_raw);                   // [16][kMqMaxUnion]
+    int* s_wu = reinterpret_cast<int*>(s_raw) + 16 * kMqMaxUnion;    // [16][kMqMaxUnion]
+    __shared__ int s_wn[16];
+    static_assert(2 * 16 * kMqMaxUnion * sizeof(float) <= (size_t)kTileBytes, "the part lists fit in the tiles");
+    for (int r = w; r < 16; r += kRowWaves) {
+        const int q = r / G;
+        if (q >= nq) continue;
+        float hm[UPL], hl_[UPL], hs[UPL];
+        bool isl[UPL], isr[UPL];
+#pragma unroll
+        for (int t = 0; t < UPL; ++t) {
+            const int u = lane + t * kWave;
+            const unsigned f = u < U ? s_flag[u] : 0u;
+            isl[t] = (f >> q) & 1u;
+            isr[t] = (f >> (16 + q)) & 1u;
+            const float* rc = recs + ((size_t)min(u, U - 1) * 16 + r) * RECF;
+            hm[t] = rc[0];
+            hl_[t] = rc[1];
+            hs[t] = rc[2];
+        }
+        // local pieces (window chunks of query q) by online softmax, then the chunks it retrieved
+        float m0 = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < UPL; ++t)
+            if (isl[t]) m0 = fmaxf(m0, hm[t]);
+        m0 = wave_max(m0);
+        float l0 = 0.f, zmax = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < UPL; ++t) {
+            if (isl[t] && hl_[t] > 0.f) l0 += hl_[t] * fexp(hm[t] - m0);
+            if (isr[t] && hl_[t] > 0.f) zmax = fmaxf(zmax, hs[t]);
+        }
+        l0 = wave_sum(l0);
+        const float lam0 = m0 + __logf(l0);
+        const float M = fmaxf(wave_max(zmax), lam0);
+        float Z = 0.f;
+#pragma unroll
+        for (int t = 0; t < UPL; ++t)
+            if (isr[t] && hl_[t] > 0.f) Z += fexp(hs[t] - M);
+        Z = wave_sum(Z) + fexp(lam0 - M);
+        const float L = M + __logf(Z);
+        const float a0 = fexp(lam0 - L) / l0;
+        int base = 0;
+#pragma unroll
+        for (int t = 0; t < UPL; ++t) {
+            float wt = 0.f;
+            if (isl[t] && hl_[t] > 0.f) wt = a0 * fexp(hm[t] - m0);
+            else if (isr[t] && hl_[t] > 0.f) wt = fexp(hs[t] - L) / hl_[t];
+            const bool nz = wt != 0.f;
+            const uint64_t bal = __ballot(nz);
+            if (nz) {
+                const int at = base + popc64(bal & ((1ull << lane) - 1ull));
+                s_wt[r * kMqMaxUnion + at] = wt;
+                s_wu[r * kMqMaxUnion + at] = lane + t * kWave;
+            }
+            base += popc64(bal);
+        }
+        if (lane == 0) {
+            s_lse[r] = L;
+            s_wn[r] = base;
+        }
+    }
+    __syncthreads();
+    // outputs: thread t -> row t / (D/4), dims 4 (t % (D/4)) ...; the row's listed
+    // parts in batches of 16 loads in flight
+    constexpr int TPR = D / 4;     // threads per row
+    constexpr int RPP = NT / TPR;  // rows per pass
+    for (int r = tid / TPR; r < 16; r += RPP) {
+        const int q = r / G, d0 = (tid % TPR) * 4;
+        if (q >= nq) continue;
+        const int cnt = s_wn[r];
+        f32x4 acc = zero4();
+        for (int j0 = 0; j0 < cnt; j0 += 16) {
+            f32x4 v[16];
+            float wt[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int jj = min(j0 + j, cnt - 1);
+                wt[j] = j0 + j < cnt ? s_wt[r * kMqMaxUnion + jj] : 0.f;
+                v[j] = *reinterpret_cast<const f32x4*>(recs + ((size_t)s_wu[r * kMqMaxUnion + jj] * 16 + r) * RECF + 4 + d0);
+            }
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+                if (wt[j] != 0.f) acc += wt[j] * v[j];
+        }
+        const size_t orow = q_row(a, b, g * G + r % G, n0 + q);
+        *reinterpret_cast<uint2*>(as_mut<bf16>(a.out) + orow * D + d0) =
+            make_uint2(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]));
+        if (d0 == 0) a.lse[orow] = s_lse[r];
+    }
+}
+
 // Compute units of the current device (a host-side attribute query; nothing cached).
 int device_cus() {
     int dev = 0, n = 0;
@@ -1189,7 +1580,7 @@ struct DecRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
         const int R = a.B * a.N;  // rows (sequence, new query); the host keeps R <= 65535
-        const DecLayout ly = dec_layout(R, a.Hkv, G, D, a.L, a.K, a.W);
+        const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
         if (!a.given_idx) {
             // one new query per sequence: a workgroup per (slice, group, row); several:
             // the sequence's queries four at a time share each landmark read
@@ -1218,7 +1609,26 @@ struct DecRun {
         if constexpr (sizeof(T) == 2) {
             const int surv = ly.nslices * a.K;  // the scan's survivors per row
             const int rows = R * a.Hkv;
-            if (rows >= kRowPassMinRows && rows <= device_cus()) {
+            constexpr int NQ = MqCfg<G>::NQ, WPQ = MqCfg<G>::WPQ;
+            if (a.N > 1 && ly.mq_umax <= kMqMaxUnion) {
+                // several new queries per sequence: a workgroup per group of NQ of them
+                const dim3 mgrid(a.Hkv, a.B * ((a.N + NQ - 1) / NQ)), mblock(kRowWaves * kWave);
+                auto mq = [&](auto e_tag) {
+                    constexpr int EE = decltype(e_tag)::value;
+                    if (a.q_route)
+                        HILS_LAUNCH("k_dec_mq", (k_dec_mq<D, G, EE, true>), mgrid, mblock, 0, s, a);
+                    else
+                        HILS_LAUNCH("k_dec_mq", (k_dec_mq<D, G, EE, false>), mgrid, mblock, 0, s, a);
+                };
+                if (a.given_idx)
+                    mq(std::integral_constant<int, 0>{});
+                else if (surv <= WPQ * kWave * 4)
+                    mq(std::integral_constant<int, 4>{});
+                else if (surv <= WPQ * kWave * 8)
+                    mq(std::integral_constant<int, 8>{});
+                else
+                    mq(std::integral_constant<int, 16>{});
+            } else if (rows >= kRowPassMinRows && rows <= device_cus()) {
                 // a workgroup per row; one merge round covers kRowWaves * 64 * E survivors
                 const dim3 rgrid(a.Hkv, R), rblock(kRowWaves * kWave);
                 auto row = [&](auto e_tag) {
@@ -1265,7 +1675,7 @@ struct DecRun {
 }  // namespace
 
 size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W) {
-    return dec_layout(B * N, Hkv, G, d, L, K, W).total;
+    return dec_layout(B, N, Hkv, G, d, L, K, W).total;
 }
 
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s) {

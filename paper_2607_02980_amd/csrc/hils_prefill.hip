@@ -1,6 +1,6 @@
 // HiLS attention prefill forward on MFMA (bf16 storage, fp32 accumulation), gfx950.
 //
-//   P1 k_pf_score    per 64-query tile: s^_hc = scale * q^_h . k'_c (+ b') on 16x16x32
+//   P1 k_pf_score    per 32-query tile: s^_hc = scale * q^_h . k'_c (+ b') on 16x16x32
 //                    MFMA tiles, the group max over the G heads (App. C), and the
 //                    top-K of every row (exact register radix select, Eq. (9)).  Also
 //                    writes ref = the row's best group score (>= every selected s^_hc).
@@ -38,7 +38,7 @@ namespace hils {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kSQ = 64;   // queries per score tile (4 waves x 16)
+constexpr int kSQ = 32;   // queries per score tile (two 16-row MFMA tiles)
 constexpr int kSL = 256;  // candidate chunks per score slice
 
 struct PfLayout {
@@ -143,40 +143,53 @@ __device__ __forceinline__ void lse16_merge(float& m, float& s) {
 // gives each (row, head) its log-sum-exp over C_i; the second subtracts it
 // before the maximum over the group's heads.  ref is then the largest of the
 // row's per-head log-sum-exps (>= every raw s^ of the row).
+//
+// Four waves per 32-row tile: wave w scores chunk blocks w, w + 4, ... of each
+// slice against all rows, then selects rows 8w .. 8w + 7 one after another.  Both
+// phases are latency-bound (L2 loads, then chains of ballots), so the tile is kept
+// small enough (33 KB of scores in LDS, <= 128 VGPRs) for four blocks per CU.  The
+// rows' running best lists (K entries each) live in dynamic LDS, so the row loop
+// is not unrolled: one copy of the selection code.
+constexpr int kSW = 4;           // waves per score block
+constexpr int kSR = kSQ / kSW;   // rows selected per wave
+size_t score_dyn_lds(int K) { return (size_t)kSQ * K * (sizeof(float) + sizeof(int)) + kSQ * sizeof(int); }
 template <int D, int G, bool NORM>
-__global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) {
+__global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs a, float* ref_out) {
     constexpr int KS = Tiles<D>::KS;
     constexpr int NCB = kSL / 16;
     constexpr int E = kSL / kWave;
+    constexpr int NJ = NCB / kSW, NT = kSQ / 16;
+    static_assert(NJ * kSW == NCB, "chunk blocks split evenly over the waves");
     __shared__ float s_sig[kSQ][kSL + 1];
-    __shared__ int s_tid[4][64], s_oid[4][64];
-    __shared__ float s_tsc[4][64], s_osc[4][64];
+    __shared__ int s_tid[kSW][64];
+    __shared__ float s_tsc[kSW][64];
     __shared__ float s_lse[NORM ? G : 1][kSQ];
+    extern __shared__ int s_dyn[];
+    const int K = a.K;
+    float* s_bsc = reinterpret_cast<float*>(s_dyn);          // [kSQ][K] running best scores
+    int* s_bid = reinterpret_cast<int*>(s_bsc + kSQ * K);    // [kSQ][K] their chunks (ascending)
+    int* s_nb = s_bid + kSQ * K;                             // [kSQ] list lengths
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
+    // 1-D grid, KV group fastest: workgroups are dealt round-robin to the 8 XCDs, so
+    // with Hkv = 8 each XCD scores one group and keeps that group's landmarks in its
+    // L2; tiles in descending order, the longest candidate lists first
     const int ntiles = (a.N + kSQ - 1) / kSQ;
-    const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
+    const int g = blockIdx.x % a.Hkv, rest = blockIdx.x / a.Hkv;
+    const int tile = ntiles - 1 - rest % ntiles, b = rest / ntiles;
     const int q0 = tile * kSQ;
     const int qlast = min(q0 + kSQ - 1, a.N - 1);
     const int nct = n_candidates(qlast, a.W);
     const int nC = a.L / kChunk;
-    const int qw0 = q0 + 16 * w;
+    const int qw0 = q0 + kSR * w;
     const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q);
     const bf16* lmk = as<bf16>(a.lmk);
+    if (lane < kSR) s_nb[kSR * w + lane] = 0;  // a wave's rows are its own: no barrier needed
 
-    float bsc[16];
-    int bid[16], nb[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        bsc[r] = 0.f;
-        bid[r] = -1;
-        nb[r] = 0;
-    }
-    constexpr int NJ = NCB / 4, NT = kSQ / 16;
     if constexpr (NORM) {
         // pass 1: per (row, head) log-sum-exp of s^ over the row's candidates; the
         // per-wave partials live in s_sig until the slices need it
-        float* s_pm = &s_sig[0][0];     // [4 waves][G][kSQ]
-        float* s_ps = s_pm + 4 * G * kSQ;
+        float* s_pm = &s_sig[0][0];     // [kSW waves][G][kSQ]
+        float* s_ps = s_pm + kSW * G * kSQ;
         const int lg = lane / 16;
         for (int hh = 0; hh < G; ++hh) {
             const int h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
@@ -194,7 +207,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
                 float bv[NJ];
 #pragma unroll
                 for (int j = 0; j < NJ; ++j) {
-                    const int c = min(s0 + (w + 4 * j) * 16 + lane % 16, nC - 1);
+                    const int c = min(s0 + (w + kSW * j) * 16 + lane % 16, nC - 1);
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks) bl[j][ks] = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + lg * 8);
                     bv[j] = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
@@ -212,7 +225,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
                         f32x4 acc4 = zero4();
 #pragma unroll
                         for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[ks], bl[j][ks], acc4);
-                        const int c = s0 + (w + 4 * j) * 16 + lane % 16;
+                        const int c = s0 + (w + kSW * j) * 16 + lane % 16;
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             const int n = q0 + 16 * t + lg * 4 + i;
@@ -245,14 +258,14 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
                 }
         }
         __syncthreads();
-        for (int e = tid; e < G * kSQ; e += kBlock) {
+        for (int e = tid; e < G * kSQ; e += kSW * kWave) {
             const int hh = e / kSQ, row = e % kSQ;
             float m = -INFINITY;
 #pragma unroll
-            for (int ww = 0; ww < 4; ++ww) m = fmaxf(m, s_pm[(ww * G + hh) * kSQ + row]);
+            for (int ww = 0; ww < kSW; ++ww) m = fmaxf(m, s_pm[(ww * G + hh) * kSQ + row]);
             float sum = 0.f;
 #pragma unroll
-            for (int ww = 0; ww < 4; ++ww) {
+            for (int ww = 0; ww < kSW; ++ww) {
                 const float pm = s_pm[(ww * G + hh) * kSQ + row];
                 sum += pm == -INFINITY ? 0.f : s_ps[(ww * G + hh) * kSQ + row] * fexp(pm - m);
             }
@@ -263,7 +276,7 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
     for (int s0 = 0; s0 < nct; s0 += kSL) {
         const int len = min(kSL, nct - s0);
         const int ncb = (len + 15) / 16;
-        // Wave w scores chunk blocks cb = w + 4j (j < NCB/4) against all kSQ rows of the
+        // Wave w scores chunk blocks cb = w + kSW j (j < NJ) against all kSQ rows of the
         // tile (4 row tiles), so each landmark operand it loads feeds 4 MFMAs; all of a
         // head's landmark loads are issued before its MFMAs.
         f32x4 sig[NT][NJ];
@@ -271,39 +284,39 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
         for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int j = 0; j < NJ; ++j) sig[t][j] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll 1
         for (int hh = 0; hh < G; ++hh) {
             const int h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
             const bf16* lbase = lmk + ((size_t)b * a.Hl + hl) * nC * D;
-            bf16x8 bl[NJ][KS];
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const int c = min(s0 + (w + 4 * j) * 16 + lane % 16, nC - 1);
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) bl[j][ks] = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + (lane / 16) * 8);
-            }
-            float bv[NJ];
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const int c = min(s0 + (w + 4 * j) * 16 + lane % 16, nC - 1);
-                bv[j] = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
-            }
+            // the tile's query operands once per head, then the landmark blocks one
+            // at a time, each feeding the NT row tiles
+            bf16x8 aq[NT][KS];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const int qa = min(q0 + 16 * t + lane % 16, a.N - 1);
-                bf16x8 aq[KS];
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks)
-                    aq[ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + h) * a.N + qa) * D + ks * 32 + (lane / 16) * 8);
-                float sub[4];
+                    aq[t][ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + h) * a.N + qa) * D + ks * 32 + (lane / 16) * 8);
+            }
+            float sub[NT][4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) sub[i] = NORM ? s_lse[hh][16 * t + (lane / 16) * 4 + i] : 0.f;
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) {
+                for (int i = 0; i < 4; ++i) sub[t][i] = NORM ? s_lse[hh][16 * t + (lane / 16) * 4 + i] : 0.f;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const int c = min(s0 + (w + kSW * j) * 16 + lane % 16, nC - 1);
+                bf16x8 bl[KS];
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) bl[ks] = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + (lane / 16) * 8);
+                const float bv = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
                     f32x4 acc4 = zero4();
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[ks], bl[j][ks], acc4);
+                    for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[t][ks], bl[ks], acc4);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) sig[t][j][i] = fmaxf(sig[t][j][i], a.scale * acc4[i] + bv[j] - sub[i]);
+                    for (int i = 0; i < 4; ++i) sig[t][j][i] = fmaxf(sig[t][j][i], a.scale * acc4[i] + bv - sub[t][i]);
                 }
             }
         }
@@ -313,14 +326,14 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
         for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
-                if (w + 4 * j < ncb)
+                if (w + kSW * j < ncb)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        s_sig[16 * t + (lane / 16) * 4 + i][(w + 4 * j) * 16 + lane % 16] = sig[t][j][i];
+                        s_sig[16 * t + (lane / 16) * 4 + i][(w + kSW * j) * 16 + lane % 16] = sig[t][j][i];
         __syncthreads();
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int n = qw0 + r;
+#pragma unroll 1
+        for (int r = 0; r < kSR; ++r) {
+            const int n = qw0 + r, row = kSR * w + r;
             if (n >= a.N) break;
             const int lim = min(n_candidates(n, a.W), s0 + len) - s0;
             if (lim <= 0) continue;
@@ -331,33 +344,34 @@ __global__ __launch_bounds__(kBlock) void k_pf_score(FwdArgs a, float* ref_out) 
             for (int e = 0; e < E; ++e) {
                 const int col = e * kWave + lane;
                 ok[e] = col < lim;
-                sc[e] = ok[e] ? s_sig[16 * w + r][col] : 0.f;
+                sc[e] = ok[e] ? s_sig[row][col] : 0.f;
                 id[e] = s0 + col;
             }
-            ok[E] = lane < nb[r];
-            sc[E] = bsc[r];
-            id[E] = bid[r];
+            const int nb = s_nb[row];
+            ok[E] = lane < nb;
+            sc[E] = ok[E] ? s_bsc[row * K + lane] : 0.f;
+            id[E] = ok[E] ? s_bid[row * K + lane] : -1;
             // ids ascend over (register E: the running best, all below s0; then
-            // registers 0.. : s0 + e*64 + lane)
-            nb[r] = wave_topk_reg<E + 1, E>(sc, id, ok, a.K, s_oid[w], s_osc[w], s_tid[w], s_tsc[w]);
-            bsc[r] = lane < nb[r] ? s_osc[w][lane] : 0.f;
-            bid[r] = lane < nb[r] ? s_oid[w][lane] : -1;
+            // registers 0.. : s0 + e*64 + lane); the selection rewrites the row's list
+            const int m = wave_topk_reg<E + 1, E>(sc, id, ok, K, s_bid + row * K, s_bsc + row * K, s_tid[w], s_tsc[w]);
+            if (lane == 0) s_nb[row] = m;
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
         }
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int n = qw0 + r;
+#pragma unroll 1
+    for (int r = 0; r < kSR; ++r) {
+        const int n = qw0 + r, row = kSR * w + r;
         if (n >= a.N) break;
-        int32_t* orow = a.idx + (((size_t)b * a.Hkv + g) * a.N + n) * a.K;
-        if (lane < a.K) orow[lane] = lane < nb[r] ? bid[r] : -1;
-        float top = wave_max(lane < nb[r] ? bsc[r] : -INFINITY);
+        const int nb = s_nb[row];
+        int32_t* orow = a.idx + (((size_t)b * a.Hkv + g) * a.N + n) * K;
+        if (lane < K) orow[lane] = lane < nb ? s_bid[row * K + lane] : -1;
+        float top = wave_max(lane < nb ? s_bsc[row * K + lane] : -INFINITY);
         if constexpr (NORM) {
             float lm = -INFINITY;
 #pragma unroll
-            for (int hh = 0; hh < G; ++hh) lm = fmaxf(lm, s_lse[hh][16 * w + r]);
-            top = nb[r] > 0 ? lm : -INFINITY;
+            for (int hh = 0; hh < G; ++hh) lm = fmaxf(lm, s_lse[hh][row]);
+            top = nb > 0 ? lm : -INFINITY;
         }
         if (lane == 0) ref_out[((size_t)b * a.Hkv + g) * a.N + n] = top;
     }
@@ -931,11 +945,12 @@ struct PfRun {
         if (a.given_idx) {
             HILS_LAUNCH("k_pf_ref_given", (k_pf_ref_given<D, G>), dim3(a.N, a.Hkv, a.B), dim3(kWave), 0, s, a, ref);
         } else {
-            const dim3 grid((a.N + kSQ - 1) / kSQ, a.Hkv, a.B);
+            const dim3 grid((unsigned)((a.N + kSQ - 1) / kSQ) * a.Hkv * a.B);
+            const size_t dyn = score_dyn_lds(a.K);
             if (a.head_norm)
-                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kBlock), 0, s, a, ref);
+                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a, ref);
             else
-                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kBlock), 0, s, a, ref);
+                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kSW * kWave), dyn, s, a, ref);
         }
         const dim3 lgrid((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B);
         if (a.union_pack && !a.given_idx) {

@@ -193,9 +193,14 @@ __global__ void k_fill_i32(int* p, size_t n, int v) {
 // Entries are processed per (b, g) in blocks of kInvRows rows; a block first
 // counts its entries per chunk in LDS and then touches each global counter
 // once, so global atomics scale with (blocks x chunks touched), not entries.
+// Counters are kept per (chunk, row bucket): every list is the concatenation of
+// its buckets' sub-lists in bucket order, so a consumer can take the entries of
+// one chunk that fall in one range of rows (the chunk pass walks the buckets in
+// order, so the query rows it gathers stay in L2).
 // List entries are (n << 6) | slot (slot < K <= 64).
 constexpr int kInvRows = 256;
 constexpr int kInvHist = 8192;  // chunks counted in LDS; larger L falls back to global atomics
+static_assert(kInvBucketRows % kInvRows == 0, "a block of rows lies in one bucket");
 
 __device__ __forceinline__ bool entry_valid(const InvArgs& a, const int32_t* irow, int slot, int n, int* c) {
     if (!idx_entry_valid(irow, slot, n_candidates(n, a.W))) return false;
@@ -203,13 +208,13 @@ __device__ __forceinline__ bool entry_valid(const InvArgs& a, const int32_t* iro
     return true;
 }
 
-// grid (ceil(N / kInvRows), B*Hkv)
-__global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int* counts) {
+// grid (ceil(N / kInvRows), B*Hkv); counts [bg][nC * nR]
+__global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int nR, int* counts) {
     __shared__ int s_hist[kInvHist];
     const int bg = blockIdx.y, n0 = blockIdx.x * kInvRows, tid = threadIdx.x;
-    const int nC = a.L / kChunk;
+    const int nC = a.L / kChunk, R = n0 / kInvBucketRows;
     const bool lds = nC <= kInvHist;
-    int* gcnt = counts + (size_t)bg * nC;
+    int* gcnt = counts + (size_t)bg * nC * nR;
     if (lds)
         for (int c = tid; c < nC; c += kBlock) s_hist[c] = 0;
     __syncthreads();
@@ -222,21 +227,21 @@ __global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int* counts) {
         if (lds)
             atomicAdd(&s_hist[c], 1);
         else
-            atomicAdd(&gcnt[c], 1);
+            atomicAdd(&gcnt[c * nR + R], 1);
     }
     __syncthreads();
     if (lds)
         for (int c = tid; c < nC; c += kBlock)
-            if (s_hist[c]) atomicAdd(&gcnt[c], s_hist[c]);
+            if (s_hist[c]) atomicAdd(&gcnt[c * nR + R], s_hist[c]);
 }
 
-__global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, const int* offsets, int* cursor, int* list) {
+__global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, const int* boff, int* cursor, int* list) {
     __shared__ int s_hist[kInvHist];
     const int bg = blockIdx.y, n0 = blockIdx.x * kInvRows, tid = threadIdx.x;
-    const int nC = a.L / kChunk;
+    const int nC = a.L / kChunk, R = n0 / kInvBucketRows;
     const bool lds = nC <= kInvHist;
-    int* gcur = cursor + (size_t)bg * nC;
-    const int* off = offsets + (size_t)bg * (nC + 1);
+    int* gcur = cursor + (size_t)bg * nC * nR;
+    const int* off = boff + (size_t)bg * (nC * nR + 1);
     int* lst = list + (size_t)bg * a.N * a.K;
     const int rows = min(kInvRows, a.N - n0);
     if (lds) {
@@ -250,28 +255,31 @@ __global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, const int* offse
         __syncthreads();
         // reserve this block's range of every chunk it touches; s_hist becomes the running position
         for (int c = tid; c < nC; c += kBlock)
-            if (s_hist[c]) s_hist[c] = off[c] + atomicAdd(&gcur[c], s_hist[c]);
+            if (s_hist[c]) s_hist[c] = off[c * nR + R] + atomicAdd(&gcur[c * nR + R], s_hist[c]);
         __syncthreads();
     }
     for (int e = tid; e < rows * a.K; e += kBlock) {
         const int n = n0 + e / a.K, slot = e % a.K;
         int c;
         if (!entry_valid(a, a.idx + ((size_t)bg * a.N + n) * a.K, slot, n, &c)) continue;
-        const int pos = lds ? atomicAdd(&s_hist[c], 1) : off[c] + atomicAdd(&gcur[c], 1);
+        const int pos = lds ? atomicAdd(&s_hist[c], 1) : off[c * nR + R] + atomicAdd(&gcur[c * nR + R], 1);
         lst[pos] = (n << 6) | slot;
     }
 }
 
-// one block per (b, g): exclusive scan of the nC counts into offsets[nC + 1]
-__global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* offsets, int nC) {
+// one block per (b, g): exclusive scan of the nC * nR counts (chunk-major) into
+// boff[nC * nR + 1], and each chunk's whole list into offsets[nC + 1]
+__global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* boff, int* offsets, int nC, int nR) {
     __shared__ int s_part[kBlock];
     const int bg = blockIdx.x, tid = threadIdx.x;
-    const int per = (nC + kBlock - 1) / kBlock;
-    const int lo = min(nC, tid * per), hi = min(nC, lo + per);
-    const int* cnt = counts + (size_t)bg * nC;
+    const int M = nC * nR;
+    const int per = (M + kBlock - 1) / kBlock;
+    const int lo = min(M, tid * per), hi = min(M, lo + per);
+    const int* cnt = counts + (size_t)bg * M;
+    int* bo = boff + (size_t)bg * (M + 1);
     int* off = offsets + (size_t)bg * (nC + 1);
     int sum = 0;
-    for (int c = lo; c < hi; ++c) sum += cnt[c];
+    for (int i = lo; i < hi; ++i) sum += cnt[i];
     s_part[tid] = sum;
     __syncthreads();
     if (tid == 0) {
@@ -281,46 +289,59 @@ __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* off
             s_part[t] = run;
             run += x;
         }
+        bo[M] = run;
         off[nC] = run;
     }
     __syncthreads();
     int run = s_part[tid];
-    for (int c = lo; c < hi; ++c) {
-        off[c] = run;
-        run += cnt[c];
+    for (int i = lo; i < hi; ++i) {
+        bo[i] = run;
+        if (i % nR == 0) off[i / nR] = run;
+        run += cnt[i];
     }
 }
 
 InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base) {
     const size_t bg = (size_t)B * Hkv, nC = (size_t)L / kChunk;
     InvLayout w;
+    w.nR = (N + kInvBucketRows - 1) / kInvBucketRows;
+    const size_t M = nC * (size_t)w.nR;
     w.counts = align256(base);
-    w.offsets = align256(w.counts + bg * nC * sizeof(int));
-    w.cursor = align256(w.offsets + bg * (nC + 1) * sizeof(int));
-    w.list = align256(w.cursor + bg * nC * sizeof(int));
-    w.max_work = bg * ((size_t)N * K / kInvSeg + nC);
+    w.offsets = align256(w.counts + bg * M * sizeof(int));
+    w.boff = align256(w.offsets + bg * (nC + 1) * sizeof(int));
+    w.cursor = align256(w.boff + bg * (M + 1) * sizeof(int));
+    w.list = align256(w.cursor + bg * M * sizeof(int));
+    // A (chunk, bucket) sub-list of len entries makes ceil(len / kInvSeg) <= len / kInvSeg
+    // + 1 items, and only the chunks c < n / kChunk of a bucket's last row n can
+    // have entries there (a candidate chunk ends before the query): at most
+    // (R + 1) * kInvBucketRows / kChunk sub-lists of bucket R are not empty.
+    size_t subl = 0;
+    for (int R = 0; R < w.nR; ++R) subl += std::min(nC, (size_t)(R + 1) * (kInvBucketRows / kChunk));
+    w.max_work_bg = (size_t)N * K / kInvSeg + subl;
     w.work = align256(w.list + bg * (size_t)N * K * sizeof(int));
-    w.nwork = align256(w.work + w.max_work * sizeof(int4));
-    w.end = align256(w.nwork + sizeof(int));
+    w.nwork = align256(w.work + bg * w.max_work_bg * sizeof(int4));
+    w.end = align256(w.nwork + bg * sizeof(int));
     return w;
 }
 
-// Work list: every (bg, c) list is cut into segments of kInvSeg entries.
-// One block: a running count over (bg, c) in order assigns each segment a slot.
-__global__ __launch_bounds__(kBlock) void k_inv_work(const int* offsets, int nbg, int nC, int4* work, int* nwork) {
+// Work items of one (b, g) (one block each): its (chunk, bucket) sub-lists cut into
+// segments of kInvSeg entries, bucket-major, so that the items in flight together
+// work on one range of rows.
+__global__ __launch_bounds__(kBlock) void k_inv_work(const int* boff, int nC, int nR, size_t max_work_bg, int4* work,
+                                                     int* nwork) {
     __shared__ int s_part[kBlock];
-    const int tid = threadIdx.x;
-    const long total = (long)nbg * nC;
-    const long per = (total + kBlock - 1) / kBlock;
-    const long lo = min(total, (long)tid * per), hi = min(total, lo + per);
-    auto nseg = [&](long i) {
-        const int bg = (int)(i / nC), c = (int)(i % nC);
-        const int* off = offsets + (size_t)bg * (nC + 1);
-        const int len = off[c + 1] - off[c];
-        return (len + kInvSeg - 1) / kInvSeg;
+    const int bg = blockIdx.x, tid = threadIdx.x;
+    const int M = nC * nR;
+    const int* bo = boff + (size_t)bg * (M + 1);
+    int4* wk = work + (size_t)bg * max_work_bg;
+    const int per = (M + kBlock - 1) / kBlock;
+    const int lo = min(M, tid * per), hi = min(M, lo + per);
+    auto nseg = [&](int i) {  // i = R * nC + c
+        const int j = (i % nC) * nR + i / nC;
+        return (bo[j + 1] - bo[j] + kInvSeg - 1) / kInvSeg;
     };
     int sum = 0;
-    for (long i = lo; i < hi; ++i) sum += nseg(i);
+    for (int i = lo; i < hi; ++i) sum += nseg(i);
     s_part[tid] = sum;
     __syncthreads();
     if (tid == 0) {
@@ -330,13 +351,13 @@ __global__ __launch_bounds__(kBlock) void k_inv_work(const int* offsets, int nbg
             s_part[t] = run;
             run += x;
         }
-        *nwork = run;
+        nwork[bg] = run;
     }
     __syncthreads();
     int run = s_part[tid];
-    for (long i = lo; i < hi; ++i) {
+    for (int i = lo; i < hi; ++i) {
         const int ns = nseg(i);
-        for (int sgi = 0; sgi < ns; ++sgi) work[run + sgi] = make_int4((int)(i / nC), (int)(i % nC), sgi, 0);
+        for (int sgi = 0; sgi < ns; ++sgi) wk[run + sgi] = make_int4(i / nC, i % nC, sgi, 0);
         run += ns;
     }
 }
@@ -345,20 +366,22 @@ void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStr
     char* base = static_cast<char*>(ws);
     int* counts = reinterpret_cast<int*>(base + w.counts);
     int* offsets = reinterpret_cast<int*>(base + w.offsets);
+    int* boff = reinterpret_cast<int*>(base + w.boff);
     int* cursor = reinterpret_cast<int*>(base + w.cursor);
     int* list = reinterpret_cast<int*>(base + w.list);
     const int nC = a.L / kChunk;
-    const size_t ncnt = (size_t)a.B * a.Hkv * nC;
+    const size_t ncnt = (size_t)a.B * a.Hkv * nC * w.nR;
     const unsigned gc = (unsigned)((ncnt + kBlock - 1) / kBlock);
     const dim3 grows((a.N + kInvRows - 1) / kInvRows, a.B * a.Hkv);
     HILS_LAUNCH("k_fill_i32", k_fill_i32, dim3(gc), dim3(kBlock), 0, s, counts, ncnt, 0);
     HILS_LAUNCH("k_fill_i32", k_fill_i32, dim3(gc), dim3(kBlock), 0, s, cursor, ncnt, 0);
-    HILS_LAUNCH("k_inv_count", k_inv_count, grows, dim3(kBlock), 0, s, a, counts);
-    HILS_LAUNCH("k_inv_scan", k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, offsets, nC);
-    HILS_LAUNCH("k_inv_fill", k_inv_fill, grows, dim3(kBlock), 0, s, a, (const int*)offsets, cursor, list);
+    HILS_LAUNCH("k_inv_count", k_inv_count, grows, dim3(kBlock), 0, s, a, w.nR, counts);
+    HILS_LAUNCH("k_inv_scan", k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, boff, offsets,
+                nC, w.nR);
+    HILS_LAUNCH("k_inv_fill", k_inv_fill, grows, dim3(kBlock), 0, s, a, w.nR, (const int*)boff, cursor, list);
     if (work_list)
-        HILS_LAUNCH("k_inv_work", k_inv_work, dim3(1), dim3(kBlock), 0, s, (const int*)offsets, a.B * a.Hkv, nC,
-                       reinterpret_cast<int4*>(base + w.work), reinterpret_cast<int*>(base + w.nwork));
+        HILS_LAUNCH("k_inv_work", k_inv_work, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)boff, nC, w.nR,
+                    w.max_work_bg, reinterpret_cast<int4*>(base + w.work), reinterpret_cast<int*>(base + w.nwork));
 }
 
 // ---------------------------------------------------------------------------
@@ -570,7 +593,7 @@ struct BwdRun {
         const int* list = reinterpret_cast<const int*>(ws + w.list);
         const int nC = a.L / kChunk;
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
-        launch_inverse_index(ia, w, a.ws, s);
+        launch_inverse_index(ia, w, a.ws, s, false);
         HILS_LAUNCH("k_bwd_dq_rows", (k_bwd_dq_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
         HILS_LAUNCH("k_bwd_dkdv_chunks", (k_bwd_dkdv_chunks<T, D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a,
                            offsets, list);

@@ -1567,15 +1567,6 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_mq(FwdArgs a) {
     }
 }
 
-// Compute units of the current device (a host-side attribute query; nothing cached).
-int device_cus() {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-        return 256;
-    return n;
-}
-
 struct DecRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
@@ -1673,6 +1664,16 @@ struct DecRun {
 };
 
 }  // namespace
+
+// Compute units of the current device (a host-side attribute query; nothing cached).
+int device_cus() {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        return 256;
+    return n;
+}
+
 
 size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W) {
     return dec_layout(B, N, Hkv, G, d, L, K, W).total;

@@ -96,27 +96,30 @@ struct InvArgs {
 };
 struct InvLayout {
     size_t counts, offsets, cursor, list;  // byte offsets from the workspace base
-    size_t work;    // work items (bg, chunk, segment) of at most kInvSeg list entries each
-    size_t nwork;   // one int: number of work items
+    size_t boff;    // [bg][nC * nR + 1]: start of the (chunk, row bucket) sub-lists
+    size_t work;    // [bg][max_work_bg] work items (row bucket, chunk, segment, 0)
+    size_t nwork;   // [bg] number of work items of each (b, g)
     size_t end;
-    size_t max_work;  // upper bound of work items (grid size of the consumers)
+    int nR;              // row buckets of kInvBucketRows rows
+    size_t max_work_bg;  // upper bound of the work items of one (b, g)
 };
-constexpr int kInvSeg = 256;  // list entries per work item
+constexpr int kInvSeg = 256;          // list entries per work item
+constexpr int kInvBucketRows = 2048;  // rows per bucket: a chunk's list is ordered by bucket
 InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base);
-// work_list = false skips the (bg, chunk, segment) work items (consumers that walk
-// whole lists do not read them).
+// Every (b, g, chunk) list is sorted by row bucket (the sub-list of bucket R starts
+// at boff[c * nR + R]); offsets[c] .. offsets[c + 1] bound the whole list.
+// work_list = false skips the work items (consumers that walk whole lists do not
+// read them).
 void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStream_t s, bool work_list = true);
-
-// Work item encoding: bg * (nC * segs_max) ... decoded by the consumers.
-struct WorkItem {
-    int bg, c, seg;
-};
 
 // Workspace layout of the backward (byte offsets from ws).
 struct BwdWorkspace {
     size_t counts, offsets, cursor, list, total;
 };
 BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K);
+
+// Compute units of the current device (a host-side attribute query; nothing cached).
+int device_cus();
 
 size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W);
 

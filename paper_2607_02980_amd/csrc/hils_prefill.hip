@@ -419,7 +419,10 @@ __global__ __launch_bounds__(kWave) void k_pf_ref_given(FwdArgs a, float* ref_ou
 // ---------------------------------------------------------------------------
 // P3: retrieved chunks, chunk-major
 // ---------------------------------------------------------------------------
-// One block per work item: kInvSeg consecutive entries of one (b, g, chunk) list.
+// One block per work item: up to kInvSeg entries of one (b, g, chunk) list that
+// lie in one bucket of 2048 rows.  The items of a (b, g) come bucket by bucket,
+// so the query rows that the blocks in flight gather (2048 rows x G heads, 2 MiB
+// at d = 128) stay in the L2s.
 // Units of work are (16 entries, head) pairs; wave w takes units w, w + 4, ...
 // K and V^T of the chunk are held in registers as MFMA operands for the whole
 // block, and the next unit's rows are fetched while the current one computes.
@@ -431,8 +434,9 @@ __global__ __launch_bounds__(kWave) void k_pf_ref_given(FwdArgs a, float* ref_ou
 // without bank conflicts), V rows by 16 (transposing 8-byte reads without
 // conflicts).
 template <int D, int G, bool ROUTE>
-__global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, const int* offsets, const int* list,
-                                                                    const int4* work, const int* nwork,
+__global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, const int* boff, int nR,
+                                                                    const int* list, const int4* work,
+                                                                    size_t max_work_bg, const int* nwork,
                                                                     const float* ref, bf16* part, float* wgt) {
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
     constexpr int KROW = Tiles<D>::KROW, VROW = D + 16;
@@ -443,13 +447,17 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
     __shared__ int s_ent[kInvSeg];  // the segment's entries (row << 6 | slot)
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
-    if ((int)blockIdx.x >= *nwork) return;
+    // blocks of (b, g) = bg are bg * max_work_bg + item: those past its item count leave
+    const size_t bg = blockIdx.x / max_work_bg;
+    const int item = (int)(blockIdx.x % max_work_bg);
+    if (item >= nwork[bg]) return;
     const int4 wi = work[blockIdx.x];
     const int c = wi.y;
-    const size_t bg = (size_t)wi.x;
     const int b = (int)(bg / a.Hkv), g = (int)(bg % a.Hkv);
-    const int beg = offsets[bg * (nC + 1) + c] + wi.z * kInvSeg;
-    const int len = min(kInvSeg, offsets[bg * (nC + 1) + c + 1] - beg);
+    const int* bo = boff + bg * ((size_t)nC * nR + 1);
+    const int jb = c * nR + wi.x;
+    const int beg = bo[jb] + wi.z * kInvSeg;
+    const int len = min(kInvSeg, bo[jb + 1] - beg);
     if (len <= 0) return;
     const int* seg = list + bg * a.N * a.K + beg;
     static_assert(kInvSeg <= kBlock, "one entry per thread");
@@ -977,16 +985,17 @@ struct PfRun {
         }
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
         launch_inverse_index(ia, ly.inv, a.ws, s);
-        const int* offsets = reinterpret_cast<const int*>(ws + ly.inv.offsets);
+        const int* boff = reinterpret_cast<const int*>(ws + ly.inv.boff);
         const int* list = reinterpret_cast<const int*>(ws + ly.inv.list);
         const int4* work = reinterpret_cast<const int4*>(ws + ly.inv.work);
         const int* nwork = reinterpret_cast<const int*>(ws + ly.inv.nwork);
+        const dim3 cgrid((unsigned)(ly.inv.max_work_bg * a.B * a.Hkv));
         if (a.q_route)
-            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, true>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
-                        offsets, list, work, nwork, (const float*)ref, part, wgt);
+            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, true>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR, list,
+                        work, ly.inv.max_work_bg, nwork, (const float*)ref, part, wgt);
         else
-            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), dim3((unsigned)ly.inv.max_work), dim3(kBlock), 0, s, a,
-                        offsets, list, work, nwork, (const float*)ref, part, wgt);
+            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR, list,
+                        work, ly.inv.max_work_bg, nwork, (const float*)ref, part, wgt);
         HILS_LAUNCH("k_pf_local", (k_pf_local<D, G, false, false>), lgrid, dim3(LocalCfg<G>::NT), 0, s, a,
                     (const float*)ref, (const bf16*)part, (const float*)wgt);
         return hipGetLastError();

@@ -251,11 +251,12 @@ __device__ inline int wave_topk(const float* sc, const int* id, int n, int K, in
 // directly.
 constexpr int kTopkUnordered = -2, kTopkNatural = -1;
 
-// m-th largest value of one 32-bit key per lane (0 if fewer than m lanes hold
+// m-th largest value of one NB-bit key per lane (0 if fewer than m lanes hold
 // a key >= 1): the bits of the threshold from the top, one ballot each.
+template <int NB = 32>
 __device__ __forceinline__ uint32_t wave_kth_key(uint32_t x, int m) {
     uint32_t T = 0;
-    for (int bit = 31; bit >= 0; --bit) {
+    for (int bit = NB - 1; bit >= 0; --bit) {
         const uint32_t t = T | (1u << bit);
         if (popc64(__ballot(x >= t)) >= m) T = t;
     }
@@ -289,14 +290,16 @@ __device__ inline int wave_topk_reg(const float (&sc)[E], const int (&id)[E], co
     const bool all = (n <= K);
     constexpr bool kOrdered = FIRST != kTopkUnordered;
     if (!all && E > 1) {
-        // Fast path.  The m-th largest of the lane maxima, T0, is a lower bound of
-        // the m-th largest key (m lanes hold a key >= T0), so the m best entries
-        // are among the survivors key >= T0.  When they fit one per lane they are
-        // compacted in visiting order and selected with one-register passes.
+        // Fast path.  The m-th largest of the lane maxima is a lower bound of the
+        // m-th largest key (m lanes hold a key at least as large), and so is T0,
+        // that bound with its low 16 bits cleared (found in 16 ballot steps), so
+        // the m best entries are among the survivors key >= T0.  When they fit one
+        // per lane they are compacted in visiting order and selected with
+        // one-register passes.
         uint32_t lmax = 0;
 #pragma unroll
         for (int r = 0; r < E; ++r) lmax = key[r] > lmax ? key[r] : lmax;
-        uint32_t T0 = wave_kth_key(lmax, m);
+        uint32_t T0 = wave_kth_key<16>(lmax >> 16, m) << 16;
         T0 = T0 ? T0 : 1u;
         const int c = count_ge(T0);
         if (c <= kWave) {

@@ -138,26 +138,13 @@ struct ScanSmem {
     float osc[NQ][64], tsc[NQ][64];
 };
 
-// 8 consecutive elements of an LDS row as floats (one 16-byte read for bf16).
-__device__ __forceinline__ void lds_load8(const unsigned char* p, float* o, bf16) {
-    const uint4 w = *reinterpret_cast<const uint4*>(p);
-    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        o[2 * t] = __uint_as_float(u[t] << 16);
-        o[2 * t + 1] = __uint_as_float(u[t] & 0xffff0000u);
-    }
-}
+// 8 consecutive elements of an fp32 LDS row.
 __device__ __forceinline__ void lds_load8(const unsigned char* p, float* o, float) {
     const float4 x = *reinterpret_cast<const float4*>(p);
     const float4 y = *reinterpret_cast<const float4*>(p + 16);
     o[0] = x.x; o[1] = x.y; o[2] = x.z; o[3] = x.w; o[4] = y.x; o[5] = y.y; o[6] = y.z; o[7] = y.w;
 }
-// 2 consecutive elements of an LDS row as floats.
-__device__ __forceinline__ float2 lds_load2(const unsigned char* p, bf16) {
-    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
-    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
-}
+// 2 consecutive elements of an fp32 LDS row.
 __device__ __forceinline__ float2 lds_load2(const unsigned char* p, float) {
     return *reinterpret_cast<const float2*>(p);
 }
@@ -1165,7 +1152,7 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
     const int pos = decode_position(a, b, n);
     const int ncand = n_candidates(pos, a.W);
-    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
+    const int tid = threadIdx.x, w = wave_id();
     if constexpr (E > 0) {
         merge_row<E, kRowWaves>(a, ly, rg, ms, w);
         if (tid < a.K) {

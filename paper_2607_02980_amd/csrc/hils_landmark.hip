@@ -187,7 +187,6 @@ __global__ __launch_bounds__(kBlock) void k_lmk_dq_sum(LmkArgs a) {
 // Backward: dK'-scores GP^T = K dK'^T the same way, ds, dq' = scale K^T DS^T, and
 // dK = [P | scale DS] [dK' ; q'] as one (keys x 32) by (32 x dims) product per
 // tile, its A operand transposed through LDS.
-constexpr int kLmkVRow(int D) { return D + 16; }
 
 template <int D>
 struct LmkWaveSmem {

@@ -126,10 +126,6 @@ __device__ __forceinline__ bf16x8 p_operand(const f32x4& e0, const f32x4& e1) {
     float x[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
     return pack_bf16x8(x);
 }
-__device__ __forceinline__ bf16x8 p_operand(const float* e0, const float* e1) {
-    float x[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
-    return pack_bf16x8(x);
-}
 
 // ---------------------------------------------------------------------------
 // P1: scores, group max, top-K
@@ -797,8 +793,6 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     if constexpr (UNION) {
         // the union's chunks, each for all rows of the tile
         const int U = s_nu;
-        const int hl = (a.Hl == a.Hq) ? g * G + hh : g;
-        const bf16* lbase = as<bf16>(a.lmk) + ((size_t)b * a.Hl + hl) * nC * D;
         bf16x8 bqr[ROUTE ? KS : 1];
         if constexpr (ROUTE) {
             const bf16* rrow = as<bf16>(a.q_route) + row * D;

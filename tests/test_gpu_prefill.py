@@ -20,6 +20,9 @@ CASES = {
     "bf16_ragged_multi_tile": (dict(B=2, Hq=8, Hkv=2, N=1000, L=1024, d=128, topk=8, window=200), 101, False, False,
                                0.0),
     "bf16_window1": (dict(B=1, Hq=4, Hkv=1, N=1024, L=1024, d=128, topk=8, window=1), 102, False, False, 0.0),
+    # three 2048-row buckets of the chunk pass's inverse index, the last one ragged
+    "bf16_row_buckets_ragged": (dict(B=2, Hq=8, Hkv=2, N=4500, L=4544, d=64, topk=8, window=256), 111, False, False,
+                                0.0),
     "bf16_bias_boosted": (dict(B=1, Hq=8, Hkv=2, N=768, L=768, d=64, topk=4, window=64), 103, True, False, 4.0),
     "bf16_route_Hl_eq_Hkv": (dict(B=1, Hq=8, Hkv=2, Hl=2, N=640, L=640, d=64, topk=6, window=100), 104, True, True,
                              0.0),

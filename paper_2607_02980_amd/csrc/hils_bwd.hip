@@ -208,7 +208,8 @@ __device__ __forceinline__ bool entry_valid(const InvArgs& a, const int32_t* iro
     return true;
 }
 
-// grid (ceil(N / kInvRows), B*Hkv); counts [bg][nC * nR]
+// grid (ceil(N / kInvRows), B*Hkv); counts [bg][nR][nC] (a block's counters are
+// contiguous: one bucket)
 __global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int nR, int* counts) {
     __shared__ int s_hist[kInvHist];
     const int bg = blockIdx.y, n0 = blockIdx.x * kInvRows, tid = threadIdx.x;
@@ -227,12 +228,12 @@ __global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int nR, int* co
         if (lds)
             atomicAdd(&s_hist[c], 1);
         else
-            atomicAdd(&gcnt[c * nR + R], 1);
+            atomicAdd(&gcnt[R * nC + c], 1);
     }
     __syncthreads();
     if (lds)
         for (int c = tid; c < nC; c += kBlock)
-            if (s_hist[c]) atomicAdd(&gcnt[c * nR + R], s_hist[c]);
+            if (s_hist[c]) atomicAdd(&gcnt[R * nC + c], s_hist[c]);
 }
 
 __global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, const int* boff, int* cursor, int* list) {
@@ -255,20 +256,20 @@ __global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, const in
         __syncthreads();
         // reserve this block's range of every chunk it touches; s_hist becomes the running position
         for (int c = tid; c < nC; c += kBlock)
-            if (s_hist[c]) s_hist[c] = off[c * nR + R] + atomicAdd(&gcur[c * nR + R], s_hist[c]);
+            if (s_hist[c]) s_hist[c] = off[c * nR + R] + atomicAdd(&gcur[R * nC + c], s_hist[c]);
         __syncthreads();
     }
     for (int e = tid; e < rows * a.K; e += kBlock) {
         const int n = n0 + e / a.K, slot = e % a.K;
         int c;
         if (!entry_valid(a, a.idx + ((size_t)bg * a.N + n) * a.K, slot, n, &c)) continue;
-        const int pos = lds ? atomicAdd(&s_hist[c], 1) : off[c * nR + R] + atomicAdd(&gcur[c * nR + R], 1);
+        const int pos = lds ? atomicAdd(&s_hist[c], 1) : off[c * nR + R] + atomicAdd(&gcur[R * nC + c], 1);
         lst[pos] = (n << 6) | slot;
     }
 }
 
-// one block per (b, g): exclusive scan of the nC * nR counts (chunk-major) into
-// boff[nC * nR + 1], and each chunk's whole list into offsets[nC + 1]
+// one block per (b, g): exclusive scan of the nR x nC counts in chunk-major order
+// into boff[nC * nR + 1], and each chunk's whole list into offsets[nC + 1]
 __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* boff, int* offsets, int nC, int nR) {
     __shared__ int s_part[kBlock];
     const int bg = blockIdx.x, tid = threadIdx.x;
@@ -279,7 +280,8 @@ __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* bof
     int* bo = boff + (size_t)bg * (M + 1);
     int* off = offsets + (size_t)bg * (nC + 1);
     int sum = 0;
-    for (int i = lo; i < hi; ++i) sum += cnt[i];
+    auto count = [&](int i) { return cnt[(i % nR) * nC + i / nR]; };  // i = c * nR + R
+    for (int i = lo; i < hi; ++i) sum += count(i);
     s_part[tid] = sum;
     __syncthreads();
     if (tid == 0) {
@@ -297,7 +299,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* bof
     for (int i = lo; i < hi; ++i) {
         bo[i] = run;
         if (i % nR == 0) off[i / nR] = run;
-        run += cnt[i];
+        run += count(i);
     }
 }
 

@@ -268,10 +268,35 @@ __global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, const in
     }
 }
 
+// Exclusive prefix sum of one int per thread over a kBlock-thread block (wave
+// scans by shuffles, then the wave totals); every thread gets the block total.
+// Contains barriers: called by every thread of the block.
+__device__ __forceinline__ int block_exclusive_scan(int x, int* s_wave, int* total) {
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    int incl = x;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+    }
+    if (lane == kWave - 1) s_wave[w] = incl;
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int i = 0; i < kBlock / kWave; ++i) {
+        const int t = s_wave[i];
+        before += i < w ? t : 0;
+        all += t;
+    }
+    __syncthreads();  // s_wave may be reused by the caller
+    *total = all;
+    return before + incl - x;
+}
+
 // one block per (b, g): exclusive scan of the nR x nC counts in chunk-major order
 // into boff[nC * nR + 1], and each chunk's whole list into offsets[nC + 1]
 __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* boff, int* offsets, int nC, int nR) {
-    __shared__ int s_part[kBlock];
+    __shared__ int s_part[kBlock / kWave];
     const int bg = blockIdx.x, tid = threadIdx.x;
     const int M = nC * nR;
     const int per = (M + kBlock - 1) / kBlock;
@@ -282,20 +307,12 @@ __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* bof
     int sum = 0;
     auto count = [&](int i) { return cnt[(i % nR) * nC + i / nR]; };  // i = c * nR + R
     for (int i = lo; i < hi; ++i) sum += count(i);
-    s_part[tid] = sum;
-    __syncthreads();
+    int total;
+    int run = block_exclusive_scan(sum, s_part, &total);
     if (tid == 0) {
-        int run = 0;
-        for (int t = 0; t < kBlock; ++t) {
-            const int x = s_part[t];
-            s_part[t] = run;
-            run += x;
-        }
-        bo[M] = run;
-        off[nC] = run;
+        bo[M] = total;
+        off[nC] = total;
     }
-    __syncthreads();
-    int run = s_part[tid];
     for (int i = lo; i < hi; ++i) {
         bo[i] = run;
         if (i % nR == 0) off[i / nR] = run;
@@ -331,7 +348,7 @@ InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base) {
 // work on one range of rows.
 __global__ __launch_bounds__(kBlock) void k_inv_work(const int* boff, int nC, int nR, size_t max_work_bg, int4* work,
                                                      int* nwork) {
-    __shared__ int s_part[kBlock];
+    __shared__ int s_part[kBlock / kWave];
     const int bg = blockIdx.x, tid = threadIdx.x;
     const int M = nC * nR;
     const int* bo = boff + (size_t)bg * (M + 1);
@@ -344,19 +361,9 @@ __global__ __launch_bounds__(kBlock) void k_inv_work(const int* boff, int nC, in
     };
     int sum = 0;
     for (int i = lo; i < hi; ++i) sum += nseg(i);
-    s_part[tid] = sum;
-    __syncthreads();
-    if (tid == 0) {
-        int run = 0;
-        for (int t = 0; t < kBlock; ++t) {
-            const int x = s_part[t];
-            s_part[t] = run;
-            run += x;
-        }
-        nwork[bg] = run;
-    }
-    __syncthreads();
-    int run = s_part[tid];
+    int total;
+    int run = block_exclusive_scan(sum, s_part, &total);
+    if (tid == 0) nwork[bg] = total;
     for (int i = lo; i < hi; ++i) {
         const int ns = nseg(i);
         for (int sgi = 0; sgi < ns; ++sgi) wk[run + sgi] = make_int4(i / nC, i % nC, sgi, 0);

@@ -210,10 +210,10 @@ __device__ __forceinline__ bool entry_valid(const InvArgs& a, const int32_t* iro
 
 // grid (ceil(N / kInvRows), B*Hkv); counts [bg][nR][nC] (a block's counters are
 // contiguous: one bucket)
-__global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int nR, int* counts) {
+__global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int nR, int brows, int* counts) {
     __shared__ int s_hist[kInvHist];
     const int bg = blockIdx.y, n0 = blockIdx.x * kInvRows, tid = threadIdx.x;
-    const int nC = a.L / kChunk, R = n0 / kInvBucketRows;
+    const int nC = a.L / kChunk, R = n0 / brows;
     const bool lds = nC <= kInvHist;
     int* gcnt = counts + (size_t)bg * nC * nR;
     if (lds)
@@ -236,10 +236,11 @@ __global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int nR, int* co
             if (s_hist[c]) atomicAdd(&gcnt[R * nC + c], s_hist[c]);
 }
 
-__global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, const int* boff, int* cursor, int* list) {
+__global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, int brows, const int* boff, int* cursor,
+                                                     int* list) {
     __shared__ int s_hist[kInvHist];
     const int bg = blockIdx.y, n0 = blockIdx.x * kInvRows, tid = threadIdx.x;
-    const int nC = a.L / kChunk, R = n0 / kInvBucketRows;
+    const int nC = a.L / kChunk, R = n0 / brows;
     const bool lds = nC <= kInvHist;
     int* gcur = cursor + (size_t)bg * nC * nR;
     const int* off = boff + (size_t)bg * (nC * nR + 1);
@@ -323,7 +324,9 @@ __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* bof
 InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base) {
     const size_t bg = (size_t)B * Hkv, nC = (size_t)L / kChunk;
     InvLayout w;
-    w.nR = (N + kInvBucketRows - 1) / kInvBucketRows;
+    w.brows = kInvBucketRows;
+    while ((size_t)w.brows * K < 64 * nC && w.brows < N) w.brows *= 2;
+    w.nR = (N + w.brows - 1) / w.brows;
     const size_t M = nC * (size_t)w.nR;
     w.counts = align256(base);
     w.offsets = align256(w.counts + bg * M * sizeof(int));
@@ -333,9 +336,9 @@ InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base) {
     // A (chunk, bucket) sub-list of len entries makes ceil(len / kInvSeg) <= len / kInvSeg
     // + 1 items, and only the chunks c < n / kChunk of a bucket's last row n can
     // have entries there (a candidate chunk ends before the query): at most
-    // (R + 1) * kInvBucketRows / kChunk sub-lists of bucket R are not empty.
+    // (R + 1) * brows / kChunk sub-lists of bucket R are not empty.
     size_t subl = 0;
-    for (int R = 0; R < w.nR; ++R) subl += std::min(nC, (size_t)(R + 1) * (kInvBucketRows / kChunk));
+    for (int R = 0; R < w.nR; ++R) subl += std::min(nC, (size_t)(R + 1) * (w.brows / kChunk));
     w.max_work_bg = (size_t)N * K / kInvSeg + subl;
     w.work = align256(w.list + bg * (size_t)N * K * sizeof(int));
     w.nwork = align256(w.work + bg * w.max_work_bg * sizeof(int4));
@@ -384,10 +387,11 @@ void launch_inverse_index(const InvArgs& a, const InvLayout& w, void* ws, hipStr
     const dim3 grows((a.N + kInvRows - 1) / kInvRows, a.B * a.Hkv);
     HILS_LAUNCH("k_fill_i32", k_fill_i32, dim3(gc), dim3(kBlock), 0, s, counts, ncnt, 0);
     HILS_LAUNCH("k_fill_i32", k_fill_i32, dim3(gc), dim3(kBlock), 0, s, cursor, ncnt, 0);
-    HILS_LAUNCH("k_inv_count", k_inv_count, grows, dim3(kBlock), 0, s, a, w.nR, counts);
+    HILS_LAUNCH("k_inv_count", k_inv_count, grows, dim3(kBlock), 0, s, a, w.nR, w.brows, counts);
     HILS_LAUNCH("k_inv_scan", k_inv_scan, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)counts, boff, offsets,
                 nC, w.nR);
-    HILS_LAUNCH("k_inv_fill", k_inv_fill, grows, dim3(kBlock), 0, s, a, w.nR, (const int*)boff, cursor, list);
+    HILS_LAUNCH("k_inv_fill", k_inv_fill, grows, dim3(kBlock), 0, s, a, w.nR, w.brows, (const int*)boff, cursor,
+                list);
     if (work_list)
         HILS_LAUNCH("k_inv_work", k_inv_work, dim3(a.B * a.Hkv), dim3(kBlock), 0, s, (const int*)boff, nC, w.nR,
                     w.max_work_bg, reinterpret_cast<int4*>(base + w.work), reinterpret_cast<int*>(base + w.nwork));

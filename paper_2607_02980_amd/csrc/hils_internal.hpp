@@ -100,11 +100,15 @@ struct InvLayout {
     size_t work;    // [bg][max_work_bg] work items (row bucket, chunk, segment, 0)
     size_t nwork;   // [bg] number of work items of each (b, g)
     size_t end;
-    int nR;              // row buckets of kInvBucketRows rows
+    int nR;              // row buckets
+    int brows;           // rows per bucket (a multiple of kInvBucketRows)
     size_t max_work_bg;  // upper bound of the work items of one (b, g)
 };
 constexpr int kInvSeg = 256;          // list entries per work item
-constexpr int kInvBucketRows = 2048;  // rows per bucket: a chunk's list is ordered by bucket
+// Rows per bucket, at least: a chunk's list is ordered by bucket.  Buckets grow
+// (doubling) until a (chunk, bucket) sub-list holds about 64 entries on average
+// (brows * K >= 64 * L/S), so that long sequences keep full work items.
+constexpr int kInvBucketRows = 2048;
 InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base);
 // Every (b, g, chunk) list is sorted by row bucket (the sub-list of bucket R starts
 // at boff[c * nR + R]); offsets[c] .. offsets[c + 1] bound the whole list.

@@ -416,9 +416,9 @@ __global__ __launch_bounds__(kWave) void k_pf_ref_given(FwdArgs a, float* ref_ou
 // P3: retrieved chunks, chunk-major
 // ---------------------------------------------------------------------------
 // One block per work item: up to kInvSeg entries of one (b, g, chunk) list that
-// lie in one bucket of 2048 rows.  The items of a (b, g) come bucket by bucket,
-// so the query rows that the blocks in flight gather (2048 rows x G heads, 2 MiB
-// at d = 128) stay in the L2s.
+// lie in one bucket of rows (2048, more for long sequences: see kInvBucketRows).
+// The items of a (b, g) come bucket by bucket, so the query rows that the blocks
+// in flight gather (2048 rows x G heads, 2 MiB at d = 128) stay in the L2s.
 // Units of work are (16 entries, head) pairs; wave w takes units w, w + 4, ...
 // K and V^T of the chunk are held in registers as MFMA operands for the whole
 // block, and the next unit's rows are fetched while the current one computes.

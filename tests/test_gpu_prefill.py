@@ -23,6 +23,9 @@ CASES = {
     # three 2048-row buckets of the chunk pass's inverse index, the last one ragged
     "bf16_row_buckets_ragged": (dict(B=2, Hq=8, Hkv=2, N=4500, L=4544, d=64, topk=8, window=256), 111, False, False,
                                 0.0),
+    # K * 2048 < 64 * L/S: the buckets double to 4096 rows
+    "bf16_row_buckets_grown": (dict(B=1, Hq=4, Hkv=1, N=8192, L=8192, d=64, topk=2, window=256), 112, False, False,
+                               0.0),
     "bf16_bias_boosted": (dict(B=1, Hq=8, Hkv=2, N=768, L=768, d=64, topk=4, window=64), 103, True, False, 4.0),
     "bf16_route_Hl_eq_Hkv": (dict(B=1, Hq=8, Hkv=2, Hl=2, N=640, L=640, d=64, topk=6, window=100), 104, True, True,
                              0.0),

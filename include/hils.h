@@ -94,8 +94,9 @@ typedef enum {
  * loads the union of their selected chunks once and computes every chunk for
  * all of its rows (rows that did not select a chunk get weight 0).  Same
  * results as the default chunk-major pass; faster when adjacent queries select
- * overlapping chunks (as trained models do), slower when they do not.  Ignored
- * with HILS_FLAG_GIVEN_IDX, by the fp32 path, decode and the backward. */
+ * overlapping chunks (as trained models do), slower when they do not.  Needs no
+ * workspace (hils_workspace_size reports 0 under this flag).  Ignored by the
+ * fp32 path, decode and the backward. */
 #define HILS_FLAG_UNION_PACKING 8u
 
 typedef enum { HILS_OP_PREFILL = 0, HILS_OP_DECODE = 1, HILS_OP_BWD = 2, HILS_OP_LANDMARK = 3 } hils_op;
@@ -201,8 +202,9 @@ int hils_decode_paged_fwd(const hils_params* p, const void* q, const void* k_pag
  *   dlmk     [B,Hl,L/S,d]    written (chunks no query selected get 0)
  *   dlmk_bias[B,Hl,L/S] f32  written, or NULL to skip
  *   dq_route [B,Hq,N,d]      written when q_route is given (must then be non-NULL)
- * Deterministic: repeated calls with equal inputs produce identical bits as
- * long as no chunk is selected by more than 8192 queries of one KV group.
+ * Deterministic: repeated calls with equal inputs produce identical bits (the
+ * per-chunk lists of selecting rows are sorted before use, so every gradient sum
+ * runs in one fixed order).
  */
 int hils_bwd(const hils_params* p, const void* dout, const void* q, const void* k, const void* v,
              const void* lmk, const float* lmk_bias, const void* q_route, const void* out, const float* lse,

@@ -105,7 +105,8 @@ size_t ws_bytes_for(const hils_params* p, int op) {
             return hils::decode_workspace_bytes(p->B, p->N, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window);
         default:
             return hils::prefill_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk,
-                                                 p->dtype == HILS_BF16);
+                                                 p->dtype == HILS_BF16,
+                                                 (p->flags & HILS_FLAG_UNION_PACKING) != 0);
     }
 }
 

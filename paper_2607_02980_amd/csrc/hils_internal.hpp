@@ -127,7 +127,7 @@ int device_cus();
 
 size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W);
 
-size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16);
+size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16, int union_pack);
 
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s);  // fp32 storage

@@ -2,21 +2,22 @@
 //
 //   P1 k_pf_score    per 32-query tile: s^_hc = scale * q^_h . k'_c (+ b') on 16x16x32
 //                    MFMA tiles, the group max over the G heads (App. C), and the
-//                    top-K of every row (exact register radix select, Eq. (9)).  Also
-//                    writes ref = the row's best group score (>= every selected s^_hc).
+//                    top-K of every row (exact register radix select, Eq. (9)).
 //   inverse index    rows that selected each (b, g, chunk)
 //   P3 k_pf_chunks   chunk-major: K_c, V_c staged once in LDS, the selecting rows
 //                    gathered 16 at a time; S^T = K_c Q^T, the intra-chunk softmax
 //                    (Eq. (10)) and s^ of the (row, head, chunk).  Each (row, head,
-//                    slot) gets its chunk output o_c (bf16 partial) and the weight
-//                    exp(s^ - ref) (float).  A chunk's rows are scattered over the
+//                    slot) gets its chunk output o_c (bf16 partial) and its raw
+//                    surrogate score s^ (float).  A chunk's rows are scattered over the
 //                    sequence, so per-slot partials replace atomics (float atomics on
 //                    gfx950 sustain ~0.3 G-ops/ms, 7 ms for the 32K workload).
 //   P2 k_pf_local    flash-style local window [l(i), i] (Eq. (1)) per tile of 16*8/G
-//                    queries x G heads (8 waves), then the fusion (Eq. (10)) with the
-//                    row's slots summed in slot order: M = max(log Z_swa, ref),
-//                    out = (e^{log Z_swa - M} o_swa + e^{ref - M} sum_k w_k o_k)
-//                          / (e^{log Z_swa - M} + e^{ref - M} sum_k w_k),
+//                    queries x G heads (8 waves), then the fusion (Eq. (10)) of each
+//                    (row, head) with its own stabiliser (App. C: the fusion weights
+//                    are per head even though the selection is shared):
+//                    M = max(log Z_swa, max_k s^_k),
+//                    out = (e^{log Z_swa - M} o_swa + sum_k e^{s^_k - M} o_k)
+//                          / (e^{log Z_swa - M} + sum_k e^{s^_k - M}),
 //                    lse = M + log(denominator).
 //
 // MFMA orientation: attention tiles compute S^T = K Q^T (keys on the M side,
@@ -42,7 +43,7 @@ constexpr int kSQ = 32;   // queries per score tile (two 16-row MFMA tiles)
 constexpr int kSL = 256;  // candidate chunks per score slice
 
 struct PfLayout {
-    size_t part, wgt, ref, inv_base;
+    size_t part, wgt, inv_base;
     InvLayout inv;
     size_t total;
 };
@@ -53,8 +54,8 @@ struct PfLayout {
 // form one contiguous run; slot k of a whole query tile is one contiguous span
 // (32 KiB), which the local pass reads while it sums slot k for all its rows
 // (the row-major order [N, K, G, d] had it jump 16 KiB between rows: 3% slower
-// here, and 4% slower writes).  wgt [B, Hkv, N/QT, K, QT, G] f32,
-// ref [B, Hkv, N] f32, inverse index; N rounded up to a multiple of QT.
+// here, and 4% slower writes).  wgt [B, Hkv, N/QT, K, QT, G] f32 (the raw s^ of
+// each (row, slot, head)), inverse index; N rounded up to a multiple of QT.
 // Element offset of the partial of (row n, slot, head hh) of KV group bg = b * Hkv + g
 // (D = 1: of its weight).
 __device__ __forceinline__ size_t part_offset(size_t bg, int N, int n, int K, int slot, int G, int hh, int D) {
@@ -68,8 +69,7 @@ PfLayout pf_layout(int B, int Hq, int Hkv, int N, int L, int d, int K) {
     const int QT = 128 / (Hq / Hkv);
     const size_t Np = (size_t)(N + QT - 1) / QT * QT;
     w.wgt = align256(w.part + (size_t)B * Hq * Np * K * d * sizeof(uint16_t));
-    w.ref = align256(w.wgt + (size_t)B * Hq * Np * K * sizeof(float));
-    w.inv_base = align256(w.ref + (size_t)B * Hkv * N * sizeof(float));
+    w.inv_base = align256(w.wgt + (size_t)B * Hq * Np * K * sizeof(float));
     w.inv = inv_layout(B, Hkv, N, L, K, w.inv_base);
     w.total = w.inv.end;
     return w;
@@ -145,8 +145,7 @@ __device__ __forceinline__ void lse16_merge(float& m, float& s) {
 
 // NORM: rank by per-head normalised scores.  A first pass over the candidates
 // gives each (row, head) its log-sum-exp over C_i; the second subtracts it
-// before the maximum over the group's heads.  ref is then the largest of the
-// row's per-head log-sum-exps (>= every raw s^ of the row).
+// before the maximum over the group's heads.
 //
 // Four waves per 32-row tile: wave w scores chunk blocks w, w + 4, ... of each
 // slice against all rows, then selects rows 8w .. 8w + 7 one after another.  Both
@@ -158,7 +157,7 @@ constexpr int kSW = 4;           // waves per score block
 constexpr int kSR = kSQ / kSW;   // rows selected per wave
 size_t score_dyn_lds(int K) { return (size_t)kSQ * K * (sizeof(float) + sizeof(int)) + kSQ * sizeof(int); }
 template <int D, int G, bool NORM>
-__global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs a, float* ref_out) {
+__global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs a) {
     constexpr int KS = Tiles<D>::KS;
     constexpr int NCB = kSL / 16;
     constexpr int E = kSL / kWave;
@@ -370,46 +369,7 @@ __global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs 
         const int nb = s_nb[row];
         int32_t* orow = a.idx + (((size_t)b * a.Hkv + g) * a.N + n) * K;
         if (lane < K) orow[lane] = lane < nb ? s_bid[row * K + lane] : -1;
-        float top = wave_max(lane < nb ? s_bsc[row * K + lane] : -INFINITY);
-        if constexpr (NORM) {
-            float lm = -INFINITY;
-#pragma unroll
-            for (int hh = 0; hh < G; ++hh) lm = fmaxf(lm, s_lse[hh][row]);
-            top = nb > 0 ? lm : -INFINITY;
-        }
-        if (lane == 0) ref_out[((size_t)b * a.Hkv + g) * a.N + n] = top;
     }
-}
-
-// Forced selection: ref = the best group score among the given chunks.
-// One wave per (n, g, b) row.
-template <int D, int G>
-__global__ __launch_bounds__(kWave) void k_pf_ref_given(FwdArgs a, float* ref_out) {
-    const int n = blockIdx.x, g = blockIdx.y, b = blockIdx.z, lane = threadIdx.x;
-    const int nC = a.L / kChunk;
-    const int32_t* irow = a.idx + (((size_t)b * a.Hkv + g) * a.N + n) * a.K;
-    const int ncand = n_candidates(n, a.W);
-    float best = -INFINITY;
-    if (lane < a.K && idx_entry_valid(irow, lane, ncand)) {
-        const int c = irow[lane];
-        const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q);
-        for (int hh = 0; hh < G; ++hh) {
-            const int h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
-            const bf16* qrow = qr + (((size_t)b * a.Hq + h) * a.N + n) * D;
-            const bf16* lrow = as<bf16>(a.lmk) + (((size_t)b * a.Hl + hl) * nC + c) * D;
-            float d0 = 0.f;
-            for (int dd = 0; dd < D; dd += 8) {
-                float x[8], y[8];
-                load8(qrow + dd, x);
-                load8(lrow + dd, y);
-#pragma unroll
-                for (int t = 0; t < 8; ++t) d0 += x[t] * y[t];
-            }
-            best = fmaxf(best, a.scale * d0 + (a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f));
-        }
-    }
-    best = wave_max(best);
-    if (lane == 0) ref_out[((size_t)b * a.Hkv + g) * a.N + n] = best;
 }
 
 // ---------------------------------------------------------------------------
@@ -433,7 +393,7 @@ template <int D, int G, bool ROUTE>
 __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, const int* boff, int nR,
                                                                     const int* list, const int4* work,
                                                                     size_t max_work_bg, const int* nwork,
-                                                                    const float* ref, bf16* part, float* wgt) {
+                                                                    bf16* part, float* wgt) {
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
     constexpr int KROW = Tiles<D>::KROW, VROW = D + 16;
     __shared__ __align__(16) bf16 s_k[kChunk * KROW];
@@ -484,7 +444,6 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
 
     struct Ops {
         uint4 q[KS], qr[ROUTE ? KS : 1];
-        float rf;
         int ent;
     };
     // branch-free loads: an entry past the end reads the last entry's row
@@ -499,7 +458,6 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
             x.q[ks] = *reinterpret_cast<const uint4*>(qbase + qrow * D + ks * 32 + lg * 8);
             if constexpr (ROUTE) x.qr[ks] = *reinterpret_cast<const uint4*>(rbase + qrow * D + ks * 32 + lg * 8);
         }
-        x.rf = ref[bg * a.N + (ent >> 6)];
     };
     // a wave's units are u = w, w + 4, ...; the operands of the next two are in flight
     auto unit = [&](int u, const Ops& cur, Ops& nxt) {
@@ -562,7 +520,7 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
             for (int i = 0; i < 4; ++i) o[db][i] *= inv;
         if (qv) {
             store_lane_order<D>(part + part_offset(bg, a.N, n, a.K, slot, G, hh, D), o, lg);
-            if (lane < 16) wgt[part_offset(bg, a.N, n, a.K, slot, G, hh, 1)] = fexp2((shat - cur.rf) * kLog2e);
+            if (lane < 16) wgt[part_offset(bg, a.N, n, a.K, slot, G, hh, 1)] = shat;
         }
     };
     Ops opa, opb, opc;
@@ -586,8 +544,9 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
 // double-buffered in LDS: block j + 1 is fetched into registers while block j
 // is used and stored into the other buffer afterwards, one barrier per block.
 // After the window, the row's retrieved-chunk slots are added into the same
-// accumulators (fusion, Eq. (10)): with M = max(log Z_swa, ref),
-//   out = (e^{log Z_swa - M} o_swa + e^{ref - M} sum_k w_k o_k) / (e^{log Z_swa - M} + e^{ref - M} sum_k w_k).
+// accumulators (fusion, Eq. (10)), stabilised per (row, head) by
+// M = max(log Z_swa, max_k s^_k):
+//   out = (e^{log Z_swa - M} o_swa + sum_k e^{s^_k - M} o_k) / (e^{log Z_swa - M} + sum_k e^{s^_k - M}).
 template <int G>
 struct LocalCfg {
     static constexpr int QB = 8 / G;   // 16-query blocks per tile
@@ -605,8 +564,7 @@ struct LocalCfg {
 // bitmap over the chunks, then the set bits in order (dynamic LDS: the bitmap,
 // the rows' valid entries, the union list).
 template <int D, int G, bool UNION, bool ROUTE>
-__global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, const float* ref, const bf16* part,
-                                                                const float* wgt) {
+__global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, const bf16* part, const float* wgt) {
     using C = LocalCfg<G>;
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
     constexpr int KROW = Tiles<D>::KROW, VROW = D + 16;
@@ -783,13 +741,11 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
 
     // fusion epilogue (lane: row l%16 of the item, dims 16 db + 4 lg + i)
     const float lam0 = (m + __log2f(l)) * (1.f / kLog2e);  // local log-sum-exp (l >= 1: key nq is in the window)
-    const float rf = ref[bg * a.N + nq];                 // best selected group score, or -inf
-    const float M = fmaxf(lam0, rf);
-    const float wl = fexp(lam0 - M) / l;
-    const float wc = fexp(rf - M);
+    // M: the (row, head)'s stabiliser, zs: the fusion denominator relative to e^M;
+    // o holds the numerator relative to e^M
+    float M = lam0, zs = 1.f;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) o[db] *= wl;
-    float zs = 0.f;
+    for (int db = 0; db < DB; ++db) o[db] *= 1.f / l;
     if constexpr (UNION) {
         // the union's chunks, each for all rows of the tile
         const int U = s_nu;
@@ -880,10 +836,17 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
                 const bf16x8 pb0 = p_operand(st[0], st[1]);
                 const bf16x8 pb1 = p_operand(st[2], st[3]);
                 psum = group4_sum(psum);
-                // weight of the chunk for this row: exp(s^ - ref) if it selected c, else 0
-                const float wk = sel ? fexp2((shat - rf) * kLog2e) : 0.f;
+                // online fusion: a selected chunk whose s^ exceeds the row's M so far
+                // rescales the numerator and denominator to the new maximum
+                const float Mn = sel ? fmaxf(M, shat) : M;
+                const float rs = fexp(M - Mn);
+#pragma unroll
+                for (int db = 0; db < DB; ++db) o[db] *= rs;
+                zs *= rs;
+                M = Mn;
+                const float wk = sel ? fexp(shat - M) : 0.f;
                 zs += wk;
-                const float f = wc * wk / psum;
+                const float f = wk / psum;
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
                     f32x4 oc = mfma16x16x32(tr_operand_perm(tv, VROW, 0, db * 16, lane), pb0, zero4());
@@ -906,6 +869,24 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     constexpr int SB = D >= 128 ? 2 : 4;  // slots whose loads are in flight together
     const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
     const int ncand = n_candidates(nq, a.W);
+    // the row's stabiliser first: the largest raw s^ among its valid slots
+    float Ms = -INFINITY;
+    {
+        int prev = -1;
+        for (int k = 0; k < a.K; ++k) {
+            const int cc = irow[k];
+            const bool ok = cc >= 0 && cc < ncand && cc > prev;
+            prev = cc;  // idx_entry_valid compares with the previous entry as written
+            if (ok) Ms = fmaxf(Ms, wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)]);
+        }
+    }
+    if (Ms > M) {
+        const float rs = fexp(M - Ms);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db] *= rs;
+        zs = rs;
+        M = Ms;
+    }
     int prev = -1;
     for (int k0 = 0; k0 < a.K; k0 += SB) {
         float wk[SB];
@@ -916,9 +897,9 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
             const int k = min(k0 + u, a.K - 1);
             const int cc = irow[k];
             const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
-            prev = cc;  // idx_entry_valid compares with the previous entry as written
-            const float wv = wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
-            wk[u] = ok ? wv : 0.f;
+            prev = cc;
+            const float sv = wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
+            wk[u] = ok ? fexp(sv - M) : 0.f;
             okk[u] = ok;
             // (address independent of idx, so these loads issue with the idx loads;
             // an invalid slot's bits are masked by fma_lane_order)
@@ -927,11 +908,11 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
 #pragma unroll
         for (int u = 0; u < SB; ++u) {
             zs += wk[u];
-            fma_lane_order<D>(pv[u], wc * wk[u], okk[u], o);
+            fma_lane_order<D>(pv[u], wk[u], okk[u], o);
         }
     }
     }
-    const float Z = fexp(lam0 - M) + wc * zs;
+    const float Z = zs;
     const float inv = 1.f / Z;
     if (nq_raw < a.N) {
         bf16* out = as_mut<bf16>(a.out);
@@ -952,29 +933,26 @@ struct PfRun {
         char* ws = static_cast<char*>(a.ws);
         bf16* part = reinterpret_cast<bf16*>(ws + ly.part);
         float* wgt = reinterpret_cast<float*>(ws + ly.wgt);
-        float* ref = reinterpret_cast<float*>(ws + ly.ref);
-        if (a.given_idx) {
-            HILS_LAUNCH("k_pf_ref_given", (k_pf_ref_given<D, G>), dim3(a.N, a.Hkv, a.B), dim3(kWave), 0, s, a, ref);
-        } else {
+        if (!a.given_idx) {
             const dim3 grid((unsigned)((a.N + kSQ - 1) / kSQ) * a.Hkv * a.B);
             const size_t dyn = score_dyn_lds(a.K);
             if (a.head_norm)
-                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a, ref);
+                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a);
             else
-                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kSW * kWave), dyn, s, a, ref);
+                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kSW * kWave), dyn, s, a);
         }
         const dim3 lgrid((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B);
-        if (a.union_pack && !a.given_idx) {
+        if (a.union_pack) {
             // one-load-multiple-compute: no inverse index, no per-slot partials
             const int nC = a.L / kChunk;
             const int qk = LocalCfg<G>::QT * a.K;
             const size_t dyn = (size_t)((nC + 31) / 32 + qk + min(nC, qk)) * sizeof(int);
             if (a.q_route)
                 HILS_LAUNCH("k_pf_union", (k_pf_local<D, G, true, true>), lgrid, dim3(LocalCfg<G>::NT), dyn, s, a,
-                            (const float*)ref, (const bf16*)part, (const float*)wgt);
+                            (const bf16*)nullptr, (const float*)nullptr);
             else
                 HILS_LAUNCH("k_pf_union", (k_pf_local<D, G, true, false>), lgrid, dim3(LocalCfg<G>::NT), dyn, s, a,
-                            (const float*)ref, (const bf16*)part, (const float*)wgt);
+                            (const bf16*)nullptr, (const float*)nullptr);
             return hipGetLastError();
         }
         const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
@@ -986,20 +964,21 @@ struct PfRun {
         const dim3 cgrid((unsigned)(ly.inv.max_work_bg * a.B * a.Hkv));
         if (a.q_route)
             HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, true>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR, list,
-                        work, ly.inv.max_work_bg, nwork, (const float*)ref, part, wgt);
+                        work, ly.inv.max_work_bg, nwork, part, wgt);
         else
             HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR, list,
-                        work, ly.inv.max_work_bg, nwork, (const float*)ref, part, wgt);
+                        work, ly.inv.max_work_bg, nwork, part, wgt);
         HILS_LAUNCH("k_pf_local", (k_pf_local<D, G, false, false>), lgrid, dim3(LocalCfg<G>::NT), 0, s, a,
-                    (const float*)ref, (const bf16*)part, (const float*)wgt);
+                    (const bf16*)part, (const float*)wgt);
         return hipGetLastError();
     }
 };
 
 }  // namespace
 
-size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16_storage) {
-    if (!bf16_storage) return 0;  // the fp32 path needs no workspace
+size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16_storage,
+                               int union_pack) {
+    if (!bf16_storage || union_pack) return 0;  // the fp32 and union paths need no workspace
     return pf_layout(B, Hq, Hkv, N, L, d, K).total;
 }
 

@@ -42,8 +42,12 @@ def oshape(p, N=None) -> oracle.Shape:
                         head_norm=bool(p.flags & HILS_FLAG_HEAD_NORM_SELECT))
 
 
-def host_inputs(p, wid: int, bias=None, route=False, dout=False, bias_shift=0.0):
-    """Seeded N(0,1) inputs on the host (float32 holding the stored values)."""
+def host_inputs(p, wid: int, bias=None, route=False, dout=False, bias_shift=0.0, head_gap=None):
+    """Seeded N(0,1) inputs on the host (float32 holding the stored values).
+
+    head_gap = (landmark head, shift): that head's biases are raised by `shift`,
+    so its surrogate scores sit far above those of the other heads of its group
+    (the per-head fusion must then stabilise every head by its own maximum)."""
     dt = p.dtype
     nc = p.L // p.chunk
     Hl = p.Hl or p.Hq
@@ -53,8 +57,10 @@ def host_inputs(p, wid: int, bias=None, route=False, dout=False, bias_shift=0.0)
         "v": synth.normal_host((p.B, p.Hkv, p.L, p.d), synth.seed_for(wid, "v"), dt),
         "lmk": synth.normal_host((p.B, Hl, nc, p.d), synth.seed_for(wid, "lmk"), dt),
     }
-    if bias:
+    if bias or head_gap:
         t["bias"] = synth.normal_host((p.B, Hl, nc), synth.seed_for(wid, "bias"), "f32", std=0.5) + bias_shift
+    if head_gap:
+        t["bias"][:, head_gap[0], :] += head_gap[1]
     if route:
         t["q_route"] = synth.normal_host((p.B, p.Hq, p.N, p.d), synth.seed_for(wid, "q_route"), dt)
     if dout:

@@ -227,3 +227,15 @@ def test_head_normalised_selection_flag(hils):
     assert hils.hils_workspace_size(params(hils, flags=f), hils.HILS_OP_BWD) >= 0  # ignored there
     with pytest.raises(hils.HilsError, match="landmark compression"):
         hils.hils_workspace_size(params(hils, flags=f), hils.HILS_OP_LANDMARK)
+
+
+def test_union_packing_needs_no_workspace(hils):
+    # union packing keeps no per-slot records: its prefill workspace is 0, while
+    # the chunk-major bf16 prefill reserves B*Hq*N*K*d bf16 partials (at least)
+    f = hils.HILS_FLAG_UNION_PACKING
+    p = params(hils, B=1, Hq=8, Hkv=2, N=1024, L=1024, d=128, topk=8)
+    assert hils.hils_workspace_size(p, hils.HILS_OP_PREFILL) >= 8 * 1024 * 8 * 128 * 2
+    pu = params(hils, B=1, Hq=8, Hkv=2, N=1024, L=1024, d=128, topk=8, flags=f)
+    assert hils.hils_workspace_size(pu, hils.HILS_OP_PREFILL) == 0
+    pg = params(hils, B=1, Hq=8, Hkv=2, N=1024, L=1024, d=128, topk=8, flags=f | hils.HILS_FLAG_GIVEN_IDX)
+    assert hils.hils_workspace_size(pg, hils.HILS_OP_PREFILL) == 0

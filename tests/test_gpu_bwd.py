@@ -23,7 +23,16 @@ CASES = {
     "bf16_G8_Hl_eq_Hkv_d64": (dict(B=1, Hq=8, Hkv=1, Hl=1, N=400, L=448, d=64, topk=4, window=64), 308, False,
                               False),
     "bf16_all_local": (dict(B=1, Hq=4, Hkv=1, N=200, L=256, d=64, topk=4, window=512), 309, False, False),
+    # bf16 at K = 32 and K = 64 (the per-slot dq partials and the chunk lists grow with K)
+    "bf16_K32": (dict(B=1, Hq=8, Hkv=2, N=2500, L=2560, d=128, topk=32, window=256), 310, False, False),
+    "bf16_K64_d64_route_bias": (dict(B=1, Hq=4, Hkv=1, N=4500, L=4544, d=64, topk=64, window=64), 311, True, True),
+    # the paper's efficiency shape (Sec. 7.1): d = 64, 16 query / 2 KV heads, K = 32, W = 512
+    "bf16_paper_shape_d64_G8_K32": (dict(B=1, Hq=16, Hkv=2, N=4096, L=4096, d=64, topk=32, window=512), 312, False,
+                                    False),
+    # one landmark head 150 above the rest of its group (per-head fusion weights)
+    "bf16_head_gap_150": (dict(B=1, Hq=8, Hkv=2, N=1100, L=1152, d=128, topk=8, window=128), 313, False, False),
 }
+HEAD_GAP = {"bf16_head_gap_150": (1, 150.0)}
 
 
 def run_case(name):
@@ -32,7 +41,8 @@ def run_case(name):
     kw, wid, bias, route = CASES[name]
     p = hils.Params(**kw)
     log(f"[bwd] case={name} params={kw}")
-    host = host_inputs(p, wid, bias=bias, route=route, dout=True, bias_shift=2.0 if bias else 0.0)
+    host = host_inputs(p, wid, bias=bias, route=route, dout=True, bias_shift=2.0 if bias else 0.0,
+                       head_gap=HEAD_GAP.get(name))
     dev = to_device(host, p)
     out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], dev.get("bias"),
                                           dev.get("q_route"))

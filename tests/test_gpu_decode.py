@@ -24,7 +24,18 @@ CASES = {
     # the per-part workgroups and a separate fusion pass)
     "bf16_many_rows_ragged": (dict(B=64, Hq=16, Hkv=4, N=1, L=1024, d=128, topk=8, window=256), 205, True, False,
                               [1024 - 13 * i for i in range(63)] + [1]),
+    # the paper's efficiency shape (Sec. 7.1): d = 64, 16 query / 2 KV heads, K = 32, W = 512
+    "bf16_paper_shape_d64_G8_K32": (dict(B=4, Hq=16, Hkv=2, N=1, L=8192, d=64, topk=32, window=512), 206, False,
+                                    False, [8192, 5000, 2600, 700]),
+    "bf16_K64": (dict(B=3, Hq=8, Hkv=2, N=1, L=8192, d=128, topk=64, window=256), 207, False, False,
+                 [8192, 4500, 4097]),
+    # one landmark head 150 above the rest of its group (per-head fusion weights)
+    "bf16_head_gap_150": (dict(B=4, Hq=8, Hkv=2, N=1, L=4096, d=128, topk=8, window=512), 208, False, False,
+                          [4096, 3000, 1500, 600]),
+    "bf16_head_gap_150_many_rows": (dict(B=64, Hq=16, Hkv=4, N=1, L=1024, d=64, topk=8, window=128), 209, False,
+                                    False, [1024 - 13 * i for i in range(64)]),
 }
+HEAD_GAP = {"bf16_head_gap_150": (1, 150.0), "bf16_head_gap_150_many_rows": (6, 150.0)}
 
 
 def run_case(name, forced=False, flags=0):
@@ -33,7 +44,7 @@ def run_case(name, forced=False, flags=0):
     kw, wid, bias, route, seqlens = CASES[name]
     p = hils.Params(flags=flags, **kw)
     log(f"[decode] case={name} forced={forced} seqlens={seqlens} params={kw}")
-    host = host_inputs(p, wid, bias=bias, route=route)
+    host = host_inputs(p, wid, bias=bias, route=route, head_gap=HEAD_GAP.get(name))
     dev = to_device(host, p)
     qpos = np.array([[(sl if seqlens else p.L) - 1] for sl in (seqlens or [p.L] * p.B)], np.int32)
     sl_dev = torch.tensor(seqlens, dtype=torch.int32, device="cuda") if seqlens else None

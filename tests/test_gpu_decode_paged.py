@@ -27,7 +27,14 @@ CASES = {
                                             dtype="f32"), 304, True, True, [2048, 1999, 130], True),
     "bf16_paged_window1_G1": (dict(B=2, Hq=4, Hkv=4, N=5, L=2048, d=64, topk=7, window=1), 305, False, True,
                               None, True),
+    # one landmark head 150 above the rest of its group (per-head fusion weights),
+    # several new queries per sequence sharing a workgroup, and a paged cache
+    "bf16_multi_token_head_gap_150": (dict(B=2, Hq=8, Hkv=2, N=3, L=4096, d=128, topk=8, window=512), 307, False,
+                                      False, [4096, 2100], False),
+    "bf16_paged_multi_token_K32_d64_G8": (dict(B=2, Hq=16, Hkv=2, N=2, L=4096, d=64, topk=32, window=512), 308,
+                                          False, False, [4096, 3500], True),
 }
+HEAD_GAP = {"bf16_multi_token_head_gap_150": (2, 150.0)}
 
 
 def make_pool(p, host, rng):
@@ -74,7 +81,7 @@ def run_case(name, flags=0):
     kw, wid, bias, route, seqlens, paged = CASES[name]
     p = hils.Params(flags=flags, **kw)
     log(f"[decode-paged] case={name} seqlens={seqlens} params={kw}")
-    host = host_inputs(p, wid, bias=bias, route=route)
+    host = host_inputs(p, wid, bias=bias, route=route, head_gap=HEAD_GAP.get(name))
     s = oshape(p)
     sl_dev = torch.tensor(seqlens, dtype=torch.int32, device="cuda") if seqlens else None
     qpos = oracle.decode_positions(s, seqlens)

@@ -38,7 +38,28 @@ CASES = {
     "bf16_all_local": (dict(B=1, Hq=4, Hkv=2, N=200, L=256, d=64, topk=4, window=512), 109, False, False, 0.0),
     "f32_large_topk_K64": (dict(B=1, Hq=4, Hkv=1, N=2048, L=2048, d=64, topk=64, window=64, dtype="f32"), 110,
                            False, False, 0.0),
+    # bf16 at the larger retrieval budgets the ABI accepts (K = 32 and 64 of up to
+    # 39 and 69 candidates)
+    "bf16_K32": (dict(B=1, Hq=8, Hkv=2, N=2500, L=2560, d=128, topk=32, window=256), 113, False, False, 0.0),
+    "bf16_K64_d64": (dict(B=1, Hq=4, Hkv=1, N=4500, L=4544, d=64, topk=64, window=64), 114, False, False, 0.0),
+    # the paper's efficiency shape (Sec. 7.1): d = 64, 16 query / 2 KV heads, S = 64,
+    # K = 32, W = 512
+    "bf16_paper_shape_d64_G8_K32": (dict(B=1, Hq=16, Hkv=2, N=4096, L=4096, d=64, topk=32, window=512), 115, False,
+                                    False, 0.0),
 }
+
+# one landmark head's scores raised by 150 (a bias of +150 on every chunk): the
+# group's selection follows that head, while every other head's window mass and
+# selected scores sit ~150 below it, where e^{-x} underflows to 0 in float; the fusion
+# weights are per head (App. C), so each head needs its own stabiliser
+GAP_CASES = {
+    "bf16_head_gap_150": (dict(B=1, Hq=8, Hkv=2, N=1100, L=1152, d=128, topk=8, window=128), 116, (1, 150.0)),
+    "bf16_head_gap_150_G8_d64": (dict(B=1, Hq=8, Hkv=1, N=900, L=960, d=64, topk=6, window=64), 117, (5, 150.0)),
+    "f32_head_gap_150": (dict(B=1, Hq=4, Hkv=1, N=700, L=704, d=64, topk=5, window=64, dtype="f32"), 118,
+                         (2, 150.0)),
+}
+for _n, (_kw, _wid, _gap) in GAP_CASES.items():
+    CASES[_n] = (_kw, _wid, False, False, 0.0)
 
 
 def run_case(name, forced=False, flags=0):
@@ -46,8 +67,9 @@ def run_case(name, forced=False, flags=0):
 
     kw, wid, bias, route, shift = CASES[name]
     p = hils.Params(flags=flags, **kw)
-    log(f"[prefill] case={name} forced={forced} flags={flags} params={kw}")
-    host = host_inputs(p, wid, bias=bias, route=route, bias_shift=shift)
+    gap = GAP_CASES[name][2] if name in GAP_CASES else None
+    log(f"[prefill] case={name} forced={forced} flags={flags} params={kw} head_gap={gap}")
+    host = host_inputs(p, wid, bias=bias, route=route, bias_shift=shift, head_gap=gap)
     dev = to_device(host, p)
     s = oshape(p)
     ref = oracle.fwd(s, np32(host["q"]), np32(host["k"]), np32(host["v"]), np32(host["lmk"]),
@@ -76,13 +98,22 @@ def test_prefill_matches_oracle(name):
     run_case(name)
 
 
-@pytest.mark.parametrize("name", ["bf16_ragged_multi_tile", "f32_route_bias_G2"])
+def test_prefill_union_packing_forced_index():
+    # union packing also serves a given selection
+    from paper_2607_02980_amd import hils
+
+    run_case("bf16_K32", forced=True, flags=hils.HILS_FLAG_UNION_PACKING)
+
+
+@pytest.mark.parametrize("name", ["bf16_ragged_multi_tile", "f32_route_bias_G2", "bf16_K32", "bf16_head_gap_150"])
 def test_prefill_forced_index(name):
     run_case(name, forced=True)
 
 
 @pytest.mark.parametrize("name", ["bf16_ragged_multi_tile", "bf16_window1", "bf16_bias_boosted", "bf16_route_Hl_eq_Hkv",
-                                  "bf16_mha_G1", "bf16_G8_d128", "bf16_topk_exceeds_candidates", "bf16_all_local"])
+                                  "bf16_mha_G1", "bf16_G8_d128", "bf16_topk_exceeds_candidates", "bf16_all_local",
+                                  "bf16_K32", "bf16_K64_d64", "bf16_paper_shape_d64_G8_K32", "bf16_head_gap_150",
+                                  "bf16_head_gap_150_G8_d64"])
 def test_prefill_union_packing(name):
     # the one-load-multiple-compute chunk terms (tiles load the union of their
     # rows' chunks) on i.i.d. inputs, against the oracle
@@ -120,7 +151,8 @@ def test_prefill_union_packing_on_locality_inputs(G):
 
 @pytest.mark.parametrize("name", ["tiny_2k_f32_full_config", "bf16_ragged_multi_tile", "bf16_bias_boosted",
                                   "bf16_route_Hl_eq_Hkv", "f32_route_bias_G2", "bf16_mha_G1", "bf16_G8_d128",
-                                  "bf16_topk_exceeds_candidates"])
+                                  "bf16_topk_exceeds_candidates", "bf16_K32", "bf16_K64_d64",
+                                  "bf16_paper_shape_d64_G8_K32", "bf16_head_gap_150", "f32_head_gap_150"])
 def test_prefill_head_normalised_selection(name):
     # the per-head normalised ranking (Sec. 4.1 wording), against the oracle's
     from paper_2607_02980_amd import hils

@@ -26,7 +26,9 @@
  *   - The caller owns every buffer.  The library never allocates device
  *     memory, never synchronises the device and keeps no state between calls
  *     other than the thread-local error string (and, only while the optional
- *     timing mode is enabled, its event records).  All work is enqueued on
+ *     timing mode is enabled, its event records) -- except that
+ *     hils_decode_fwd_noalloc uses a fixed device array of the library's own
+ *     (declared below) and keeps its address per device.  All work is enqueued on
  *     `stream` (a hipStream_t; NULL is the default stream) and is complete
  *     when the stream is.
  *   - Layouts are row-major and contiguous ("BHSD"):
@@ -169,6 +171,28 @@ int hils_prefill_fwd(const hils_params* p, const void* q, const void* k, const v
 int hils_decode_fwd(const hils_params* p, const void* q, const void* k_cache, const void* v_cache,
                     const void* lmk_cache, const float* lmk_bias, const void* q_route, const int32_t* seqlens,
                     void* out, float* lse, int32_t* idx, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Decode forward that allocates nothing, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): hils_decode_fwd with the same arguments minus the
+ * workspace, whose role is taken by a fixed array of
+ * HILS_DECODE_NOALLOC_SCRATCH_BYTES bytes that the library holds on every GPU
+ * it runs on (from the first call on that GPU until the process ends; the
+ * first call on a GPU looks up the array's device address, with that GPU
+ * current).  Same results as hils_decode_fwd (the same kernels).
+ *   Calls whose hils_workspace_size(p, HILS_OP_DECODE) exceeds
+ *   HILS_DECODE_NOALLOC_SCRATCH_BYTES return HILS_ERR_WORKSPACE before any
+ *   HIP call.  The array keeps the last call's contents; every byte a call
+ *   reads it has written first, so nothing needs clearing.  Calls that overlap
+ *   on one GPU (other streams or threads) share the array and race: serialise
+ *   them.  Nothing is allocated while the optional timing mode is off (its
+ *   default; when on, it creates HIP events).
+ */
+#define HILS_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int hils_decode_fwd_noalloc(const hils_params* p, const void* q, const void* k_cache, const void* v_cache,
+                            const void* lmk_cache, const float* lmk_bias, const void* q_route,
+                            const int32_t* seqlens, void* out, float* lse, int32_t* idx, void* stream);
 
 /*
  * Decode forward over a paged cache: a page holds one chunk (S tokens) of one

@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libhils.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["hils_api.cpp", "hils_fwd.hip", "hils_prefill.hip", "hils_bwd.hip", "hils_bwd_mfma.hip", "hils_decode.hip", "hils_landmark.hip"]
+SOURCES = ["hils_api.cpp", "hils_fwd.hip", "hils_prefill.hip", "hils_bwd.hip", "hils_bwd_mfma.hip", "hils_decode.hip", "hils_landmark.hip", "hils_noalloc.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

@@ -245,6 +245,27 @@ int hils_decode_fwd(const hils_params* p, const void* q, const void* k_cache, co
     return hip_status(hils::launch_decode_fwd(a, (hipStream_t)stream), "hils_decode_fwd launch");
 }
 
+int hils_decode_fwd_noalloc(const hils_params* p, const void* q, const void* k_cache, const void* v_cache,
+                            const void* lmk_cache, const float* lmk_bias, const void* q_route,
+                            const int32_t* seqlens, void* out, float* lse, int32_t* idx, void* stream) {
+    int rc = check_params(p, HILS_OP_DECODE);
+    if (rc) return rc;
+    REQUIRE(q); REQUIRE(k_cache); REQUIRE(v_cache); REQUIRE(lmk_cache); REQUIRE(out); REQUIRE(lse); REQUIRE(idx);
+    const size_t need = ws_bytes_for(p, HILS_OP_DECODE);
+    const size_t cap = hils::decode_noalloc_capacity();
+    if (need > cap)
+        return fail(HILS_ERR_WORKSPACE,
+                    "hils_decode_fwd_noalloc: this call needs %zu bytes of workspace, above the library's fixed "
+                    "%zu-byte array (use hils_decode_fwd with a workspace, or fewer sequences/new tokens)",
+                    need, cap);
+    void* ws = nullptr;
+    rc = hip_status(hils::decode_noalloc_scratch(&ws), "hils_decode_fwd_noalloc: device address of the array");
+    if (rc) return rc;
+    const hils::FwdArgs a = fwd_args(p, q, k_cache, v_cache, lmk_cache, lmk_bias, q_route, seqlens, out, lse, idx,
+                                     ws, cap, 1);
+    return hip_status(hils::launch_decode_fwd(a, (hipStream_t)stream), "hils_decode_fwd_noalloc launch");
+}
+
 int hils_decode_paged_fwd(const hils_params* p, const void* q, const void* k_pages, const void* v_pages,
                           const void* lmk_pages, const float* bias_pages, const void* q_route,
                           const int32_t* block_table, int num_pages, const int32_t* seqlens, void* out, float* lse,

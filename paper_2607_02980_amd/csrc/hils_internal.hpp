@@ -132,6 +132,10 @@ size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int 
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s);  // fp32 storage
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s);
+// The no-allocation decode's file-scope device array: its size, and its device
+// address on the current device (looked up once per device).
+size_t decode_noalloc_capacity();
+hipError_t decode_noalloc_scratch(void** ptr);
 hipError_t launch_landmark_fwd(const LmkArgs& a, hipStream_t s);
 hipError_t launch_landmark_bwd(const LmkArgs& a, hipStream_t s);
 size_t landmark_workspace_bytes(int B, int Hl, int nC, int d, bool shared);

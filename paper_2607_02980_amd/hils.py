@@ -53,13 +53,15 @@ def _load():
     lib.hils_prefill_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_decode_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_decode_paged_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, sz, vp]
+    lib.hils_decode_fwd_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.hils_bwd.argtypes = [P] + [vp] * 17 + [sz, vp]
     lib.hils_landmark_fwd.argtypes = [P, vp, vp, vp, vp, vp]
     lib.hils_landmark_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hils_timing_enable.argtypes = [ctypes.c_int]
     lib.hils_timing_read.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(ctypes.c_float),
                                      ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
-    for f in (lib.hils_workspace_size, lib.hils_prefill_fwd, lib.hils_decode_fwd, lib.hils_bwd,
+    for f in (lib.hils_workspace_size, lib.hils_prefill_fwd, lib.hils_decode_fwd, lib.hils_decode_fwd_noalloc,
+              lib.hils_bwd,
               lib.hils_landmark_fwd, lib.hils_landmark_bwd, lib.hils_timing_enable, lib.hils_timing_read):
         f.restype = ctypes.c_int
     return lib
@@ -197,6 +199,34 @@ def hils_decode_fwd(p: Params, q, k_cache, v_cache, lmk_cache, lmk_bias=None, q_
         _ptr(seqlens, "seqlens", (p.B,), torch.int32, False), _ptr(out, "out", S["q"], dt),
         _ptr(lse, "lse", S["lse"], torch.float32), _ptr(idx, "idx", S["idx"], torch.int32),
         _ptr(ws, "workspace"), n, _stream()))
+    return out, lse, idx
+
+
+HILS_DECODE_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def hils_decode_fwd_noalloc(p: Params, q, k_cache, v_cache, lmk_cache, lmk_bias=None, q_route=None, seqlens=None,
+                            out=None, lse=None, idx=None):
+    """hils_decode_fwd without a workspace: the library's fixed per-GPU array
+    (HILS_DECODE_NOALLOC_SCRATCH_BYTES) serves as the workspace.  Outputs not
+    given are allocated here with torch.empty (the C call itself allocates
+    nothing).  Returns (out, lse, idx)."""
+    S, dt = _shapes(p), p.torch_dtype
+    if out is None:
+        out = torch.empty(S["q"], dtype=dt, device=q.device)
+    if lse is None:
+        lse = torch.empty(S["lse"], dtype=torch.float32, device=q.device)
+    if idx is None:
+        if p.flags & HILS_FLAG_GIVEN_IDX:
+            raise ValueError("HILS_FLAG_GIVEN_IDX needs idx")
+        idx = torch.empty(S["idx"], dtype=torch.int32, device=q.device)
+    cp = p.c()
+    _check(LIB.hils_decode_fwd_noalloc(
+        ctypes.byref(cp), _ptr(q, "q", S["q"], dt), _ptr(k_cache, "k_cache", S["kv"], dt),
+        _ptr(v_cache, "v_cache", S["kv"], dt), _ptr(lmk_cache, "lmk_cache", S["lmk"], dt),
+        _ptr(lmk_bias, "lmk_bias", S["bias"], torch.float32, False), _ptr(q_route, "q_route", S["q"], dt, False),
+        _ptr(seqlens, "seqlens", (p.B,), torch.int32, False), _ptr(out, "out", S["q"], dt),
+        _ptr(lse, "lse", S["lse"], torch.float32), _ptr(idx, "idx", S["idx"], torch.int32), _stream()))
     return out, lse, idx
 
 

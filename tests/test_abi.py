@@ -239,3 +239,23 @@ def test_union_packing_needs_no_workspace(hils):
     assert hils.hils_workspace_size(pu, hils.HILS_OP_PREFILL) == 0
     pg = params(hils, B=1, Hq=8, Hkv=2, N=1024, L=1024, d=128, topk=8, flags=f | hils.HILS_FLAG_GIVEN_IDX)
     assert hils.hils_workspace_size(pg, hils.HILS_OP_PREFILL) == 0
+
+
+def test_noalloc_decode_rejects_calls_above_its_array(hils):
+    # the no-allocation decode checks its workspace need against the fixed array
+    # on the host, before any HIP call
+    cap = hils.HILS_DECODE_NOALLOC_SCRATCH_BYTES
+    small = params(hils, B=32, Hq=32, Hkv=8, N=1, L=131136, d=128, topk=16, window=512)
+    assert hils.hils_workspace_size(small, hils.HILS_OP_DECODE) <= cap
+    big = params(hils, B=256, Hq=32, Hkv=8, N=1, L=131136, d=128, topk=16, window=512)
+    need = hils.hils_workspace_size(big, hils.HILS_OP_DECODE)
+    assert need > cap
+    cp = big.c()
+    F = FAKE
+    rc = hils.LIB.hils_decode_fwd_noalloc(ctypes.byref(cp), F, F, F, F, None, None, None, F, F, F, None)
+    assert rc == hils.HILS_ERR_WORKSPACE
+    assert f"{need} bytes" in hils.hils_last_error() and str(cap) in hils.hils_last_error()
+    rc = hils.LIB.hils_decode_fwd_noalloc(ctypes.byref(small.c()), F, None, F, F, None, None, None, F, F, F, None)
+    assert rc == hils.HILS_ERR_INVALID and "k_cache" in hils.hils_last_error()
+    with open(HEADER) as f:
+        assert f"HILS_DECODE_NOALLOC_SCRATCH_BYTES ((size_t){cap >> 20} << 20)" in f.read()

@@ -403,11 +403,14 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
     __shared__ int s_ent[kInvSeg];  // the segment's entries (row << 6 | slot)
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
     const int nC = a.L / kChunk;
-    // blocks of (b, g) = bg are bg * max_work_bg + item: those past its item count leave
-    const size_t bg = blockIdx.x / max_work_bg;
-    const int item = (int)(blockIdx.x % max_work_bg);
+    // logical blocks of (b, g) = bg are bg * max_work_bg + item, those past its item
+    // count leave; each XCD takes one contiguous range of logical blocks (one (b, g)
+    // and range of row buckets), so its L2 holds only the query rows of its buckets
+    const int lb = xcd_remap((int)blockIdx.x, (int)gridDim.x);
+    const size_t bg = (size_t)lb / max_work_bg;
+    const int item = (int)((size_t)lb % max_work_bg);
     if (item >= nwork[bg]) return;
-    const int4 wi = work[blockIdx.x];
+    const int4 wi = work[lb];
     const int c = wi.y;
     const int b = (int)(bg / a.Hkv), g = (int)(bg % a.Hkv);
     const int* bo = boff + bg * ((size_t)nC * nR + 1);
@@ -869,27 +872,11 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     constexpr int SB = D >= 128 ? 2 : 4;  // slots whose loads are in flight together
     const int32_t* irow = a.idx + (bg * a.N + nq) * a.K;
     const int ncand = n_candidates(nq, a.W);
-    // the row's stabiliser first: the largest raw s^ among its valid slots
-    float Ms = -INFINITY;
-    {
-        int prev = -1;
-        for (int k = 0; k < a.K; ++k) {
-            const int cc = irow[k];
-            const bool ok = cc >= 0 && cc < ncand && cc > prev;
-            prev = cc;  // idx_entry_valid compares with the previous entry as written
-            if (ok) Ms = fmaxf(Ms, wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)]);
-        }
-    }
-    if (Ms > M) {
-        const float rs = fexp(M - Ms);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) o[db] *= rs;
-        zs = rs;
-        M = Ms;
-    }
+    // online fusion over the slots: each group of SB slots may raise the
+    // (row, head)'s maximum M, which rescales the numerator and denominator
     int prev = -1;
     for (int k0 = 0; k0 < a.K; k0 += SB) {
-        float wk[SB];
+        float sv[SB];
         bool okk[SB];
         uint4 pv[SB][D / 32];
 #pragma unroll
@@ -897,18 +884,26 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
             const int k = min(k0 + u, a.K - 1);
             const int cc = irow[k];
             const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
-            prev = cc;
-            const float sv = wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
-            wk[u] = ok ? fexp(sv - M) : 0.f;
+            prev = cc;  // idx_entry_valid compares with the previous entry as written
+            sv[u] = wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
             okk[u] = ok;
             // (address independent of idx, so these loads issue with the idx loads;
             // an invalid slot's bits are masked by fma_lane_order)
             load_lane_order<D>(part + part_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, pv[u]);
         }
+        float Mn = M;
+#pragma unroll
+        for (int u = 0; u < SB; ++u) Mn = okk[u] ? fmaxf(Mn, sv[u]) : Mn;
+        const float rs = fexp(M - Mn);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db] *= rs;
+        zs *= rs;
+        M = Mn;
 #pragma unroll
         for (int u = 0; u < SB; ++u) {
-            zs += wk[u];
-            fma_lane_order<D>(pv[u], wk[u], okk[u], o);
+            const float wk = okk[u] ? fexp(sv[u] - M) : 0.f;
+            zs += wk;
+            fma_lane_order<D>(pv[u], wk, okk[u], o);
         }
     }
     }

@@ -10,11 +10,17 @@ attention and the fusion epilogue.  ``value`` is prefill tokens/s with all
 inputs resident in HBM.  Decode (32 x 131K-token caches) and fwd+bwd at
 4 x 16K are reported beside it in ``extra``.
 
-Timing uses HIP events on the stream the library launches on: the step is
-bracketed by two events, and the library's optional per-kernel timing mode
-brackets every kernel launch inside the timed steps.  The roofline object
-describes the dominant kernel (largest total time): its average launch
-duration against its algorithmic FLOPs or bytes, whichever bound is tighter.
+Timing uses HIP events on the stream the library launches on: every step is
+bracketed by two events and the reported step time is the median over the
+timed steps (the mean is given beside it); the library's optional per-kernel
+timing mode brackets every kernel launch in a second pass over the same
+number of steps.  The roofline object describes the dominant kernel (largest
+total time): its average launch duration against the method's work in that
+kernel -- FLOPs of the selected pairs and the causal band only, bytes of the
+method's inputs read once and outputs written once -- under whichever bound
+is tighter (bf16 MFMA for the prefill kernels).  Bytes the design adds (the
+chunk pass's per-slot records) are not method bytes: they appear in the
+rocprofv3 traffic and its ratio to the method bytes.
 """
 from __future__ import annotations
 
@@ -34,6 +40,15 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 METRIC = "HiLS attn tokens/s + decode HBM GB/s & prefill MFMA util vs MI355X peak"
+# The paper's own efficiency figures (Sec. 7.1, Fig. 5): end-to-end latencies of a
+# 345M-parameter model (16 layers, 16 query / 2 KV heads, d = 64; S = 64, K = 32,
+# W = 512) served by SGLang with Triton kernels on one NVIDIA H800, bf16, batch 1.
+# Context only: whole-model latencies on other hardware, not operator figures.
+PAPER_CONTEXT = {"hardware": "1x NVIDIA H800", "model": "345M, 16 layers, 16/2 heads, d 64",
+                 "prefill_512k_latency_s": {"hils": 5.0, "full_attention": 67.0},
+                 "decode_512k_ms_per_token": {"hils": 5.5, "full_attention": 85.9},
+                 "crossover_context_tokens": 16384,
+                 "source": "Sec. 7.1 and Fig. 5 (end-to-end, SGLang + Triton)"}
 
 
 def n_candidates(i, S, W):
@@ -52,15 +67,18 @@ def prefill_work(B, Hq, Hkv, N, d, S, K, W):
 
 
 def prefill_kernel_model(B, Hq, Hkv, N, L, d, S, K, W, elem=2):
-    """Per-kernel algorithmic FLOPs and HBM bytes of one bf16 prefill launch.
+    """Per-kernel method FLOPs and method bytes of one bf16 prefill launch (the
+    design's own intermediates -- per-slot records, the inverse index -- are not
+    counted; they show in the measured traffic).
 
-    k_pf_score : landmark scores over C_i (2d per head-candidate); reads q, the
-                 landmarks once, writes idx and the row reference score.
-    k_pf_chunks: per selected (row, head, chunk) QK^T + PV over 64 keys (4d*64)
-                 and the surrogate score (2d); reads q and the chunk's K/V once
-                 per chunk, writes one bf16 partial (d) + weight per (row, head, slot).
-    k_pf_local : window QK^T + PV (4d per key); reads q, K/V, the partials and
-                 weights, writes out and lse.
+    k_pf_score : landmark scores over C_i, 2d per (head, candidate); reads q and
+                 the landmarks once, writes idx.
+    k_pf_chunks: per selected (row, head, chunk) QK^T + PV over S keys (4dS) and
+                 the surrogate score (2d); reads q and the K/V once.
+    k_pf_local : window QK^T + PV, 4d per (row, head, window key), and the fusion;
+                 reads q and K/V once, writes out and lse.
+    design_bytes: the records k_pf_chunks writes and k_pf_local reads back (the bf16
+                 chunk output and the fp32 score per (row, head, slot)).
     """
     i = np.arange(N, dtype=np.int64)
     ncand = n_candidates(i, S, W)
@@ -68,15 +86,23 @@ def prefill_kernel_model(B, Hq, Hkv, N, L, d, S, K, W, elem=2):
     nsel = float(np.minimum(K, ncand).sum())
     qbytes = B * Hq * N * d * elem
     kvbytes = 2 * B * Hkv * L * d * elem
-    partials = B * Hq * nsel * (d * elem + 4)
+    lmkbytes = B * Hq * (L // S) * d * elem
+    idxbytes = B * Hkv * N * K * 4
+    records = B * Hq * nsel * (d * elem + 4)
     return {
-        "k_pf_score": {"flop": B * Hq * 2 * d * float(ncand.sum()),
-                       "bytes": qbytes + B * Hq * (L // S) * d * elem + B * Hkv * N * (K + 1) * 4},
-        "k_pf_chunks": {"flop": B * Hq * (4 * d * S + 2 * d) * nsel,
-                        "bytes": qbytes + kvbytes + partials},
-        "k_pf_local": {"flop": B * Hq * 4 * d * float(nloc.sum()),
-                       "bytes": qbytes + kvbytes + partials + qbytes + B * Hq * N * 4 + B * Hkv * N * K * 4},
+        "k_pf_score": {"flop": B * Hq * 2 * d * float(ncand.sum()), "bytes": qbytes + lmkbytes + idxbytes},
+        "k_pf_chunks": {"flop": B * Hq * (4 * d * S + 2 * d) * nsel, "bytes": qbytes + kvbytes,
+                        "design_bytes": records},
+        "k_pf_local": {"flop": B * Hq * 4 * d * float(nloc.sum()), "bytes": qbytes + kvbytes + qbytes + B * Hq * N * 4,
+                       "design_bytes": records},
     }
+
+
+def prefill_method_bytes(B, Hq, Hkv, N, L, d, S, K, elem=2):
+    """Bytes the whole prefill must move at least: q, k, v, landmarks read once;
+    out, lse, idx written once."""
+    return (2 * B * Hq * N * d + 2 * B * Hkv * L * d + B * Hq * (L // S) * d) * elem + B * Hq * N * 4 + \
+        B * Hkv * N * K * 4
 
 
 def decode_bytes(B, Hq, Hkv, Hl, ctx, d, S, K, W, elem=2, N=1):
@@ -110,25 +136,49 @@ def load_traffic(kernel_tag):
     return rec["bytes_per_dispatch"]
 
 
+def measured_peaks(torch):
+    """What this machine sustains with plain library kernels: a 1 GiB device copy
+    (torch's copy kernel, bytes read + written) and an 8192^3 bf16 GEMM
+    (hipBLASLt through torch.matmul).  Context for the published peaks."""
+    x = torch.ones(2 ** 28, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    a = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+    b = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+    t = Timer(torch)
+    copy_ms, _ = t.run(lambda: y.copy_(x), 20, 3)
+    gemm_ms, _ = t.run(lambda: torch.matmul(a, b), 20, 3)
+    out = {"copy_1gib_gbs": round(2 * x.numel() * 4 / (copy_ms * 1e-3) / 1e9, 1),
+           "bf16_gemm_8192_tflops": round(2 * 8192 ** 3 / (gemm_ms * 1e-3) / 1e12, 1),
+           "note": "torch copy kernel (read + write bytes) and hipBLASLt GEMM; published peaks: "
+                   f"HBM {HBM_PEAK_GBS:.0f} GB/s, dense bf16 MFMA {BF16_MFMA_PEAK_TFLOPS:.0f} TFLOP/s"}
+    del x, y, a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 class Timer:
-    """HIP events on the current (library) stream."""
+    """HIP events on the current (library) stream around every step; returns the
+    median and the mean step time in ms."""
 
     def __init__(self, torch):
         self.torch = torch
 
-    def run(self, fn, steps, warmup):
+    def run(self, fn, steps, warmup, before=None):
         t = self.torch
         for _ in range(warmup):
             fn()
         t.cuda.synchronize()
         st = t.cuda.current_stream()
-        e0, e1 = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
-        e0.record(st)
-        for _ in range(steps):
+        ev = [(t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for e0, e1 in ev:
+            if before is not None:
+                before()
+            e0.record(st)
             fn()
-        e1.record(st)
+            e1.record(st)
         t.cuda.synchronize()
-        return e0.elapsed_time(e1) / steps  # ms
+        ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)
+        return float(np.median(ms)), float(np.mean(ms))
 
 
 def chunk_overlap(idx, M=16):
@@ -170,34 +220,36 @@ def bench_prefill(torch, hils, synth, W_, steps, warmup, flags=0, rho=None):
     def step():
         hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], out=out, lse=lse, idx=idx, workspace=ws)
 
-    ms = Timer(torch).run(step, steps, warmup)
+    ms, ms_mean = Timer(torch).run(step, steps, warmup)
     hils.hils_timing_enable(True)
     Timer(torch).run(step, steps, 0)
     kernels = hils.hils_timing_read()
     hils.hils_timing_enable(False)
     for k in kernels.values():
         k["avg_ms"] = k["total_ms"] / max(1, k["launches"])
-    p.overlap16 = chunk_overlap(idx.cpu().numpy(), 16)
+    p.overlap16 = chunk_overlap(idx.cpu().numpy(), 16) if p.topk <= 64 and p.dtype == "bf16" else float("nan")
+    p.ms_mean = ms_mean
     del dev, ws
     torch.cuda.empty_cache()
     return p, host, ms, kernels
 
 
-def bench_decode(torch, hils, synth, W_, steps, warmup, paged=False, N=1, flags=0):
+def bench_decode(torch, hils, synth, W_, steps, warmup, paged=False, N=1, flags=0, Hl=0):
     """One decode step of N new queries per sequence after W_.ctx cached tokens.
     paged: the caches are pools of one-chunk pages in a seeded random order (a
-    random permutation as the page table)."""
+    random permutation as the page table).  Hl: landmark heads (0: Hq)."""
     p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
-                    window=W_.window, dtype=W_.dtype, flags=flags)
+                    window=W_.window, dtype=W_.dtype, flags=flags, Hl=Hl)
+    Hl = Hl or p.Hq
     nc = p.L // p.chunk
     if paged:
         P = p.B * nc
         gen = torch.Generator(device="cpu")
         gen.manual_seed(synth.seed_for(W_.wid, "page_table"))
         table = torch.randperm(P, generator=gen).to(torch.int32).reshape(p.B, nc).cuda()
-        kv_shape, lmk_shape = (P, p.Hkv, p.chunk, p.d), (P, p.Hq, p.d)
+        kv_shape, lmk_shape = (P, p.Hkv, p.chunk, p.d), (P, Hl, p.d)
     else:
-        kv_shape, lmk_shape = (p.B, p.Hkv, p.L, p.d), (p.B, p.Hq, nc, p.d)
+        kv_shape, lmk_shape = (p.B, p.Hkv, p.L, p.d), (p.B, Hl, nc, p.d)
     dev = {
         "q": synth.normal_device((p.B, p.Hq, N, p.d), synth.seed_for(W_.wid, "q"), p.dtype, "cuda"),
         "k": synth.normal_device(kv_shape, synth.seed_for(W_.wid, "k"), p.dtype, "cuda"),
@@ -228,28 +280,21 @@ def bench_decode(torch, hils, synth, W_, steps, warmup, paged=False, N=1, flags=
     st = torch.cuda.current_stream()
 
     def timed(instrumented):
-        total = 0.0
         hils.hils_timing_enable(instrumented)
-        for _ in range(steps):
-            torch.sum(flush, dim=0, out=sink)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(st)
-            step()
-            e1.record(st)
-            torch.cuda.synchronize()
-            total += e0.elapsed_time(e1)
+        med, mean = Timer(torch).run(step, steps, 0, before=lambda: torch.sum(flush, dim=0, out=sink))
         kern = hils.hils_timing_read() if instrumented else None
         hils.hils_timing_enable(False)
-        return total / steps, kern
+        return med, mean, kern
 
     # the step time is taken without per-kernel events (they add a few us per
     # launch to a ~0.2 ms step); a second, instrumented pass gives the breakdown
-    ms, _ = timed(False)
-    _, kernels = timed(True)
-    nbytes, parts = decode_bytes(p.B, p.Hq, p.Hkv, p.Hq, W_.ctx, p.d, p.chunk, p.topk, p.window, N=N)
+    ms, ms_mean, _ = timed(False)
+    _, _, kernels = timed(True)
+    nbytes, parts = decode_bytes(p.B, p.Hq, p.Hkv, Hl, W_.ctx, p.d, p.chunk, p.topk, p.window, N=N)
     del dev, flush, sink
     torch.cuda.empty_cache()
-    return {"workload": W_.name, "paged": paged, "new_tokens_per_seq": N, "ms_per_step": round(ms, 4),
+    return {"workload": W_.name, "paged": paged, "new_tokens_per_seq": N, "landmark_heads": Hl,
+            "ms_per_step": round(ms, 4), "ms_per_step_mean": round(ms_mean, 4), "steps": steps,
             "tokens_per_s": round(p.B * N / (ms * 1e-3), 1),
             "algorithmic_bytes": nbytes, "bytes_breakdown": parts,
             "hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
@@ -277,8 +322,9 @@ def bench_train(torch, hils, synth, W_, steps, warmup):
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
+    ms, ms_mean = Timer(torch).run(step, steps, 0)
     hils.hils_timing_enable(True)
-    ms = Timer(torch).run(step, steps, 0)
+    Timer(torch).run(step, steps, 0)
     kernels = hils.hils_timing_read()
     hils.hils_timing_enable(False)
     attn, score = prefill_work(p.B, p.Hq, p.Hkv, p.N, p.d, p.chunk, p.topk, p.window)
@@ -286,7 +332,8 @@ def bench_train(torch, hils, synth, W_, steps, warmup):
     bwd = 2.5 * attn + 2 * score  # dq, dk, dv recompute: 10d vs 4d per attended pair; score grads
     del dev
     torch.cuda.empty_cache()
-    return {"workload": W_.name, "ms_per_step": round(ms, 3), "tokens_per_s": round(p.B * p.N / (ms * 1e-3), 1),
+    return {"workload": W_.name, "ms_per_step": round(ms, 3), "ms_per_step_mean": round(ms_mean, 3), "steps": steps,
+            "tokens_per_s": round(p.B * p.N / (ms * 1e-3), 1),
             "algorithmic_tflop": round((fwd + bwd) / 1e12, 3),
             "mfma_frac_useful": round((fwd + bwd) / (ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 5),
             "kernels_avg_ms": {k: round(v["total_ms"] / max(1, v["launches"]), 3) for k, v in kernels.items()}}
@@ -310,8 +357,8 @@ def bench_landmark(torch, hils, synth, W_, steps, warmup):
     out = {"workload": W_.name, "landmark_heads": Hl}
     for name, fn, nbytes in (("fwd", lambda: hils.hils_landmark_fwd(p, lq, k, lmk, bias), kb + 2 * lb + bb),
                              ("bwd", lambda: hils.hils_landmark_bwd(p, lq, k, dl, db, dlq, dk), 2 * kb + 3 * lb + bb)):
-        ms = Timer(torch).run(fn, steps, warmup)
-        out[name] = {"avg_ms": round(ms, 4), "bytes": nbytes, "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+        ms, _ = Timer(torch).run(fn, steps, warmup)
+        out[name] = {"ms": round(ms, 4), "bytes": nbytes, "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
                      "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     del lq, k, dl, db, lmk, bias, dlq, dk
     torch.cuda.empty_cache()
@@ -355,7 +402,7 @@ def cpu_baseline(W_, host, target_s=20.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-train", action="store_true")
@@ -391,16 +438,26 @@ def main():
         if name in model:
             t = k["avg_ms"] * 1e-3
             f, b = model[name]["flop"], model[name]["bytes"]
-            row.update({"flop": f, "bytes": b, "tflops": round(f / t / 1e12, 2), "gbs": round(b / t / 1e9, 1),
+            row.update({"method_flop": f, "method_bytes": b, "tflops": round(f / t / 1e12, 2),
+                        "mfma_frac": round(f / t / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                        "method_gbs": round(b / t / 1e9, 1), "hbm_frac_method": round(b / t / 1e9 / HBM_PEAK_GBS, 4),
                         "bound": "mfma" if f / (BF16_MFMA_PEAK_TFLOPS * 1e12) >= b / (HBM_PEAK_GBS * 1e9) else "hbm"})
+            if "design_bytes" in model[name]:
+                row["design_bytes"] = model[name]["design_bytes"]
+            tr = load_traffic(f"{name}_{Wp.name}")
+            if tr is not None:
+                row.update({"traffic": tr, "traffic_gbs": round(tr / t / 1e9, 1),
+                            "traffic_over_method_bytes": round(tr / b, 2)})
         table[name] = row
     dom = max((n for n in table if n in model), key=lambda n: kernels[n]["total_ms"])
     d = table[dom]
     if d["bound"] == "mfma":
         achieved, peak, unit = d["tflops"], BF16_MFMA_PEAK_TFLOPS, "TFLOP/s"
     else:
-        achieved, peak, unit = d["gbs"], HBM_PEAK_GBS, "GB/s"
+        achieved, peak, unit = d["method_gbs"], HBM_PEAK_GBS, "GB/s"
     attn_flops, score_flops = prefill_work(p.B, p.Hq, p.Hkv, p.N, p.d, p.chunk, p.topk, p.window)
+    traffic = load_traffic(f"{dom}_{Wp.name}")
+    mbytes = prefill_method_bytes(p.B, p.Hq, p.Hkv, p.N, p.L, p.d, p.chunk, p.topk)
     res = {
         "metric": METRIC, "value": round(p.B * p.N / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
@@ -408,26 +465,39 @@ def main():
         "config": {"workload": Wp.name, "B": p.B, "Hq": p.Hq, "Hkv": p.Hkv, "d": p.d, "seq_len": p.N,
                    "chunk": p.chunk, "topk": p.topk, "window": p.window, "landmark_heads": p.Hq},
         "roofline": {"bound": d["bound"], "kernel": dom, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": round(achieved / peak, 5), "traffic": load_traffic(f"{dom}_{Wp.name}"),
-                     "algorithmic_per_launch": {"flop": d["flop"], "bytes": d["bytes"]},
+                     "frac": round(achieved / peak, 5), "traffic": traffic,
+                     "traffic_over_method_bytes": round(traffic / d["method_bytes"], 2) if traffic else None,
+                     "per_launch": {"method_flop": d["method_flop"], "method_bytes": d["method_bytes"],
+                                    "design_bytes": d.get("design_bytes")},
+                     "hbm_on_method_bytes": {"gbs": d["method_gbs"], "frac": d["hbm_frac_method"]},
                      "kernel_avg_ms": d["avg_ms"]},
-        "extra": {"prefill_kernels": table,
+        "extra": {"ms_per_step_mean": round(p.ms_mean, 4),
+                  "prefill_kernels": table,
                   "prefill_useful_mfma_frac": round((attn_flops + score_flops) / (ms * 1e-3) / 1e12
-                                                    / BF16_MFMA_PEAK_TFLOPS, 5)},
+                                                    / BF16_MFMA_PEAK_TFLOPS, 5),
+                  "prefill_method_bytes": mbytes,
+                  "prefill_hbm_frac_on_method_bytes": round(mbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 5),
+                  "paper_context": PAPER_CONTEXT},
     }
     del p
     torch.cuda.empty_cache()
     if not args.no_decode:
-        res["extra"]["decode"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
-                                              max(3, args.steps // 2), 2)
-        res["extra"]["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"],
-                                                 max(3, args.steps // 2), 2)
-        res["extra"]["decode_paged"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
-                                                    max(3, args.steps // 2), 2, paged=True)
-        res["extra"]["decode_4_new_tokens"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
-                                                           max(3, args.steps // 2), 2, N=4)
+        Wd = WORKLOADS["decode_131k_bf16_b32"]
+        res["extra"]["decode"] = bench_decode(torch, hils, synth, Wd, args.steps, 2)
+        res["extra"]["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"], args.steps, 2)
+        res["extra"]["decode_paged"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, paged=True)
+        res["extra"]["decode_4_new_tokens"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, N=4)
+        res["extra"]["decode_Hl_eq_Hkv"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
+                                                        args.steps, 2, Hl=WORKLOADS["decode_131k_bf16_b32"].Hkv)
     if not args.no_train:
-        res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], 3, 1)
+        res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], args.steps, 1)
+    # the tiny fp32 workload (2K tokens, 4/1 heads, d 64, top-4): latency of one prefill
+    Wt = WORKLOADS["prefill_2k_f32_tiny"]
+    pt, _, mst, kt = bench_prefill(torch, hils, synth, Wt, args.steps, args.warmup)
+    res["extra"]["prefill_2k_f32_tiny"] = {"ms_per_step": round(mst, 4), "ms_per_step_mean": round(pt.ms_mean, 4),
+                                           "tokens_per_s": round(pt.B * pt.N / (mst * 1e-3), 1),
+                                           "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kt.items()}}
+    res["extra"]["measured_peaks"] = measured_peaks(torch)
     if not args.no_landmark:
         res["extra"]["landmark"] = bench_landmark(torch, hils, synth, Wp, args.steps, args.warmup)
     if not args.no_variants:
@@ -438,14 +508,13 @@ def main():
                                   ("prefill_union_packing", Wp, U, None),
                                   ("prefill_locality_chunk_major", Wp, 0, 0.97),
                                   ("prefill_locality_union_packing", Wp, U, 0.97)):
-            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, max(3, args.steps // 2), 1, flags=fl, rho=rho)
+            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, args.steps, 1, flags=fl, rho=rho)
             res["extra"][name] = {"ms_per_step": round(msv, 4), "tokens_per_s": round(pv.B * pv.N / (msv * 1e-3), 1),
                                   "Hq": pv.Hq, "Hkv": pv.Hkv, "query_rho": rho,
                                   "chunk_overlap_16": round(pv.overlap16, 4),
                                   "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kv.items()}}
         res["extra"]["decode_head_norm"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
-                                                        max(3, args.steps // 2), 2,
-                                                        flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
+                                                        args.steps, 2, flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(Wp, host)
     print(json.dumps(res), flush=True)

@@ -87,8 +87,10 @@ typedef enum {
  * the wording of Sec. 4.1 (each query head's chunk weights are normalised before
  * the maximum over the group's heads): the group score of chunk c becomes
  * max_h (s^_hc - log sum_{c' in C_i} exp(s^_hc')) instead of max_h s^_hc.  Only
- * the selection changes; the fusion weights use the raw s^_hc.  Costs a second
- * pass over the landmark scores.  Ignored by hils_bwd (the selection is given). */
+ * the selection changes; the fusion weights use the raw s^_hc.  Prefill scores the
+ * candidates twice; decode reads the landmarks once (keeping each head's top-K of
+ * every slice, ranked once the log-sum-exps are known) and its workspace grows by
+ * the kept candidates.  Ignored by hils_bwd (the selection is given). */
 #define HILS_FLAG_HEAD_NORM_SELECT 4u
 
 /* Prefill flag (bf16): compute the retrieved-chunk terms by union packing, the

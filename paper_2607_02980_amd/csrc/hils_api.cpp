@@ -102,7 +102,8 @@ size_t ws_bytes_for(const hils_params* p, int op) {
                 return hils::bwd_mfma_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk);
             return hils::bwd_workspace_layout(p->B, p->Hkv, p->N, p->L, p->topk).total;
         case HILS_OP_DECODE:
-            return hils::decode_workspace_bytes(p->B, p->N, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window);
+            return hils::decode_workspace_bytes(p->B, p->N, p->Hkv, p->Hq / p->Hkv, p->d, p->L, p->topk, p->window,
+                                                (p->flags & HILS_FLAG_HEAD_NORM_SELECT) != 0);
         default:
             return hils::prefill_workspace_bytes(p->B, p->Hq, p->Hkv, p->N, p->L, p->d, p->topk,
                                                  p->dtype == HILS_BF16,

@@ -52,14 +52,18 @@ constexpr int kMqMaxUnion = 256;  // union chunks of a multi-query workgroup (la
 struct DecLayout {
     int nC, nslices, nlocal, nparts;  // nparts = K + nlocal records per (b, g)
     int mq_umax;                      // union chunks per multi-query workgroup (at most)
-    size_t cand, parts, lse, mq, total;  // byte offsets
+    int hn_words;                     // 4-byte words of one (row, slice) record of hn
+    size_t cand, parts, lse, mq, hn, total;  // byte offsets
 };
 
 __host__ __device__ inline int local_pieces_max(int W) { return (W + 62) / 64 + 1; }
 
 // R = B * N rows; with N > 1 also the records of the multi-query pass
-// (k_dec_mq: per workgroup mq_umax union chunks x 16 tile rows)
-__host__ __device__ inline DecLayout dec_layout(int B, int N, int Hkv, int G, int d, int L, int K, int W) {
+// (k_dec_mq: per workgroup mq_umax union chunks x 16 tile rows); under the per-head
+// normalised ranking (HN) also, per (row, slice), the union of the G heads' top-K
+// chunks of the slice by raw score: its size, ids and G raw scores each.
+__host__ __device__ inline DecLayout dec_layout(int B, int N, int Hkv, int G, int d, int L, int K, int W,
+                                                int HN) {
     const int R = B * N;
     DecLayout o;
     o.nC = L / kChunk;
@@ -75,7 +79,9 @@ __host__ __device__ inline DecLayout dec_layout(int B, int N, int Hkv, int G, in
     const int nq = 16 / G < 8 ? 16 / G : 8;  // queries per multi-query workgroup
     o.mq_umax = nq * K + o.nlocal + 1;
     const size_t mq_groups = N > 1 ? (size_t)B * ((N + nq - 1) / nq) * Hkv : 0;
-    o.total = o.mq + ((mq_groups * o.mq_umax * 16 * (4 + d) * 4 + 255) & ~(size_t)255);
+    o.hn = o.mq + ((mq_groups * o.mq_umax * 16 * (4 + d) * 4 + 255) & ~(size_t)255);
+    o.hn_words = (1 + G * K * (1 + G) + 3) & ~3;
+    o.total = o.hn + (HN ? ((bg * o.nslices * o.hn_words * 4 + 255) & ~(size_t)255) : 0);
     return o;
 }
 
@@ -136,6 +142,9 @@ struct ScanSmem {
     int id[kSlice];
     int oid[NQ][64], tid[NQ][64];
     float osc[NQ][64], tsc[NQ][64];
+    unsigned hb[NQ][kSlice / 32];          // per query: the union of its heads' top-K (bitmap)
+    int hw_id[4][64], hw_tid[4][64];       // per wave: one head's top-K (normalised ranking)
+    float hw_sc[4][64], hw_tsc[4][64];
 };
 
 // 8 consecutive elements of an fp32 LDS row.
@@ -569,7 +578,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_parts_w(FwdArgs a) {
     const int w = wave_id();
     const int part = blockIdx.x * NW + w, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     const int pos = decode_position(a, b, n);
     const int lane = threadIdx.x % kWave;
     int csel = -1;  // this wave's chunk if part < K
@@ -684,23 +693,27 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
 
 // PAGED is a kernel parameter so that the contiguous scan keeps its small
 // register footprint (the paged loads need a 64-bit address per row).
-// mode kScanSelect: group scores and the slice's top-K.  For the per-head
-// normalised ranking the scan runs twice: kScanLse leaves each head's (max, sum
-// of exp) over the slice, kScanNormSelect subtracts each head's log-sum-exp over
-// all of C_i (from those partials) before the maximum over the heads.
+// mode kScanSelect: group scores and the slice's top-K.  mode kScanNormKeep (the
+// per-head normalised ranking, one pass over the landmarks): each head's (max, sum
+// of exp) over the slice, and the union of the G heads' top-K of the slice by raw
+// score with every member's G raw scores.  The group score max_h (s^_h - LSE_h)
+// needs each head's log-sum-exp over all of C_i, known only after every slice; the
+// union holds every chunk that can be among the row's K best by it (if a head's own
+// top-K of the slice misses c, K chunks of the slice beat c in that head, and so in
+// the normalised ranking wherever that head attains c's maximum), and k_dec_hnsel
+// ranks the unions once the log-sum-exps are known.
 // NQ new queries of one sequence share a workgroup (grid z = B x ceil(N / NQ)):
 // the landmark rows are read once for all of them; wave q selects for query q.
 // Each query row keeps its own candidate count (its own position).
-constexpr int kScanSelect = 0, kScanLse = 1, kScanNormSelect = 2;
+constexpr int kScanSelect = 0, kScanNormKeep = 1;
 template <typename T, int D, int G, int NQ, bool PAGED>
 __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
     static_assert(NQ <= kBlock / kWave, "one selecting wave per query");
     const int ngrp = (a.N + NQ - 1) / NQ;
     const int b = blockIdx.z / ngrp, n0 = (blockIdx.z % ngrp) * NQ, g = blockIdx.y;
     const int nq = min(NQ, a.N - n0);
-    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     __shared__ ScanSmem<G, NQ> ss;
-    __shared__ float s_lse[NQ][G];
     const int tid = threadIdx.x, wave = wave_id(), lane = tid % kWave;
     const int c0 = blockIdx.x * kSlice;
     float* cand_sc = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.cand);
@@ -713,16 +726,19 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
     int len = 0;  // the longest of the queries' slices (the last query's)
 #pragma unroll
     for (int q = 0; q < NQ; ++q) len = max(len, len_of(q));
-    // rows whose slice is empty: empty survivors (or lse partials) now
+    // rows whose slice is empty: empty survivors (or lse partials and an empty union) now
     for (int q = 0; q < nq; ++q) {
         if (len_of(q) > 0) continue;
         const size_t rg = row_of(q);
-        if (mode == kScanLse) {
+        if (mode == kScanNormKeep) {
             float* lp = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.lse) + (rg * ly.nslices) * G * 2;
             for (int t = tid; t < G; t += kBlock) {
                 lp[(blockIdx.x * G + t) * 2] = -INFINITY;
                 lp[(blockIdx.x * G + t) * 2 + 1] = 0.f;
             }
+            int* rec = reinterpret_cast<int*>(static_cast<char*>(a.ws) + ly.hn) +
+                       (rg * ly.nslices + blockIdx.x) * ly.hn_words;
+            if (tid == 0) rec[0] = 0;
         } else {
             const size_t cbase = (rg * ly.nslices + blockIdx.x) * a.K;
             for (int t = tid; t < a.K; t += kBlock) {
@@ -732,20 +748,6 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
         }
     }
     if (len <= 0) return;
-    if (mode == kScanNormSelect && tid < nq * G) {
-        // log-sum-exp of head hh of query q over all its candidates, from the slices' partials
-        const int q = tid / G, hh = tid % G;
-        const float* lp = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.lse) +
-                          (row_of(q) * ly.nslices) * G * 2;
-        float m = -INFINITY;
-        for (int sl = 0; sl < ly.nslices; ++sl) m = fmaxf(m, lp[(sl * G + hh) * 2]);
-        float sum = 0.f;
-        for (int sl = 0; sl < ly.nslices; ++sl) {
-            const float pm = lp[(sl * G + hh) * 2], ps = lp[(sl * G + hh) * 2 + 1];
-            sum += ps > 0.f ? ps * fexp(pm - m) : 0.f;
-        }
-        s_lse[q][hh] = m + __logf(sum);
-    }
     if constexpr (PAGED) {
         // the slice's page ids (s_id is free until the selection pass)
         for (int r = tid; r < len; r += kBlock) ss.id[r] = page_of(a, ly.nC, b, c0 + r);
@@ -768,7 +770,8 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
         }
         __syncthreads();
     }
-    if (mode == kScanLse) {
+    if (mode == kScanNormKeep) {
+        for (int i = tid; i < NQ * (kSlice / 32); i += kBlock) (&ss.hb[0][0])[i] = 0u;
         for (int e = wave; e < nq * G; e += kBlock / kWave) {
             const int q = e / G, hh = e % G, lq = len_of(q);
             if (lq <= 0) continue;
@@ -784,6 +787,58 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
                 lp[(blockIdx.x * G + hh) * 2 + 1] = sum;
             }
         }
+        __syncthreads();  // the bitmaps are clear
+        // each (query, head): its top-K of the slice by raw score, into the query's bitmap
+        for (int e = wave; e < nq * G; e += kBlock / kWave) {
+            const int q = e / G, hh = e % G, lq = len_of(q);
+            if (lq <= 0) continue;
+            constexpr int E = kSlice / kWave;
+            float sc[E];
+            int id[E];
+            bool ok[E];
+#pragma unroll
+            for (int r = 0; r < E; ++r) {
+                const int el = r * kWave + lane;
+                ok[r] = el < lq;
+                sc[r] = ok[r] ? ss.score[q][hh][el] : 0.f;
+                id[r] = ok[r] ? el : -1;
+            }
+            const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, ss.hw_id[wave], ss.hw_sc[wave],
+                                                         ss.hw_tid[wave], ss.hw_tsc[wave]);
+            for (int t = lane; t < m; t += kWave) {
+                const int el = ss.hw_id[wave][t];
+                atomicOr(&ss.hb[q][el >> 5], 1u << (el & 31));
+            }
+        }
+        __syncthreads();
+        // the union, ascending, with the G raw scores of each member
+        if (wave < nq) {
+            const int q = wave;
+            int* rec = reinterpret_cast<int*>(static_cast<char*>(a.ws) + ly.hn) +
+                       (row_of(q) * ly.nslices + blockIdx.x) * ly.hn_words;
+            int* rid = rec + 1;
+            float* rsc = reinterpret_cast<float*>(rec + 1 + G * a.K);
+            constexpr int NWD = kSlice / 32;
+            unsigned word = lane < NWD ? ss.hb[q][lane] : 0u;
+            const int cnt = __popc(word);
+            int incl = cnt;
+#pragma unroll
+            for (int o = 1; o < NWD; o <<= 1) {
+                const int y = __shfl_up(incl, o, kWave);
+                if (lane >= o) incl += y;
+            }
+            int pos = incl - cnt;
+            while (word) {
+                const int el = lane * 32 + __ffs(word) - 1;
+                rid[pos] = c0 + el;
+#pragma unroll
+                for (int hh = 0; hh < G; ++hh) rsc[pos * G + hh] = ss.score[q][hh][el];
+                ++pos;
+                word &= word - 1u;
+            }
+            const int U = __shfl(incl, NWD - 1, kWave);
+            if (lane == 0) rec[0] = U;
+        }
         return;
     }
     for (int e = tid; e < NQ * len; e += kBlock) {
@@ -791,7 +846,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
         float m = -INFINITY;
 #pragma unroll
         for (int hh = 0; hh < G; ++hh)
-            m = fmaxf(m, ss.score[q][hh][r] - (mode == kScanNormSelect ? s_lse[q][hh] : 0.f));
+            m = fmaxf(m, ss.score[q][hh][r]);
         ss.sig[q][r] = m;
     }
     __syncthreads();
@@ -820,13 +875,83 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
     }
 }
 
+// Per-head normalised ranking, after the one-pass scan: one wave per (row, slice).
+// The row's per-head log-sum-exps over all of C_i from the slices' (max, sum of
+// exp) partials, then the slice's union ranked by max_h (s^_h - LSE_h) and its
+// top-K written as the slice's survivors, which the merge then takes as usual.
+// E: registers per lane for the union (G * K <= 64 E).
+template <int E>
+__global__ __launch_bounds__(kBlock) void k_dec_hnsel(FwdArgs a, int G, int D) {
+    __shared__ int s_oid[kBlock / kWave][64], s_tid[kBlock / kWave][64];
+    __shared__ float s_osc[kBlock / kWave][64], s_tsc[kBlock / kWave][64];
+    const int w = wave_id(), lane = threadIdx.x % kWave;
+    const int g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
+    const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
+    const int sl = blockIdx.x * (kBlock / kWave) + w;
+    if (sl >= ly.nslices) return;  // the whole wave; no block barriers below
+    // LSE of every head: lane l takes head l % G over slices l / G, l / G + 64 / G, ...
+    // (G a power of two), then the lanes of one head merge their (max, sum of exp)
+    const float* lp = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.lse) +
+                      (rg * ly.nslices) * G * 2;
+    float mx = -INFINITY, sm = 0.f;
+    for (int t = lane / G; t < ly.nslices; t += kWave / G) {
+        const float pm = lp[(t * G + lane % G) * 2], ps = lp[(t * G + lane % G) * 2 + 1];
+        if (ps > 0.f) {
+            const float nm = fmaxf(mx, pm);
+            sm = sm * fexp(mx - nm) + ps * fexp(pm - nm);
+            mx = nm;
+        }
+    }
+    for (int o = G; o < kWave; o <<= 1) {
+        const float om = __shfl_xor(mx, o, kWave), os = __shfl_xor(sm, o, kWave);
+        const float nm = fmaxf(mx, om);
+        if (nm != -INFINITY) {
+            sm = (mx == -INFINITY ? 0.f : sm * fexp(mx - nm)) + (om == -INFINITY ? 0.f : os * fexp(om - nm));
+            mx = nm;
+        }
+    }
+    const float lse = mx + __logf(sm);  // lanes h < G hold head h's
+    float lh[8];
+#pragma unroll
+    for (int h = 0; h < 8; ++h) lh[h] = __shfl(lse, h, kWave);
+    const int* rec = reinterpret_cast<const int*>(static_cast<const char*>(a.ws) + ly.hn) +
+                     (rg * ly.nslices + sl) * ly.hn_words;
+    const int U = min(rec[0], G * a.K);
+    const int* rid = rec + 1;
+    const float* rsc = reinterpret_cast<const float*>(rec + 1 + G * a.K);
+    float sc[E];
+    int id[E];
+    bool ok[E];
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+        const int e = r * kWave + lane;
+        ok[r] = e < U;
+        id[r] = ok[r] ? rid[e] : -1;
+        float m = -INFINITY;
+#pragma unroll
+        for (int h = 0; h < 8; ++h)
+            if (h < G && ok[r]) m = fmaxf(m, rsc[e * G + h] - lh[h]);
+        sc[r] = ok[r] ? m : 0.f;
+    }
+    // the union's ids ascend over (register, lane)
+    const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, s_oid[w], s_osc[w], s_tid[w], s_tsc[w]);
+    float* cand_sc = reinterpret_cast<float*>(static_cast<char*>(a.ws) + ly.cand);
+    int* cand_id = reinterpret_cast<int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
+    const size_t cbase = (rg * ly.nslices + sl) * a.K;
+    for (int t = lane; t < a.K; t += kWave) {
+        cand_sc[cbase + t] = t < m ? s_osc[w][t] : -INFINITY;
+        cand_id[cbase + t] = t < m ? s_oid[w][t] : -1;
+    }
+}
+
 // fp32 path: the merge as its own pass (one workgroup per row) before k_dec_parts.
 template <int E>
 __global__ __launch_bounds__(kBlock) void k_dec_merge(FwdArgs a, int G, int D) {
     __shared__ MergeSmem<kBlock / kWave> ms;
     const int b = blockIdx.y / a.N, n = blockIdx.y % a.N, g = blockIdx.x;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     merge_row<E, kBlock / kWave>(a, ly, rg, ms, wave_id());
     for (int t = threadIdx.x; t < a.K; t += kBlock) a.idx[rg * a.K + t] = t < ms.nbest ? ms.bid[t] : -1;
 }
@@ -840,7 +965,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_parts(FwdArgs a) {
     __shared__ int s_c;
     const int slot = blockIdx.x, g = blockIdx.y, b = blockIdx.z / a.N, n = blockIdx.z % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     const int pos = decode_position(a, b, n);
     auto run = [&](int part, int c, int nk, bool is_chunk) {
         if constexpr (kMfma)
@@ -951,7 +1076,7 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
     __shared__ CombineSmem<G> cs;
     const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     combine_row<T, D, G, kBlock>(a, ly, cs, b, n, g, rg);
 }
 
@@ -1149,7 +1274,7 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     bf16* tiles = reinterpret_cast<bf16*>(s_raw);
     const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
-    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     const int pos = decode_position(a, b, n);
     const int ncand = n_candidates(pos, a.W);
     const int tid = threadIdx.x, w = wave_id();
@@ -1210,7 +1335,7 @@ __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_mq(FwdArgs a) {
     const int ngrp = (a.N + NQ - 1) / NQ;
     const int g = blockIdx.x, b = blockIdx.y / ngrp, n0 = (blockIdx.y % ngrp) * NQ;
     const int nq = min(NQ, a.N - n0);
-    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+    const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16, n16 = lane % 16;
     auto row_of = [&](int q) { return ((size_t)b * a.Hkv + g) * a.N + n0 + q; };
 
@@ -1558,7 +1683,7 @@ struct DecRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
         const int R = a.B * a.N;  // rows (sequence, new query); the host keeps R <= 65535
-        const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W);
+        const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
         if (!a.given_idx) {
             // one new query per sequence: a workgroup per (slice, group, row); several:
             // the sequence's queries four at a time share each landmark read
@@ -1578,8 +1703,17 @@ struct DecRun {
                 }
             };
             if (a.head_norm) {
-                scan(kScanLse);
-                scan(kScanNormSelect);
+                scan(kScanNormKeep);
+                const dim3 hgrid((ly.nslices + kBlock / kWave - 1) / (kBlock / kWave), a.Hkv, R);
+                const int gk = G * a.K;
+                if (gk <= 64)
+                    HILS_LAUNCH("k_dec_hnsel", (k_dec_hnsel<1>), hgrid, dim3(kBlock), 0, s, a, G, D);
+                else if (gk <= 128)
+                    HILS_LAUNCH("k_dec_hnsel", (k_dec_hnsel<2>), hgrid, dim3(kBlock), 0, s, a, G, D);
+                else if (gk <= 256)
+                    HILS_LAUNCH("k_dec_hnsel", (k_dec_hnsel<4>), hgrid, dim3(kBlock), 0, s, a, G, D);
+                else
+                    HILS_LAUNCH("k_dec_hnsel", (k_dec_hnsel<8>), hgrid, dim3(kBlock), 0, s, a, G, D);
             } else {
                 scan(kScanSelect);
             }
@@ -1662,8 +1796,8 @@ int device_cus() {
 }
 
 
-size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W) {
-    return dec_layout(B, N, Hkv, G, d, L, K, W).total;
+size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W, int head_norm) {
+    return dec_layout(B, N, Hkv, G, d, L, K, W, head_norm).total;
 }
 
 hipError_t launch_decode_fwd(const FwdArgs& a, hipStream_t s) {

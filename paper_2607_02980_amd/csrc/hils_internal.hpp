@@ -125,7 +125,7 @@ BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K);
 // Compute units of the current device (a host-side attribute query; nothing cached).
 int device_cus();
 
-size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W);
+size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W, int head_norm);
 
 size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16, int union_pack);
 

@@ -760,112 +760,124 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
         }
         const int* myidx = s_idx + (qb * 16 + lane % 16) * a.K;
         int ptr = 0;
-        // two chunks in flight: chunk u + 1 waits in registers (nx) while chunk u + 2
-        // is being fetched (nx2) and chunk u is computed from LDS; the chunk's G
-        // landmark rows and biases travel with its K/V (threads < G * D / 8)
+        // Four union chunks in flight: chunk u is computed from LDS buffer u % 2 while
+        // chunks u + 1 .. u + 3 wait in a ring of registers (named slots, the loop
+        // unrolled four times, so that no register copy waits on a pending load) and
+        // chunk u + 4 is fetched into the slot chunk u + 1 leaves when it is staged.
+        // The chunk's G landmark rows and biases travel with its K/V (threads <
+        // G * D / 8).  Past the union's end the fetches re-read the last chunk (in
+        // bounds, never staged), so the loads are the same in every iteration.
         const bool lm_thread = tid < G * D / 8;
         const int lm_h = tid / (D / 8), lm_d8 = (tid % (D / 8)) * 8;
         const int lm_hl = (a.Hl == a.Hq) ? g * G + min(lm_h, G - 1) : g;
         const bf16* lm_base = as<bf16>(a.lmk) + ((size_t)b * a.Hl + lm_hl) * nC * D + lm_d8;
-        auto fetch_lm = [&](int cc) { return lm_thread ? *reinterpret_cast<const uint4*>(lm_base + (size_t)cc * D) : make_uint4(0, 0, 0, 0); };
-        auto fetch_lb = [&](int cc) { return (lm_thread && lm_d8 == 0 && a.bias) ? a.bias[((size_t)b * a.Hl + lm_hl) * nC + cc] : 0.f; };
-        auto stage_lm = [&](int bb, uint4 x, float bv) {
+        struct Slot {
+            KV kv;
+            uint4 lm;
+            float lb;
+        };
+        auto fetch_slot = [&](int u) {
+            Slot x;
+            const int cc = U > 0 ? s_list[min(u, U - 1)] : 0;
+            x.kv = fetch(cc * kChunk);
+            x.lm = lm_thread ? *reinterpret_cast<const uint4*>(lm_base + (size_t)cc * D) : make_uint4(0, 0, 0, 0);
+            x.lb = (lm_thread && lm_d8 == 0 && a.bias) ? a.bias[((size_t)b * a.Hl + lm_hl) * nC + cc] : 0.f;
+            return x;
+        };
+        auto stage_slot = [&](int bb, const Slot& x) {
+            stage(bb, x.kv);
             if (lm_thread) {
-                *reinterpret_cast<uint4*>(&s_lm[bb][lm_h * D + lm_d8]) = x;
-                if (lm_d8 == 0) s_lb[bb][lm_h] = bv;
+                *reinterpret_cast<uint4*>(&s_lm[bb][lm_h * D + lm_d8]) = x.lm;
+                if (lm_d8 == 0) s_lb[bb][lm_h] = x.lb;
             }
         };
-        KV nx2;
-        uint4 lx = make_uint4(0, 0, 0, 0), lx2 = lx;
-        float bx = 0.f, bx2 = 0.f;
-        if (U > 0) {
-            nx = fetch(s_list[0] * kChunk);
-            stage(0, nx);
-            stage_lm(0, fetch_lm(s_list[0]), fetch_lb(s_list[0]));
-            if (U > 1) {
-                nx = fetch(s_list[1] * kChunk);
-                lx = fetch_lm(s_list[1]);
-                bx = fetch_lb(s_list[1]);
-            }
-        }
-        __syncthreads();
-        buf = 0;
-        for (int u = 0; u < U; ++u, buf ^= 1) {
-            const bool more = u + 1 < U;
-            if (u + 2 < U) {
-                nx2 = fetch(s_list[u + 2] * kChunk);
-                lx2 = fetch_lm(s_list[u + 2]);
-                bx2 = fetch_lb(s_list[u + 2]);
-            }
+        // chunk u from buffer u % 2: s^, the intra-chunk softmax and O^T for the rows
+        // that selected it, folded into the row's online fusion
+        auto compute = [&](int u) {
+            const int bb = u & 1;
             const int c = s_list[u];
             const bool sel = nq_raw < a.N && myidx[min(ptr, a.K - 1)] == c && ptr < a.K;
             ptr += sel ? 1 : 0;
-            if (__ballot(sel) != 0ull) {
-                const bf16* tk = s_k[buf];
-                const bf16* tv = s_v[buf];
-                // s^ of the rows for chunk c: the landmark row is row 0 of the A tile
-                f32x4 sh4 = zero4();
+            if (__ballot(sel) == 0ull) return;
+            const bf16* tk = s_k[bb];
+            const bf16* tv = s_v[bb];
+            // s^ of the rows for chunk c: the landmark row is row 0 of the A tile
+            f32x4 sh4 = zero4();
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const bf16x8 lrow = ld_bf16x8(&s_lm[buf][hh * D + ks * 32 + lg * 8]);
-                    const bf16x8 aL = (lane % 16 == 0) ? lrow : as_bf16x8(make_uint4(0, 0, 0, 0));
-                    sh4 = mfma16x16x32(aL, ROUTE ? bqr[ks] : bq[ks], sh4);
-                }
-                const float shat = a.scale * group0_bcast(sh4[0]) + s_lb[buf][hh];
-                f32x4 st[4];
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    st[kb] = zero4();
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks)
-                        st[kb] = mfma16x16x32(ld_bf16x8(tk + (kb * 16 + lane % 16) * KROW + ks * 32 + lg * 8), bq[ks],
-                                              st[kb]);
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-                float mx = -INFINITY;
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[kb][i]);
-                mx = group4_max(mx) * c1;
-                float psum = 0.f;
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        st[kb][i] = fexp2(fmaf(st[kb][i], c1, -mx));
-                        psum += st[kb][i];
-                    }
-                const bf16x8 pb0 = p_operand(st[0], st[1]);
-                const bf16x8 pb1 = p_operand(st[2], st[3]);
-                psum = group4_sum(psum);
-                // online fusion: a selected chunk whose s^ exceeds the row's M so far
-                // rescales the numerator and denominator to the new maximum
-                const float Mn = sel ? fmaxf(M, shat) : M;
-                const float rs = fexp(M - Mn);
-#pragma unroll
-                for (int db = 0; db < DB; ++db) o[db] *= rs;
-                zs *= rs;
-                M = Mn;
-                const float wk = sel ? fexp(shat - M) : 0.f;
-                zs += wk;
-                const float f = wk / psum;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    f32x4 oc = mfma16x16x32(tr_operand_perm(tv, VROW, 0, db * 16, lane), pb0, zero4());
-                    oc = mfma16x16x32(tr_operand_perm(tv, VROW, 32, db * 16, lane), pb1, oc);
-                    o[db] += f * oc;
-                    if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
-                }
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 lrow = ld_bf16x8(&s_lm[bb][hh * D + ks * 32 + lg * 8]);
+                const bf16x8 aL = (lane % 16 == 0) ? lrow : as_bf16x8(make_uint4(0, 0, 0, 0));
+                sh4 = mfma16x16x32(aL, ROUTE ? bqr[ks] : bq[ks], sh4);
             }
-            if (more) {
-                stage(buf ^ 1, nx);
-                stage_lm(buf ^ 1, lx, bx);
+            const float shat = a.scale * group0_bcast(sh4[0]) + s_lb[bb][hh];
+            f32x4 st[4];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                st[kb] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    st[kb] = mfma16x16x32(ld_bf16x8(tk + (kb * 16 + lane % 16) * KROW + ks * 32 + lg * 8), bq[ks],
+                                          st[kb]);
+                __builtin_amdgcn_sched_barrier(0);
             }
-            nx = nx2;
-            lx = lx2;
-            bx = bx2;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[kb][i]);
+            mx = group4_max(mx) * c1;
+            float psum = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    st[kb][i] = fexp2(fmaf(st[kb][i], c1, -mx));
+                    psum += st[kb][i];
+                }
+            const bf16x8 pb0 = p_operand(st[0], st[1]);
+            const bf16x8 pb1 = p_operand(st[2], st[3]);
+            psum = group4_sum(psum);
+            // online fusion: a selected chunk whose s^ exceeds the row's M so far
+            // rescales the numerator and denominator to the new maximum
+            const float Mn = sel ? fmaxf(M, shat) : M;
+            const float rs = fexp(M - Mn);
+            zs *= rs;
+            M = Mn;
+            const float wk = sel ? fexp(shat - M) : 0.f;
+            zs += wk;
+            const float f = wk / psum;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                f32x4 oc = mfma16x16x32(tr_operand_perm(tv, VROW, 0, db * 16, lane), pb0, zero4());
+                oc = mfma16x16x32(tr_operand_perm(tv, VROW, 32, db * 16, lane), pb1, oc);
+                o[db] = o[db] * rs + f * oc;
+                if (db % 2 == 1) __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        // one step: fetch chunk u + 4 into `ld`, compute chunk u, stage chunk u + 1
+        // (held in `st`) into the other buffer
+        auto step = [&](int u, Slot& st, Slot& ld) {
+            ld = fetch_slot(u + 4);
+            compute(u);
+            if (u + 1 < U) stage_slot((u + 1) & 1, st);
             __syncthreads();
+        };
+        Slot r0, r1, r2, r3;
+        if (U > 0) {
+            stage_slot(0, fetch_slot(0));
+            r1 = fetch_slot(1);
+            r2 = fetch_slot(2);
+            r3 = fetch_slot(3);
+        }
+        __syncthreads();
+        for (int u = 0; u < U; u += 4) {
+            step(u, r1, r0);
+            if (u + 1 >= U) break;
+            step(u + 1, r2, r1);
+            if (u + 2 >= U) break;
+            step(u + 2, r3, r2);
+            if (u + 3 >= U) break;
+            step(u + 3, r0, r3);
         }
     } else {
     // the row's retrieved chunks: slots in idx order, valid entries only

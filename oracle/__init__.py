@@ -24,6 +24,10 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "hils_oracle.c")
 _LIBS = {"f64": os.path.join(_HERE, "liboracle_f64.so"), "f32": os.path.join(_HERE, "liboracle_f32.so")}
+# HILS_ORACLE_SANITIZED=1 loads the AddressSanitizer/UBSan builds instead (build_sanitized;
+# the process must preload clang's ASan runtime)
+_SAN_LIBS = {k: v.replace(".so", "_san.so") for k, v in _LIBS.items()}
+_CLANG = "/opt/rocm/llvm/bin/clang"
 
 
 def build(verbose: bool = False) -> None:
@@ -32,6 +36,21 @@ def build(verbose: bool = False) -> None:
         out = _LIBS[tag]
         cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", f"-DREAL={real}",
                f"-DSUFFIX={tag}", f"-DREAL_IS_FLOAT={isf}", "-o", out + ".tmp", _SRC, "-lm"]
+        if verbose:
+            print(" ".join(cmd))
+        subprocess.check_call(cmd)
+        os.replace(out + ".tmp", out)
+
+
+def build_sanitized(verbose: bool = False) -> None:
+    """Both precisions compiled with clang under AddressSanitizer and
+    UndefinedBehaviorSanitizer (single-threaded: no OpenMP), for the CPU
+    sanitizer run of the pins."""
+    for tag, real, isf in (("f64", "double", 0), ("f32", "float", 1)):
+        out = _SAN_LIBS[tag]
+        cmd = [_CLANG, "-O1", "-g", "-fPIC", "-shared", "-std=c11", "-fsanitize=address,undefined",
+               "-fno-omit-frame-pointer", "-fno-sanitize-recover=undefined", f"-DREAL={real}",
+               f"-DSUFFIX={tag}", f"-DREAL_IS_FLOAT={isf}", "-Wno-unknown-pragmas", "-o", out + ".tmp", _SRC, "-lm"]
         if verbose:
             print(" ".join(cmd))
         subprocess.check_call(cmd)
@@ -70,7 +89,7 @@ _loaded: dict[str, ctypes.CDLL] = {}
 
 def _lib(prec: str) -> ctypes.CDLL:
     if prec not in _loaded:
-        path = _LIBS[prec]
+        path = (_SAN_LIBS if os.environ.get("HILS_ORACLE_SANITIZED") == "1" else _LIBS)[prec]
         if not os.path.exists(path):
             build()
         _loaded[prec] = ctypes.CDLL(path)

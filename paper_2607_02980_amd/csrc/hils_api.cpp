@@ -60,7 +60,12 @@ int check_params(const hils_params* p, int op) {
     if (p->Hl != p->Hq && p->Hl != p->Hkv)
         return fail(HILS_ERR_INVALID, "Hl=%d must equal Hq=%d or Hkv=%d", p->Hl, p->Hq, p->Hkv);
     if (p->L % p->chunk) return fail(HILS_ERR_INVALID, "L=%d is not a multiple of chunk=%d", p->L, p->chunk);
-    if (p->dtype != HILS_F32 && p->dtype != HILS_BF16) return fail(HILS_ERR_INVALID, "unknown dtype %d", (int)p->dtype);
+    // the field's bits as an int: a C caller may store any value there, and loading
+    // one outside the enumerators as the enum type is undefined in C++
+    int dtype_raw = 0;
+    static_assert(sizeof(p->dtype) == sizeof(int), "hils_dtype has the size of an int");
+    memcpy(&dtype_raw, &p->dtype, sizeof dtype_raw);
+    if (dtype_raw != HILS_F32 && dtype_raw != HILS_BF16) return fail(HILS_ERR_INVALID, "unknown dtype %d", dtype_raw);
     if (!isfinite(p->scale)) return fail(HILS_ERR_INVALID, "scale is not finite");
     if (p->flags & ~(HILS_FLAG_GIVEN_IDX | HILS_FLAG_SHARED_LMK_QUERY | HILS_FLAG_HEAD_NORM_SELECT |
                      HILS_FLAG_UNION_PACKING))

@@ -1,7 +1,8 @@
 """ctypes binding of libhils.so -- argument marshalling only.
 
 The entry points keep the C names (``hils_prefill_fwd``, ``hils_decode_fwd``,
-``hils_bwd``, ``hils_landmark_fwd``, ``hils_landmark_bwd``,
+``hils_decode_fwd_noalloc``, ``hils_decode_paged_fwd``, ``hils_bwd``,
+``hils_landmark_fwd``, ``hils_landmark_bwd``,
 ``hils_workspace_size``, ``hils_last_error``, ``hils_version``).
 They take torch tensors already resident on the GPU, check dtype, shape,
 device and contiguity, allocate missing outputs and the workspace with
@@ -17,7 +18,9 @@ from dataclasses import dataclass
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhils.so")
+# HILS_LIB names another build of the same sources (the sanitizer build of the
+# host code, libhils_san.so); by default the in-tree libhils.so
+_LIB_PATH = os.environ.get("HILS_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhils.so")
 
 HILS_F32, HILS_BF16 = 0, 1
 HILS_OK, HILS_ERR_INVALID, HILS_ERR_UNSUPPORTED, HILS_ERR_WORKSPACE, HILS_ERR_HIP = range(5)

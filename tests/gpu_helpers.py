@@ -6,9 +6,11 @@ Tolerances (stated once, used by every GPU test):
     group score lies within 1e-4 of the oracle's K-th score (a tie in fp32 vs fp64);
   * f32 outputs: max |d| <= 1e-4;  lse <= 1e-4 (both storage dtypes);
   * bf16 outputs: max |d| <= 2e-2 and mean |d| <= 2e-3;
-  * gradients: the same bars, relative to max(1, max |ref|) (max) and
-    max(1, mean |ref|) (mean), since gradient magnitudes grow with the number
-    of rows that touch a key.
+  * gradients (stored in the input dtype; their magnitudes grow with the number
+    of rows that touch a key, up to ~10 here): every element within the max bar
+    times max(1, |its reference|) (bf16 storage rounds each element relative to
+    its own size), the mean bar times max(1, mean |ref|), and the norm of the
+    error within 5e-3 (bf16) / 1e-5 (f32) of the reference's norm.
 Outputs are compared with the oracle re-run in forced-index mode on the GPU's
 own selection once that selection has been accepted, so a legal tie flip never
 shows up as an output error.
@@ -105,6 +107,9 @@ def check_selection(p, host: dict, gpu_idx: np.ndarray, ref_idx: np.ndarray, qpo
     return diff
 
 
+REL_NORM_TOL = {"f32": 1e-5, "bf16": 5e-3}
+
+
 def check_close(name, got, ref, dtype, rel=False):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
@@ -112,13 +117,20 @@ def check_close(name, got, ref, dtype, rel=False):
     assert np.isfinite(got).all(), f"{name}: non-finite values"
     d = np.abs(got - ref)
     mx_tol, mean_tol = OUT_TOL[dtype]
-    if rel:
-        mx_tol *= max(1.0, float(np.abs(ref).max()))
-        mean_tol *= max(1.0, float(np.abs(ref).mean()))
     rel_err = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
-    log(f"  {name}: max|d|={d.max():.3e} (tol {mx_tol:.1e}) mean|d|={d.mean():.3e} (tol {mean_tol:.1e}) "
-        f"rel={rel_err:.2e}")
-    assert d.max() <= mx_tol, f"{name}: max |d| {d.max():.3e} > {mx_tol:.1e}"
+    if rel:
+        # gradients: each element against its own magnitude
+        scale = np.maximum(1.0, np.abs(ref))
+        worst = float((d / scale).max())
+        mean_tol *= max(1.0, float(np.abs(ref).mean()))
+        log(f"  {name}: max|d|={d.max():.3e} max|d|/max(1,|ref|)={worst:.3e} (tol {mx_tol:.1e}) "
+            f"mean|d|={d.mean():.3e} (tol {mean_tol:.1e}) rel={rel_err:.2e} (tol {REL_NORM_TOL[dtype]:.0e})")
+        assert worst <= mx_tol, f"{name}: an element's |d| / max(1, |ref|) is {worst:.3e} > {mx_tol:.1e}"
+        assert rel_err <= REL_NORM_TOL[dtype], f"{name}: |d| / |ref| = {rel_err:.2e}"
+    else:
+        log(f"  {name}: max|d|={d.max():.3e} (tol {mx_tol:.1e}) mean|d|={d.mean():.3e} (tol {mean_tol:.1e}) "
+            f"rel={rel_err:.2e}")
+        assert d.max() <= mx_tol, f"{name}: max |d| {d.max():.3e} > {mx_tol:.1e}"
     assert d.mean() <= mean_tol, f"{name}: mean |d| {d.mean():.3e} > {mean_tol:.1e}"
 
 

@@ -399,6 +399,38 @@ def cpu_baseline(W_, host, target_s=20.0):
                       f"fp32 oracle, {dt:.2f} s wall on {threads} threads of a {model}"}
 
 
+def run_part(part, torch, hils, synth, WORKLOADS, args):
+    """One part of the bench on its own (each of its workloads as in the full run)."""
+    Wp, Wd = WORKLOADS["prefill_32k_bf16"], WORKLOADS["decode_131k_bf16_b32"]
+    out = {"part": part}
+    if part == "prefill":
+        _, _, ms, kt = bench_prefill(torch, hils, synth, Wp, args.steps, args.warmup)
+        out[Wp.name] = {"ms_per_step": round(ms, 4), "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kt.items()}}
+    elif part == "decode":
+        out["decode"] = bench_decode(torch, hils, synth, Wd, args.steps, 2)
+        out["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"], args.steps, 2)
+        out["decode_paged"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, paged=True)
+        out["decode_4_new_tokens"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, N=4)
+        out["decode_Hl_eq_Hkv"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, Hl=Wd.Hkv)
+        out["decode_head_norm"] = bench_decode(torch, hils, synth, Wd, args.steps, 2,
+                                               flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
+    elif part == "train":
+        out["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], args.steps, 1)
+    elif part == "landmark":
+        out["landmark"] = bench_landmark(torch, hils, synth, Wp, args.steps, args.warmup)
+    elif part == "variants":
+        U = hils.HILS_FLAG_UNION_PACKING
+        for name, W_, fl, rho in (("prefill_head_norm", Wp, hils.HILS_FLAG_HEAD_NORM_SELECT, None),
+                                  ("prefill_mha_G1", Wp.with_(Hkv=Wp.Hq), 0, None),
+                                  ("prefill_union_packing", Wp, U, None),
+                                  ("prefill_locality_chunk_major", Wp, 0, 0.97),
+                                  ("prefill_locality_union_packing", Wp, U, 0.97)):
+            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, args.steps, 1, flags=fl, rho=rho)
+            out[name] = {"ms_per_step": round(msv, 4), "chunk_overlap_16": round(pv.overlap16, 4),
+                         "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kv.items()}}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -409,6 +441,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-landmark", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
+    ap.add_argument("--part", default="all", choices=["all", "prefill", "decode", "train", "landmark", "variants"],
+                    help="run one part only and print its JSON (for per-workload profiles); the contract "
+                         "line is printed by the default, all")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 1 GiB device-to-device (a plain copy kernel of known size, used to "
                          "calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -430,6 +465,9 @@ def main():
         torch.cuda.synchronize()
         del x, y
     Wp = WORKLOADS["prefill_32k_bf16"]
+    if args.part != "all":
+        print(json.dumps(run_part(args.part, torch, hils, synth, WORKLOADS, args)), flush=True)
+        return
     p, host, ms, kernels = bench_prefill(torch, hils, synth, Wp, args.steps, args.warmup)
     model = prefill_kernel_model(p.B, p.Hq, p.Hkv, p.N, p.L, p.d, p.chunk, p.topk, p.window)
     table = {}

@@ -543,7 +543,7 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
 // ---------------------------------------------------------------------------
 // One block of 8 waves per tile of QT = 16 * 8 / G queries of one KV group:
 // wave w owns the item (head w / QB, 16-query block w % QB), i.e. 16 rows of
-// one head.  The 64-key blocks of K and V that the tile's windows cover are
+// one head (under UNION: queries 16/G w .. 16/G (w + 1) - 1, all G heads).  The 64-key blocks of K and V that the tile's windows cover are
 // double-buffered in LDS: block j + 1 is fetched into registers while block j
 // is used and stored into the other buffer afterwards, one barrier per block.
 // After the window, the row's retrieved-chunk slots are added into the same
@@ -587,8 +587,13 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     const bf16* kbase = as<bf16>(a.k) + bg * a.L * D;
     const bf16* vbase = as<bf16>(a.v) + bg * a.L * D;
     const float c1 = a.scale * kLog2e;
-    const int hh = w / C::QB, qb = w % C::QB;
-    const int nq_raw = q0 + qb * 16 + lane % 16;
+    // row of the tile and query head of this lane's MFMA column: 16 queries of
+    // one head per wave, or under UNION the paper's packing (Sec. 4.2) of 16 / G
+    // queries x the G heads, so that a wave's chunks are the union of only 16 / G
+    // queries' selections (the heads share the selection)
+    const int hh = UNION ? (lane % 16) % G : w / C::QB;
+    const int trow = UNION ? w * (16 / G) + (lane % 16) / G : (w % C::QB) * 16 + lane % 16;
+    const int nq_raw = q0 + trow;
     const int nq = min(nq_raw, a.N - 1);
     const size_t row = ((size_t)b * a.Hq + g * G + hh) * a.N + nq;
 
@@ -758,7 +763,7 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) bqr[ks] = ld_bf16x8(rrow + ks * 32 + lg * 8);
         }
-        const int* myidx = s_idx + (qb * 16 + lane % 16) * a.K;
+        const int* myidx = s_idx + trow * a.K;
         int ptr = 0;
         // Four union chunks in flight: chunk u is computed from LDS buffer u % 2 while
         // chunks u + 1 .. u + 3 wait in a ring of registers (named slots, the loop
@@ -801,15 +806,25 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
             if (__ballot(sel) == 0ull) return;
             const bf16* tk = s_k[bb];
             const bf16* tv = s_v[bb];
-            // s^ of the rows for chunk c: the landmark row is row 0 of the A tile
+            // s^ of the rows for chunk c: the G heads' landmark rows are rows 0..G-1
+            // of the A tile, so column p's own head hh sits in accumulator row hh,
+            // held by lane group hh / 4 as element hh % 4
             f32x4 sh4 = zero4();
+            const int ar = min(lane % 16, G - 1);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 lrow = ld_bf16x8(&s_lm[bb][hh * D + ks * 32 + lg * 8]);
-                const bf16x8 aL = (lane % 16 == 0) ? lrow : as_bf16x8(make_uint4(0, 0, 0, 0));
+                const bf16x8 lrow = ld_bf16x8(&s_lm[bb][ar * D + ks * 32 + lg * 8]);
+                const bf16x8 aL = (lane % 16 < G) ? lrow : as_bf16x8(make_uint4(0, 0, 0, 0));
                 sh4 = mfma16x16x32(aL, ROUTE ? bqr[ks] : bq[ks], sh4);
             }
-            const float shat = a.scale * group0_bcast(sh4[0]) + s_lb[bb][hh];
+            const int hi = hh & 3;
+            const float shv = hi == 0 ? sh4[0] : hi == 1 ? sh4[1] : hi == 2 ? sh4[2] : sh4[3];
+            float shr;
+            if constexpr (G <= 4)
+                shr = group0_bcast(shv);
+            else
+                shr = __shfl(shv, (hh >> 2) * 16 + lane % 16, kWave);
+            const float shat = a.scale * shr + s_lb[bb][hh];
             f32x4 st[4];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) {

@@ -31,6 +31,7 @@ CASES = {
                              0.0),
     "f32_route_bias_G2": (dict(B=2, Hq=4, Hkv=2, N=700, L=704, d=128, topk=5, window=130, dtype="f32"), 105, True,
                           True, 0.0),
+    "bf16_G2_route_bias": (dict(B=1, Hq=4, Hkv=2, N=700, L=704, d=128, topk=5, window=130), 119, True, True, 0.0),
     "bf16_mha_G1": (dict(B=1, Hq=2, Hkv=2, N=512, L=512, d=64, topk=3, window=70), 106, False, False, 0.0),
     "bf16_G8_d128": (dict(B=1, Hq=8, Hkv=1, N=576, L=576, d=128, topk=16, window=64), 107, True, False, 0.0),
     "bf16_topk_exceeds_candidates": (dict(B=1, Hq=4, Hkv=1, N=300, L=320, d=64, topk=16, window=64), 108, False,
@@ -111,7 +112,7 @@ def test_prefill_forced_index(name):
 
 
 @pytest.mark.parametrize("name", ["bf16_ragged_multi_tile", "bf16_window1", "bf16_bias_boosted", "bf16_route_Hl_eq_Hkv",
-                                  "bf16_mha_G1", "bf16_G8_d128", "bf16_topk_exceeds_candidates", "bf16_all_local",
+                                  "bf16_G2_route_bias", "bf16_mha_G1", "bf16_G8_d128", "bf16_topk_exceeds_candidates", "bf16_all_local",
                                   "bf16_K32", "bf16_K64_d64", "bf16_paper_shape_d64_G8_K32", "bf16_head_gap_150",
                                   "bf16_head_gap_150_G8_d64"])
 def test_prefill_union_packing(name):

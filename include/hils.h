@@ -278,6 +278,21 @@ int hils_landmark_bwd(const hils_params* p, const void* lq, const void* k, const
                       void* stream);
 
 /*
+ * Prefill (bf16, chunk-major): the most bytes of per-slot records (the chunk
+ * outputs o_c and scores s^ of Eq. (10), B * Hq * K * (2 d + 4) bytes per query
+ * row) that one pass over the rows may hold.  A longer prefill runs its inverse
+ * index, chunk pass and local pass over consecutive segments of rows (multiples of
+ * 2048) whose records fit, reusing one workspace, so that the workspace stays
+ * bounded whatever N (at 32 query heads, K = 16 and d = 128 the records take 133
+ * KB per row: 69 GB for a 512K-token prefill).  Results are bitwise the same for
+ * any cap.  The default, 16 GiB, keeps one segment up to 126K rows of that shape.
+ * Process-wide; hils_workspace_size reflects the value at the time of the call, so
+ * set it before sizing workspaces.  Returns the previous cap; bytes = 0 only
+ * reads it.
+ */
+size_t hils_prefill_record_cap(size_t bytes);
+
+/*
  * Optional per-kernel timing, for profiling (not needed to use the operator).
  * hils_timing_enable(1) makes every kernel that the library launches from the
  * calling thread be bracketed by two HIP events on the launch's stream (this

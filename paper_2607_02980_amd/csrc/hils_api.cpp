@@ -215,6 +215,8 @@ int hils_timing_read(char* names, size_t names_len, float* total_ms, int* launch
 
 int hils_version(void) { return 100; }
 
+size_t hils_prefill_record_cap(size_t bytes) { return hils::prefill_record_cap(bytes); }
+
 const char* hils_last_error(void) { return g_err.c_str(); }
 
 int hils_workspace_size(const hils_params* p, int op, size_t* bytes) {

@@ -27,9 +27,6 @@ namespace hils {
 constexpr int kBlock = 256;
 constexpr int kSortCap = 4096;  // retrieval lists up to this length are sorted (deterministic order)
 
-
-InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base);
-
 BwdWorkspace bwd_workspace_layout(int B, int Hkv, int N, int L, int K) {
     const InvLayout iv = inv_layout(B, Hkv, N, L, K, 0);
     BwdWorkspace w;
@@ -202,8 +199,9 @@ constexpr int kInvRows = 256;
 constexpr int kInvHist = 8192;  // chunks counted in LDS; larger L falls back to global atomics
 static_assert(kInvBucketRows % kInvRows == 0, "a block of rows lies in one bucket");
 
+// (n: the row relative to a.n0)
 __device__ __forceinline__ bool entry_valid(const InvArgs& a, const int32_t* irow, int slot, int n, int* c) {
-    if (!idx_entry_valid(irow, slot, n_candidates(n, a.W))) return false;
+    if (!idx_entry_valid(irow, slot, n_candidates(a.n0 + n, a.W))) return false;
     *c = irow[slot];
     return true;
 }
@@ -222,7 +220,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_count(InvArgs a, int nR, int bro
     const int rows = min(kInvRows, a.N - n0);
     for (int e = tid; e < rows * a.K; e += kBlock) {
         const int n = n0 + e / a.K, slot = e % a.K;
-        const int32_t* irow = a.idx + ((size_t)bg * a.N + n) * a.K;
+        const int32_t* irow = a.idx + ((size_t)bg * a.Nrow + a.n0 + n) * a.K;
         int c;
         if (!entry_valid(a, irow, slot, n, &c)) continue;
         if (lds)
@@ -252,7 +250,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, int brow
         for (int e = tid; e < rows * a.K; e += kBlock) {
             const int n = n0 + e / a.K, slot = e % a.K;
             int c;
-            if (entry_valid(a, a.idx + ((size_t)bg * a.N + n) * a.K, slot, n, &c)) atomicAdd(&s_hist[c], 1);
+            if (entry_valid(a, a.idx + ((size_t)bg * a.Nrow + a.n0 + n) * a.K, slot, n, &c)) atomicAdd(&s_hist[c], 1);
         }
         __syncthreads();
         // reserve this block's range of every chunk it touches; s_hist becomes the running position
@@ -263,7 +261,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_fill(InvArgs a, int nR, int brow
     for (int e = tid; e < rows * a.K; e += kBlock) {
         const int n = n0 + e / a.K, slot = e % a.K;
         int c;
-        if (!entry_valid(a, a.idx + ((size_t)bg * a.N + n) * a.K, slot, n, &c)) continue;
+        if (!entry_valid(a, a.idx + ((size_t)bg * a.Nrow + a.n0 + n) * a.K, slot, n, &c)) continue;
         const int pos = lds ? atomicAdd(&s_hist[c], 1) : off[c * nR + R] + atomicAdd(&gcur[R * nC + c], 1);
         lst[pos] = (n << 6) | slot;
     }
@@ -321,7 +319,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_scan(const int* counts, int* bof
     }
 }
 
-InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base) {
+InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base, int row_end) {
     const size_t bg = (size_t)B * Hkv, nC = (size_t)L / kChunk;
     InvLayout w;
     w.brows = kInvBucketRows;
@@ -336,9 +334,13 @@ InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base) {
     // A (chunk, bucket) sub-list of len entries makes ceil(len / kInvSeg) <= len / kInvSeg
     // + 1 items, and only the chunks c < n / kChunk of a bucket's last row n can
     // have entries there (a candidate chunk ends before the query): at most
-    // (R + 1) * brows / kChunk sub-lists of bucket R are not empty.
+    // (R + 1) * brows / kChunk sub-lists of bucket R are not empty; for a segment of
+    // rows that starts later, bucket R's rows lie below row_end, whose candidate
+    // chunks number at most row_end / kChunk + 1.
     size_t subl = 0;
-    for (int R = 0; R < w.nR; ++R) subl += std::min(nC, (size_t)(R + 1) * (w.brows / kChunk));
+    for (int R = 0; R < w.nR; ++R)
+        subl += row_end < 0 ? std::min(nC, (size_t)(R + 1) * (w.brows / kChunk))
+                            : std::min(nC, (size_t)row_end / kChunk + 1);
     w.max_work_bg = (size_t)N * K / kInvSeg + subl;
     w.work = align256(w.list + bg * (size_t)N * K * sizeof(int));
     w.nwork = align256(w.work + bg * w.max_work_bg * sizeof(int4));
@@ -605,7 +607,7 @@ struct BwdRun {
         const int* offsets = reinterpret_cast<const int*>(ws + w.offsets);
         const int* list = reinterpret_cast<const int*>(ws + w.list);
         const int nC = a.L / kChunk;
-        const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
+        const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L, 0, a.N};
         launch_inverse_index(ia, w, a.ws, s, false);
         HILS_LAUNCH("k_bwd_dq_rows", (k_bwd_dq_rows<T, D, G>), dim3(a.N, a.Hkv, a.B), dim3(kBlock), 0, s, a);
         HILS_LAUNCH("k_bwd_dkdv_chunks", (k_bwd_dkdv_chunks<T, D, G>), dim3(nC, a.Hkv, a.B), dim3(kBlock), 0, s, a,

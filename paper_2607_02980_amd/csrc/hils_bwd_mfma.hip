@@ -810,7 +810,7 @@ struct BwRun {
         const size_t rows = (size_t)a.B * a.Hq * a.N;
         constexpr int upb = kBlock / (D / 8);  // rows per k_bwd_u block
         HILS_LAUNCH("k_bwd_u", (k_bwd_u<D>), dim3((unsigned)((rows + upb - 1) / upb)), dim3(kBlock), 0, s, a, u);
-        const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
+        const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L, 0, a.N};
         launch_inverse_index(ia, ly.inv, a.ws, s, false);
         HILS_LAUNCH("k_inv_sort", k_inv_sort, dim3(nC, a.B * a.Hkv), dim3(kBlock), 0, s, offsets,
                     reinterpret_cast<const int*>(ws + ly.inv.list), sorted, a.N, a.K, nC, a.W);

@@ -90,9 +90,12 @@ void timing_end(hipStream_t s);
     } while (0)
 
 // Inverse index of a selection: for every (b, g, chunk) the rows n that chose it.
+// The inverse index of rows n0 .. n0 + N - 1 of idx ([B, Hkv, Nrow, K]); list
+// entries hold the row relative to n0.
 struct InvArgs {
     const int32_t* idx;
     int B, Hkv, N, K, W, L;
+    int n0, Nrow;
 };
 struct InvLayout {
     size_t counts, offsets, cursor, list;  // byte offsets from the workspace base
@@ -109,7 +112,9 @@ constexpr int kInvSeg = 256;          // list entries per work item
 // (doubling) until a (chunk, bucket) sub-list holds about 64 entries on average
 // (brows * K >= 64 * L/S), so that long sequences keep full work items.
 constexpr int kInvBucketRows = 2048;
-InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base);
+// row_end >= 0: the layout serves segments of up to N rows anywhere below row row_end
+// (the work-item bound then allows every candidate chunk of those rows per bucket)
+InvLayout inv_layout(int B, int Hkv, int N, int L, int K, size_t base, int row_end = -1);
 // Every (b, g, chunk) list is sorted by row bucket (the sub-list of bucket R starts
 // at boff[c * nR + R]); offsets[c] .. offsets[c + 1] bound the whole list.
 // work_list = false skips the work items (consumers that walk whole lists do not
@@ -128,6 +133,9 @@ int device_cus();
 size_t decode_workspace_bytes(int B, int N, int Hkv, int G, int d, int L, int K, int W, int head_norm);
 
 size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16, int union_pack);
+// The chunk-major prefill's cap on the records of one segment of rows (bytes): set
+// (bytes > 0) and read; returns the previous value.
+size_t prefill_record_cap(size_t bytes);
 
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_prefill_rows(const FwdArgs& a, hipStream_t s);  // fp32 storage

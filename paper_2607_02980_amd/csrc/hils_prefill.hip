@@ -29,6 +29,8 @@
 // (ds_read_b64_tr_b16).  Every O^T value a lane holds belongs to its own query,
 // so softmax rescaling is lane-local.  Per-slot partial vectors are stored in
 // the accumulators' lane order (store_lane_order).
+#include <atomic>
+
 #include "hils_device.hpp"
 #include "hils_dispatch.hpp"
 #include "hils_internal.hpp"
@@ -63,14 +65,16 @@ __device__ __forceinline__ size_t part_offset(size_t bg, int N, int n, int K, in
     return (((((bg * nt + n / QT) * K + slot) * QT + n % QT) * G) + hh) * (size_t)D;
 }
 
-PfLayout pf_layout(int B, int Hq, int Hkv, int N, int L, int d, int K) {
+// N: rows of one segment; row_end: the rows of every segment lie below it (-1: one
+// segment from row 0)
+PfLayout pf_layout(int B, int Hq, int Hkv, int N, int L, int d, int K, int row_end = -1) {
     PfLayout w;
     w.part = 0;
     const int QT = 128 / (Hq / Hkv);
     const size_t Np = (size_t)(N + QT - 1) / QT * QT;
     w.wgt = align256(w.part + (size_t)B * Hq * Np * K * d * sizeof(uint16_t));
     w.inv_base = align256(w.wgt + (size_t)B * Hq * Np * K * sizeof(float));
-    w.inv = inv_layout(B, Hkv, N, L, K, w.inv_base);
+    w.inv = inv_layout(B, Hkv, N, L, K, w.inv_base, row_end);
     w.total = w.inv.end;
     return w;
 }
@@ -393,7 +397,7 @@ template <int D, int G, bool ROUTE>
 __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, const int* boff, int nR,
                                                                     const int* list, const int4* work,
                                                                     size_t max_work_bg, const int* nwork,
-                                                                    bf16* part, float* wgt) {
+                                                                    bf16* part, float* wgt, int n0, int Ns) {
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
     constexpr int KROW = Tiles<D>::KROW, VROW = D + 16;
     __shared__ __align__(16) bf16 s_k[kChunk * KROW];
@@ -418,7 +422,7 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
     const int beg = bo[jb] + wi.z * kInvSeg;
     const int len = min(kInvSeg, bo[jb + 1] - beg);
     if (len <= 0) return;
-    const int* seg = list + bg * a.N * a.K + beg;
+    const int* seg = list + bg * (size_t)Ns * a.K + beg;
     static_assert(kInvSeg <= kBlock, "one entry per thread");
     if (tid < len) s_ent[tid] = seg[tid];
     {
@@ -455,7 +459,7 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
         const int e = min(grp * 16 + lane % 16, len - 1);
         const int ent = s_ent[e];
         x.ent = (u < nunits && grp * 16 + lane % 16 < len) ? ent : -1;
-        const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + (ent >> 6);
+        const size_t qrow = ((size_t)b * a.Hq + g * G + hh) * a.N + n0 + (ent >> 6);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             x.q[ks] = *reinterpret_cast<const uint4*>(qbase + qrow * D + ks * 32 + lg * 8);
@@ -522,8 +526,8 @@ __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, 
 #pragma unroll
             for (int i = 0; i < 4; ++i) o[db][i] *= inv;
         if (qv) {
-            store_lane_order<D>(part + part_offset(bg, a.N, n, a.K, slot, G, hh, D), o, lg);
-            if (lane < 16) wgt[part_offset(bg, a.N, n, a.K, slot, G, hh, 1)] = shat;
+            store_lane_order<D>(part + part_offset(bg, Ns, n, a.K, slot, G, hh, D), o, lg);
+            if (lane < 16) wgt[part_offset(bg, Ns, n, a.K, slot, G, hh, 1)] = shat;
         }
     };
     Ops opa, opb, opc;
@@ -567,7 +571,8 @@ struct LocalCfg {
 // bitmap over the chunks, then the set bits in order (dynamic LDS: the bitmap,
 // the rows' valid entries, the union list).
 template <int D, int G, bool UNION, bool ROUTE>
-__global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, const bf16* part, const float* wgt) {
+__global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, const bf16* part, const float* wgt, int n0,
+                                                                 int Ns) {
     using C = LocalCfg<G>;
     constexpr int KS = Tiles<D>::KS, DB = Tiles<D>::DB;
     constexpr int KROW = Tiles<D>::KROW, VROW = D + 16;
@@ -577,9 +582,10 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     __shared__ __align__(16) bf16 s_k[2][kChunk * KROW];
     __shared__ __align__(16) bf16 s_v[2][kChunk * VROW];
     const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
-    const int ntiles = (a.N + C::QT - 1) / C::QT;
+    // the tiles of rows n0 .. n0 + Ns - 1 (the partials are indexed from n0)
+    const int ntiles = (Ns + C::QT - 1) / C::QT;
     const int tile = xcd_remap(blockIdx.x, ntiles), g = blockIdx.y, b = blockIdx.z;
-    const int q0 = tile * C::QT;
+    const int q0 = n0 + tile * C::QT;
     const int qlast = min(q0 + C::QT - 1, a.N - 1);
     const int kbeg = n_candidates(q0, a.W) * kChunk;
     const int kfull = n_candidates(qlast, a.W) * kChunk;  // keys >= kfull are in every row's window...
@@ -912,11 +918,11 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
             const int cc = irow[k];
             const bool ok = k0 + u < a.K && cc >= 0 && cc < ncand && cc > prev;
             prev = cc;  // idx_entry_valid compares with the previous entry as written
-            sv[u] = wgt[part_offset(bg, a.N, nq, a.K, k, G, hh, 1)];
+            sv[u] = wgt[part_offset(bg, Ns, nq - n0, a.K, k, G, hh, 1)];
             okk[u] = ok;
             // (address independent of idx, so these loads issue with the idx loads;
             // an invalid slot's bits are masked by fma_lane_order)
-            load_lane_order<D>(part + part_offset(bg, a.N, nq, a.K, k, G, hh, D), lg, pv[u]);
+            load_lane_order<D>(part + part_offset(bg, Ns, nq - n0, a.K, k, G, hh, D), lg, pv[u]);
         }
         float Mn = M;
 #pragma unroll
@@ -948,10 +954,31 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
     }
 }
 
+// Rows of one segment of the chunk-major pass.  The per-slot records of a row
+// take B Hq K (2 d + 4) bytes (133 KB per row at 32 query heads, K = 16, d = 128):
+// with many rows the inverse index, chunk pass and local pass run once per
+// segment of rows over one workspace, so that the records stay under the cap
+// (hils_prefill_record_cap, 16 GiB by default) whatever the sequence length (the
+// paper's 512K-token prefill would otherwise need 69 GB).  Segments are multiples
+// of kPfSegAlign rows (whole query tiles of the local pass).  Each row's terms are
+// computed the same way in any segment, so the results do not depend on the cap;
+// a segment costs its own inverse index and launch tails (a 32K prefill split in
+// 4 segments: 3.47 -> 3.76 ms).
+std::atomic<size_t> g_record_cap{size_t(16) << 30};
+constexpr int kPfSegAlign = 2048;
+int pf_segment_rows(int B, int Hq, int N, int d, int K) {
+    const size_t cap = g_record_cap.load(std::memory_order_relaxed);
+    const size_t per_row = (size_t)B * Hq * K * (2 * (size_t)d + 4);
+    if ((size_t)N * per_row <= cap) return N;
+    const size_t rows = cap / per_row / kPfSegAlign * kPfSegAlign;
+    return (int)std::min((size_t)N, std::max((size_t)kPfSegAlign, rows));
+}
+
 struct PfRun {
     template <typename T, int D, int G>
     static hipError_t run(const FwdArgs& a, hipStream_t s) {
-        const PfLayout ly = pf_layout(a.B, a.Hq, a.Hkv, a.N, a.L, D, a.K);
+        const int seg = pf_segment_rows(a.B, a.Hq, a.N, D, a.K);
+        const PfLayout ly = pf_layout(a.B, a.Hq, a.Hkv, seg, a.L, D, a.K, seg < a.N ? a.N : -1);
         char* ws = static_cast<char*>(a.ws);
         bf16* part = reinterpret_cast<bf16*>(ws + ly.part);
         float* wgt = reinterpret_cast<float*>(ws + ly.wgt);
@@ -971,37 +998,46 @@ struct PfRun {
             const size_t dyn = (size_t)((nC + 31) / 32 + qk + min(nC, qk)) * sizeof(int);
             if (a.q_route)
                 HILS_LAUNCH("k_pf_union", (k_pf_local<D, G, true, true>), lgrid, dim3(LocalCfg<G>::NT), dyn, s, a,
-                            (const bf16*)nullptr, (const float*)nullptr);
+                            (const bf16*)nullptr, (const float*)nullptr, 0, a.N);
             else
                 HILS_LAUNCH("k_pf_union", (k_pf_local<D, G, true, false>), lgrid, dim3(LocalCfg<G>::NT), dyn, s, a,
-                            (const bf16*)nullptr, (const float*)nullptr);
+                            (const bf16*)nullptr, (const float*)nullptr, 0, a.N);
             return hipGetLastError();
         }
-        const InvArgs ia{a.idx, a.B, a.Hkv, a.N, a.K, a.W, a.L};
-        launch_inverse_index(ia, ly.inv, a.ws, s);
         const int* boff = reinterpret_cast<const int*>(ws + ly.inv.boff);
         const int* list = reinterpret_cast<const int*>(ws + ly.inv.list);
         const int4* work = reinterpret_cast<const int4*>(ws + ly.inv.work);
         const int* nwork = reinterpret_cast<const int*>(ws + ly.inv.nwork);
         const dim3 cgrid((unsigned)(ly.inv.max_work_bg * a.B * a.Hkv));
-        if (a.q_route)
-            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, true>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR, list,
-                        work, ly.inv.max_work_bg, nwork, part, wgt);
-        else
-            HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR, list,
-                        work, ly.inv.max_work_bg, nwork, part, wgt);
-        HILS_LAUNCH("k_pf_local", (k_pf_local<D, G, false, false>), lgrid, dim3(LocalCfg<G>::NT), 0, s, a,
-                    (const bf16*)part, (const float*)wgt);
+        for (int n0 = 0; n0 < a.N; n0 += seg) {
+            const int Ns = std::min(seg, a.N - n0);
+            const InvArgs ia{a.idx, a.B, a.Hkv, Ns, a.K, a.W, a.L, n0, a.N};
+            launch_inverse_index(ia, ly.inv, a.ws, s);
+            if (a.q_route)
+                HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, true>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR,
+                            list, work, ly.inv.max_work_bg, nwork, part, wgt, n0, Ns);
+            else
+                HILS_LAUNCH("k_pf_chunks", (k_pf_chunks<D, G, false>), cgrid, dim3(kBlock), 0, s, a, boff, ly.inv.nR,
+                            list, work, ly.inv.max_work_bg, nwork, part, wgt, n0, Ns);
+            const dim3 sgrid((Ns + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B);
+            HILS_LAUNCH("k_pf_local", (k_pf_local<D, G, false, false>), sgrid, dim3(LocalCfg<G>::NT), 0, s, a,
+                        (const bf16*)part, (const float*)wgt, n0, Ns);
+        }
         return hipGetLastError();
     }
 };
 
 }  // namespace
 
+size_t prefill_record_cap(size_t bytes) {
+    return bytes ? g_record_cap.exchange(bytes) : g_record_cap.load();
+}
+
 size_t prefill_workspace_bytes(int B, int Hq, int Hkv, int N, int L, int d, int K, int bf16_storage,
                                int union_pack) {
     if (!bf16_storage || union_pack) return 0;  // the fp32 and union paths need no workspace
-    return pf_layout(B, Hq, Hkv, N, L, d, K).total;
+    const int seg = pf_segment_rows(B, Hq, N, d, K);
+    return pf_layout(B, Hq, Hkv, seg, L, d, K, seg < N ? N : -1).total;
 }
 
 hipError_t launch_prefill_fwd(const FwdArgs& a, hipStream_t s) {

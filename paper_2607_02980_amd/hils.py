@@ -3,7 +3,7 @@
 The entry points keep the C names (``hils_prefill_fwd``, ``hils_decode_fwd``,
 ``hils_decode_fwd_noalloc``, ``hils_decode_paged_fwd``, ``hils_bwd``,
 ``hils_landmark_fwd``, ``hils_landmark_bwd``,
-``hils_workspace_size``, ``hils_last_error``, ``hils_version``).
+``hils_workspace_size``, ``hils_prefill_record_cap``, ``hils_last_error``, ``hils_version``).
 They take torch tensors already resident on the GPU, check dtype, shape,
 device and contiguity, allocate missing outputs and the workspace with
 ``torch.empty`` and pass raw pointers plus the current HIP stream.  Every step
@@ -60,6 +60,8 @@ def _load():
     lib.hils_bwd.argtypes = [P] + [vp] * 17 + [sz, vp]
     lib.hils_landmark_fwd.argtypes = [P, vp, vp, vp, vp, vp]
     lib.hils_landmark_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.hils_prefill_record_cap.argtypes = [sz]
+    lib.hils_prefill_record_cap.restype = sz
     lib.hils_timing_enable.argtypes = [ctypes.c_int]
     lib.hils_timing_read.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(ctypes.c_float),
                                      ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
@@ -102,6 +104,12 @@ class Params:
 
 def hils_version() -> int:
     return LIB.hils_version()
+
+
+def hils_prefill_record_cap(nbytes: int = 0) -> int:
+    """Set (nbytes > 0) and/or read the chunk-major prefill's cap on the per-slot
+    records of one segment of rows; returns the previous cap."""
+    return int(LIB.hils_prefill_record_cap(int(nbytes)))
 
 
 def hils_last_error() -> str:

@@ -259,3 +259,32 @@ def test_noalloc_decode_rejects_calls_above_its_array(hils):
     assert rc == hils.HILS_ERR_INVALID and "k_cache" in hils.hils_last_error()
     with open(HEADER) as f:
         assert f"HILS_DECODE_NOALLOC_SCRATCH_BYTES ((size_t){cap >> 20} << 20)" in f.read()
+
+
+def test_prefill_record_cap_bounds_the_workspace(hils):
+    # a long prefill runs its chunk-major passes over segments of rows whose
+    # per-slot records fit the cap: the workspace shrinks with the cap, and bytes = 0
+    # only reads it
+    p = params(hils, B=1, Hq=32, Hkv=8, N=32768, L=32768, d=128, topk=16, window=512)
+    full = hils.hils_workspace_size(p, hils.HILS_OP_PREFILL)
+    per_row = 32 * 16 * (2 * 128 + 4)
+    assert full >= 32768 * per_row
+    old = hils.hils_prefill_record_cap(1 << 30)
+    try:
+        assert hils.hils_prefill_record_cap() == 1 << 30
+        seg = hils.hils_workspace_size(p, hils.HILS_OP_PREFILL)
+        # segments of the most whole 2048-row blocks that fit: 6144 rows, whose records
+        # (plus the inverse index) make the workspace
+        rows = (1 << 30) // per_row // 2048 * 2048
+        assert rows == 6144
+        assert rows * per_row <= seg < (rows + 2048) * per_row
+        # a segment is at least 2048 rows, whatever the cap
+        hils.hils_prefill_record_cap(1)
+        tiny = hils.hils_workspace_size(p, hils.HILS_OP_PREFILL)
+        assert 2048 * per_row <= tiny < seg
+    finally:
+        hils.hils_prefill_record_cap(old)
+    assert hils.hils_workspace_size(p, hils.HILS_OP_PREFILL) == full
+    # the default keeps the 512K-token prefill's workspace far below its 69 GB of records
+    p512 = params(hils, B=1, Hq=32, Hkv=8, N=524288, L=524288, d=128, topk=16, window=512)
+    assert hils.hils_workspace_size(p512, hils.HILS_OP_PREFILL) < 20e9 < 524288 * per_row

@@ -1,0 +1,107 @@
+"""GPU parity of the segmented chunk-major prefill: with a small record cap the
+inverse index, chunk pass and local pass run over 2048-row segments reusing one
+workspace.  Every row is compared with the oracle, and the outputs must equal
+those of the unsegmented run bit for bit (each row's terms are computed the same
+way in any segment)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_helpers import check_close, check_lse, check_selection, host_inputs, log, np32, oshape, to_device
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # name: (params, wid, bias, route, flags)
+    "bf16_ragged_3_segments": (dict(B=2, Hq=8, Hkv=2, N=4500, L=4544, d=64, topk=8, window=256), 201, False, False,
+                               0),
+    "bf16_route_bias_G4_K32": (dict(B=1, Hq=8, Hkv=2, N=5000, L=5056, d=128, topk=32, window=512), 202, True, True,
+                               0),
+    "bf16_head_norm_G8_d64": (dict(B=1, Hq=8, Hkv=1, N=4096, L=4096, d=64, topk=16, window=512), 203, False, False,
+                              4),
+    "bf16_mha_G1": (dict(B=1, Hq=2, Hkv=2, N=6200, L=6208, d=64, topk=4, window=100), 204, False, False, 0),
+}
+
+
+def _run(hils, p, dev, idx_in=None):
+    out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"], dev.get("bias"),
+                                          dev.get("q_route"), idx=idx_in)
+    torch.cuda.synchronize()
+    return out, lse, idx
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_segmented_prefill_matches_oracle_and_unsegmented(name):
+    from paper_2607_02980_amd import hils
+
+    kw, wid, bias, route, flags = CASES[name]
+    p = hils.Params(flags=flags, **kw)
+    host = host_inputs(p, wid, bias=bias, route=route)
+    dev = to_device(host, p)
+    full_ws = hils.hils_workspace_size(p, hils.HILS_OP_PREFILL)
+    out0, lse0, idx0 = _run(hils, p, dev)
+    old = hils.hils_prefill_record_cap(1)  # 2048-row segments
+    try:
+        seg_ws = hils.hils_workspace_size(p, hils.HILS_OP_PREFILL)
+        log(f"[segments] case={name} params={kw} flags={flags} workspace {full_ws} -> {seg_ws} bytes")
+        assert seg_ws < full_ws
+        out1, lse1, idx1 = _run(hils, p, dev)
+    finally:
+        hils.hils_prefill_record_cap(old)
+    assert torch.equal(idx0, idx1)
+    assert torch.equal(out0, out1) and torch.equal(lse0, lse1), "segmented outputs differ from one segment"
+    s = oshape(p)
+    ref = oracle.fwd(s, np32(host["q"]), np32(host["k"]), np32(host["v"]), np32(host["lmk"]),
+                     bias=np32(host.get("bias")), q_route=np32(host.get("q_route")))
+    gidx = idx1.cpu().numpy()
+    if check_selection(p, host, gidx, ref["idx"]):
+        ref = oracle.fwd(s, np32(host["q"]), np32(host["k"]), np32(host["v"]), np32(host["lmk"]),
+                         bias=np32(host.get("bias")), q_route=np32(host.get("q_route")), idx=gidx)
+    check_close("out", np32(out1), ref["out"], p.dtype)
+    check_lse(np32(lse1), ref["lse"], p.dtype)
+
+
+def test_segmented_prefill_given_index():
+    # the forced-index path segments the same way
+    from paper_2607_02980_amd import hils
+
+    kw, wid, bias, route, flags = CASES["bf16_ragged_3_segments"]
+    p = hils.Params(**kw)
+    dev = to_device(host_inputs(p, wid), p)
+    out0, lse0, idx0 = _run(hils, p, dev)
+    p.flags = hils.HILS_FLAG_GIVEN_IDX
+    old = hils.hils_prefill_record_cap(1)
+    try:
+        out1, lse1, _ = _run(hils, p, dev, idx_in=idx0.clone())
+    finally:
+        hils.hils_prefill_record_cap(old)
+    assert torch.equal(out0, out1) and torch.equal(lse0, lse1)
+
+
+def test_segmented_32k_prefill_is_bitwise_the_unsegmented_one():
+    # the full 32K prefill (32/8 heads, d 128, top-16) in 8 segments of 4096 rows
+    # against one segment: identical bits
+    from paper_2607_02980_amd import hils, synth
+    from paper_2607_02980_amd.configs import WORKLOADS
+
+    W_ = WORKLOADS["prefill_32k_bf16"]
+    p = hils.Params(B=W_.B, Hq=W_.Hq, Hkv=W_.Hkv, N=W_.N, L=W_.L, d=W_.d, chunk=W_.chunk, topk=W_.topk,
+                    window=W_.window, dtype=W_.dtype)
+    nc = p.L // p.chunk
+    dev = {"q": synth.normal_device((p.B, p.Hq, p.N, p.d), synth.seed_for(W_.wid, "q"), p.dtype, "cuda"),
+           "k": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "k"), p.dtype, "cuda"),
+           "v": synth.normal_device((p.B, p.Hkv, p.L, p.d), synth.seed_for(W_.wid, "v"), p.dtype, "cuda"),
+           "lmk": synth.normal_device((p.B, p.Hq, nc, p.d), synth.seed_for(W_.wid, "lmk"), p.dtype, "cuda")}
+    out0, lse0, idx0 = _run(hils, p, dev)
+    per_row = p.Hq * p.topk * (2 * p.d + 4)
+    old = hils.hils_prefill_record_cap(4096 * per_row)
+    try:
+        log(f"[segments] 32K prefill in 8 segments, workspace "
+            f"{hils.hils_workspace_size(p, hils.HILS_OP_PREFILL)} bytes")
+        out1, lse1, idx1 = _run(hils, p, dev)
+    finally:
+        hils.hils_prefill_record_cap(old)
+    assert torch.equal(idx0, idx1)
+    assert torch.equal(out0, out1) and torch.equal(lse0, lse1)
+    assert bool(torch.isfinite(lse1).all())

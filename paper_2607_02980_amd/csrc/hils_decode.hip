@@ -691,6 +691,69 @@ __device__ __forceinline__ void scan_head(const FwdArgs& a, const DecLayout& ly,
     }
 }
 
+// The same with one landmark head per KV group (Hl = Hkv): the G heads share each
+// landmark row, so the waves split the slice's rows instead of the heads and score
+// every row they load against all G heads' queries (each row read once).
+template <typename T, int D, int G, int NQ, bool PAGED, bool STREAM>
+__device__ __forceinline__ void scan_shared(const FwdArgs& a, const DecLayout& ly, int b, int n0, int nq, int g,
+                                            int wv, int nw, int c0, int len, const int* s_page,
+                                            float (*s_score)[G][kSlice]) {
+    constexpr int LPR = D * (int)sizeof(T) / 16;
+    constexpr int EPL = 16 / (int)sizeof(T);
+    constexpr int RPS = kWave / LPR;
+    const int lane = threadIdx.x % kWave, sub = lane / LPR, seg = lane % LPR;
+    float qv[G][NQ][EPL];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const T* qr =
+                as<T>(a.q_route ? a.q_route : a.q) + q_row(a, b, g * G + hh, n0 + min(q, nq - 1)) * D + seg * EPL;
+#pragma unroll
+            for (int t = 0; t < EPL; ++t) qv[hh][q][t] = to_f32(qr[t]);
+        }
+    const T* lm = as<T>(a.lmk) + seg * EPL;
+    const T* base = lm + (PAGED ? 0 : lmk_row(a, ly.nC, b, g, c0) * D);
+    constexpr int NB = 16;
+    for (int r0 = wv * RPS * NB; r0 < len; r0 += nw * RPS * NB) {
+        uint4 x[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int r = min(r0 + u * RPS + sub, len - 1);
+            const T* src = PAGED ? lm + ((size_t)s_page[r] * a.Hl + g) * D : base + (size_t)r * D;
+            x[u] = STREAM ? ld_stream16(src) : *reinterpret_cast<const uint4*>(src);
+        }
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            float xf[EPL];
+            if constexpr (sizeof(T) == 2) {
+                const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    xf[2 * t] = __uint_as_float(w[t] << 16);
+                    xf[2 * t + 1] = __uint_as_float(w[t] & 0xffff0000u);
+                }
+            } else {
+                xf[0] = __uint_as_float(x[u].x);
+                xf[1] = __uint_as_float(x[u].y);
+                xf[2] = __uint_as_float(x[u].z);
+                xf[3] = __uint_as_float(x[u].w);
+            }
+            const int r = r0 + u * RPS + sub;
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    float part = 0.f;
+#pragma unroll
+                    for (int t = 0; t < EPL; ++t) part += qv[hh][q][t] * xf[t];
+                    part = group_sum<LPR>(part);
+                    if (seg == 0 && r < len) s_score[q][hh][r] = a.scale * part;
+                }
+        }
+    }
+}
+
 // PAGED is a kernel parameter so that the contiguous scan keeps its small
 // register footprint (the paged loads need a 64-bit address per row).
 // mode kScanSelect: group scores and the slice's top-K.  mode kScanNormKeep (the
@@ -754,11 +817,24 @@ __global__ __launch_bounds__(kBlock) void k_dec_scan(FwdArgs a, int mode) {
         __syncthreads();
     }
     const bool stream = a.N <= NQ;
-    for (int hh = wave; hh < G; hh += kBlock / kWave)
-        if (stream)
-            scan_head<T, D, G, NQ, PAGED, true>(a, ly, b, n0, nq, g, hh, c0, len, ss.id, ss.score);
-        else
-            scan_head<T, D, G, NQ, PAGED, false>(a, ly, b, n0, nq, g, hh, c0, len, ss.id, ss.score);
+    bool shared_lmk = false;  // one landmark row per KV group: read once for the G heads
+    if constexpr (G > 1 && G * NQ <= 4) shared_lmk = a.Hl != a.Hq;
+    if (shared_lmk) {
+        if constexpr (G > 1 && G * NQ <= 4) {
+            if (stream)
+                scan_shared<T, D, G, NQ, PAGED, true>(a, ly, b, n0, nq, g, wave, kBlock / kWave, c0, len, ss.id,
+                                                      ss.score);
+            else
+                scan_shared<T, D, G, NQ, PAGED, false>(a, ly, b, n0, nq, g, wave, kBlock / kWave, c0, len, ss.id,
+                                                       ss.score);
+        }
+    } else {
+        for (int hh = wave; hh < G; hh += kBlock / kWave)
+            if (stream)
+                scan_head<T, D, G, NQ, PAGED, true>(a, ly, b, n0, nq, g, hh, c0, len, ss.id, ss.score);
+            else
+                scan_head<T, D, G, NQ, PAGED, false>(a, ly, b, n0, nq, g, hh, c0, len, ss.id, ss.score);
+    }
     __syncthreads();
     if (a.bias) {
         for (int e = tid; e < G * len; e += kBlock) {

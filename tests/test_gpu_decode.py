@@ -34,6 +34,14 @@ CASES = {
                           [4096, 3000, 1500, 600]),
     "bf16_head_gap_150_many_rows": (dict(B=64, Hq=16, Hkv=4, N=1, L=1024, d=64, topk=8, window=128), 209, False,
                                     False, [1024 - 13 * i for i in range(64)]),
+    # one landmark head per KV group with G <= 4 heads: the scan reads each landmark
+    # row once and scores it against the group's heads (several slices, ragged)
+    "bf16_route_bias_Hl_eq_Hkv_G4": (dict(B=3, Hq=8, Hkv=2, Hl=2, N=1, L=20480, d=128, topk=16, window=512), 210,
+                                     True, True, [20480, 9000, 300]),
+    "bf16_Hl_eq_Hkv_G2_d64": (dict(B=2, Hq=4, Hkv=2, Hl=2, N=1, L=8192, d=64, topk=8, window=256), 211, False, False,
+                              [8192, 4100]),
+    "f32_Hl_eq_Hkv_G4": (dict(B=2, Hq=4, Hkv=1, Hl=1, N=1, L=4096, d=64, topk=8, window=128, dtype="f32"), 212, True,
+                         False, [4096, 1800]),
 }
 HEAD_GAP = {"bf16_head_gap_150": (1, 150.0), "bf16_head_gap_150_many_rows": (6, 150.0)}
 

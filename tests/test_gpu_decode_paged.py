@@ -33,6 +33,9 @@ CASES = {
                                       False, [4096, 2100], False),
     "bf16_paged_multi_token_K32_d64_G8": (dict(B=2, Hq=16, Hkv=2, N=2, L=4096, d=64, topk=32, window=512), 308,
                                           False, False, [4096, 3500], True),
+    # one landmark page row per KV group (Hl = Hkv, G = 4): read once for the group's heads
+    "bf16_paged_Hl_eq_Hkv_G4": (dict(B=2, Hq=8, Hkv=2, Hl=2, N=1, L=16384, d=128, topk=16, window=512), 309, True,
+                                True, [16384, 7000], True),
 }
 HEAD_GAP = {"bf16_multi_token_head_gap_150": (2, 150.0)}
 

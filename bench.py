@@ -407,15 +407,15 @@ def run_part(part, torch, hils, synth, WORKLOADS, args):
         _, _, ms, kt = bench_prefill(torch, hils, synth, Wp, args.steps, args.warmup)
         out[Wp.name] = {"ms_per_step": round(ms, 4), "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kt.items()}}
     elif part == "decode":
-        out["decode"] = bench_decode(torch, hils, synth, Wd, args.steps, 2)
-        out["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"], args.steps, 2)
-        out["decode_paged"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, paged=True)
-        out["decode_4_new_tokens"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, N=4)
-        out["decode_Hl_eq_Hkv"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, Hl=Wd.Hkv)
-        out["decode_head_norm"] = bench_decode(torch, hils, synth, Wd, args.steps, 2,
+        out["decode"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup)
+        out["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"], args.steps, args.warmup)
+        out["decode_paged"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup, paged=True)
+        out["decode_4_new_tokens"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup, N=4)
+        out["decode_Hl_eq_Hkv"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup, Hl=Wd.Hkv)
+        out["decode_head_norm"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup,
                                                flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
     elif part == "train":
-        out["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], args.steps, 1)
+        out["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], args.steps, args.warmup)
     elif part == "landmark":
         out["landmark"] = bench_landmark(torch, hils, synth, Wp, args.steps, args.warmup)
     elif part == "variants":
@@ -425,7 +425,7 @@ def run_part(part, torch, hils, synth, WORKLOADS, args):
                                   ("prefill_union_packing", Wp, U, None),
                                   ("prefill_locality_chunk_major", Wp, 0, 0.97),
                                   ("prefill_locality_union_packing", Wp, U, 0.97)):
-            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, args.steps, 1, flags=fl, rho=rho)
+            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, args.steps, args.warmup, flags=fl, rho=rho)
             out[name] = {"ms_per_step": round(msv, 4), "chunk_overlap_16": round(pv.overlap16, 4),
                          "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kv.items()}}
     return out
@@ -435,7 +435,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-train", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
@@ -521,14 +521,14 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_decode:
         Wd = WORKLOADS["decode_131k_bf16_b32"]
-        res["extra"]["decode"] = bench_decode(torch, hils, synth, Wd, args.steps, 2)
-        res["extra"]["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"], args.steps, 2)
-        res["extra"]["decode_paged"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, paged=True)
-        res["extra"]["decode_4_new_tokens"] = bench_decode(torch, hils, synth, Wd, args.steps, 2, N=4)
+        res["extra"]["decode"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup)
+        res["extra"]["decode_1m"] = bench_decode(torch, hils, synth, WORKLOADS["decode_1m_bf16_b4"], args.steps, args.warmup)
+        res["extra"]["decode_paged"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup, paged=True)
+        res["extra"]["decode_4_new_tokens"] = bench_decode(torch, hils, synth, Wd, args.steps, args.warmup, N=4)
         res["extra"]["decode_Hl_eq_Hkv"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
-                                                        args.steps, 2, Hl=WORKLOADS["decode_131k_bf16_b32"].Hkv)
+                                                        args.steps, args.warmup, Hl=WORKLOADS["decode_131k_bf16_b32"].Hkv)
     if not args.no_train:
-        res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], args.steps, 1)
+        res["extra"]["train"] = bench_train(torch, hils, synth, WORKLOADS["train_16k_bf16_b4"], args.steps, args.warmup)
     # the tiny fp32 workload (2K tokens, 4/1 heads, d 64, top-4): latency of one prefill
     Wt = WORKLOADS["prefill_2k_f32_tiny"]
     pt, _, mst, kt = bench_prefill(torch, hils, synth, Wt, args.steps, args.warmup)
@@ -546,13 +546,13 @@ def main():
                                   ("prefill_union_packing", Wp, U, None),
                                   ("prefill_locality_chunk_major", Wp, 0, 0.97),
                                   ("prefill_locality_union_packing", Wp, U, 0.97)):
-            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, args.steps, 1, flags=fl, rho=rho)
+            pv, _, msv, kv = bench_prefill(torch, hils, synth, W_, args.steps, args.warmup, flags=fl, rho=rho)
             res["extra"][name] = {"ms_per_step": round(msv, 4), "tokens_per_s": round(pv.B * pv.N / (msv * 1e-3), 1),
                                   "Hq": pv.Hq, "Hkv": pv.Hkv, "query_rho": rho,
                                   "chunk_overlap_16": round(pv.overlap16, 4),
                                   "kernels_avg_ms": {k: round(v["avg_ms"], 4) for k, v in kv.items()}}
         res["extra"]["decode_head_norm"] = bench_decode(torch, hils, synth, WORKLOADS["decode_131k_bf16_b32"],
-                                                        args.steps, 2, flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
+                                                        args.steps, args.warmup, flags=hils.HILS_FLAG_HEAD_NORM_SELECT)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(Wp, host)
     print(json.dumps(res), flush=True)

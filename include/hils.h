@@ -28,7 +28,8 @@
  *     other than the thread-local error string (and, only while the optional
  *     timing mode is enabled, its event records) -- except that
  *     hils_decode_fwd_noalloc uses a fixed device array of the library's own
- *     (declared below) and keeps its address per device.  All work is enqueued on
+ *     (declared below) and keeps its address per device, and that the prefill
+ *     record cap (hils_prefill_record_cap) is one process-wide setting.  All work is enqueued on
  *     `stream` (a hipStream_t; NULL is the default stream) and is complete
  *     when the stream is.
  *   - Layouts are row-major and contiguous ("BHSD"):
@@ -295,8 +296,8 @@ size_t hils_prefill_record_cap(size_t bytes);
 /*
  * Optional per-kernel timing, for profiling (not needed to use the operator).
  * hils_timing_enable(1) makes every kernel that the library launches from the
- * calling thread be bracketed by two HIP events on the launch's stream (this
- * is the one piece of state the library keeps, per thread, while enabled);
+ * calling thread be bracketed by two HIP events on the launch's stream (state
+ * the library keeps per thread while enabled);
  * hils_timing_enable(0) discards the records.
  * hils_timing_read() waits for the recorded events, then reports per kernel
  * name (in first-launch order): names as a '\n'-separated list in `names`

@@ -963,7 +963,8 @@ __global__ __launch_bounds__(LocalCfg<G>::NT, 2) void k_pf_local(FwdArgs a, cons
 // of kPfSegAlign rows (whole query tiles of the local pass).  Each row's terms are
 // computed the same way in any segment, so the results do not depend on the cap;
 // a segment costs its own inverse index and launch tails (a 32K prefill split in
-// 4 segments: 3.47 -> 3.76 ms).
+// 4 segments: 3.47 -> 3.76 ms), so the default cap keeps the 32K and training
+// shapes in one.
 std::atomic<size_t> g_record_cap{size_t(16) << 30};
 constexpr int kPfSegAlign = 2048;
 int pf_segment_rows(int B, int Hq, int N, int d, int K) {

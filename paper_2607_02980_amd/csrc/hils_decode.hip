@@ -449,6 +449,52 @@ __device__ void merge_row(const FwdArgs& a, const DecLayout& ly, size_t rg, Merg
     __syncthreads();
 }
 
+// The same merge by one wave alone, without block barriers (the rest of the
+// workgroup does other work meanwhile): rounds of 64*E survivors, each round's top-K
+// merged with the running best.  The result is left in ms.bid[0, ms.nbest).
+template <int E>
+__device__ void merge_row_wave(const FwdArgs& a, const DecLayout& ly, size_t rg, MergeSmem<1>& ms) {
+    const int lane = threadIdx.x % kWave;
+    const float* cand_sc = reinterpret_cast<const float*>(static_cast<const char*>(a.ws) + ly.cand);
+    const int* cand_id = reinterpret_cast<const int*>(cand_sc + (size_t)a.B * a.N * a.Hkv * ly.nslices * a.K);
+    const size_t base = rg * ly.nslices * a.K;
+    const int total = ly.nslices * a.K;
+    int nbest = 0;
+    for (int r0 = 0; r0 < total; r0 += kWave * E) {
+        float sc[E];
+        int id[E];
+        bool ok[E];
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const int e = r0 + r * kWave + lane;
+            id[r] = e < total ? cand_id[base + e] : -1;
+            sc[r] = e < total ? cand_sc[base + e] : 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < E; ++r) ok[r] = id[r] >= 0;
+        const int nw = wave_topk_reg<E>(sc, id, ok, a.K, ms.wid[0], ms.wsc[0], ms.tid[0], ms.tsc[0]);
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        float sc2[2];
+        int id2[2];
+        bool ok2[2];
+        ok2[0] = lane < nw;
+        id2[0] = ok2[0] ? ms.wid[0][lane] : -1;
+        sc2[0] = ok2[0] ? ms.wsc[0][lane] : 0.f;
+        ok2[1] = lane < nbest;
+        id2[1] = ok2[1] ? ms.bid[lane] : -1;
+        sc2[1] = ok2[1] ? ms.bsc[lane] : 0.f;
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        nbest = wave_topk_reg<2>(sc2, id2, ok2, a.K, ms.bid, ms.bsc, ms.tid[0], ms.tsc[0]);
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    }
+    if (lane == 0) ms.nbest = nbest;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+}
+
 // One part per wavefront (bf16): no block barriers.  S^T = K Q^T for the 64 keys
 // (K rows and q straight from HBM as MFMA operands), the softmax per head over the
 // four lane groups with permlane swaps, and O^T = V^T P^T with V^T from the
@@ -1167,11 +1213,13 @@ __global__ __launch_bounds__(kBlock) void k_dec_combine(FwdArgs a) {
 struct RowPart {
     int c, nk, chunk;  // chunk (c < 0: nothing to attend), its first nk keys, retrieved or local
 };
-template <int D, int G, bool ROUTE>
+// The wave takes entries j = j0, j0 + kRowWaves, ... < nj of a list of record slots,
+// slot_of(j) (slot < K: retrieved chunk slot; K + p: window piece p).
+template <int D, int G, bool ROUTE, typename SlotOf>
 __device__ void row_parts(const FwdArgs& a, const DecLayout& ly, bf16* sv, const int* s_sel, int b, int n, int g,
-                          size_t rg, int pos, int ncand) {
+                          size_t rg, int pos, int ncand, int j0, int nj, SlotOf&& slot_of) {
     constexpr int KS = D / 32, DB = D / 16, VROW = PartWaveSmem<D>::VROW, PV = kChunk * D / 8 / kWave;
-    const int lane = threadIdx.x % kWave, lg = lane / 16, n16 = lane % 16, w = wave_id();
+    const int lane = threadIdx.x % kWave, lg = lane / 16, n16 = lane % 16;
     const float c1 = a.scale * kLog2e;
     const bf16x8 zero8 = as_bf16x8(make_uint4(0, 0, 0, 0));
     auto part_of = [&](int part) {
@@ -1244,13 +1292,14 @@ __device__ void row_parts(const FwdArgs& a, const DecLayout& ly, bf16* sv, const
         for (int ks = 0; ks < KS; ++ks) x.l[ks] = ld_bf16x8(lr + (real ? ks * 32 + lg * 8 : 0));
         return x;
     };
-    RowPart p = part_of(w);
+    RowPart p = part_of(slot_of(j0));
     VOp vx = load_v(p, true);
     LOp lx = load_l(p, true);
     KOp kx = load_k(p, true);
-    for (int part = w; part < ly.nparts; part += kRowWaves) {
-        const bool real = part + kRowWaves < ly.nparts;  // uniform over the wave
-        const RowPart pn = part_of(real ? part + kRowWaves : part);
+    for (int j = j0; j < nj; j += kRowWaves) {
+        const int part = slot_of(j);
+        const bool real = j + kRowWaves < nj;  // uniform over the wave
+        const RowPart pn = part_of(slot_of(real ? j + kRowWaves : j));
         const int nk = p.nk;
         // V rows into the wave's tile (rows at or past nk zeroed); the next V
 #pragma unroll
@@ -1332,44 +1381,63 @@ __device__ void row_parts(const FwdArgs& a, const DecLayout& ly, bf16* sv, const
 }
 
 // ---- bf16: one workgroup of kRowWaves waves per row ----------------------------
-// Selection (E > 0: the merge of the scan's survivors, which also writes the row
-// of idx; E = 0: idx given), then the row's parts, wave w taking parts w, w + 8,
-// ... (one at a time, run_part_wave), then the fusion: one launch after the scan,
-// and the records only cross between waves of one workgroup (a barrier orders
-// them), never between workgroups.
+// Two phases.  In the first, the last wave selects (E > 0: the merge of the scan's
+// survivors, which also writes the row of idx; E = 0: idx given) while the other
+// waves each take one piece of the local window, which does not depend on the
+// selection.  After a barrier, the remaining window pieces and the K retrieved
+// chunks are spread over all the waves (one part at a time per wave), and after a
+// second barrier the fusion combines the row's records: one launch after the scan,
+// and the records only cross between waves of one workgroup, never between
+// workgroups.
 template <int D, int G, int E, bool ROUTE>
 __global__ __launch_bounds__(kRowWaves * kWave) void k_dec_row(FwdArgs a) {
     constexpr int NT = kRowWaves * kWave;
     constexpr int kTileBytes = (int)sizeof(PartWaveSmem<D>) * kRowWaves;
     static_assert(sizeof(MergeSmem<kRowWaves>) <= (size_t)kTileBytes, "the merge scratch fits in the part tiles");
-    // the waves' part tiles; before the parts, the merge's scratch in the same bytes
+    // the waves' part tiles; the merging wave's tile holds its scratch until the
+    // parts of the selection start
+    constexpr int kMergeWave = kRowWaves - 1;
+    constexpr int kTileElems = (int)(sizeof(PartWaveSmem<D>) / sizeof(bf16));
+    static_assert(sizeof(MergeSmem<1>) <= sizeof(PartWaveSmem<D>), "the merge scratch fits in one part tile");
     __shared__ __align__(16) unsigned char s_raw[kTileBytes];
     __shared__ CombineSmem<G> cs;
     __shared__ int s_sel[64];
-    auto& ms = *reinterpret_cast<MergeSmem<kRowWaves>*>(s_raw);
     bf16* tiles = reinterpret_cast<bf16*>(s_raw);
+    auto& ms = *reinterpret_cast<MergeSmem<1>*>(tiles + (size_t)kMergeWave * kTileElems);
     const int g = blockIdx.x, b = blockIdx.y / a.N, n = blockIdx.y % a.N;
     const size_t rg = ((size_t)b * a.Hkv + g) * a.N + n;
     const DecLayout ly = dec_layout(a.B, a.N, a.Hkv, G, D, a.L, a.K, a.W, a.head_norm);
     const int pos = decode_position(a, b, n);
     const int ncand = n_candidates(pos, a.W);
-    const int tid = threadIdx.x, w = wave_id();
-    if constexpr (E > 0) {
-        merge_row<E, kRowWaves>(a, ly, rg, ms, w);
-        if (tid < a.K) {
-            const int v = tid < ms.nbest ? ms.bid[tid] : -1;
-            s_sel[tid] = v;
-            a.idx[rg * a.K + tid] = v;
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave;
+    bf16* mytile = tiles + (size_t)w * kTileElems;
+    // phase 1: the last wave selects (merging the scan's survivors) while the others
+    // take the local window's first pieces, which do not depend on the selection
+    const int nlA = min(ly.nlocal, kMergeWave);  // window pieces of phase 1
+    if (w == kMergeWave) {
+        if constexpr (E > 0) {
+            merge_row_wave<E>(a, ly, rg, ms);
+            for (int t = lane; t < a.K; t += kWave) {
+                const int v = t < ms.nbest ? ms.bid[t] : -1;
+                s_sel[t] = v;
+                a.idx[rg * a.K + t] = v;
+            }
+        } else {
+            for (int t = lane; t < a.K; t += kWave) {
+                const int32_t* irow = a.idx + rg * a.K;
+                s_sel[t] = idx_entry_valid(irow, t, ncand) ? irow[t] : -1;
+            }
         }
-    } else {
-        if (tid < a.K) {
-            const int32_t* irow = a.idx + rg * a.K;
-            s_sel[tid] = idx_entry_valid(irow, tid, ncand) ? irow[tid] : -1;
-        }
+    } else if (w < nlA) {
+        row_parts<D, G, ROUTE>(a, ly, mytile, s_sel, b, n, g, rg, pos, ncand, w, w + 1,
+                               [&](int j) { return a.K + j; });
     }
-    __syncthreads();  // s_sel is set; the merge scratch is free for the tiles
-    if (w < ly.nparts) row_parts<D, G, ROUTE>(a, ly, tiles + (size_t)w * (sizeof(PartWaveSmem<D>) / sizeof(bf16)), s_sel,
-                                              b, n, g, rg, pos, ncand);
+    __syncthreads();  // s_sel is set; the merge scratch is free
+    // phase 2: the rest of the window's pieces, then the retrieved chunks
+    const int nwB = ly.nlocal - nlA, nB = nwB + a.K;
+    if (w < nB)
+        row_parts<D, G, ROUTE>(a, ly, mytile, s_sel, b, n, g, rg, pos, ncand, w, nB,
+                               [&](int j) { return j < nwB ? a.K + nlA + j : j - nwB; });
     __syncthreads();  // every record of the row is written
     combine_row<bf16, D, G, NT>(a, ly, cs, b, n, g, rg);
 }

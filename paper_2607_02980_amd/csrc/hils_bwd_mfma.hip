@@ -199,7 +199,7 @@ __global__ __launch_bounds__(kBlock) void k_inv_sort(const int* offsets, const i
 constexpr int kKeyWaves = 8;
 constexpr int kKeyThreads = kKeyWaves * kWave;
 
-// Tiles k, q, g, qr, p, ds are staggered (st_off), rows of D or 64 bf16.
+// Tiles k, q, g, qr, p, ds are swizzled (st_off), rows of D or 64 bf16.
 template <int D, bool ROUTE>
 struct KeySmem {
     static constexpr int KROW = BT<D>::KROW, TD = st_size<D>(64), TP = st_size<kChunk>(kPairs);
@@ -616,7 +616,7 @@ struct DqCfg {
 template <int D>
 struct DqSmem {
     static constexpr int KROW = BT<D>::KROW;
-    bf16 k[2][st_size<D>(kChunk)];  // staggered: row-wise and transposing reads
+    bf16 k[2][st_size<D>(kChunk)];  // swizzled: row-wise and transposing reads
     bf16 v[2][kChunk * KROW];
 };
 

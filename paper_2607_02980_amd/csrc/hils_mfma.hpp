@@ -80,47 +80,76 @@ __device__ __forceinline__ bf16x8 tr_operand_perm(const E* X, int ld, int k0, in
     return __builtin_bit_cast(bf16x8, c);
 }
 
-// Staggered LDS tiles: rows of W = 64 or 128 bf16 at a stride of W + 16, rows with
-// r % 8 >= 4 shifted by 8 more.  Relative to the 128-byte LDS bank cycle (32 banks
-// of 4 bytes) rows r = 0..7 then start at 16-byte slots 0, 2, 4, 6, 1, 3, 5, 7, so
-// that row-wise 16-byte operand reads (8 lanes = 8 rows per cycle) and transposing
-// reads (16 lanes = 4 rows x 32 bytes per cycle) are both free of bank conflicts,
-// which no uniform row padding gives (+8 suits the first, +16 the second); unlike
-// an XOR swizzle, offsets along a row stay linear, so that the column steps of
-// unrolled loops fold into the instruction offsets.
+// Swizzled LDS tiles ("st"), rows of W = 64 or 128 bf16.  On gfx950 the LDS
+// serves 16-byte reads to four groups of 16 lanes (lanes 0-31 or 32-63, split by
+// the parity of lane bits 2-4) and 8-byte (also transposing) reads to lanes 0-31
+// and 32-63, each group over 64 banks of 4 bytes; 16-byte stores go 8 lanes at a
+// time and 8-byte stores 16 lanes at a time, over 32 banks (measured with the
+// bank-conflict counters).  The layouts below put the row-wise 16-byte operand
+// reads (16 rows of one column piece), the transposing reads (4 rows x 32 bytes
+// per 16 lanes, rows r and r + 4 or r + 16), the 16-byte stores of a row piece per
+// lane and of whole rows on distinct banks:
+//   W = 128: rows padded to 144, rows 8..15 of every 16 shifted by 64 more, 64
+//     elements between groups of 16 rows, and the two 16-byte pieces of each
+//     32-byte pair swapped in rows with r % 8 >= 4.  The swap only touches the
+//     lowest bit of the piece index, so column offsets that are multiples of 16
+//     stay linear and fold into the instructions' offsets.
+//   W = 64: unpadded, the 16-byte pieces of row r permuted by XOR with
+//     (r & 7) ^ 5 (r >> 3 & 1) (its 8-byte stores of one column still meet two
+//     rows per bank).
 template <int W>
 __device__ __forceinline__ int st_off(int r, int c) {
-    return r * (W + 16) + 8 * ((r >> 2) & 1) + c;
+    static_assert(W == 64 || W == 128, "swizzled tiles are 64 or 128 wide");
+    if constexpr (W == 128)
+        return (r >> 4) * (16 * (W + 16) + 64) + (r & 15) * (W + 16) + 64 * ((r >> 3) & 1) +
+               8 * ((c >> 3) ^ ((r >> 2) & 1)) + (c & 7);
+    else
+        return r * W + 8 * ((c >> 3) ^ (r & 7) ^ (((r >> 3) & 1) * 5)) + (c & 7);
 }
 template <int W>
 constexpr int st_size(int rows) {
-    return rows * (W + 16) + 8;
+    return W == 128 ? (rows + 15) / 16 * (16 * (W + 16) + 64) : rows * W;
 }
-// row_operand / tr_operand of a staggered tile (r0, k0 multiples of 8: the shift of
-// a row then depends on the lane alone, and the compiler keeps one address per lane)
+// Elements per 16 rows of a swizzled tile: row r + 16 m is row r moved by m groups.
+template <int W>
+constexpr int st_group() {
+    return W == 128 ? 16 * (W + 16) + 64 : 16 * W;
+}
+// Offset of (r, c0 + c) for a column offset c0 that the layout keeps linear (a
+// multiple of 16 for W = 128; none for W = 64, whose XOR reaches bit 2 of the piece
+// index): the lane-dependent part and the constant part apart, so that the latter
+// folds into the instructions' offsets.
+template <int W>
+__device__ __forceinline__ int st_off_lin(int r, int c0, int c) {
+    if constexpr (W == 128)
+        return st_off<W>(r, c) + c0;
+    else
+        return st_off<W>(r, c0 + c);
+}
+// row_operand / tr_operand of a swizzled tile (r0 and k0 multiples of 16)
 template <int W>
 __device__ __forceinline__ bf16x8 row_operand_st(const bf16* X, int r0, int k0, int lane) {
-    return ld_bf16x8(X + (r0 + lane % 16) * (W + 16) + 8 * ((lane >> 2) & 1) + k0 + (lane / 16) * 8);
+    return ld_bf16x8(X + (r0 / 16) * st_group<W>() + st_off_lin<W>(lane % 16, k0, (lane / 16) * 8));
 }
 template <int W>
 __device__ __forceinline__ bf16x8 tr_operand_st(const bf16* X, int k0, int n0, int lane) {
     const int g = lane / 16, s = lane % 16;
-    // rows k0 + 8g + s/4 have r % 8 < 4; the second read's rows (+4) have r % 8 >= 4
-    const bf16* p = X + (k0 + g * 8 + s / 4) * (W + 16) + n0 + 4 * (s % 4);
-    const v4i16 a = lds_read_tr16(p);
-    const v4i16 b = lds_read_tr16(p + 4 * (W + 16) + 8);
+    const int r = g * 8 + s / 4, c = 4 * (s % 4);
+    const bf16* base = X + (k0 / 16) * st_group<W>();
+    const v4i16 a = lds_read_tr16(base + st_off_lin<W>(r, n0, c));
+    const v4i16 b = lds_read_tr16(base + st_off_lin<W>(r + 4, n0, c));
     typedef short v8i16 __attribute__((ext_vector_type(8)));
     const v8i16 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(bf16x8, v);
 }
-// tr_operand_perm of a staggered tile (k0 a multiple of 8)
+// tr_operand_perm of a swizzled tile (k0 and n0 multiples of 16)
 template <int W>
 __device__ __forceinline__ bf16x8 tr_operand_perm_st(const bf16* X, int k0, int n0, int lane) {
     const int g = lane / 16, s = lane % 16;
-    // rows k0 + 4g + s/4: r % 8 >= 4 for odd g
-    const bf16* p = X + (k0 + g * 4 + s / 4) * (W + 16) + 8 * (g & 1) + n0 + 4 * (s % 4);
-    const v4i16 a = lds_read_tr16(p);
-    const v4i16 b = lds_read_tr16(p + 16 * (W + 16));  // rows + 16: the same r % 8
+    const int r = g * 4 + s / 4, c = 4 * (s % 4);
+    const bf16* base = X + (k0 / 16) * st_group<W>();
+    const v4i16 a = lds_read_tr16(base + st_off_lin<W>(r, n0, c));
+    const v4i16 b = lds_read_tr16(base + st_group<W>() + st_off_lin<W>(r, n0, c));
     typedef short v8i16 __attribute__((ext_vector_type(8)));
     const v8i16 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(bf16x8, v);

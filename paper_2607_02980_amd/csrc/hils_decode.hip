@@ -502,7 +502,7 @@ __device__ void merge_row_wave(const FwdArgs& a, const DecLayout& ly, size_t rg,
 // that hold it.  Keys at or past nk are masked.
 template <int D>
 struct PartWaveSmem {
-    static constexpr int VROW = D + 16;  // conflict-free transposing reads
+    static constexpr int VROW = D + 16;  // padded rows (transposing reads meet two addresses per bank)
     bf16 v[kChunk * VROW];
 };
 

@@ -383,16 +383,17 @@ __global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs 
 // lie in one bucket of rows (2048, more for long sequences: see kInvBucketRows).
 // The items of a (b, g) come bucket by bucket, so the query rows that the blocks
 // in flight gather (2048 rows x G heads, 2 MiB at d = 128) stay in the L2s.
-// Units of work are (16 entries, head) pairs; wave w takes units w, w + 4, ...
-// K and V^T of the chunk are held in registers as MFMA operands for the whole
-// block, and the next unit's rows are fetched while the current one computes.
-// K and V of the chunk, and the landmark rows of the group's heads, stay in LDS
-// and every unit reads its MFMA operands from there, so that a wave holds only
-// one unit's state and the prefetched operands of the next: four waves per
-// SIMD keep the gathers of many units in flight (the kernel waits on memory,
-// not on the matrix cores).  K rows are padded by 8 elements (16-byte row reads
-// without bank conflicts), V rows by 16 (transposing 8-byte reads without
-// conflicts).
+// Units of work are (16 entries, head) pairs; wave w takes units w, w + 4, ...,
+// and the next unit's rows are fetched while the current one computes.  K and V
+// of the chunk, and the landmark rows of the group's heads, stay in LDS and every
+// unit reads its MFMA operands from there, so that a wave holds only one unit's
+// state and the prefetched operands of the next: four waves per SIMD keep the
+// gathers of many units in flight (the kernel waits on memory, not on the matrix
+// cores).  K rows are padded by 8 elements, V rows by 16: on gfx950 both the
+// 16-byte row reads and the transposing reads of these tiles meet two addresses
+// per bank (the bank-conflict counters put that at about a third of the LDS
+// cycles), but LDS waits are about 1 % of the wave cycles here, so the simpler
+// padded layouts stay.
 template <int D, int G, bool ROUTE>
 __global__ __launch_bounds__(kBlock, ROUTE ? 2 : 4) void k_pf_chunks(FwdArgs a, const int* boff, int nR,
                                                                     const int* list, const int4* work,

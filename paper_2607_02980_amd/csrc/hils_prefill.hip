@@ -1,5 +1,6 @@
 // HiLS attention prefill forward on MFMA (bf16 storage, fp32 accumulation), gfx950.
 //
+//   P0 k_pf_lse      (per-head normalised ranking) LSE_h over C_i of every (row, head)
 //   P1 k_pf_score    per 32-query tile: s^_hc = scale * q^_h . k'_c (+ b') on 16x16x32
 //                    MFMA tiles, the group max over the G heads (App. C), and the
 //                    top-K of every row (exact register radix select, Eq. (9)).
@@ -147,9 +148,9 @@ __device__ __forceinline__ void lse16_merge(float& m, float& s) {
     step(dpp<0x140>(m), dpp<0x140>(s));
 }
 
-// NORM: rank by per-head normalised scores.  A first pass over the candidates
-// gives each (row, head) its log-sum-exp over C_i; the second subtracts it
-// before the maximum over the group's heads.
+// NORM: rank by per-head normalised scores: k_pf_lse has left each (row, head)'s
+// log-sum-exp over C_i in the lse output, and the scores here subtract it before
+// the maximum over the group's heads.
 //
 // Four waves per 32-row tile: wave w scores chunk blocks w, w + 4, ... of each
 // slice against all rows, then selects rows 8w .. 8w + 7 one after another.  Both
@@ -161,7 +162,7 @@ constexpr int kSW = 4;           // waves per score block
 constexpr int kSR = kSQ / kSW;   // rows selected per wave
 size_t score_dyn_lds(int K) { return (size_t)kSQ * K * (sizeof(float) + sizeof(int)) + kSQ * sizeof(int); }
 template <int D, int G, bool NORM>
-__global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs a) {
+__global__ __launch_bounds__(kSW * kWave, NORM ? 3 : 4) void k_pf_score(FwdArgs a) {
     constexpr int KS = Tiles<D>::KS;
     constexpr int NCB = kSL / 16;
     constexpr int E = kSL / kWave;
@@ -193,90 +194,10 @@ __global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs 
     if (lane < kSR) s_nb[kSR * w + lane] = 0;  // a wave's rows are its own: no barrier needed
 
     if constexpr (NORM) {
-        // pass 1: per (row, head) log-sum-exp of s^ over the row's candidates; the
-        // per-wave partials live in s_sig until the slices need it
-        float* s_pm = &s_sig[0][0];     // [kSW waves][G][kSQ]
-        float* s_ps = s_pm + kSW * G * kSQ;
-        const int lg = lane / 16;
-        for (int hh = 0; hh < G; ++hh) {
-            const int h = g * G + hh, hl = (a.Hl == a.Hq) ? h : g;
-            const bf16* lbase = lmk + ((size_t)b * a.Hl + hl) * nC * D;
-            float rm[NT][4], rs[NT][4];
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    rm[t][i] = -INFINITY;
-                    rs[t][i] = 0.f;
-                }
-            for (int s0 = 0; s0 < nct; s0 += kSL) {
-                bf16x8 bl[NJ][KS];
-                float bv[NJ];
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    const int c = min(s0 + (w + kSW * j) * 16 + lane % 16, nC - 1);
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) bl[j][ks] = ld_bf16x8(lbase + (size_t)c * D + ks * 32 + lg * 8);
-                    bv[j] = a.bias ? a.bias[((size_t)b * a.Hl + hl) * nC + c] : 0.f;
-                }
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const int qa = min(q0 + 16 * t + lane % 16, a.N - 1);
-                    bf16x8 aq[KS];
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks)
-                        aq[ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + h) * a.N + qa) * D + ks * 32 + lg * 8);
-                    float x[NJ][4];
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) {
-                        f32x4 acc4 = zero4();
-#pragma unroll
-                        for (int ks = 0; ks < KS; ++ks) acc4 = mfma16x16x32(aq[ks], bl[j][ks], acc4);
-                        const int c = s0 + (w + kSW * j) * 16 + lane % 16;
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const int n = q0 + 16 * t + lg * 4 + i;
-                            x[j][i] = (n < a.N && c < n_candidates(n, a.W)) ? a.scale * acc4[i] + bv[j] : -INFINITY;
-                        }
-                    }
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        float mx = rm[t][i];
-#pragma unroll
-                        for (int j = 0; j < NJ; ++j) mx = fmaxf(mx, x[j][i]);
-                        if (mx == -INFINITY) continue;
-                        float sum = rs[t][i] * fexp(rm[t][i] - mx);
-#pragma unroll
-                        for (int j = 0; j < NJ; ++j) sum += fexp(x[j][i] - mx);
-                        rm[t][i] = mx;
-                        rs[t][i] = sum;
-                    }
-                }
-            }
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    lse16_merge(rm[t][i], rs[t][i]);
-                    if (lane % 16 == 0) {
-                        s_pm[(w * G + hh) * kSQ + 16 * t + lg * 4 + i] = rm[t][i];
-                        s_ps[(w * G + hh) * kSQ + 16 * t + lg * 4 + i] = rs[t][i];
-                    }
-                }
-        }
-        __syncthreads();
+        // the per-(row, head) log-sum-exps that k_pf_lse left in the lse output
         for (int e = tid; e < G * kSQ; e += kSW * kWave) {
-            const int hh = e / kSQ, row = e % kSQ;
-            float m = -INFINITY;
-#pragma unroll
-            for (int ww = 0; ww < kSW; ++ww) m = fmaxf(m, s_pm[(ww * G + hh) * kSQ + row]);
-            float sum = 0.f;
-#pragma unroll
-            for (int ww = 0; ww < kSW; ++ww) {
-                const float pm = s_pm[(ww * G + hh) * kSQ + row];
-                sum += pm == -INFINITY ? 0.f : s_ps[(ww * G + hh) * kSQ + row] * fexp(pm - m);
-            }
-            s_lse[hh][row] = m == -INFINITY ? -INFINITY : m + __logf(sum);
+            const int hh = e / kSQ, row = e % kSQ, n = min(q0 + row, a.N - 1);
+            s_lse[hh][row] = a.lse[((size_t)b * a.Hq + g * G + hh) * a.N + n];
         }
         __syncthreads();
     }
@@ -373,6 +294,121 @@ __global__ __launch_bounds__(kSW * kWave, NORM ? 2 : 4) void k_pf_score(FwdArgs 
         const int nb = s_nb[row];
         int32_t* orow = a.idx + (((size_t)b * a.Hkv + g) * a.N + n) * K;
         if (lane < K) orow[lane] = lane < nb ? s_bid[row * K + lane] : -1;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// P0 (per-head normalised ranking only): the log-sum-exp over the candidate chunks
+// of every (row, query head), LSE_h(i) = log sum_{c in C_i} exp(s^_hc) (Sec. 4.1),
+// which the ranking subtracts before the group max.  One block of 8 waves per
+// (128 rows, query head): wave w holds the q^ rows of its 16 queries as A operands,
+// the candidates' landmark rows come through LDS 64 at a time (double-buffered:
+// the next block is fetched into registers while the current one is used), and
+// every lane keeps a running (max, sum of exp) for its 4 rows over the candidate
+// columns it holds, merged over the 16 lanes of its group at the end.  The result
+// goes to the prefill's lse output, which the fusion overwrites at the end of the
+// call.
+constexpr int kLseRows = 128;
+constexpr int kLseCand = 64;
+template <int D>
+__global__ __launch_bounds__(8 * kWave) void k_pf_lse(FwdArgs a) {
+    constexpr int KS = D / 32, NT = 8 * kWave;
+    constexpr int PPT = kLseCand * D / 8 / NT;  // 16-byte pieces per thread of a landmark block
+    static_assert(PPT >= 1 && PPT * NT == kLseCand * D / 8, "landmark blocks split evenly over the threads");
+    __shared__ __align__(16) bf16 s_l[2][st_size<D>(kLseCand)];
+    __shared__ float s_b[2][kLseCand];
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
+    const int q0 = blockIdx.x * kLseRows, h = blockIdx.y, b = blockIdx.z;
+    const int G = a.Hq / a.Hkv, hl = (a.Hl == a.Hq) ? h : h / G;
+    const int nC = a.L / kChunk;
+    const int qlast = min(q0 + kLseRows - 1, a.N - 1);
+    const int nct = min(nC, n_candidates(qlast, a.W));
+    const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q);
+    const bf16* lbase = as<bf16>(a.lmk) + ((size_t)b * a.Hl + hl) * nC * D;
+    const float* bbase = a.bias ? a.bias + ((size_t)b * a.Hl + hl) * nC : nullptr;
+    // the wave's 16 q^ rows as A operands (row l%16, dims 32 ks + 8 (l/16) ...)
+    bf16x8 aq[KS];
+    {
+        const int qa = min(q0 + 16 * w + lane % 16, a.N - 1);
+        const bf16* qrow = qr + (((size_t)b * a.Hq + h) * a.N + qa) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) aq[ks] = ld_bf16x8(qrow + ks * 32 + lg * 8);
+    }
+    struct LRegs {
+        uint4 x[PPT];
+        float bv;
+    };
+    auto fetch = [&](int c0) {
+        LRegs r;
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            const int c = min(c0 + j, nC - 1);
+            r.x[u] = *reinterpret_cast<const uint4*>(lbase + (size_t)c * D + d8);
+        }
+        r.bv = (bbase && tid < kLseCand) ? bbase[min(c0 + tid, nC - 1)] : 0.f;
+        return r;
+    };
+    auto store = [&](int buf, const LRegs& r) {
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            *reinterpret_cast<uint4*>(&s_l[buf][st_off<D>(j, d8)]) = r.x[u];
+        }
+        if (tid < kLseCand) s_b[buf][tid] = r.bv;
+    };
+    // running (max, sum of exp) of rows q0 + 16 w + 4 lg + i over this lane's columns
+    float rm[4], rs[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        rm[i] = -INFINITY;
+        rs[i] = 0.f;
+    }
+    const int nblk = (nct + kLseCand - 1) / kLseCand;
+    if (nblk > 0) {
+        LRegs nx = fetch(0);
+        store(0, nx);
+        __syncthreads();
+        for (int blk = 0; blk < nblk; ++blk) {
+            const int buf = blk & 1;
+            const bool more = blk + 1 < nblk;  // uniform over the block
+            if (more) nx = fetch((blk + 1) * kLseCand);
+            float x[4][4];
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) {
+                f32x4 acc = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    acc = mfma16x16x32(aq[ks], row_operand_st<D>(s_l[buf], nb * 16, ks * 32, lane), acc);
+                const int j = nb * 16 + lane % 16, c = blk * kLseCand + j;
+                const float bv = s_b[buf][j];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int n = q0 + 16 * w + 4 * lg + i;
+                    x[nb][i] = (n < a.N && c < n_candidates(n, a.W)) ? a.scale * acc[i] + bv : -INFINITY;
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float mx = fmaxf(fmaxf(x[0][i], x[1][i]), fmaxf(x[2][i], x[3][i]));
+                if (mx == -INFINITY) continue;
+                const float nm = fmaxf(rm[i], mx);
+                float sum = rs[i] * fexp(rm[i] - nm);
+#pragma unroll
+                for (int nb = 0; nb < 4; ++nb) sum += fexp(x[nb][i] - nm);
+                rm[i] = nm;
+                rs[i] = sum;
+            }
+            if (more) store(buf ^ 1, nx);
+            __syncthreads();
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        lse16_merge(rm[i], rs[i]);
+        const int n = q0 + 16 * w + 4 * lg + i;
+        if (lane % 16 == 0 && n < a.N)
+            a.lse[((size_t)b * a.Hq + h) * a.N + n] = rm[i] == -INFINITY ? -INFINITY : rm[i] + __logf(rs[i]);
     }
 }
 
@@ -987,9 +1023,11 @@ struct PfRun {
         if (!a.given_idx) {
             const dim3 grid((unsigned)((a.N + kSQ - 1) / kSQ) * a.Hkv * a.B);
             const size_t dyn = score_dyn_lds(a.K);
-            if (a.head_norm)
+            if (a.head_norm) {
+                const dim3 lgr((unsigned)((a.N + kLseRows - 1) / kLseRows), a.Hq, a.B);
+                HILS_LAUNCH("k_pf_lse", k_pf_lse<D>, lgr, dim3(8 * kWave), 0, s, a);
                 HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a);
-            else
+            } else
                 HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kSW * kWave), dyn, s, a);
         }
         const dim3 lgrid((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B);

@@ -1,9 +1,14 @@
 // HiLS attention prefill forward on MFMA (bf16 storage, fp32 accumulation), gfx950.
 //
 //   P0 k_pf_lse      (per-head normalised ranking) LSE_h over C_i of every (row, head)
-//   P1 k_pf_score    per 32-query tile: s^_hc = scale * q^_h . k'_c (+ b') on 16x16x32
-//                    MFMA tiles, the group max over the G heads (App. C), and the
-//                    top-K of every row (exact register radix select, Eq. (9)).
+//   P1 k_pf_sigma    per 128 queries of a KV group: s^_hc = scale * q^_h . k'_c (+ b')
+//      k_pf_select   on 16x16x32 MFMA tiles and the group max over the G heads (App.
+//                    C) into the workspace, then the top-K of every row (exact
+//                    register radix select, Eq. (9)), one wave per row.  With more
+//                    than 512 candidate chunks, when that array does not fit the
+//                    records' area, under union packing and under the per-head
+//                    normalised ranking, k_pf_score does both in one pass per
+//                    32-query tile.
 //   inverse index    rows that selected each (b, g, chunk)
 //   P3 k_pf_chunks   chunk-major: K_c, V_c staged once in LDS, the selecting rows
 //                    gathered 16 at a time; S^T = K_c Q^T, the intra-chunk softmax
@@ -410,6 +415,146 @@ __global__ __launch_bounds__(8 * kWave) void k_pf_lse(FwdArgs a) {
         if (lane % 16 == 0 && n < a.N)
             a.lse[((size_t)b * a.Hq + h) * a.N + n] = rm[i] == -INFINITY ? -INFINITY : rm[i] + __logf(rs[i]);
     }
+}
+
+// ---------------------------------------------------------------------------
+// P1 split in two (raw ranking, up to 512 candidate chunks): the group scores
+// sigma_ic = max_h s^_hc (App. C) of every (row, KV group, candidate), then the
+// top-K of each row from them.  k_pf_sigma takes 128 rows of one KV group per
+// block of 8 waves: each wave holds the q^ rows of its 16 queries for the G heads
+// as MFMA A operands, the candidates' landmark rows come through LDS 64 at a time
+// (one tile per landmark head, double-buffered) and serve all 8 waves, and the
+// max over the heads stays in registers until a block of 64 candidates is done
+// and written out.  With 128 rows behind every landmark load the scoring runs at
+// about three times the rate of the fused 32-row scorer, whose selection is then
+// the only part left to it; k_pf_select ranks each row in one wave
+// (wave_topk_reg over E registers of 64 candidates, ties to the smaller id, the
+// same selection as the fused scorer makes).  sigma [B, Hkv, N, L/S] f32 lives in
+// the records' area of the workspace, which the chunk pass fills only after the
+// selection.
+template <int D, int G>
+__global__ __launch_bounds__(8 * kWave) void k_pf_sigma(FwdArgs a, float* sig) {
+    constexpr int KS = D / 32, NT = 8 * kWave;
+    constexpr int PPT = kLseCand * D / 8 / NT;  // 16-byte pieces per thread of a landmark block
+    static_assert(PPT >= 1 && PPT * NT == kLseCand * D / 8, "landmark blocks split evenly over the threads");
+    __shared__ __align__(16) bf16 s_l[2][st_size<D>(kLseCand)];
+    __shared__ float s_b[2][kLseCand];
+    const int tid = threadIdx.x, w = wave_id(), lane = tid % kWave, lg = lane / 16;
+    const int q0 = blockIdx.x * kLseRows, g = blockIdx.y, b = blockIdx.z;
+    const int nC = a.L / kChunk;
+    const int qlast = min(q0 + kLseRows - 1, a.N - 1);
+    const int nct = min(nC, n_candidates(qlast, a.W));
+    const bool shared_lmk = a.Hl != a.Hq;  // one landmark head per KV group
+    const int NH = shared_lmk ? 1 : G;     // landmark tiles per block of candidates
+    const size_t bg = (size_t)b * a.Hkv + g;
+    const bf16* qr = as<bf16>(a.q_route ? a.q_route : a.q);
+    // the wave's 16 q^ rows of each head (row l%16, dims 32 ks + 8 (l/16) ...)
+    bf16x8 aq[G][KS];
+    {
+        const int qa = min(q0 + 16 * w + lane % 16, a.N - 1);
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                aq[hh][ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + g * G + hh) * a.N + qa) * D + ks * 32 + lg * 8);
+    }
+    struct LRegs {
+        uint4 x[PPT];
+        float bv;
+    };
+    // step t: candidate block t / NH, landmark head t % NH
+    auto fetch = [&](int t) {
+        const int hl = shared_lmk ? g : g * G + t % NH;
+        const size_t lrow0 = ((size_t)b * a.Hl + hl) * nC;
+        const int c0 = (t / NH) * kLseCand;
+        LRegs r;
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            r.x[u] = *reinterpret_cast<const uint4*>(as<bf16>(a.lmk) + (lrow0 + min(c0 + j, nC - 1)) * D + d8);
+        }
+        r.bv = (a.bias && tid < kLseCand) ? a.bias[lrow0 + min(c0 + tid, nC - 1)] : 0.f;
+        return r;
+    };
+    auto store = [&](int buf, const LRegs& r) {
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * NT, j = e / (D / 8), d8 = (e % (D / 8)) * 8;
+            *reinterpret_cast<uint4*>(&s_l[buf][st_off<D>(j, d8)]) = r.x[u];
+        }
+        if (tid < kLseCand) s_b[buf][tid] = r.bv;
+    };
+    const int nsteps = (nct + kLseCand - 1) / kLseCand * NH;
+    if (nsteps == 0) return;  // uniform over the block: no row of the tile has candidates
+    LRegs nx = fetch(0);
+    store(0, nx);
+    __syncthreads();
+    f32x4 sg[4];  // sigma of rows 16 w + 4 lg + i, candidates 16 nb + l%16 of the block
+    for (int t = 0; t < nsteps; ++t) {
+        const int buf = t & 1, lh = t % NH;
+        const bool more = t + 1 < nsteps;  // uniform over the block
+        if (more) nx = fetch(t + 1);
+        if (lh == 0)
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) sg[nb] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            if (!shared_lmk && hh != lh) continue;  // this tile is head lh's landmark rows
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) {
+                f32x4 acc = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    acc = mfma16x16x32(aq[hh][ks], row_operand_st<D>(s_l[buf], nb * 16, ks * 32, lane), acc);
+                const float bv = s_b[buf][nb * 16 + lane % 16];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sg[nb][i] = fmaxf(sg[nb][i], a.scale * acc[i] + bv);
+            }
+        }
+        if (lh == NH - 1) {
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) {
+                const int c = (t / NH) * kLseCand + nb * 16 + lane % 16;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int n = q0 + 16 * w + 4 * lg + i;
+                    if (n < a.N && c < nC) sig[(bg * a.N + n) * nC + c] = sg[nb][i];
+                }
+            }
+        }
+        if (more) store(buf ^ 1, nx);
+        __syncthreads();
+    }
+}
+
+// One wave per (row, KV group): the K best of sigma over the row's candidates
+// C_i (E registers of 64 candidates per lane, ids ascending over (register, lane)).
+constexpr int kSelWaves = 4;
+template <int E>
+__global__ __launch_bounds__(kSelWaves * kWave) void k_pf_select(FwdArgs a, const float* sig) {
+    __shared__ int s_tid[kSelWaves][kWave];
+    __shared__ float s_tsc[kSelWaves][kWave];
+    __shared__ int s_oid[kSelWaves][kWave];
+    __shared__ float s_osc[kSelWaves][kWave];
+    const int w = wave_id(), lane = threadIdx.x % kWave;
+    const size_t r = (size_t)blockIdx.x * kSelWaves + w;  // (b, g, n) row
+    if (r >= (size_t)a.B * a.Hkv * a.N) return;           // whole wave
+    const int n = (int)(r % a.N);
+    const int nC = a.L / kChunk, lim = min(nC, n_candidates(n, a.W));
+    const float* row = sig + r * nC;
+    float sc[E];
+    int id[E];
+    bool ok[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int c = e * kWave + lane;
+        ok[e] = c < lim;
+        sc[e] = ok[e] ? row[c] : 0.f;
+        id[e] = c;
+    }
+    const int m = wave_topk_reg<E, kTopkNatural>(sc, id, ok, a.K, s_oid[w], s_osc[w], s_tid[w], s_tsc[w]);
+    int32_t* orow = a.idx + r * a.K;
+    if (lane < a.K) orow[lane] = lane < m ? s_oid[w][lane] : -1;
 }
 
 // ---------------------------------------------------------------------------
@@ -1027,6 +1172,24 @@ struct PfRun {
                 const dim3 lgr((unsigned)((a.N + kLseRows - 1) / kLseRows), a.Hq, a.B);
                 HILS_LAUNCH("k_pf_lse", k_pf_lse<D>, lgr, dim3(8 * kWave), 0, s, a);
                 HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a);
+            } else if (const int nC = a.L / kChunk;
+                       nC <= 8 * kWave && !a.union_pack &&
+                       (size_t)a.B * a.Hkv * a.N * nC * sizeof(float) <= ly.wgt - ly.part) {
+                // the split scorer: sigma in the records' area (see k_pf_sigma)
+                float* sigma = reinterpret_cast<float*>(ws + ly.part);
+                const dim3 sgr((unsigned)((a.N + kLseRows - 1) / kLseRows), a.Hkv, a.B);
+                HILS_LAUNCH("k_pf_sigma", (k_pf_sigma<D, G>), sgr, dim3(8 * kWave), 0, s, a, sigma);
+                const size_t rows = (size_t)a.B * a.Hkv * a.N;
+                const dim3 rgr((unsigned)((rows + kSelWaves - 1) / kSelWaves));
+                const dim3 rbl(kSelWaves * kWave);
+                if (nC <= kWave)
+                    HILS_LAUNCH("k_pf_select", k_pf_select<1>, rgr, rbl, 0, s, a, (const float*)sigma);
+                else if (nC <= 2 * kWave)
+                    HILS_LAUNCH("k_pf_select", k_pf_select<2>, rgr, rbl, 0, s, a, (const float*)sigma);
+                else if (nC <= 4 * kWave)
+                    HILS_LAUNCH("k_pf_select", k_pf_select<4>, rgr, rbl, 0, s, a, (const float*)sigma);
+                else
+                    HILS_LAUNCH("k_pf_select", k_pf_select<8>, rgr, rbl, 0, s, a, (const float*)sigma);
             } else
                 HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kSW * kWave), dyn, s, a);
         }

@@ -6,9 +6,8 @@
 //                    C) into the workspace, then the top-K of every row (exact
 //                    register radix select, Eq. (9)), one wave per row.  With more
 //                    than 512 candidate chunks, when that array does not fit the
-//                    records' area, under union packing and under the per-head
-//                    normalised ranking, k_pf_score does both in one pass per
-//                    32-query tile.
+//                    records' area and under union packing, k_pf_score does both
+//                    in one pass per 32-query tile.
 //   inverse index    rows that selected each (b, g, chunk)
 //   P3 k_pf_chunks   chunk-major: K_c, V_c staged once in LDS, the selecting rows
 //                    gathered 16 at a time; S^T = K_c Q^T, the intra-chunk softmax
@@ -431,8 +430,9 @@ __global__ __launch_bounds__(8 * kWave) void k_pf_lse(FwdArgs a) {
 // (wave_topk_reg over E registers of 64 candidates, ties to the smaller id, the
 // same selection as the fused scorer makes).  sigma [B, Hkv, N, L/S] f32 lives in
 // the records' area of the workspace, which the chunk pass fills only after the
-// selection.
-template <int D, int G>
+// selection.  NORM (per-head normalised ranking): each head's scores less the
+// (row, head) log-sum-exp that k_pf_lse left in lse, before the max over heads.
+template <int D, int G, bool NORM>
 __global__ __launch_bounds__(8 * kWave) void k_pf_sigma(FwdArgs a, float* sig) {
     constexpr int KS = D / 32, NT = 8 * kWave;
     constexpr int PPT = kLseCand * D / 8 / NT;  // 16-byte pieces per thread of a landmark block
@@ -458,6 +458,14 @@ __global__ __launch_bounds__(8 * kWave) void k_pf_sigma(FwdArgs a, float* sig) {
             for (int ks = 0; ks < KS; ++ks)
                 aq[hh][ks] = ld_bf16x8(qr + (((size_t)b * a.Hq + g * G + hh) * a.N + qa) * D + ks * 32 + lg * 8);
     }
+    // NORM: the log-sum-exps of rows 16 w + 4 lg + i (k_pf_lse left them in lse)
+    float sub[NORM ? G : 1][4];
+#pragma unroll
+    for (int hh = 0; hh < (NORM ? G : 1); ++hh)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            sub[hh][i] = NORM ? a.lse[((size_t)b * a.Hq + g * G + hh) * a.N + min(q0 + 16 * w + 4 * lg + i, a.N - 1)]
+                              : 0.f;
     struct LRegs {
         uint4 x[PPT];
         float bv;
@@ -508,7 +516,7 @@ __global__ __launch_bounds__(8 * kWave) void k_pf_sigma(FwdArgs a, float* sig) {
                     acc = mfma16x16x32(aq[hh][ks], row_operand_st<D>(s_l[buf], nb * 16, ks * 32, lane), acc);
                 const float bv = s_b[buf][nb * 16 + lane % 16];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) sg[nb][i] = fmaxf(sg[nb][i], a.scale * acc[i] + bv);
+                for (int i = 0; i < 4; ++i) sg[nb][i] = fmaxf(sg[nb][i], a.scale * acc[i] + bv - sub[NORM ? hh : 0][i]);
             }
         }
         if (lh == NH - 1) {
@@ -1171,14 +1179,17 @@ struct PfRun {
             if (a.head_norm) {
                 const dim3 lgr((unsigned)((a.N + kLseRows - 1) / kLseRows), a.Hq, a.B);
                 HILS_LAUNCH("k_pf_lse", k_pf_lse<D>, lgr, dim3(8 * kWave), 0, s, a);
-                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a);
-            } else if (const int nC = a.L / kChunk;
-                       nC <= 8 * kWave && !a.union_pack &&
-                       (size_t)a.B * a.Hkv * a.N * nC * sizeof(float) <= ly.wgt - ly.part) {
+            }
+            const int nC = a.L / kChunk;
+            if (nC <= 8 * kWave && !a.union_pack &&
+                (size_t)a.B * a.Hkv * a.N * nC * sizeof(float) <= ly.wgt - ly.part) {
                 // the split scorer: sigma in the records' area (see k_pf_sigma)
                 float* sigma = reinterpret_cast<float*>(ws + ly.part);
                 const dim3 sgr((unsigned)((a.N + kLseRows - 1) / kLseRows), a.Hkv, a.B);
-                HILS_LAUNCH("k_pf_sigma", (k_pf_sigma<D, G>), sgr, dim3(8 * kWave), 0, s, a, sigma);
+                if (a.head_norm)
+                    HILS_LAUNCH("k_pf_sigma", (k_pf_sigma<D, G, true>), sgr, dim3(8 * kWave), 0, s, a, sigma);
+                else
+                    HILS_LAUNCH("k_pf_sigma", (k_pf_sigma<D, G, false>), sgr, dim3(8 * kWave), 0, s, a, sigma);
                 const size_t rows = (size_t)a.B * a.Hkv * a.N;
                 const dim3 rgr((unsigned)((rows + kSelWaves - 1) / kSelWaves));
                 const dim3 rbl(kSelWaves * kWave);
@@ -1190,8 +1201,11 @@ struct PfRun {
                     HILS_LAUNCH("k_pf_select", k_pf_select<4>, rgr, rbl, 0, s, a, (const float*)sigma);
                 else
                     HILS_LAUNCH("k_pf_select", k_pf_select<8>, rgr, rbl, 0, s, a, (const float*)sigma);
-            } else
+            } else if (a.head_norm) {
+                HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a);
+            } else {
                 HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, false>), grid, dim3(kSW * kWave), dyn, s, a);
+            }
         }
         const dim3 lgrid((a.N + LocalCfg<G>::QT - 1) / LocalCfg<G>::QT, a.Hkv, a.B);
         if (a.union_pack) {

@@ -2,7 +2,10 @@
 inverse index, chunk pass and local pass run over 2048-row segments reusing one
 workspace.  Every row is compared with the oracle, and the outputs must equal
 those of the unsegmented run bit for bit (each row's terms are computed the same
-way in any segment)."""
+way in any segment).  Where the group scores of all rows do not fit a segment's
+records the selection falls back from the split scorer (k_pf_sigma, k_pf_select)
+to the fused one (k_pf_score); both compute the same scores in the same order, so
+the selections must agree exactly too (the MHA and fallback cases)."""
 import numpy as np
 import pytest
 import torch
@@ -21,6 +24,11 @@ CASES = {
     "bf16_head_norm_G8_d64": (dict(B=1, Hq=8, Hkv=1, N=4096, L=4096, d=64, topk=16, window=512), 203, False, False,
                               4),
     "bf16_mha_G1": (dict(B=1, Hq=2, Hkv=2, N=6200, L=6208, d=64, topk=4, window=100), 204, False, False, 0),
+    # the group scores of all rows (4.8 MB) fit the records' area of the whole sequence
+    # but not that of a 2048-row segment: the unsegmented run takes the split scorer,
+    # the segmented one the fused scorer, and both must select the same chunks
+    "bf16_head_norm_fused_fallback": (dict(B=1, Hq=4, Hkv=2, N=6200, L=6208, d=64, topk=2, window=100), 205, True,
+                                      False, 4),
 }
 
 

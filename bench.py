@@ -72,7 +72,11 @@ def prefill_kernel_model(B, Hq, Hkv, N, L, d, S, K, W, elem=2):
     counted; they show in the measured traffic).
 
     k_pf_score : landmark scores over C_i, 2d per (head, candidate); reads q and
-                 the landmarks once, writes idx.
+                 the landmarks once, writes idx (the fused scorer).
+    k_pf_sigma : the same scores and their group max, the split scorer's first
+                 pass (the group-score array it writes is the design's).
+    k_pf_select: the top-K of every row from the group scores: no method FLOPs;
+                 writes idx.
     k_pf_chunks: per selected (row, head, chunk) QK^T + PV over S keys (4dS) and
                  the surrogate score (2d); reads q and the K/V once.
     k_pf_local : window QK^T + PV, 4d per (row, head, window key), and the fusion;
@@ -91,6 +95,9 @@ def prefill_kernel_model(B, Hq, Hkv, N, L, d, S, K, W, elem=2):
     records = B * Hq * nsel * (d * elem + 4)
     return {
         "k_pf_score": {"flop": B * Hq * 2 * d * float(ncand.sum()), "bytes": qbytes + lmkbytes + idxbytes},
+        "k_pf_sigma": {"flop": B * Hq * 2 * d * float(ncand.sum()), "bytes": qbytes + lmkbytes,
+                       "design_bytes": B * Hkv * 4 * float(ncand.sum())},
+        "k_pf_select": {"flop": 0.0, "bytes": idxbytes, "design_bytes": B * Hkv * 4 * float(ncand.sum())},
         "k_pf_chunks": {"flop": B * Hq * (4 * d * S + 2 * d) * nsel, "bytes": qbytes + kvbytes,
                         "design_bytes": records},
         "k_pf_local": {"flop": B * Hq * 4 * d * float(nloc.sum()), "bytes": qbytes + kvbytes + qbytes + B * Hq * N * 4,

@@ -86,6 +86,50 @@ def test_prefill_32k_bf16_sampled_rows():
     check_lse(l[0][:, rows_n], ref["lse"][0][:, rows_n], p.dtype)
 
 
+@pytest.mark.parametrize("flags", [0, 4], ids=["raw_ranking", "head_norm"])
+def test_prefill_long_sequence_fused_scorer(flags):
+    # 625 candidate chunks (more than 512): the selection takes the fused scorer,
+    # three 256-candidate slices per row (the path of every prefill beyond 32K
+    # tokens), and under the per-head normalised ranking the log-sum-exp pass first
+    from paper_2607_02980_amd import hils
+
+    p = hils.Params(B=1, Hq=8, Hkv=2, N=40000, L=40000, d=64, topk=16, window=512, dtype="bf16", flags=flags)
+    nc = p.L // p.chunk
+    wid = 31
+    host = {
+        "q": synth.normal_host((p.B, p.Hq, p.N, p.d), synth.seed_for(wid, "q"), p.dtype),
+        "k": synth.normal_host((p.B, p.Hkv, p.L, p.d), synth.seed_for(wid, "k"), p.dtype),
+        "v": synth.normal_host((p.B, p.Hkv, p.L, p.d), synth.seed_for(wid, "v"), p.dtype),
+        "lmk": synth.normal_host((p.B, p.Hq, nc, p.d), synth.seed_for(wid, "lmk"), p.dtype),
+    }
+    dev = {k: v.to("cuda", torch.bfloat16).contiguous() for k, v in host.items()}
+    log(f"[long] N=L={p.N} ({nc} chunks) flags={flags}: GPU prefill")
+    out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"])
+    torch.cuda.synchronize()
+    gidx = idx.cpu().numpy()
+    ncand = np.maximum(0, (np.arange(p.N) - p.window + 1) // p.chunk)
+    valid = gidx >= 0
+    assert (valid.sum(-1) == np.minimum(p.topk, ncand)[None, None, :]).all(), "selection sizes"
+    assert (valid[..., 1:] <= valid[..., :-1]).all(), "-1 only as trailing padding"
+    steps = np.diff(gidx.astype(np.int64), axis=-1)
+    assert (steps[valid[..., 1:]] > 0).all(), "valid entries strictly ascending"
+    assert (np.where(valid, gidx, -1) < ncand[None, None, :, None]).all(), "chunks in C_i"
+    assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all(), "finite outputs"
+    # rows past 32K + W have more than 512 candidates
+    rows_n = sorted(set(sampled_rows(p.N, p.window, 120, 7) + [33280, 33343, 33344, 36000, 39999]))
+    rows = np.array([(0, n) for n in rows_n], np.int32)
+    s = oshape(p)
+    arr = {k: v.numpy() for k, v in host.items()}
+    log(f"  oracle on {len(rows)} rows")
+    ref = oracle.fwd(s, arr["q"], arr["k"], arr["v"], arr["lmk"], rows=rows)
+    nd = check_selection(p, host, gidx, ref["idx"], rows=[tuple(r) for r in rows])
+    log(f"  selection: {nd} rows differ only by accepted ties")
+    ref = oracle.fwd(s, arr["q"], arr["k"], arr["v"], arr["lmk"], rows=rows, idx=gidx)
+    o, l = np32(out), np32(lse)
+    check_close("out(sampled rows)", o[0][:, rows_n], ref["out"][0][:, rows_n], p.dtype)
+    check_lse(l[0][:, rows_n], ref["lse"][0][:, rows_n], p.dtype)
+
+
 def _decode_device_inputs(W, p):
     nc = p.L // p.chunk
     return {

@@ -5,7 +5,7 @@
 //      k_pf_select   on 16x16x32 MFMA tiles and the group max over the G heads (App.
 //                    C) into the workspace, then the top-K of every row (exact
 //                    register radix select, Eq. (9)), one wave per row.  With more
-//                    than 512 candidate chunks, when that array does not fit the
+//                    than 1024 candidate chunks, when that array does not fit the
 //                    records' area and under union packing, k_pf_score does both
 //                    in one pass per 32-query tile.
 //   inverse index    rows that selected each (b, g, chunk)
@@ -417,7 +417,7 @@ __global__ __launch_bounds__(8 * kWave) void k_pf_lse(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// P1 split in two (raw ranking, up to 512 candidate chunks): the group scores
+// P1 split in two (up to 1024 candidate chunks): the group scores
 // sigma_ic = max_h s^_hc (App. C) of every (row, KV group, candidate), then the
 // top-K of each row from them.  k_pf_sigma takes 128 rows of one KV group per
 // block of 8 waves: each wave holds the q^ rows of its 16 queries for the G heads
@@ -1181,7 +1181,7 @@ struct PfRun {
                 HILS_LAUNCH("k_pf_lse", k_pf_lse<D>, lgr, dim3(8 * kWave), 0, s, a);
             }
             const int nC = a.L / kChunk;
-            if (nC <= 8 * kWave && !a.union_pack &&
+            if (nC <= 16 * kWave && !a.union_pack &&
                 (size_t)a.B * a.Hkv * a.N * nC * sizeof(float) <= ly.wgt - ly.part) {
                 // the split scorer: sigma in the records' area (see k_pf_sigma)
                 float* sigma = reinterpret_cast<float*>(ws + ly.part);
@@ -1199,8 +1199,10 @@ struct PfRun {
                     HILS_LAUNCH("k_pf_select", k_pf_select<2>, rgr, rbl, 0, s, a, (const float*)sigma);
                 else if (nC <= 4 * kWave)
                     HILS_LAUNCH("k_pf_select", k_pf_select<4>, rgr, rbl, 0, s, a, (const float*)sigma);
-                else
+                else if (nC <= 8 * kWave)
                     HILS_LAUNCH("k_pf_select", k_pf_select<8>, rgr, rbl, 0, s, a, (const float*)sigma);
+                else
+                    HILS_LAUNCH("k_pf_select", k_pf_select<16>, rgr, rbl, 0, s, a, (const float*)sigma);
             } else if (a.head_norm) {
                 HILS_LAUNCH("k_pf_score", (k_pf_score<D, G, true>), grid, dim3(kSW * kWave), dyn, s, a);
             } else {

@@ -86,14 +86,25 @@ def test_prefill_32k_bf16_sampled_rows():
     check_lse(l[0][:, rows_n], ref["lse"][0][:, rows_n], p.dtype)
 
 
-@pytest.mark.parametrize("flags", [0, 4], ids=["raw_ranking", "head_norm"])
-def test_prefill_long_sequence_fused_scorer(flags):
-    # 625 candidate chunks (more than 512): the selection takes the fused scorer,
-    # three 256-candidate slices per row (the path of every prefill beyond 32K
-    # tokens), and under the per-head normalised ranking the log-sum-exp pass first
+LONG_CASES = {
+    # name: (N = L, Hq, Hkv, flags, extra rows).  40K tokens: 625 candidate chunks,
+    # the split scorer with 16 registers of candidates per lane; 66,560 tokens: 1,040
+    # chunks, beyond the split scorer, so the fused one with five 256-candidate slices
+    # per row (every prefill beyond 64K tokens takes it); each under the raw and the
+    # per-head normalised ranking (the log-sum-exp pass first)
+    "split_625_chunks": (40000, 8, 2, 0, [33280, 33343, 33344, 36000]),
+    "split_625_chunks_head_norm": (40000, 8, 2, 4, [33280, 33343, 33344, 36000]),
+    "fused_1040_chunks": (66560, 4, 1, 0, [65600, 66111, 66112, 66500]),
+    "fused_1040_chunks_head_norm": (66560, 4, 1, 4, [65600, 66111, 66112, 66500]),
+}
+
+
+@pytest.mark.parametrize("name", list(LONG_CASES))
+def test_prefill_long_sequence_scorers(name):
     from paper_2607_02980_amd import hils
 
-    p = hils.Params(B=1, Hq=8, Hkv=2, N=40000, L=40000, d=64, topk=16, window=512, dtype="bf16", flags=flags)
+    N, Hq, Hkv, flags, extra = LONG_CASES[name]
+    p = hils.Params(B=1, Hq=Hq, Hkv=Hkv, N=N, L=N, d=64, topk=16, window=512, dtype="bf16", flags=flags)
     nc = p.L // p.chunk
     wid = 31
     host = {
@@ -103,7 +114,7 @@ def test_prefill_long_sequence_fused_scorer(flags):
         "lmk": synth.normal_host((p.B, p.Hq, nc, p.d), synth.seed_for(wid, "lmk"), p.dtype),
     }
     dev = {k: v.to("cuda", torch.bfloat16).contiguous() for k, v in host.items()}
-    log(f"[long] N=L={p.N} ({nc} chunks) flags={flags}: GPU prefill")
+    log(f"[long] case={name} N=L={p.N} ({nc} chunks) flags={flags}: GPU prefill")
     out, lse, idx = hils.hils_prefill_fwd(p, dev["q"], dev["k"], dev["v"], dev["lmk"])
     torch.cuda.synchronize()
     gidx = idx.cpu().numpy()
@@ -115,8 +126,7 @@ def test_prefill_long_sequence_fused_scorer(flags):
     assert (steps[valid[..., 1:]] > 0).all(), "valid entries strictly ascending"
     assert (np.where(valid, gidx, -1) < ncand[None, None, :, None]).all(), "chunks in C_i"
     assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all(), "finite outputs"
-    # rows past 32K + W have more than 512 candidates
-    rows_n = sorted(set(sampled_rows(p.N, p.window, 120, 7) + [33280, 33343, 33344, 36000, 39999]))
+    rows_n = sorted(set(sampled_rows(p.N, p.window, 120, 7) + extra))
     rows = np.array([(0, n) for n in rows_n], np.int32)
     s = oshape(p)
     arr = {k: v.numpy() for k, v in host.items()}

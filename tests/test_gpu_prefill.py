@@ -123,6 +123,16 @@ def test_prefill_union_packing(name):
     run_case(name, flags=hils.HILS_FLAG_UNION_PACKING)
 
 
+@pytest.mark.parametrize("name", ["bf16_ragged_multi_tile", "bf16_route_Hl_eq_Hkv", "bf16_G8_d128",
+                                  "bf16_head_gap_150"])
+def test_prefill_union_packing_head_normalised(name):
+    # union packing (no workspace, so the fused scorer) under the per-head normalised
+    # ranking, whose log-sum-exps come from the separate pass
+    from paper_2607_02980_amd import hils
+
+    run_case(name, flags=hils.HILS_FLAG_UNION_PACKING | hils.HILS_FLAG_HEAD_NORM_SELECT)
+
+
 @pytest.mark.parametrize("G", [4, 1])
 def test_prefill_union_packing_on_locality_inputs(G):
     # queries correlated along the sequence (adjacent queries share most chunks):
